@@ -1,0 +1,170 @@
+"""Fully-connected surrogate, MSE loss, back-propagation and Adam (oracle side, fp64).
+
+What the paper fixes (Sec. 4.1): the direct surrogate maps the 6 inputs (X, t)
+to the whole field u_X^t (Eq. 1 and Sec. 2); it is a multilayer perceptron
+with ReLU hidden layers trained with Adam at learning rate 1e-3; the training
+and validation metric is the mean squared error (Sec. 4.4-4.6).
+
+Readings where the paper is silent (each is listed with its reason in the
+design notes):
+  * the output layer is the identity (a field of temperatures, no squashing);
+  * the loss is the mean of (Y - U)^2 over all B*D entries;
+  * Adam (Kingma and Ba, 2015, Algorithm 1) with beta1 = 0.9, beta2 = 0.999,
+    eps = 1e-8, bias correction, no weight decay, t counted from 1;
+  * ReLU'(0) = 0;
+  * weights W_l are stored out x in, row-major; Z_l = A_{l-1} W_l^T + b_l;
+  * initialisation U(-1/sqrt(fan_in), +1/sqrt(fan_in)) for W and b, drawn from
+    Philox4x64-10 (kind INIT, counter (e, layer), e = flat index over W then b)
+    and rounded to fp32.
+
+bf16 mode mirrors the rounding points of the mixed-precision path: layer 1
+(K = 6 raw inputs) stays fp32 in the forward pass; the operands of every other
+forward GEMM (activations A_{l-1}, the bf16 copy of W_l) are rounded to bf16
+(round to nearest even from fp32); the output-layer gradient dY is rounded to
+bf16 before the backward GEMMs, as is every back-propagated dZ_l; bias
+gradients are sums of those rounded values; Adam works on fp32 master weights
+and fp32 gradients.  All accumulation here is fp64.
+
+Pins: central finite differences of the loss on tiny nets, torch fp64
+autograd of the same net, Adam's step-1 closed form (-lr * sign(g) up to eps),
+hand-computed MSE values.
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass, field
+from typing import List, Tuple
+
+import numpy as np
+
+from .philox import init_uniform_vec
+
+Params = List[Tuple[np.ndarray, np.ndarray]]
+
+
+def bf16_round(x: np.ndarray) -> np.ndarray:
+    """Round to bf16 (8 significant bits), nearest-even, via the fp32 value; fp64 out.
+
+    An fp32 bit pattern keeps its top 16 bits after adding 0x7FFF plus the
+    lowest kept bit (round half to even); NaN is not expected here.
+    """
+    f = np.asarray(x, dtype=np.float64).astype(np.float32)
+    bits = f.view(np.uint32).astype(np.uint64)
+    lsb = (bits >> np.uint64(16)) & np.uint64(1)
+    rounded = ((bits + np.uint64(0x7FFF) + lsb) >> np.uint64(16)) << np.uint64(16)
+    return rounded.astype(np.uint32).view(np.float32).astype(np.float64)
+
+
+def init_params(widths, seed: int) -> Params:
+    """Seeded U(+-1/sqrt(fan_in)) initialisation, fp32 values held in fp64."""
+    params: Params = []
+    for l in range(len(widths) - 1):
+        fan_in, fan_out = widths[l], widths[l + 1]
+        n_w = fan_out * fan_in
+        e = np.arange(n_w + fan_out, dtype=np.uint64)
+        bound = 1.0 / np.sqrt(float(fan_in))
+        vals = (init_uniform_vec(seed, e, l) * bound).astype(np.float32).astype(np.float64)
+        params.append((vals[:n_w].reshape(fan_out, fan_in).copy(), vals[n_w:].copy()))
+    return params
+
+
+def init_rows(widths, seed: int, layer: int, rows) -> Tuple[np.ndarray, np.ndarray]:
+    """Initial W[rows, :] and b[rows] of one layer without materialising the layer."""
+    fan_in, fan_out = widths[layer], widths[layer + 1]
+    rows = np.asarray(rows, dtype=np.int64)
+    bound = 1.0 / np.sqrt(float(fan_in))
+    e = (rows[:, None] * fan_in + np.arange(fan_in)[None, :]).reshape(-1).astype(np.uint64)
+    w = (init_uniform_vec(seed, e, layer) * bound).astype(np.float32).astype(np.float64)
+    eb = (fan_out * fan_in + rows).astype(np.uint64)
+    b = (init_uniform_vec(seed, eb, layer) * bound).astype(np.float32).astype(np.float64)
+    return w.reshape(len(rows), fan_in), b
+
+
+def forward(params: Params, X: np.ndarray, bf16: bool = False):
+    """Return (Zs, As, Y): pre-activations, activations (As[0] = X), output."""
+    A = np.asarray(X, dtype=np.float64)
+    As, Zs = [A], []
+    L = len(params)
+    for l, (W, b) in enumerate(params):
+        if bf16 and l > 0:
+            Z = bf16_round(A) @ bf16_round(W).T + b
+        else:
+            Z = A @ W.T + b
+        Zs.append(Z)
+        if l < L - 1:
+            A = np.maximum(Z, 0.0)
+            As.append(A)
+    return Zs, As, Zs[-1]
+
+
+def mse(Y: np.ndarray, U: np.ndarray) -> float:
+    """Mean over all entries of (Y - U)^2."""
+    R = np.asarray(Y, dtype=np.float64) - np.asarray(U, dtype=np.float64)
+    return float(np.sum(R * R) / R.size)
+
+
+def loss_and_grads(params: Params, X: np.ndarray, U: np.ndarray, bf16: bool = False):
+    """MSE loss and its gradients with respect to every W_l and b_l."""
+    Zs, As, Y = forward(params, X, bf16=bf16)
+    U = np.asarray(U, dtype=np.float64)
+    R = Y - U
+    loss = float(np.sum(R * R) / R.size)
+    dZ = 2.0 * R / R.size                     # dLoss/dY
+    if bf16:
+        dZ = bf16_round(dZ)
+    L = len(params)
+    grads: Params = [None] * L                # type: ignore[list-item]
+    for l in range(L - 1, -1, -1):
+        W = params[l][0]
+        A_in = As[l]
+        if bf16 and l > 0:
+            dW = dZ.T @ bf16_round(A_in)
+        else:
+            dW = dZ.T @ A_in
+        db = dZ.sum(axis=0)
+        grads[l] = (dW, db)
+        if l > 0:
+            dA = dZ @ (bf16_round(W) if bf16 else W)
+            dZ = dA * (Zs[l - 1] > 0.0)
+            if bf16:
+                dZ = bf16_round(dZ)
+    return loss, grads
+
+
+@dataclass
+class Adam:
+    """Adam with bias correction (Kingma and Ba, 2015, Algorithm 1)."""
+    lr: float = 1e-3
+    beta1: float = 0.9
+    beta2: float = 0.999
+    eps: float = 1e-8
+    t: int = 0
+    m: list = field(default_factory=list)
+    v: list = field(default_factory=list)
+
+    def step(self, params: Params, grads: Params) -> Params:
+        if not self.m:
+            self.m = [(np.zeros_like(W), np.zeros_like(b)) for W, b in params]
+            self.v = [(np.zeros_like(W), np.zeros_like(b)) for W, b in params]
+        self.t += 1
+        c1 = 1.0 - self.beta1 ** self.t
+        c2 = 1.0 - self.beta2 ** self.t
+        out: Params = []
+        for l, ((W, b), (gW, gb)) in enumerate(zip(params, grads)):
+            new = []
+            for i, (p, g) in enumerate(((W, gW), (b, gb))):
+                m = self.beta1 * self.m[l][i] + (1.0 - self.beta1) * g
+                v = self.beta2 * self.v[l][i] + (1.0 - self.beta2) * g * g
+                self._store(l, i, m, v)
+                new.append(p - self.lr * (m / c1) / (np.sqrt(v / c2) + self.eps))
+            out.append((new[0], new[1]))
+        return out
+
+    def _store(self, l, i, m, v):
+        ms, vs = list(self.m[l]), list(self.v[l])
+        ms[i], vs[i] = m, v
+        self.m[l], self.v[l] = tuple(ms), tuple(vs)
+
+
+def predict(params: Params, X: np.ndarray, bf16: bool = False) -> np.ndarray:
+    """Surrogate output f_theta(X, t) for each input row."""
+    return forward(params, X, bf16=bf16)[2]
