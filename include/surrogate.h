@@ -1,0 +1,93 @@
+/* Fully-connected deep surrogate and its train step (the paper's use case,
+ * Sec. 4.1): an MLP that maps the 6 inputs (X, t) to the whole field u_X^t
+ * (Eq. 1 defines the mapping X -> {u_X^t}), ReLU on hidden layers, identity
+ * output, mean-squared-error loss, Adam with learning rate 1e-3.
+ *
+ * Layer l (1..L) has W_l of widths[l] x widths[l-1] (out x in, row-major)
+ * and b_l of widths[l]; Z_l = A_{l-1} W_l^T + b_l, A_l = ReLU(Z_l) for l < L,
+ * Y = Z_L.  Loss = mean over the B x D batch of (Y - U)^2.  Adam (Kingma and
+ * Ba, 2015): beta1, beta2, eps as given, bias-corrected, no weight decay, step
+ * counter t from 1.  ReLU'(0) = 0.
+ *
+ * Precision OT_FP32: every GEMM on fp32 operands with fp32 accumulation.
+ * Precision OT_BF16: layer 1 (K = widths[0]) in fp32; every other GEMM takes
+ * bf16 operands (activations, a bf16 copy of W refreshed by each Adam step,
+ * and back-propagated dY / dZ), accumulates in fp32; master weights, Adam
+ * moments and gradients stay fp32.
+ *
+ * Initialisation: W and b ~ U(-1/sqrt(fan_in), 1/sqrt(fan_in)); element e of
+ * layer l (flat index over W then b) is (2 m / 2^24 - 1) / sqrt(fan_in) rounded
+ * to fp32, m = top 24 bits of Philox4x64-10 word 0 at counter (e, l-1, 3, 0),
+ * key (seed, 0).
+ *
+ * Ownership: the surrogate owns its parameters, gradients, Adam state and
+ * workspaces (device memory on the device current at creation).  Device
+ * pointers passed in are the caller's; they must be 16-byte aligned and field
+ * rows must have leading dimensions that are multiples of 4.  Calls on one
+ * surrogate must not overlap (one training thread, as in the paper's server);
+ * train_step and predict are asynchronous on the given stream.
+ */
+#ifndef OT_SURROGATE_H
+#define OT_SURROGATE_H
+
+#include <stdint.h>
+
+#include "ot_status.h"
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct ot_surrogate ot_surrogate;
+
+enum ot_precision { OT_FP32 = 0, OT_BF16 = 1 };
+
+/* Create an MLP with n_widths - 1 layers (2 <= n_widths <= 16, every width in
+ * [1, 2^26]), parameters initialised from `seed` as above, Adam state zero.
+ * max_batch: rows the train / predict workspaces are first sized for (grown
+ * on demand).  flags must be 0.
+ * Errors: OT_E_INVAL, OT_E_NOMEM, OT_E_HIP. */
+int surrogate_create(ot_surrogate** out, const int64_t* widths, int32_t n_widths,
+                     int32_t precision, float lr, float beta1, float beta2, float eps,
+                     uint64_t seed, int64_t max_batch, uint32_t flags);
+
+/* Replace layer `layer` (0-based) parameters from dense host arrays W
+ * (widths[layer+1] x widths[layer]) and b (widths[layer+1]); either may be
+ * NULL.  Synchronous.  Refreshes the bf16 weight copy. */
+int surrogate_set_params(ot_surrogate* s, int32_t layer, const float* W_host, const float* b_host);
+
+/* Copy layer parameters (fp32 master) to dense host arrays.  Synchronous. */
+int surrogate_get_params(ot_surrogate* s, int32_t layer, float* W_host, float* b_host);
+
+/* Copy the gradients of the last train step of one layer.  Synchronous. */
+int surrogate_get_grads(ot_surrogate* s, int32_t layer, float* dW_host, float* db_host);
+
+/* Copy Adam moments of one layer and the step counter t (each nullable). */
+int surrogate_get_adam_state(ot_surrogate* s, int32_t layer, float* mW_host, float* mb_host,
+                             float* vW_host, float* vb_host, int64_t* t_out);
+
+/* Set the learning rate used by later train steps (schedules). */
+int surrogate_set_lr(ot_surrogate* s, float lr);
+
+/* One train step on a batch of b rows: forward, MSE loss, backward, Adam.
+ * x: b rows of widths[0] fp32 at stride ldx; u: b target rows of widths[L]
+ * fp32 at stride ldu (multiple of 4).  loss_dev: device fp32 scalar that
+ * receives the batch loss (nullable).  1 <= b <= 2^20.
+ * Errors: OT_E_INVAL, OT_E_NOMEM, OT_E_HIP. */
+int surrogate_train_step(ot_surrogate* s, const float* x, int64_t ldx, const float* u,
+                         int64_t ldu, int64_t b, void* stream, float* loss_dev);
+
+/* Surrogate prediction Y = f_theta(x) (Eq. 1's u_X^t estimate) for n rows.
+ * x: n rows at stride ldx; y: n rows of widths[L] fp32 at stride ldy
+ * (multiple of 4).  Errors: OT_E_INVAL, OT_E_NOMEM, OT_E_HIP. */
+int surrogate_predict(ot_surrogate* s, const float* x, int64_t ldx, int64_t n, float* y,
+                      int64_t ldy, void* stream);
+
+/* Synchronise and free everything the surrogate owns. */
+int surrogate_destroy(ot_surrogate* s);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* OT_SURROGATE_H */

@@ -1,0 +1,67 @@
+// Internal helpers of the online-training library: error state, HIP checks,
+// small device utilities.  Not part of the public C ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include <cstdarg>
+#include <string>
+
+#include "ot_status.h"
+
+namespace ot {
+
+// Record a message for ot_last_error() on this thread and return `code`.
+int set_error(int code, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
+void clear_error();
+
+inline int64_t round_up(int64_t v, int64_t m) { return (v + m - 1) / m * m; }
+inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+}  // namespace ot
+
+// Evaluate a HIP call; on failure record the message and return OT_E_HIP.
+#define OT_HIP(call)                                                                    \
+  do {                                                                                  \
+    hipError_t e_ = (call);                                                             \
+    if (e_ != hipSuccess)                                                               \
+      return ot::set_error(OT_E_HIP, "%s failed: %s", #call, hipGetErrorString(e_));    \
+  } while (0)
+
+// Check the last kernel launch.
+#define OT_LAUNCHED(name)                                                               \
+  do {                                                                                  \
+    hipError_t e_ = hipGetLastError();                                                  \
+    if (e_ != hipSuccess)                                                               \
+      return ot::set_error(OT_E_HIP, "launch of %s failed: %s", name,                   \
+                           hipGetErrorString(e_));                                      \
+  } while (0)
+
+#define OT_REQUIRE(cond, ...)                                                           \
+  do {                                                                                  \
+    if (!(cond)) return ot::set_error(OT_E_INVAL, __VA_ARGS__);                         \
+  } while (0)
+
+// Device helpers -------------------------------------------------------------------
+namespace ot {
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+}  // namespace ot
+
+#ifdef __HIPCC__
+namespace ot {
+
+__device__ inline float warp_sum(float v) {
+  // Fixed butterfly order over the 64 lanes of a wavefront: deterministic.
+  for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
+  return v;
+}
+
+__device__ inline double warp_sum(double v) {
+  for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
+  return v;
+}
+
+}  // namespace ot
+#endif

@@ -1,0 +1,331 @@
+// fp32 GEMM on CDNA4 matrix cores (v_mfma_f32_16x16x4_f32) with fused
+// epilogues for the surrogate's dense layers.
+//
+//   C[m, n] = sum_k A(m, k) * B(n, k)
+//
+// A(m, k) is stored k-contiguous (A[m * lda + k], "KMajor") or m-contiguous
+// (A[k * lda + m], "MNMajor"); B(n, k) likewise.  The three products of a
+// dense layer map onto it as
+//   forward  Z  = A_in W^T : A = activations (KMajor), B = W (KMajor)
+//   input grad dA = dZ W   : A = dZ (KMajor),         B = W viewed [k][n] (MNMajor)
+//   weight grad dW = dZ^T A_in : A = dZ viewed [k][m] (MNMajor), B = A_in (MNMajor)
+//
+// Tiling: 64 * WGM * WGN threads (WGM x WGN wavefronts), block tile
+// BM x BN = (16 FM WGM) x (16 FN WGN), k tile 16, double-buffered LDS tiles
+// stored m/n-contiguous (As[k][m], Bs[k][n]).  Within a wavefront, fragment f
+// of MFMA row i covers tile row 16*FM*wm + FM*i + f, so each lane fetches its
+// FM A values (and FN B values) for one k with a single LDS vector read.
+// MFMA lane layout (16x16x4 f32): lane l supplies A[i = l%16][k = l/16] and
+// B[k = l/16][j = l%16]; accumulator element r of lane l is D[4*(l/16)+r][l%16].
+// A lane therefore owns a (4 FM) x FN block of C: rows 4*FM*(l/16) + q,
+// q = FM*r + f, and columns FN*(l%16) + g.
+//
+// Blocks are numbered so that the WGM-by-... m tiles that share one n tile
+// are consecutive and land on the same XCD (L2) of the 8 on the chip.
+#pragma once
+
+#include "common.h"
+
+namespace ot {
+
+enum class Lay : int { KMajor = 0, MNMajor = 1 };
+enum class Epi : int {
+  Store = 0,     // C = acc
+  Bias = 1,      // C = acc + bias[n]
+  BiasRelu = 2,  // C = max(acc + bias[n], 0)
+  Mse = 3,       // Y = acc + bias[n]; R = Y - T; C = scale * R; partial sum of R^2 per block
+  SplitK = 4,    // C[split] = acc (partial sums, reduced by a separate pass)
+  Mask = 5       // C = acc * (mask[m, n] > 0)
+};
+
+struct GemmArgs {
+  const float* A;
+  int64_t lda;
+  const float* B;
+  int64_t ldb;
+  float* C;
+  int64_t ldc;
+  int64_t M, N, K;
+  int64_t k_chunk;          // k range per split (multiple of 16); >= K without split
+  int64_t split_stride;     // SplitK: elements between consecutive split slices of C
+  const float* bias;        // Bias, BiasRelu, Mse
+  const float* target;      // Mse
+  int64_t ldt;
+  float scale;              // Mse
+  double* loss_partials;    // Mse: one per block
+  const float* mask;        // Mask
+  int64_t ldmask;
+  float* rowsum;            // optional: sum_k A(m, k) for m of the block's rows (n tile 0 only)
+};
+
+constexpr int kNumXcd = 8;
+
+// Map the hardware block id to a logical tile id such that each XCD (blocks
+// are dispatched round-robin over the 8 XCDs) receives a contiguous range of
+// logical ids.
+__device__ __forceinline__ int64_t xcd_remap(int64_t p, int64_t g) {
+  const int64_t xcd = p % kNumXcd, q = p / kNumXcd;
+  const int64_t per = g / kNumXcd, rem = g % kNumXcd;
+  return xcd * per + (xcd < rem ? xcd : rem) + q;
+}
+
+template <int FM>
+struct FragVec;
+template <>
+struct FragVec<4> { typedef f32x4 T; };
+template <>
+struct FragVec<2> { typedef f32x2 T; };
+template <>
+struct FragVec<1> { typedef float T; };
+
+template <int WGM, int WGN, int FM, int FN, Lay LA, Lay LB, Epi EPI>
+__global__ __launch_bounds__(64 * WGM * WGN) void gemm_f32_kernel(GemmArgs g) {
+  constexpr int NT = 64 * WGM * WGN;
+  constexpr int BK = 16;
+  constexpr int BM = 16 * FM * WGM;
+  constexpr int BN = 16 * FN * WGN;
+  constexpr int PAD = 4;
+  constexpr int LDA_S = BM + PAD;
+  constexpr int LDB_S = BN + PAD;
+  constexpr int VA = BM * BK / 4 / NT;  // float4 loads per thread per k tile
+  constexpr int VB = BN * BK / 4 / NT;
+  static_assert(VA >= 1 && VA * NT * 4 == BM * BK, "A tile does not split evenly");
+  static_assert(VB >= 1 && VB * NT * 4 == BN * BK, "B tile does not split evenly");
+
+  __shared__ __attribute__((aligned(16))) float As[2][BK * LDA_S];
+  __shared__ __attribute__((aligned(16))) float Bs[2][BK * LDB_S];
+  __shared__ double s_red[NT / 64];
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63, wid = tid >> 6;
+  const int wm = wid % WGM, wn = wid / WGM;
+
+  const int64_t tiles_m = (g.M + BM - 1) / BM;
+  const int64_t tiles_n = (g.N + BN - 1) / BN;
+  const int64_t logical = xcd_remap(blockIdx.x, (int64_t)gridDim.x);
+  const int64_t tm = logical % tiles_m, tn = logical / tiles_m;
+  (void)tiles_n;
+  const int64_t m0 = tm * BM, n0 = tn * BN;
+  const int64_t split = blockIdx.y;
+  const int64_t kbeg = split * g.k_chunk;
+  const int64_t kend = (kbeg + g.k_chunk < g.K) ? kbeg + g.k_chunk : g.K;
+  const int64_t nk = (kend > kbeg) ? (kend - kbeg + BK - 1) / BK : 0;
+
+  // Global -> register staging of one k tile.
+  f32x4 ra[VA], rb[VB];
+
+  auto load_tile = [&](int64_t k0) {
+#pragma unroll
+    for (int i = 0; i < VA; ++i) {
+      const int v = tid + i * NT;
+      if constexpr (LA == Lay::MNMajor) {
+        const int kr = v / (BM / 4), mc = (v % (BM / 4)) * 4;
+        const int64_t k = k0 + kr, m = m0 + mc;
+        f32x4 t = {0.f, 0.f, 0.f, 0.f};
+        if (k < kend) {
+          const float* p = g.A + k * g.lda + m;
+          if (m + 3 < g.M) t = *reinterpret_cast<const f32x4*>(p);
+          else
+            for (int c = 0; c < 4; ++c) t[c] = (m + c < g.M) ? p[c] : 0.f;
+        }
+        ra[i] = t;
+      } else {
+        const int mr = v / 4, kc = (v % 4) * 4;
+        const int64_t m = m0 + mr, k = k0 + kc;
+        f32x4 t = {0.f, 0.f, 0.f, 0.f};
+        if (m < g.M) {
+          const float* p = g.A + m * g.lda + k;
+          if (k + 3 < kend) t = *reinterpret_cast<const f32x4*>(p);
+          else
+            for (int c = 0; c < 4; ++c) t[c] = (k + c < kend) ? p[c] : 0.f;
+        }
+        ra[i] = t;
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < VB; ++i) {
+      const int v = tid + i * NT;
+      if constexpr (LB == Lay::MNMajor) {
+        const int kr = v / (BN / 4), nc = (v % (BN / 4)) * 4;
+        const int64_t k = k0 + kr, n = n0 + nc;
+        f32x4 t = {0.f, 0.f, 0.f, 0.f};
+        if (k < kend) {
+          const float* p = g.B + k * g.ldb + n;
+          if (n + 3 < g.N) t = *reinterpret_cast<const f32x4*>(p);
+          else
+            for (int c = 0; c < 4; ++c) t[c] = (n + c < g.N) ? p[c] : 0.f;
+        }
+        rb[i] = t;
+      } else {
+        const int nr = v / 4, kc = (v % 4) * 4;
+        const int64_t n = n0 + nr, k = k0 + kc;
+        f32x4 t = {0.f, 0.f, 0.f, 0.f};
+        if (n < g.N) {
+          const float* p = g.B + n * g.ldb + k;
+          if (k + 3 < kend) t = *reinterpret_cast<const f32x4*>(p);
+          else
+            for (int c = 0; c < 4; ++c) t[c] = (k + c < kend) ? p[c] : 0.f;
+        }
+        rb[i] = t;
+      }
+    }
+  };
+
+  auto store_tile = [&](int buf) {
+    float* as = As[buf];
+    float* bs = Bs[buf];
+#pragma unroll
+    for (int i = 0; i < VA; ++i) {
+      const int v = tid + i * NT;
+      if constexpr (LA == Lay::MNMajor) {
+        const int kr = v / (BM / 4), mc = (v % (BM / 4)) * 4;
+        *reinterpret_cast<f32x4*>(as + kr * LDA_S + mc) = ra[i];
+      } else {
+        const int mr = v / 4, kc = (v % 4) * 4;
+#pragma unroll
+        for (int c = 0; c < 4; ++c) as[(kc + c) * LDA_S + mr] = ra[i][c];
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < VB; ++i) {
+      const int v = tid + i * NT;
+      if constexpr (LB == Lay::MNMajor) {
+        const int kr = v / (BN / 4), nc = (v % (BN / 4)) * 4;
+        *reinterpret_cast<f32x4*>(bs + kr * LDB_S + nc) = rb[i];
+      } else {
+        const int nr = v / 4, kc = (v % 4) * 4;
+#pragma unroll
+        for (int c = 0; c < 4; ++c) bs[(kc + c) * LDB_S + nr] = rb[i][c];
+      }
+    }
+  };
+
+  f32x4 acc[FM][FN];
+#pragma unroll
+  for (int f = 0; f < FM; ++f)
+#pragma unroll
+    for (int h = 0; h < FN; ++h) acc[f][h] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  // Optional row sums of A over k (bias gradient of the weight-gradient GEMM).
+  const bool do_rowsum = (g.rowsum != nullptr) && (tn == 0);
+  float rsum = 0.f;
+
+  const int a_off = 16 * FM * wm + FM * (lane % 16);
+  const int b_off = 16 * FN * wn + FN * (lane % 16);
+  const int kl = lane / 16;
+
+  if (nk > 0) {
+    load_tile(kbeg);
+    store_tile(0);
+    __syncthreads();
+  }
+  for (int64_t kt = 0; kt < nk; ++kt) {
+    const int buf = (int)(kt & 1);
+    if (kt + 1 < nk) load_tile(kbeg + (kt + 1) * BK);
+    const float* as = As[buf];
+    const float* bs = Bs[buf];
+#pragma unroll
+    for (int kk = 0; kk < BK / 4; ++kk) {
+      const int kr = 4 * kk + kl;
+      const typename FragVec<FM>::T av = *reinterpret_cast<const typename FragVec<FM>::T*>(as + kr * LDA_S + a_off);
+      const typename FragVec<FN>::T bv = *reinterpret_cast<const typename FragVec<FN>::T*>(bs + kr * LDB_S + b_off);
+#pragma unroll
+      for (int f = 0; f < FM; ++f) {
+        float a_f;
+        if constexpr (FM == 1) a_f = av; else a_f = av[f];
+#pragma unroll
+        for (int h = 0; h < FN; ++h) {
+          float b_h;
+          if constexpr (FN == 1) b_h = bv; else b_h = bv[h];
+          acc[f][h] = __builtin_amdgcn_mfma_f32_16x16x4f32(a_f, b_h, acc[f][h], 0, 0, 0);
+        }
+      }
+    }
+    if (do_rowsum && tid < BM) {
+#pragma unroll
+      for (int k = 0; k < BK; ++k) rsum += as[k * LDA_S + tid];
+    }
+    if (kt + 1 < nk) store_tile(buf ^ 1);
+    __syncthreads();
+  }
+  if (do_rowsum && tid < BM && m0 + tid < g.M) g.rowsum[m0 + tid] = rsum;
+
+  // ---------------------------------------------------------------- epilogue
+  double lsum = 0.0;
+  const int64_t row_base = m0 + 16 * FM * wm + 4 * FM * (lane / 16);
+  const int64_t col_base = n0 + 16 * FN * wn + FN * (lane % 16);
+  float* Cb = g.C + (EPI == Epi::SplitK ? split * g.split_stride : 0);
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+#pragma unroll
+    for (int f = 0; f < FM; ++f) {
+      const int64_t m = row_base + FM * r + f;
+      if (m >= g.M) continue;
+      float v[FN];
+#pragma unroll
+      for (int h = 0; h < FN; ++h) v[h] = acc[f][h][r];
+      const bool full = (col_base + FN - 1 < g.N);
+      if constexpr (EPI == Epi::Bias || EPI == Epi::BiasRelu || EPI == Epi::Mse) {
+#pragma unroll
+        for (int h = 0; h < FN; ++h)
+          if (col_base + h < g.N) v[h] += g.bias[col_base + h];
+      }
+      if constexpr (EPI == Epi::BiasRelu) {
+#pragma unroll
+        for (int h = 0; h < FN; ++h) v[h] = v[h] > 0.f ? v[h] : 0.f;
+      }
+      if constexpr (EPI == Epi::Mse) {
+        const float* tp = g.target + m * g.ldt + col_base;
+#pragma unroll
+        for (int h = 0; h < FN; ++h) {
+          if (col_base + h < g.N) {
+            const float rr = v[h] - tp[h];
+            lsum += (double)(rr * rr);
+            v[h] = g.scale * rr;
+          }
+        }
+      }
+      if constexpr (EPI == Epi::Mask) {
+        const float* mp = g.mask + m * g.ldmask + col_base;
+#pragma unroll
+        for (int h = 0; h < FN; ++h)
+          if (col_base + h < g.N) v[h] = mp[h] > 0.f ? v[h] : 0.f;
+      }
+      float* cp = Cb + m * g.ldc + col_base;
+      if (FN == 4 && full) {
+        *reinterpret_cast<f32x4*>(cp) = f32x4{v[0], v[FN > 1 ? 1 : 0], v[FN > 2 ? 2 : 0], v[FN > 3 ? 3 : 0]};
+      } else {
+#pragma unroll
+        for (int h = 0; h < FN; ++h)
+          if (col_base + h < g.N) cp[h] = v[h];
+      }
+    }
+  }
+  if constexpr (EPI == Epi::Mse) {
+    lsum = warp_sum(lsum);
+    if (lane == 0) s_red[wid] = lsum;
+    __syncthreads();
+    if (tid == 0) {
+      double t = 0.0;
+      for (int w = 0; w < NT / 64; ++w) t += s_red[w];
+      g.loss_partials[blockIdx.y * gridDim.x + blockIdx.x] = t;
+    }
+  }
+}
+
+// Host launcher.  Returns the hipError_t of the launch.
+template <int WGM, int WGN, int FM, int FN, Lay LA, Lay LB, Epi EPI>
+hipError_t launch_gemm_f32(const GemmArgs& g, int64_t splits, hipStream_t stream) {
+  constexpr int BM = 16 * FM * WGM, BN = 16 * FN * WGN;
+  const int64_t tiles = ((g.M + BM - 1) / BM) * ((g.N + BN - 1) / BN);
+  dim3 grid((unsigned)tiles, (unsigned)splits);
+  hipLaunchKernelGGL((gemm_f32_kernel<WGM, WGN, FM, FN, LA, LB, EPI>), grid, dim3(64 * WGM * WGN), 0, stream, g);
+  return hipGetLastError();
+}
+
+template <int WGM, int WGN, int FM, int FN>
+constexpr int64_t gemm_tiles(int64_t M, int64_t N) {
+  return ((M + 16 * FM * WGM - 1) / (16 * FM * WGM)) * ((N + 16 * FN * WGN - 1) / (16 * FN * WGN));
+}
+
+}  // namespace ot

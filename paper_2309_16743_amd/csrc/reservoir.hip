@@ -1,0 +1,637 @@
+// GPU-resident training reservoir: the paper's Algorithm 1 ("Reservoir",
+// Sec. 3.2.3) as slot-encoded device state plus four kernels per operation
+// pair (put: assign + copy, sample: select + gather).
+//
+// State on the device: an x slab (C x ldxs fp32) and a u slab (C x ldus fp32),
+// per-slot seen counts (int32, -1 = empty slot) and sample ids (int64), the
+// drain order `occ` (int32, used after reception ends), a histogram of seen
+// counts of samples that left the buffer, and a counter block.  In the normal
+// phase (reception not over) the occupied slots are exactly [0, N), so the
+// draw index is the slot.
+//
+// Every state-changing call runs in ticket order on the reservoir's ordering
+// stream, so the device state after ticket p depends only on the calls with
+// tickets <= p.  N is known on the host from the call sequence alone: a put
+// of k rows leaves N = min(C, N + k) (each row fills a free slot or replaces a
+// seen sample, and a = min(k, C - U) >= min(k, C - N)); a drain batch removes
+// min(b, N).  So readiness (N > T) never needs a device read-back.
+#include <algorithm>
+#include <mutex>
+
+#include "common.h"
+#include "philox.h"
+#include "reservoir.h"
+
+namespace ot {
+
+constexpr int kHistLen = 64;           // eviction histogram buckets (last = overflow)
+constexpr int64_t kMaxPut = 4096;      // rows per put (bounded LDS of the assign kernel)
+constexpr int64_t kMaxDrainBatch = 4096;
+constexpr int64_t kMaxBatch = 65536;
+constexpr int kAssignThreads = 1024;
+
+struct ResCounters {
+  long long U, S, N, total_put, total_evicted, total_deleted, total_draws, next_sample_id;
+  long long last_accepted;
+  long long pad[7];
+};
+
+// ------------------------------------------------------------------ device helpers
+__device__ inline void atomic_add_ll(long long* p, long long v) {
+  atomicAdd(reinterpret_cast<unsigned long long*>(p), static_cast<unsigned long long>(v));
+}
+
+// Exclusive scan of one int per thread over a block of NT threads.
+template <int NT>
+__device__ int block_exclusive_scan(int v, int* wave_tot, int* total) {
+  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+  int incl = v;
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    int t = __shfl_up(incl, off, 64);
+    if (lane >= off) incl += t;
+  }
+  if (lane == 63) wave_tot[wid] = incl;
+  __syncthreads();
+  if (wid == 0) {
+    const int w = lane < NT / 64 ? wave_tot[lane] : 0;
+    int wi = w;
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+      int t = __shfl_up(wi, off, 64);
+      if (lane >= off) wi += t;
+    }
+    if (lane < NT / 64) wave_tot[lane] = wi - w;
+    if (lane == NT / 64 - 1) *total = wi;
+  }
+  __syncthreads();
+  return incl - v + wave_tot[wid];
+}
+
+// Partial Fisher-Yates over a virtual array A (A[p] = base[p]) without
+// materialising the swaps.  Step j (0 <= j < E) swaps A[j] and A[r_j]
+// (r_j >= j) and takes A[j].  Position j is never touched after step j, so:
+//   pre_j   = A[j] just before step j = pre_i for the latest i < j with r_i = j,
+//             else base[j];
+//   taken_j = A[r_j] just before step j = pre_j if r_j = j, else pre_i for the
+//             latest i < j with r_i = r_j, else base[r_j].
+// The latest-writer searches run in parallel (O(E^2) comparisons in LDS) and
+// the pre_j chains are resolved by pointer jumping.  Inputs: r[0..E) in LDS.
+// Outputs: pre[0..E), taken[0..E) in LDS; last_writer[j] = 1 when no later
+// step writes position r_j (used by the drain to persist the shuffle).
+__device__ void resolve_partial_shuffle(int E, const int* r, const int* base, int* par, int* par2,
+                                        int* lv, int* pre, int* taken, int* last_writer) {
+  const int nt = blockDim.x;
+  for (int j = threadIdx.x; j < E; j += nt) {
+    const int rj = r[j];
+    int lp = -1, lvj = -1;
+    for (int i = j - 1; i >= 0 && (lp < 0 || lvj < 0); --i) {
+      const int ri = r[i];
+      if (lp < 0 && ri == j) lp = i;
+      if (lvj < 0 && ri == rj) lvj = i;
+    }
+    par[j] = lp >= 0 ? lp : j;
+    lv[j] = lvj;
+    int later = 1;
+    for (int i = j + 1; i < E; ++i)
+      if (r[i] == rj) { later = 0; break; }
+    last_writer[j] = later;
+  }
+  __syncthreads();
+  // Pointer jumping: after ceil(log2 E) rounds par[j] is the root of j's chain.
+  int* src = par;
+  int* dst = par2;
+  for (int span = 1; span < E; span <<= 1) {
+    for (int j = threadIdx.x; j < E; j += nt) dst[j] = src[src[j]];
+    __syncthreads();
+    int* t = src; src = dst; dst = t;
+  }
+  for (int j = threadIdx.x; j < E; j += nt) pre[j] = base[src[j]];
+  __syncthreads();
+  for (int j = threadIdx.x; j < E; j += nt) {
+    const int rj = r[j];
+    taken[j] = (rj == j) ? pre[j] : (lv[j] >= 0 ? pre[lv[j]] : base[rj]);
+  }
+  __syncthreads();
+}
+
+// ------------------------------------------------------------------ kernels
+__global__ void init_meta_kernel(int32_t* seen, long long* sample_id, int64_t C,
+                                 unsigned long long* hist, ResCounters* ctr) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < C) {
+    seen[i] = -1;
+    sample_id[i] = -1;
+  }
+  if (i < kHistLen) hist[i] = 0;
+  if (i < (int64_t)(sizeof(ResCounters) / sizeof(long long)))
+    reinterpret_cast<long long*>(ctr)[i] = 0;
+}
+
+// Put, metadata half.  One block.  a = min(k, C - U) rows are accepted; the
+// first F = min(a, C - N) go to free slots N.., the other E = a - F replace
+// seen samples chosen by a partial Fisher-Yates over the ascending list of
+// seen slots (Philox kind 2, j = replacement index, range S - j).
+__global__ __launch_bounds__(kAssignThreads) void put_assign_kernel(
+    int64_t k, uint64_t ticket, uint64_t seed, int64_t C, int32_t* __restrict__ seen,
+    long long* __restrict__ sample_id, int32_t* __restrict__ sarr, int32_t* __restrict__ put_slots,
+    unsigned long long* __restrict__ hist, ResCounters* __restrict__ ctr,
+    long long* __restrict__ accepted_out) {
+  __shared__ int s_r[kMaxPut];
+  __shared__ int s_par[kMaxPut];
+  __shared__ int s_par2[kMaxPut];
+  __shared__ int s_lv[kMaxPut];
+  __shared__ int s_pre[kMaxPut];
+  __shared__ int s_taken[kMaxPut];
+  __shared__ int s_last[kMaxPut];
+  __shared__ int s_wave[kAssignThreads / 64];
+  __shared__ int s_total;
+
+  const long long U = ctr->U, S = ctr->S, N = ctr->N, base_id = ctr->next_sample_id;
+  const long long a = min((long long)k, (long long)C - U);
+  const long long F = min(a, (long long)C - N);
+  const long long E = a - F;
+  const int tid = threadIdx.x, nt = blockDim.x;
+
+  for (long long i = tid; i < F; i += nt) {
+    const long long slot = N + i;
+    put_slots[i] = (int32_t)slot;
+    seen[slot] = 0;
+    sample_id[slot] = base_id + i;
+  }
+
+  if (E > 0) {
+    // E > 0 implies the buffer is full (N + F == C); list seen slots of [0, N).
+    const long long chunk = (N + nt - 1) / nt;
+    const long long lo = min((long long)tid * chunk, N), hi = min(lo + chunk, N);
+    int cnt = 0;
+    for (long long s = lo; s < hi; ++s) cnt += seen[s] >= 1;
+    int off = block_exclusive_scan<kAssignThreads>(cnt, s_wave, &s_total);
+    for (long long s = lo; s < hi; ++s)
+      if (seen[s] >= 1) sarr[off++] = (int32_t)s;
+    __syncthreads();
+    // s_total == S here (every occupied slot is unseen or seen).
+    for (long long j = tid; j < E; j += nt) {
+      const uint64_t w = draw_word(seed, (uint64_t)j, ticket, kKindEvict);
+      s_r[j] = (int)(j + (long long)range_map(w, (uint64_t)(S - j)));
+    }
+    __syncthreads();
+    resolve_partial_shuffle((int)E, s_r, sarr, s_par, s_par2, s_lv, s_pre, s_taken, s_last);
+    for (long long j = tid; j < E; j += nt) {
+      const int victim = s_taken[j];
+      const int c = seen[victim];
+      atomicAdd(&hist[min(c, kHistLen - 1)], 1ull);
+      seen[victim] = 0;
+      sample_id[victim] = base_id + F + j;
+      put_slots[F + j] = victim;
+    }
+  }
+  __syncthreads();
+  if (tid == 0) {
+    ctr->U = U + a;
+    ctr->S = S - E;
+    ctr->N = N + F;
+    ctr->total_put += a;
+    ctr->total_evicted += E;
+    ctr->next_sample_id = base_id + a;
+    ctr->last_accepted = a;
+    if (accepted_out) *accepted_out = a;
+  }
+}
+
+constexpr int kCopyThreads = 256;
+constexpr int kCopyVecPerThread = 4;
+constexpr int64_t kCopySeg = (int64_t)kCopyThreads * kCopyVecPerThread * 4;  // floats per block
+
+// Copy one row segment: dst[0..n) = src[0..n), float4 granules when aligned.
+template <bool kNtLoad, bool kNtStore>
+__device__ __forceinline__ void copy_segment(float* __restrict__ dst, const float* __restrict__ src,
+                                             int64_t n, bool vec_ok) {
+  const int t = threadIdx.x;
+  if (vec_ok) {
+    const int64_t n4 = n >> 2;
+    const f32x4* s4 = reinterpret_cast<const f32x4*>(src);
+    f32x4* d4 = reinterpret_cast<f32x4*>(dst);
+    f32x4 v[kCopyVecPerThread];
+#pragma unroll
+    for (int u = 0; u < kCopyVecPerThread; ++u) {
+      const int64_t i = (int64_t)u * kCopyThreads + t;
+      if (i < n4) v[u] = kNtLoad ? __builtin_nontemporal_load(s4 + i) : s4[i];
+    }
+#pragma unroll
+    for (int u = 0; u < kCopyVecPerThread; ++u) {
+      const int64_t i = (int64_t)u * kCopyThreads + t;
+      if (i < n4) {
+        if (kNtStore) __builtin_nontemporal_store(v[u], d4 + i);
+        else d4[i] = v[u];
+      }
+    }
+    for (int64_t i = (n4 << 2) + t; i < n; i += kCopyThreads) dst[i] = src[i];
+  } else {
+    for (int64_t i = t; i < n; i += kCopyThreads) dst[i] = src[i];
+  }
+}
+
+// Put, data half: row i < a of the chunk goes to slot put_slots[i].
+// grid = k rows x `segs` segments per row, flattened (row-major).
+__global__ __launch_bounds__(kCopyThreads) void put_copy_kernel(
+    const float* __restrict__ x, int64_t ldx, const float* __restrict__ u, int64_t ldu,
+    const int32_t* __restrict__ put_slots, const ResCounters* __restrict__ ctr,
+    float* __restrict__ xslab, int64_t ldxs, float* __restrict__ uslab, int64_t ldus, int64_t x_dim,
+    int64_t u_dim, int64_t segs, int vec_ok) {
+  const int64_t row = (int64_t)blockIdx.x / segs, seg = (int64_t)blockIdx.x % segs;
+  if (row >= ctr->last_accepted) return;
+  const int64_t slot = put_slots[row];
+  const int64_t seg0 = seg * kCopySeg;
+  const int64_t n = min(kCopySeg, u_dim - seg0);
+  copy_segment<true, true>(uslab + slot * ldus + seg0, u + row * ldu + seg0, n, vec_ok != 0);
+  if (seg == 0)
+    for (int64_t c = threadIdx.x; c < x_dim; c += kCopyThreads)
+      xslab[slot * ldxs + c] = x ? x[row * ldx + c] : 0.0f;
+}
+
+// Batch draw, normal phase: draw j picks slot floor(w_j N / 2^64), with
+// replacement; a first draw turns the slot from unseen to seen.
+__global__ void select_kernel(uint64_t seed, uint64_t ticket, int64_t N, int64_t b,
+                              int32_t* __restrict__ slots, int32_t* __restrict__ seen,
+                              ResCounters* __restrict__ ctr) {
+  const int64_t j = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (j == 0) atomic_add_ll(&ctr->total_draws, b);
+  if (j >= b) return;
+  const uint64_t w = draw_word(seed, (uint64_t)j, ticket, kKindSample);
+  const int32_t slot = (int32_t)range_map(w, (uint64_t)N);
+  slots[j] = slot;
+  const int old = atomicAdd(&seen[slot], 1);
+  if (old == 0) {
+    atomic_add_ll(&ctr->U, -1);
+    atomic_add_ll(&ctr->S, 1);
+  }
+}
+
+// Batch draw after reception ends: b' = min(b, N) distinct samples by
+// partial Fisher-Yates over the drain order occ[base, base + N); the drawn
+// samples are removed.  One block.
+__global__ __launch_bounds__(kAssignThreads) void drain_select_kernel(
+    uint64_t seed, uint64_t ticket, int64_t N, int64_t bb, int64_t occ_base,
+    int32_t* __restrict__ occ, int32_t* __restrict__ slots, int32_t* __restrict__ seen,
+    long long* __restrict__ sample_id, unsigned long long* __restrict__ hist,
+    ResCounters* __restrict__ ctr) {
+  __shared__ int s_r[kMaxDrainBatch];
+  __shared__ int s_par[kMaxDrainBatch];
+  __shared__ int s_par2[kMaxDrainBatch];
+  __shared__ int s_lv[kMaxDrainBatch];
+  __shared__ int s_pre[kMaxDrainBatch];
+  __shared__ int s_taken[kMaxDrainBatch];
+  __shared__ int s_last[kMaxDrainBatch];
+  __shared__ long long s_dU, s_dS;
+  const int tid = threadIdx.x, nt = blockDim.x;
+  int32_t* base = occ + occ_base;
+  if (tid == 0) { s_dU = 0; s_dS = 0; }
+  for (long long j = tid; j < bb; j += nt) {
+    const uint64_t w = draw_word(seed, (uint64_t)j, ticket, kKindSample);
+    s_r[j] = (int)(j + (long long)range_map(w, (uint64_t)(N - j)));
+  }
+  __syncthreads();
+  resolve_partial_shuffle((int)bb, s_r, base, s_par, s_par2, s_lv, s_pre, s_taken, s_last);
+  // Persist the shuffle for positions that stay in the buffer.
+  for (long long j = tid; j < bb; j += nt)
+    if (s_r[j] >= bb && s_last[j]) base[s_r[j]] = s_pre[j];
+  for (long long j = tid; j < bb; j += nt) {
+    const int slot = s_taken[j];
+    slots[j] = slot;
+    const int c = seen[slot] + 1;
+    atomicAdd(&hist[min(c, kHistLen - 1)], 1ull);
+    if (c == 1) atomicAdd((unsigned long long*)&s_dU, 1ull);
+    else atomicAdd((unsigned long long*)&s_dS, 1ull);
+    seen[slot] = -1;
+    sample_id[slot] = -1;
+  }
+  __syncthreads();
+  if (tid == 0) {
+    ctr->U -= s_dU;
+    ctr->S -= s_dS;
+    ctr->N -= bb;
+    ctr->total_deleted += bb;
+    ctr->total_draws += bb;
+  }
+}
+
+__global__ void iota_kernel(int32_t* occ, int64_t n) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) occ[i] = (int32_t)i;
+}
+
+// Gather rows of the drawn slots into the caller's batch buffers.
+// grid = b rows x `segs` segments per row, flattened (row-major).
+__global__ __launch_bounds__(kCopyThreads) void gather_kernel(
+    const int32_t* __restrict__ slots, const float* __restrict__ xslab, int64_t ldxs,
+    const float* __restrict__ uslab, int64_t ldus, float* __restrict__ x_out, int64_t ldxo,
+    float* __restrict__ u_out, int64_t lduo, int64_t x_dim, int64_t u_dim, int64_t segs, int vec_ok) {
+  const int64_t row = (int64_t)blockIdx.x / segs, seg = (int64_t)blockIdx.x % segs;
+  const int64_t slot = slots[row];
+  const int64_t seg0 = seg * kCopySeg;
+  if (u_out) {
+    const int64_t n = min(kCopySeg, u_dim - seg0);
+    copy_segment<true, false>(u_out + row * lduo + seg0, uslab + slot * ldus + seg0, n, vec_ok != 0);
+  }
+  if (x_out && seg == 0)
+    for (int64_t c = threadIdx.x; c < x_dim; c += kCopyThreads)
+      x_out[row * ldxo + c] = xslab[slot * ldxs + c];
+}
+
+}  // namespace ot
+
+// ===================================================================== host side
+using ot::ResCounters;
+
+struct ot_reservoir {
+  int device = 0;
+  int64_t C = 0, T = 0, x_dim = 0, u_dim = 0, ldxs = 0, ldus = 0;
+  uint64_t seed = 0;
+  float* xslab = nullptr;
+  float* uslab = nullptr;
+  int32_t* seen = nullptr;
+  long long* sample_id = nullptr;
+  int32_t* occ = nullptr;
+  int32_t* sarr = nullptr;
+  int32_t* put_slots = nullptr;
+  unsigned long long* hist = nullptr;
+  ResCounters* ctr = nullptr;
+  hipStream_t stream = nullptr;
+  bool own_stream = false;
+  hipEvent_t ev_in = nullptr, ev_out = nullptr;
+  std::mutex mu;
+  uint64_t next_ticket = 0;
+  int64_t n_host = 0;      // N, known from the call sequence
+  int64_t occ_base = 0;    // drain order offset
+  bool reception_over = false;
+};
+
+namespace {
+
+void free_reservoir(ot_reservoir* r) {
+  if (!r) return;
+  if (r->stream) (void)hipStreamSynchronize(r->stream);
+  (void)hipFree(r->xslab);
+  (void)hipFree(r->uslab);
+  (void)hipFree(r->seen);
+  (void)hipFree(r->sample_id);
+  (void)hipFree(r->occ);
+  (void)hipFree(r->sarr);
+  (void)hipFree(r->put_slots);
+  (void)hipFree(r->hist);
+  (void)hipFree(r->ctr);
+  if (r->ev_in) (void)hipEventDestroy(r->ev_in);
+  if (r->ev_out) (void)hipEventDestroy(r->ev_out);
+  if (r->own_stream && r->stream) (void)hipStreamDestroy(r->stream);
+  delete r;
+}
+
+template <class T>
+int dev_alloc(T** p, size_t count) {
+  hipError_t e = hipMalloc(reinterpret_cast<void**>(p), count * sizeof(T) + 16);
+  if (e != hipSuccess) {
+    (void)hipGetLastError();
+    return ot::set_error(OT_E_NOMEM, "hipMalloc of %zu bytes failed: %s", count * sizeof(T),
+                         hipGetErrorString(e));
+  }
+  return OT_OK;
+}
+
+// Order the reservoir's stream after the caller's work.
+int enter(ot_reservoir* r, hipStream_t caller) {
+  if (caller == r->stream) return OT_OK;
+  OT_HIP(hipEventRecord(r->ev_in, caller));
+  OT_HIP(hipStreamWaitEvent(r->stream, r->ev_in, 0));
+  return OT_OK;
+}
+
+// Order the caller's stream after the reservoir's work.
+int leave(ot_reservoir* r, hipStream_t caller) {
+  if (caller == r->stream) return OT_OK;
+  OT_HIP(hipEventRecord(r->ev_out, r->stream));
+  OT_HIP(hipStreamWaitEvent(caller, r->ev_out, 0));
+  return OT_OK;
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+}  // namespace
+
+extern "C" int reservoir_create(ot_reservoir** out, int64_t capacity, int64_t threshold,
+                                int64_t x_dim, int64_t u_dim, uint64_t seed, void* order_stream) {
+  ot::clear_error();
+  OT_REQUIRE(out != nullptr, "reservoir_create: out is NULL");
+  *out = nullptr;
+  OT_REQUIRE(capacity >= 1 && capacity <= 0x7fffffffLL, "reservoir_create: capacity %lld outside [1, 2^31-1]",
+             (long long)capacity);
+  OT_REQUIRE(threshold >= 0, "reservoir_create: threshold < 0");
+  OT_REQUIRE(x_dim >= 1 && x_dim <= 4096, "reservoir_create: x_dim outside [1, 4096]");
+  OT_REQUIRE(u_dim >= 1 && u_dim <= (1LL << 31), "reservoir_create: u_dim outside [1, 2^31]");
+  ot_reservoir* r = new ot_reservoir();
+  r->C = capacity;
+  r->T = threshold;
+  r->x_dim = x_dim;
+  r->u_dim = u_dim;
+  r->ldxs = ot::round_up(x_dim, 4);
+  r->ldus = ot::round_up(u_dim, 64);
+  r->seed = seed;
+  int rc = OT_OK;
+  auto fail = [&](int code) {
+    free_reservoir(r);
+    return code;
+  };
+  if (hipGetDevice(&r->device) != hipSuccess) return fail(ot::set_error(OT_E_HIP, "hipGetDevice failed"));
+  if ((rc = dev_alloc(&r->xslab, (size_t)capacity * r->ldxs))) return fail(rc);
+  if ((rc = dev_alloc(&r->uslab, (size_t)capacity * r->ldus))) return fail(rc);
+  if ((rc = dev_alloc(&r->seen, (size_t)capacity))) return fail(rc);
+  if ((rc = dev_alloc(&r->sample_id, (size_t)capacity))) return fail(rc);
+  if ((rc = dev_alloc(&r->occ, (size_t)capacity))) return fail(rc);
+  if ((rc = dev_alloc(&r->sarr, (size_t)capacity))) return fail(rc);
+  if ((rc = dev_alloc(&r->put_slots, (size_t)ot::kMaxPut))) return fail(rc);
+  if ((rc = dev_alloc(&r->hist, (size_t)ot::kHistLen))) return fail(rc);
+  if ((rc = dev_alloc(&r->ctr, 1))) return fail(rc);
+  if (order_stream) {
+    r->stream = static_cast<hipStream_t>(order_stream);
+  } else {
+    if (hipStreamCreateWithFlags(&r->stream, hipStreamNonBlocking) != hipSuccess)
+      return fail(ot::set_error(OT_E_HIP, "hipStreamCreate failed"));
+    r->own_stream = true;
+  }
+  if (hipEventCreateWithFlags(&r->ev_in, hipEventDisableTiming) != hipSuccess ||
+      hipEventCreateWithFlags(&r->ev_out, hipEventDisableTiming) != hipSuccess)
+    return fail(ot::set_error(OT_E_HIP, "hipEventCreate failed"));
+  const int64_t n_init = std::max<int64_t>(capacity, 64);
+  hipLaunchKernelGGL(ot::init_meta_kernel, dim3((unsigned)ot::ceil_div(n_init, 256)), dim3(256), 0,
+                     r->stream, r->seen, r->sample_id, capacity, r->hist, r->ctr);
+  if (hipGetLastError() != hipSuccess) return fail(ot::set_error(OT_E_HIP, "init_meta_kernel launch failed"));
+  if (hipStreamSynchronize(r->stream) != hipSuccess)
+    return fail(ot::set_error(OT_E_HIP, "reservoir_create: stream synchronise failed"));
+  *out = r;
+  return OT_OK;
+}
+
+extern "C" int reservoir_put(ot_reservoir* r, const float* x, int64_t ldx, const float* u,
+                             int64_t ldu, int64_t k, void* stream, int64_t* accepted_dev,
+                             uint64_t* ticket_out) {
+  ot::clear_error();
+  OT_REQUIRE(r != nullptr, "reservoir_put: NULL reservoir");
+  OT_REQUIRE(k >= 0 && k <= ot::kMaxPut, "reservoir_put: k=%lld outside [0, %lld]", (long long)k,
+             (long long)ot::kMaxPut);
+  if (k > 0) {
+    OT_REQUIRE(u != nullptr, "reservoir_put: u is NULL");
+    OT_REQUIRE(ldu >= r->u_dim, "reservoir_put: ldu < u_dim");
+    OT_REQUIRE(x == nullptr || ldx >= r->x_dim, "reservoir_put: ldx < x_dim");
+  }
+  hipStream_t cs = static_cast<hipStream_t>(stream);
+  std::lock_guard<std::mutex> lock(r->mu);
+  if (r->reception_over) return ot::set_error(OT_E_CLOSED, "reservoir_put: reception is over");
+  const uint64_t ticket = r->next_ticket++;
+  if (ticket_out) *ticket_out = ticket;
+  int rc = enter(r, cs);
+  if (rc) return rc;
+  hipLaunchKernelGGL(ot::put_assign_kernel, dim3(1), dim3(ot::kAssignThreads), 0, r->stream, k, ticket,
+                     r->seed, r->C, r->seen, r->sample_id, r->sarr, r->put_slots, r->hist, r->ctr,
+                     reinterpret_cast<long long*>(accepted_dev));
+  OT_LAUNCHED("put_assign_kernel");
+  if (k > 0) {
+    const int vec_ok = aligned16(u) && (ldu % 4 == 0);
+    const int64_t segs = ot::ceil_div(r->u_dim, ot::kCopySeg);
+    hipLaunchKernelGGL(ot::put_copy_kernel, dim3((unsigned)(segs * k)), dim3(ot::kCopyThreads), 0, r->stream,
+                       x, ldx, u, ldu, r->put_slots, r->ctr, r->xslab, r->ldxs, r->uslab, r->ldus, r->x_dim,
+                       r->u_dim, segs, vec_ok);
+    OT_LAUNCHED("put_copy_kernel");
+  }
+  r->n_host = std::min<int64_t>(r->C, r->n_host + k);
+  return leave(r, cs);
+}
+
+extern "C" int reservoir_sample_batch(ot_reservoir* r, int64_t b, void* stream, int32_t* slots,
+                                      float* x_out, int64_t ldxo, float* u_out, int64_t lduo,
+                                      int64_t* count_out, uint64_t* ticket_out) {
+  ot::clear_error();
+  if (count_out) *count_out = 0;
+  OT_REQUIRE(r != nullptr, "reservoir_sample_batch: NULL reservoir");
+  OT_REQUIRE(b >= 1 && b <= ot::kMaxBatch, "reservoir_sample_batch: b=%lld outside [1, %lld]", (long long)b,
+             (long long)ot::kMaxBatch);
+  OT_REQUIRE(slots != nullptr, "reservoir_sample_batch: slots is NULL");
+  OT_REQUIRE(u_out == nullptr || lduo >= r->u_dim, "reservoir_sample_batch: lduo < u_dim");
+  OT_REQUIRE(x_out == nullptr || ldxo >= r->x_dim, "reservoir_sample_batch: ldxo < x_dim");
+  hipStream_t cs = static_cast<hipStream_t>(stream);
+  std::lock_guard<std::mutex> lock(r->mu);
+  int64_t drawn = b;
+  if (r->reception_over) {
+    if (r->n_host == 0) return OT_EMPTY;
+    OT_REQUIRE(b <= ot::kMaxDrainBatch, "reservoir_sample_batch: b=%lld above %lld while draining",
+               (long long)b, (long long)ot::kMaxDrainBatch);
+    drawn = std::min<int64_t>(b, r->n_host);
+  } else if (r->n_host <= r->T) {
+    return OT_NOT_READY;
+  }
+  const uint64_t ticket = r->next_ticket++;
+  if (ticket_out) *ticket_out = ticket;
+  int rc = enter(r, cs);
+  if (rc) return rc;
+  if (!r->reception_over) {
+    hipLaunchKernelGGL(ot::select_kernel, dim3((unsigned)ot::ceil_div(b, 256)), dim3(256), 0, r->stream,
+                       r->seed, ticket, r->n_host, b, slots, r->seen, r->ctr);
+    OT_LAUNCHED("select_kernel");
+  } else {
+    hipLaunchKernelGGL(ot::drain_select_kernel, dim3(1), dim3(ot::kAssignThreads), 0, r->stream, r->seed,
+                       ticket, r->n_host, drawn, r->occ_base, r->occ, slots, r->seen, r->sample_id,
+                       r->hist, r->ctr);
+    OT_LAUNCHED("drain_select_kernel");
+    r->occ_base += drawn;
+    r->n_host -= drawn;
+  }
+  if (u_out || x_out) {
+    const int vec_ok = (u_out == nullptr) || (aligned16(u_out) && (lduo % 4 == 0));
+    const int64_t segs = ot::ceil_div(r->u_dim, ot::kCopySeg);
+    hipLaunchKernelGGL(ot::gather_kernel, dim3((unsigned)(segs * drawn)), dim3(ot::kCopyThreads), 0, r->stream,
+                       slots, r->xslab, r->ldxs, r->uslab, r->ldus, x_out, ldxo, u_out, lduo, r->x_dim,
+                       r->u_dim, segs, vec_ok);
+    OT_LAUNCHED("gather_kernel");
+  }
+  if (count_out) *count_out = drawn;
+  return leave(r, cs);
+}
+
+extern "C" int reservoir_end_reception(ot_reservoir* r) {
+  ot::clear_error();
+  OT_REQUIRE(r != nullptr, "reservoir_end_reception: NULL reservoir");
+  std::lock_guard<std::mutex> lock(r->mu);
+  if (r->reception_over) return ot::set_error(OT_E_STATE, "reservoir_end_reception: already over");
+  r->reception_over = true;
+  r->T = 0;
+  r->occ_base = 0;
+  if (r->n_host > 0) {
+    hipLaunchKernelGGL(ot::iota_kernel, dim3((unsigned)ot::ceil_div(r->n_host, 256)), dim3(256), 0, r->stream,
+                       r->occ, r->n_host);
+    OT_LAUNCHED("iota_kernel");
+  }
+  return OT_OK;
+}
+
+extern "C" int reservoir_stats(ot_reservoir* r, ot_reservoir_stats* out) {
+  ot::clear_error();
+  OT_REQUIRE(r != nullptr && out != nullptr, "reservoir_stats: NULL argument");
+  std::lock_guard<std::mutex> lock(r->mu);
+  OT_HIP(hipStreamSynchronize(r->stream));
+  ResCounters c;
+  OT_HIP(hipMemcpy(&c, r->ctr, sizeof c, hipMemcpyDeviceToHost));
+  out->capacity = r->C;
+  out->threshold = r->T;
+  out->n = c.N;
+  out->unseen = c.U;
+  out->seen = c.S;
+  out->total_put = c.total_put;
+  out->total_evicted = c.total_evicted;
+  out->total_deleted = c.total_deleted;
+  out->total_draws = c.total_draws;
+  out->next_ticket = (int64_t)r->next_ticket;
+  out->next_sample_id = c.next_sample_id;
+  out->reception_over = r->reception_over ? 1 : 0;
+  out->hist_len = ot::kHistLen;
+  return OT_OK;
+}
+
+extern "C" int reservoir_read_meta(ot_reservoir* r, int32_t* seen_count, int64_t* sample_id,
+                                   int64_t* evict_hist) {
+  ot::clear_error();
+  OT_REQUIRE(r != nullptr, "reservoir_read_meta: NULL reservoir");
+  std::lock_guard<std::mutex> lock(r->mu);
+  OT_HIP(hipStreamSynchronize(r->stream));
+  if (seen_count) OT_HIP(hipMemcpy(seen_count, r->seen, r->C * sizeof(int32_t), hipMemcpyDeviceToHost));
+  if (sample_id) OT_HIP(hipMemcpy(sample_id, r->sample_id, r->C * sizeof(int64_t), hipMemcpyDeviceToHost));
+  if (evict_hist)
+    OT_HIP(hipMemcpy(evict_hist, r->hist, ot::kHistLen * sizeof(int64_t), hipMemcpyDeviceToHost));
+  return OT_OK;
+}
+
+extern "C" int reservoir_read_rows(ot_reservoir* r, const int32_t* slots_host, int64_t n, float* x_host,
+                                   float* u_host) {
+  ot::clear_error();
+  OT_REQUIRE(r != nullptr && slots_host != nullptr && n >= 0, "reservoir_read_rows: bad argument");
+  for (int64_t i = 0; i < n; ++i)
+    OT_REQUIRE(slots_host[i] >= 0 && slots_host[i] < r->C, "reservoir_read_rows: slot %d out of range",
+               (int)slots_host[i]);
+  std::lock_guard<std::mutex> lock(r->mu);
+  OT_HIP(hipStreamSynchronize(r->stream));
+  for (int64_t i = 0; i < n; ++i) {
+    const int64_t s = slots_host[i];
+    if (x_host)
+      OT_HIP(hipMemcpy(x_host + i * r->x_dim, r->xslab + s * r->ldxs, r->x_dim * sizeof(float),
+                       hipMemcpyDeviceToHost));
+    if (u_host)
+      OT_HIP(hipMemcpy(u_host + i * r->u_dim, r->uslab + s * r->ldus, r->u_dim * sizeof(float),
+                       hipMemcpyDeviceToHost));
+  }
+  return OT_OK;
+}
+
+extern "C" int reservoir_destroy(ot_reservoir* r) {
+  ot::clear_error();
+  if (!r) return OT_OK;
+  free_reservoir(r);
+  return OT_OK;
+}

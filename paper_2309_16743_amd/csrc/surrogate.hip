@@ -1,0 +1,669 @@
+// Surrogate MLP train step and prediction (the paper's deep surrogate of the
+// heat equation, Sec. 4.1): forward through ReLU hidden layers and an
+// identity output layer whose GEMM epilogue forms the mean-squared-error
+// residual, back-propagation, and one fused Adam update over all parameters.
+//
+// Parameter layout (device, fp32): one flat buffer; layer l holds W_l as
+// out x ldw (ldw = round_up(in, 4), pad columns stay 0) followed by b_l, each
+// segment starting on a 64-float boundary.  Gradients and the Adam moments
+// use the same layout, so Adam is a single elementwise pass.
+#include <algorithm>
+#include <cmath>
+#include <vector>
+
+#include "common.h"
+#include "gemm_f32.h"
+#include "philox.h"
+#include "surrogate.h"
+
+namespace ot {
+
+constexpr int kMaxSmallK = 16;   // layer 1 with in <= 16 uses the small-K kernels
+
+// ------------------------------------------------------------------ small kernels
+// Parameter initialisation: element e of layer `layer` (flat over W then b)
+// is (2 m / 2^24 - 1) * bound rounded to fp32, m = top 24 bits of Philox word 0
+// at counter (e, layer, INIT, 0), key (seed, 0).
+__global__ void init_layer_kernel(float* __restrict__ W, float* __restrict__ b, int64_t in,
+                                  int64_t out, int64_t ldw, uint64_t seed, uint64_t layer,
+                                  double bound) {
+  const int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int64_t nw = in * out;
+  if (e >= nw + out) return;
+  const uint64_t w = draw_word(seed, (uint64_t)e, layer, kKindInit);
+  const double u = 2.0 * ((double)(w >> 40) / 16777216.0) - 1.0;
+  const float val = (float)(u * bound);
+  if (e < nw) W[(e / in) * ldw + (e % in)] = val;
+  else b[e - nw] = val;
+}
+
+__global__ void fill_kernel(float* __restrict__ p, int64_t n, float v) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) p[i] = v;
+}
+
+// First layer with a small input width K (the 6 inputs (X, t)):
+// A1[m][n] = max(sum_k X[m][k] W[n][k] + b[n], 0) (or without ReLU when the
+// net has a single layer).  One thread per 4 consecutive outputs.
+__global__ void small_k_forward_kernel(const float* __restrict__ X, int64_t ldx,
+                                       const float* __restrict__ W, int64_t ldw,
+                                       const float* __restrict__ bias, float* __restrict__ out,
+                                       int64_t ldo, int64_t M, int64_t N, int64_t K, int relu) {
+  const int64_t groups = (N + 3) / 4;
+  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (t >= M * groups) return;
+  const int64_t m = t / groups, n0 = (t % groups) * 4;
+  float x[kMaxSmallK];
+#pragma unroll
+  for (int k = 0; k < kMaxSmallK; ++k) x[k] = k < K ? X[m * ldx + k] : 0.f;
+  for (int c = 0; c < 4; ++c) {
+    const int64_t n = n0 + c;
+    if (n >= N) break;
+    float acc = 0.f;
+#pragma unroll
+    for (int k = 0; k < kMaxSmallK; ++k)
+      if (k < K) acc = fmaf(x[k], W[n * ldw + k], acc);
+    acc += bias[n];
+    out[m * ldo + n] = relu ? (acc > 0.f ? acc : 0.f) : acc;
+  }
+}
+
+// First-layer weight gradient, partial sums over a slice of rows:
+// part[p][n][k] = sum_{m in slice p} dZ[m][n] X[m][k] (k < K), part[p][n][K] = sum dZ[m][n].
+// grid = (ceil(N / 64), P); 256 threads = 64 columns x 4 row groups.
+__global__ __launch_bounds__(256) void small_k_wgrad_partial_kernel(
+    const float* __restrict__ dZ, int64_t ldz, const float* __restrict__ X, int64_t ldx,
+    float* __restrict__ part, int64_t M, int64_t N, int64_t K, int64_t rows_per_part) {
+  __shared__ float red[4][64][kMaxSmallK + 1];
+  const int cn = threadIdx.x % 64, grp = threadIdx.x / 64;
+  const int64_t n = (int64_t)blockIdx.x * 64 + cn;
+  const int64_t mb = (int64_t)blockIdx.y * rows_per_part;
+  const int64_t me = min(M, mb + rows_per_part);
+  float acc[kMaxSmallK + 1];
+#pragma unroll
+  for (int k = 0; k <= kMaxSmallK; ++k) acc[k] = 0.f;
+  if (n < N) {
+    for (int64_t m = mb + grp; m < me; m += 4) {
+      const float d = dZ[m * ldz + n];
+#pragma unroll
+      for (int k = 0; k < kMaxSmallK; ++k)
+        if (k < K) acc[k] = fmaf(d, X[m * ldx + k], acc[k]);
+      acc[kMaxSmallK] += d;
+    }
+  }
+#pragma unroll
+  for (int k = 0; k <= kMaxSmallK; ++k) red[grp][cn][k] = acc[k];
+  __syncthreads();
+  if (grp == 0 && n < N) {
+    float* dst = part + ((int64_t)blockIdx.y * N + n) * (K + 1);
+    for (int k = 0; k < K; ++k) dst[k] = ((red[0][cn][k] + red[1][cn][k]) + red[2][cn][k]) + red[3][cn][k];
+    dst[K] = ((red[0][cn][kMaxSmallK] + red[1][cn][kMaxSmallK]) + red[2][cn][kMaxSmallK]) +
+             red[3][cn][kMaxSmallK];
+  }
+}
+
+// Sum the P partial slices in order into dW (ld ldw) and db.
+__global__ void small_k_wgrad_reduce_kernel(const float* __restrict__ part, int64_t P, int64_t N,
+                                            int64_t K, float* __restrict__ dW, int64_t ldw,
+                                            float* __restrict__ db) {
+  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (t >= N * (K + 1)) return;
+  const int64_t n = t / (K + 1), k = t % (K + 1);
+  float s = 0.f;
+  for (int64_t p = 0; p < P; ++p) s += part[(p * N + n) * (K + 1) + k];
+  if (k < K) dW[n * ldw + k] = s;
+  else db[n] = s;
+}
+
+// dZ[m][n] = (sum_s ws[s][m][n]) * (mask[m][n] > 0), splits summed in order.
+__global__ void splitk_reduce_mask_kernel(const float* __restrict__ ws, int64_t splits,
+                                          int64_t split_stride, int64_t M, int64_t N, int64_t ldw_s,
+                                          const float* __restrict__ mask, int64_t ldm,
+                                          float* __restrict__ out, int64_t ldo) {
+  const int64_t groups = (N + 3) / 4;
+  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (t >= M * groups) return;
+  const int64_t m = t / groups, n = (t % groups) * 4;
+  if (n + 3 < N) {
+    f32x4 s = *reinterpret_cast<const f32x4*>(ws + m * ldw_s + n);
+    for (int64_t p = 1; p < splits; ++p) s += *reinterpret_cast<const f32x4*>(ws + p * split_stride + m * ldw_s + n);
+    if (mask) {
+      const f32x4 mk = *reinterpret_cast<const f32x4*>(mask + m * ldm + n);
+      for (int c = 0; c < 4; ++c) s[c] = mk[c] > 0.f ? s[c] : 0.f;
+    }
+    *reinterpret_cast<f32x4*>(out + m * ldo + n) = s;
+  } else {
+    for (int64_t c = n; c < N; ++c) {
+      float s = ws[m * ldw_s + c];
+      for (int64_t p = 1; p < splits; ++p) s += ws[p * split_stride + m * ldw_s + c];
+      if (mask) s = mask[m * ldm + c] > 0.f ? s : 0.f;
+      out[m * ldo + c] = s;
+    }
+  }
+}
+
+// loss = sum(partials) / count, partials added in a fixed order.
+__global__ __launch_bounds__(256) void loss_finalize_kernel(const double* __restrict__ partials, int64_t n,
+                                                            double inv_count, float* __restrict__ loss_a,
+                                                            float* __restrict__ loss_b) {
+  __shared__ double red[256];
+  double s = 0.0;
+  for (int64_t i = threadIdx.x; i < n; i += 256) s += partials[i];
+  red[threadIdx.x] = s;
+  __syncthreads();
+  for (int w = 128; w > 0; w >>= 1) {
+    if ((int)threadIdx.x < w) red[threadIdx.x] += red[threadIdx.x + w];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) {
+    const float l = (float)(red[0] * inv_count);
+    if (loss_a) *loss_a = l;
+    if (loss_b) *loss_b = l;
+  }
+}
+
+// Adam (Kingma and Ba, 2015, Algorithm 1) over the flat parameter buffer, fp32:
+//   m = b1 m + (1 - b1) g;  v = b2 v + (1 - b2) g^2;
+//   p = p - lr * (m / c1) / (sqrt(v / c2) + eps),  c1 = 1 - b1^t, c2 = 1 - b2^t.
+__global__ __launch_bounds__(256) void adam_kernel(float* __restrict__ p, const float* __restrict__ g,
+                                                   float* __restrict__ m, float* __restrict__ v,
+                                                   int64_t n4, float lr, float b1, float b2, float eps,
+                                                   float c1, float c2) {
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n4; i += stride) {
+    f32x4 pp = reinterpret_cast<f32x4*>(p)[i];
+    const f32x4 gg = reinterpret_cast<const f32x4*>(g)[i];
+    f32x4 mm = reinterpret_cast<f32x4*>(m)[i];
+    f32x4 vv = reinterpret_cast<f32x4*>(v)[i];
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      mm[c] = b1 * mm[c] + (1.0f - b1) * gg[c];
+      vv[c] = b2 * vv[c] + (1.0f - b2) * (gg[c] * gg[c]);
+      const float mhat = mm[c] / c1;
+      const float vhat = vv[c] / c2;
+      pp[c] = pp[c] - lr * mhat / (sqrtf(vhat) + eps);
+    }
+    reinterpret_cast<f32x4*>(p)[i] = pp;
+    reinterpret_cast<f32x4*>(m)[i] = mm;
+    reinterpret_cast<f32x4*>(v)[i] = vv;
+  }
+}
+
+}  // namespace ot
+
+// ===================================================================== host side
+namespace {
+
+struct Layer {
+  int64_t in = 0, out = 0, ldw = 0;
+  int64_t w_off = 0, b_off = 0;
+};
+
+}  // namespace
+
+struct ot_surrogate {
+  int device = 0;
+  int precision = OT_FP32;
+  std::vector<int64_t> widths;
+  std::vector<Layer> layers;
+  int L = 0;
+  int64_t n_flat = 0;
+  float* params = nullptr;
+  float* grads = nullptr;
+  float* m = nullptr;
+  float* v = nullptr;
+  float lr = 1e-3f, beta1 = 0.9f, beta2 = 0.999f, eps = 1e-8f;
+  int64_t t = 0;
+  // Workspaces, sized for ws_rows batch rows.
+  int64_t ws_rows = 0;
+  std::vector<float*> act;   // act[l] = A_l, l = 1..L-1 (index 0 unused)
+  std::vector<float*> dz;    // dz[l] = dZ_l, l = 1..L (dz[L] = dY)
+  std::vector<int64_t> ld;   // ld[l] = round_up(widths[l], 4)
+  float* splitws = nullptr;
+  int64_t splitws_elems = 0;
+  double* loss_partials = nullptr;
+  int64_t n_partials_cap = 0;
+  float* l1_part = nullptr;
+  int64_t l1_part_elems = 0;
+  float* loss_last = nullptr;
+};
+
+namespace {
+
+using ot::Epi;
+using ot::GemmArgs;
+using ot::Lay;
+
+int salloc(void** p, size_t bytes) {
+  hipError_t e = hipMalloc(p, bytes ? bytes : 16);
+  if (e != hipSuccess) {
+    (void)hipGetLastError();
+    *p = nullptr;
+    return ot::set_error(OT_E_NOMEM, "hipMalloc of %zu bytes failed: %s", bytes, hipGetErrorString(e));
+  }
+  return OT_OK;
+}
+
+void free_workspace(ot_surrogate* s) {
+  for (float* p : s->act) (void)hipFree(p);
+  for (float* p : s->dz) (void)hipFree(p);
+  s->act.assign(s->L + 1, nullptr);
+  s->dz.assign(s->L + 1, nullptr);
+  (void)hipFree(s->splitws);
+  (void)hipFree(s->loss_partials);
+  (void)hipFree(s->l1_part);
+  s->splitws = nullptr;
+  s->loss_partials = nullptr;
+  s->l1_part = nullptr;
+  s->ws_rows = 0;
+}
+
+void free_surrogate(ot_surrogate* s) {
+  if (!s) return;
+  (void)hipDeviceSynchronize();
+  free_workspace(s);
+  (void)hipFree(s->params);
+  (void)hipFree(s->grads);
+  (void)hipFree(s->m);
+  (void)hipFree(s->v);
+  (void)hipFree(s->loss_last);
+  delete s;
+}
+
+// Split count for the output-layer input-gradient GEMM (K = D can be large).
+int64_t choose_splits(int64_t tiles, int64_t K) {
+  int64_t splits = 1;
+  while (tiles * splits < 512 && K / (splits * 2) >= 256) splits *= 2;
+  return splits;
+}
+
+constexpr int64_t kSplitCap = 64;
+constexpr int64_t kL1Parts = 32;
+
+int ensure_workspace(ot_surrogate* s, int64_t rows) {
+  if (rows <= s->ws_rows) return OT_OK;
+  OT_HIP(hipDeviceSynchronize());
+  free_workspace(s);
+  const int L = s->L;
+  int rc;
+  for (int l = 1; l < L; ++l)
+    if ((rc = salloc((void**)&s->act[l], (size_t)rows * s->ld[l] * sizeof(float)))) return rc;
+  for (int l = 1; l <= L; ++l)
+    if ((rc = salloc((void**)&s->dz[l], (size_t)rows * s->ld[l] * sizeof(float)))) return rc;
+  // split-K partials of an input gradient: splits x rows x (widest hidden ld)
+  int64_t hl = 4;
+  for (int l = 1; l < L; ++l) hl = std::max(hl, s->ld[l]);
+  s->splitws_elems = kSplitCap * rows * hl;
+  if ((rc = salloc((void**)&s->splitws, (size_t)s->splitws_elems * sizeof(float)))) return rc;
+  // one loss partial per block of the output GEMM (64 x 64 tiles bound the count)
+  s->n_partials_cap = ot::ceil_div(rows, 64) * ot::ceil_div(s->widths[L], 64) + 64;
+  if ((rc = salloc((void**)&s->loss_partials, (size_t)s->n_partials_cap * sizeof(double)))) return rc;
+  s->l1_part_elems = kL1Parts * s->widths[1] * (s->widths[0] + 1);
+  if ((rc = salloc((void**)&s->l1_part, (size_t)s->l1_part_elems * sizeof(float)))) return rc;
+  s->ws_rows = rows;
+  return OT_OK;
+}
+
+// Dispatch one fp32 GEMM: 128 x 128 tiles when that fills the chip, else 64 x 64.
+template <Lay LA, Lay LB, Epi EPI>
+int gemm(const GemmArgs& g, int64_t splits, hipStream_t st, const char* what) {
+  hipError_t e;
+  const int64_t big = ot::gemm_tiles<2, 2, 4, 4>(g.M, g.N);
+  if (big * splits >= 240) e = ot::launch_gemm_f32<2, 2, 4, 4, LA, LB, EPI>(g, splits, st);
+  else e = ot::launch_gemm_f32<2, 2, 2, 2, LA, LB, EPI>(g, splits, st);
+  if (e != hipSuccess) return ot::set_error(OT_E_HIP, "launch of %s GEMM failed: %s", what, hipGetErrorString(e));
+  return OT_OK;
+}
+
+template <Lay LA, Lay LB, Epi EPI>
+int64_t gemm_blocks(const GemmArgs& g, int64_t splits) {
+  const int64_t big = ot::gemm_tiles<2, 2, 4, 4>(g.M, g.N);
+  if (big * splits >= 240) return big * splits;
+  return ot::gemm_tiles<2, 2, 2, 2>(g.M, g.N) * splits;
+}
+
+GemmArgs args0() {
+  GemmArgs g{};
+  return g;
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+// Forward pass of layers 1..L-1 into act[]; rows x widths[0] input at X.
+int forward_hidden(ot_surrogate* s, const float* X, int64_t ldx, int64_t rows, hipStream_t st) {
+  const int L = s->L;
+  for (int l = 1; l < L; ++l) {
+    const Layer& ly = s->layers[l - 1];
+    const float* W = s->params + ly.w_off;
+    const float* b = s->params + ly.b_off;
+    if (l == 1 && ly.in <= ot::kMaxSmallK) {
+      const int64_t work = rows * ot::ceil_div(ly.out, 4);
+      hipLaunchKernelGGL(ot::small_k_forward_kernel, dim3((unsigned)ot::ceil_div(work, 256)), dim3(256), 0, st, X,
+                         ldx, W, ly.ldw, b, s->act[1], s->ld[1], rows, ly.out, ly.in, 1);
+      OT_LAUNCHED("small_k_forward_kernel");
+      continue;
+    }
+    GemmArgs g = args0();
+    g.A = (l == 1) ? X : s->act[l - 1];
+    g.lda = (l == 1) ? ldx : s->ld[l - 1];
+    g.B = W;
+    g.ldb = ly.ldw;
+    g.C = s->act[l];
+    g.ldc = s->ld[l];
+    g.M = rows;
+    g.N = ly.out;
+    g.K = ly.in;
+    g.k_chunk = ly.in;
+    g.bias = b;
+    int rc = gemm<Lay::KMajor, Lay::KMajor, Epi::BiasRelu>(g, 1, st, "hidden forward");
+    if (rc) return rc;
+  }
+  return OT_OK;
+}
+
+int check_input(ot_surrogate* s, const float* X, int64_t ldx) {
+  OT_REQUIRE(X != nullptr, "input x is NULL");
+  OT_REQUIRE(ldx >= s->widths[0], "ldx < input width");
+  if (s->widths[0] > ot::kMaxSmallK)
+    OT_REQUIRE(aligned16(X) && ldx % 4 == 0, "input width > %d needs 16-byte aligned x and ldx %% 4 == 0",
+               ot::kMaxSmallK);
+  return OT_OK;
+}
+
+}  // namespace
+
+extern "C" int surrogate_create(ot_surrogate** out, const int64_t* widths, int32_t n_widths, int32_t precision,
+                                float lr, float beta1, float beta2, float eps, uint64_t seed, int64_t max_batch,
+                                uint32_t flags) {
+  ot::clear_error();
+  OT_REQUIRE(out != nullptr && widths != nullptr, "surrogate_create: NULL argument");
+  *out = nullptr;
+  OT_REQUIRE(n_widths >= 2 && n_widths <= 16, "surrogate_create: n_widths outside [2, 16]");
+  for (int i = 0; i < n_widths; ++i)
+    OT_REQUIRE(widths[i] >= 1 && widths[i] <= (1LL << 26), "surrogate_create: width %d outside [1, 2^26]", i);
+  OT_REQUIRE(precision == OT_FP32, "surrogate_create: precision %d not available", (int)precision);
+  OT_REQUIRE(flags == 0, "surrogate_create: flags must be 0");
+  OT_REQUIRE(max_batch >= 1 && max_batch <= (1LL << 20), "surrogate_create: max_batch outside [1, 2^20]");
+  OT_REQUIRE(lr >= 0.f && beta1 >= 0.f && beta1 < 1.f && beta2 >= 0.f && beta2 < 1.f && eps > 0.f,
+             "surrogate_create: bad Adam hyper-parameters");
+  ot_surrogate* s = new ot_surrogate();
+  s->precision = precision;
+  s->widths.assign(widths, widths + n_widths);
+  s->L = n_widths - 1;
+  s->lr = lr;
+  s->beta1 = beta1;
+  s->beta2 = beta2;
+  s->eps = eps;
+  s->ld.resize(n_widths);
+  for (int i = 0; i < n_widths; ++i) s->ld[i] = ot::round_up(widths[i], 4);
+  int64_t off = 0;
+  for (int l = 0; l < s->L; ++l) {
+    Layer ly;
+    ly.in = widths[l];
+    ly.out = widths[l + 1];
+    ly.ldw = ot::round_up(ly.in, 4);
+    ly.w_off = off;
+    off = ot::round_up(off + ly.out * ly.ldw, 64);
+    ly.b_off = off;
+    off = ot::round_up(off + ly.out, 64);
+    s->layers.push_back(ly);
+  }
+  s->n_flat = off;
+  s->act.assign(s->L + 1, nullptr);
+  s->dz.assign(s->L + 1, nullptr);
+  auto fail = [&](int code) {
+    free_surrogate(s);
+    return code;
+  };
+  if (hipGetDevice(&s->device) != hipSuccess) return fail(ot::set_error(OT_E_HIP, "hipGetDevice failed"));
+  int rc;
+  const size_t bytes = (size_t)s->n_flat * sizeof(float);
+  if ((rc = salloc((void**)&s->params, bytes))) return fail(rc);
+  if ((rc = salloc((void**)&s->grads, bytes))) return fail(rc);
+  if ((rc = salloc((void**)&s->m, bytes))) return fail(rc);
+  if ((rc = salloc((void**)&s->v, bytes))) return fail(rc);
+  if ((rc = salloc((void**)&s->loss_last, 16))) return fail(rc);
+  const unsigned fb = (unsigned)ot::ceil_div(s->n_flat, 256);
+  for (float* p : {s->params, s->grads, s->m, s->v}) {
+    hipLaunchKernelGGL(ot::fill_kernel, dim3(fb), dim3(256), 0, 0, p, s->n_flat, 0.f);
+  }
+  for (int l = 0; l < s->L; ++l) {
+    const Layer& ly = s->layers[l];
+    const int64_t n = ly.in * ly.out + ly.out;
+    hipLaunchKernelGGL(ot::init_layer_kernel, dim3((unsigned)ot::ceil_div(n, 256)), dim3(256), 0, 0,
+                       s->params + ly.w_off, s->params + ly.b_off, ly.in, ly.out, ly.ldw, seed, (uint64_t)l,
+                       1.0 / std::sqrt((double)ly.in));
+  }
+  if (hipGetLastError() != hipSuccess) return fail(ot::set_error(OT_E_HIP, "initialisation launch failed"));
+  if ((rc = ensure_workspace(s, max_batch))) return fail(rc);
+  if (hipDeviceSynchronize() != hipSuccess) return fail(ot::set_error(OT_E_HIP, "initialisation failed"));
+  *out = s;
+  return OT_OK;
+}
+
+extern "C" int surrogate_destroy(ot_surrogate* s) {
+  ot::clear_error();
+  free_surrogate(s);
+  return OT_OK;
+}
+
+namespace {
+
+int copy_layer(ot_surrogate* s, int32_t layer, const float* buf, float* W_host, float* b_host) {
+  OT_REQUIRE(s != nullptr && layer >= 0 && layer < s->L, "layer index out of range");
+  const Layer& ly = s->layers[layer];
+  OT_HIP(hipDeviceSynchronize());
+  if (W_host)
+    OT_HIP(hipMemcpy2D(W_host, ly.in * sizeof(float), buf + ly.w_off, ly.ldw * sizeof(float), ly.in * sizeof(float),
+                       ly.out, hipMemcpyDeviceToHost));
+  if (b_host) OT_HIP(hipMemcpy(b_host, buf + ly.b_off, ly.out * sizeof(float), hipMemcpyDeviceToHost));
+  return OT_OK;
+}
+
+}  // namespace
+
+extern "C" int surrogate_set_params(ot_surrogate* s, int32_t layer, const float* W_host, const float* b_host) {
+  ot::clear_error();
+  OT_REQUIRE(s != nullptr && layer >= 0 && layer < s->L, "surrogate_set_params: layer index out of range");
+  const Layer& ly = s->layers[layer];
+  OT_HIP(hipDeviceSynchronize());
+  if (W_host)
+    OT_HIP(hipMemcpy2D(s->params + ly.w_off, ly.ldw * sizeof(float), W_host, ly.in * sizeof(float),
+                       ly.in * sizeof(float), ly.out, hipMemcpyHostToDevice));
+  if (b_host) OT_HIP(hipMemcpy(s->params + ly.b_off, b_host, ly.out * sizeof(float), hipMemcpyHostToDevice));
+  return OT_OK;
+}
+
+extern "C" int surrogate_get_params(ot_surrogate* s, int32_t layer, float* W_host, float* b_host) {
+  ot::clear_error();
+  OT_REQUIRE(s != nullptr, "surrogate_get_params: NULL surrogate");
+  return copy_layer(s, layer, s->params, W_host, b_host);
+}
+
+extern "C" int surrogate_get_grads(ot_surrogate* s, int32_t layer, float* dW_host, float* db_host) {
+  ot::clear_error();
+  OT_REQUIRE(s != nullptr, "surrogate_get_grads: NULL surrogate");
+  return copy_layer(s, layer, s->grads, dW_host, db_host);
+}
+
+extern "C" int surrogate_get_adam_state(ot_surrogate* s, int32_t layer, float* mW_host, float* mb_host,
+                                        float* vW_host, float* vb_host, int64_t* t_out) {
+  ot::clear_error();
+  OT_REQUIRE(s != nullptr, "surrogate_get_adam_state: NULL surrogate");
+  int rc = copy_layer(s, layer, s->m, mW_host, mb_host);
+  if (rc) return rc;
+  rc = copy_layer(s, layer, s->v, vW_host, vb_host);
+  if (rc) return rc;
+  if (t_out) *t_out = s->t;
+  return OT_OK;
+}
+
+extern "C" int surrogate_set_lr(ot_surrogate* s, float lr) {
+  ot::clear_error();
+  OT_REQUIRE(s != nullptr && lr >= 0.f, "surrogate_set_lr: bad argument");
+  s->lr = lr;
+  return OT_OK;
+}
+
+extern "C" int surrogate_train_step(ot_surrogate* s, const float* x, int64_t ldx, const float* u, int64_t ldu,
+                                    int64_t b, void* stream, float* loss_dev) {
+  ot::clear_error();
+  OT_REQUIRE(s != nullptr, "surrogate_train_step: NULL surrogate");
+  OT_REQUIRE(b >= 1 && b <= (1LL << 20), "surrogate_train_step: b outside [1, 2^20]");
+  int rc = check_input(s, x, ldx);
+  if (rc) return rc;
+  const int L = s->L;
+  const int64_t D = s->widths[L];
+  OT_REQUIRE(u != nullptr && ldu >= D && ldu % 4 == 0 && aligned16(u),
+             "surrogate_train_step: targets need 16-byte alignment and ldu >= D, ldu %% 4 == 0");
+  if ((rc = ensure_workspace(s, b))) return rc;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+
+  // ---- forward: hidden layers
+  if ((rc = forward_hidden(s, x, ldx, b, st))) return rc;
+  // ---- output layer with fused bias + MSE: dY = 2 (Y - U) / (B D), loss partials
+  const Layer& lo = s->layers[L - 1];
+  int64_t n_partials = 0;
+  {
+    GemmArgs g = args0();
+    g.A = (L == 1) ? x : s->act[L - 1];
+    g.lda = (L == 1) ? ldx : s->ld[L - 1];
+    g.B = s->params + lo.w_off;
+    g.ldb = lo.ldw;
+    g.C = s->dz[L];
+    g.ldc = s->ld[L];
+    g.M = b;
+    g.N = D;
+    g.K = lo.in;
+    g.k_chunk = lo.in;
+    g.bias = s->params + lo.b_off;
+    g.target = u;
+    g.ldt = ldu;
+    g.scale = (float)(2.0 / ((double)b * (double)D));
+    g.loss_partials = s->loss_partials;
+    if (L == 1 && lo.in <= ot::kMaxSmallK)
+      OT_REQUIRE(aligned16(x) && ldx % 4 == 0, "single-layer nets need 16-byte aligned x, ldx %% 4 == 0");
+    n_partials = gemm_blocks<Lay::KMajor, Lay::KMajor, Epi::Mse>(g, 1);
+    if (n_partials > s->n_partials_cap) return ot::set_error(OT_E_STATE, "loss partial buffer too small");
+    if ((rc = gemm<Lay::KMajor, Lay::KMajor, Epi::Mse>(g, 1, st, "output forward+MSE"))) return rc;
+  }
+  hipLaunchKernelGGL(ot::loss_finalize_kernel, dim3(1), dim3(256), 0, st, s->loss_partials, n_partials,
+                     1.0 / ((double)b * (double)D), loss_dev, s->loss_last);
+  OT_LAUNCHED("loss_finalize_kernel");
+
+  // ---- backward, layer by layer from the output
+  for (int l = L; l >= 1; --l) {
+    const Layer& ly = s->layers[l - 1];
+    const float* A_in = (l == 1) ? x : s->act[l - 1];
+    const int64_t ld_in = (l == 1) ? ldx : s->ld[l - 1];
+    float* dW = s->grads + ly.w_off;
+    float* db = s->grads + ly.b_off;
+    // weight and bias gradient: dW = dZ^T A_in, db = column sums of dZ
+    if (l == 1 && ly.in <= ot::kMaxSmallK) {
+      const int64_t rows_per = ot::ceil_div(b, kL1Parts);
+      const int64_t P = ot::ceil_div(b, rows_per);
+      hipLaunchKernelGGL(ot::small_k_wgrad_partial_kernel, dim3((unsigned)ot::ceil_div(ly.out, 64), (unsigned)P),
+                         dim3(256), 0, st, s->dz[1], s->ld[1], x, ldx, s->l1_part, b, ly.out, ly.in, rows_per);
+      OT_LAUNCHED("small_k_wgrad_partial_kernel");
+      const int64_t n = ly.out * (ly.in + 1);
+      hipLaunchKernelGGL(ot::small_k_wgrad_reduce_kernel, dim3((unsigned)ot::ceil_div(n, 256)), dim3(256), 0, st,
+                         s->l1_part, P, ly.out, ly.in, dW, ly.ldw, db);
+      OT_LAUNCHED("small_k_wgrad_reduce_kernel");
+    } else {
+      GemmArgs g = args0();
+      g.A = s->dz[l];
+      g.lda = s->ld[l];
+      g.B = A_in;
+      g.ldb = ld_in;
+      g.C = dW;
+      g.ldc = ly.ldw;
+      g.M = ly.out;
+      g.N = ly.in;
+      g.K = b;
+      g.k_chunk = b;
+      g.rowsum = db;
+      if ((rc = gemm<Lay::MNMajor, Lay::MNMajor, Epi::Store>(g, 1, st, "weight gradient"))) return rc;
+    }
+    if (l == 1) break;
+    // input gradient dA_{l-1} = dZ_l W_l, then the ReLU mask of layer l-1
+    GemmArgs g = args0();
+    g.A = s->dz[l];
+    g.lda = s->ld[l];
+    g.B = s->params + ly.w_off;
+    g.ldb = ly.ldw;
+    g.M = b;
+    g.N = ly.in;
+    g.K = ly.out;
+    const int64_t tiles = ot::gemm_tiles<2, 2, 4, 4>(b, ly.in);
+    const int64_t splits = std::min<int64_t>(kSplitCap, choose_splits(tiles, ly.out));
+    if (splits > 1) {
+      g.k_chunk = ot::round_up(ot::ceil_div(ly.out, splits), 16);
+      const int64_t used = ot::ceil_div(ly.out, g.k_chunk);
+      g.C = s->splitws;
+      g.ldc = s->ld[l - 1];
+      g.split_stride = b * s->ld[l - 1];
+      if ((rc = gemm<Lay::KMajor, Lay::MNMajor, Epi::SplitK>(g, used, st, "input gradient (split)"))) return rc;
+      const int64_t work = b * ot::ceil_div(ly.in, 4);
+      hipLaunchKernelGGL(ot::splitk_reduce_mask_kernel, dim3((unsigned)ot::ceil_div(work, 256)), dim3(256), 0, st,
+                         s->splitws, used, g.split_stride, b, ly.in, s->ld[l - 1], s->act[l - 1], s->ld[l - 1],
+                         s->dz[l - 1], s->ld[l - 1]);
+      OT_LAUNCHED("splitk_reduce_mask_kernel");
+    } else {
+      g.k_chunk = ly.out;
+      g.C = s->dz[l - 1];
+      g.ldc = s->ld[l - 1];
+      g.mask = s->act[l - 1];
+      g.ldmask = s->ld[l - 1];
+      if ((rc = gemm<Lay::KMajor, Lay::MNMajor, Epi::Mask>(g, 1, st, "input gradient"))) return rc;
+    }
+  }
+
+  // ---- Adam over every parameter
+  s->t += 1;
+  const double c1 = 1.0 - std::pow((double)s->beta1, (double)s->t);
+  const double c2 = 1.0 - std::pow((double)s->beta2, (double)s->t);
+  const int64_t n4 = s->n_flat / 4;
+  const int64_t blocks = std::min<int64_t>(ot::ceil_div(n4, 256), 8192);
+  hipLaunchKernelGGL(ot::adam_kernel, dim3((unsigned)blocks), dim3(256), 0, st, s->params, s->grads, s->m, s->v, n4,
+                     s->lr, s->beta1, s->beta2, s->eps, (float)c1, (float)c2);
+  OT_LAUNCHED("adam_kernel");
+  return OT_OK;
+}
+
+extern "C" int surrogate_predict(ot_surrogate* s, const float* x, int64_t ldx, int64_t n, float* y, int64_t ldy,
+                                 void* stream) {
+  ot::clear_error();
+  OT_REQUIRE(s != nullptr, "surrogate_predict: NULL surrogate");
+  OT_REQUIRE(n >= 0, "surrogate_predict: n < 0");
+  if (n == 0) return OT_OK;
+  int rc = check_input(s, x, ldx);
+  if (rc) return rc;
+  const int L = s->L;
+  const int64_t D = s->widths[L];
+  OT_REQUIRE(y != nullptr && ldy >= D && ldy % 4 == 0 && aligned16(y),
+             "surrogate_predict: y needs 16-byte alignment and ldy >= D, ldy %% 4 == 0");
+  if (L == 1)
+    OT_REQUIRE(aligned16(x) && ldx % 4 == 0, "single-layer nets need 16-byte aligned x, ldx %% 4 == 0");
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  const int64_t chunk = std::max<int64_t>(s->ws_rows, 1);
+  const Layer& lo = s->layers[L - 1];
+  for (int64_t r0 = 0; r0 < n; r0 += chunk) {
+    const int64_t rows = std::min(chunk, n - r0);
+    const float* xr = x + r0 * ldx;
+    if ((rc = forward_hidden(s, xr, ldx, rows, st))) return rc;
+    GemmArgs g = args0();
+    g.A = (L == 1) ? xr : s->act[L - 1];
+    g.lda = (L == 1) ? ldx : s->ld[L - 1];
+    g.B = s->params + lo.w_off;
+    g.ldb = lo.ldw;
+    g.C = y + r0 * ldy;
+    g.ldc = ldy;
+    g.M = rows;
+    g.N = D;
+    g.K = lo.in;
+    g.k_chunk = lo.in;
+    g.bias = s->params + lo.b_off;
+    if ((rc = gemm<Lay::KMajor, Lay::KMajor, Epi::Bias>(g, 1, st, "output forward"))) return rc;
+  }
+  return OT_OK;
+}

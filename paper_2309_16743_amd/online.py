@@ -1,0 +1,93 @@
+"""Online training loop over the library: one aggregator put and one training
+step per iteration, as the paper's server alternates its data-aggregator and
+training threads (Sec. 3.1); all work is enqueued on one HIP stream.
+"""
+from __future__ import annotations
+
+from typing import Optional
+
+import torch
+
+from . import OT_FP32, OT_BF16, OT_OK, Reservoir, Surrogate
+
+
+def _round_up(v: int, m: int) -> int:
+    return (v + m - 1) // m * m
+
+
+class OnlineTrainer:
+    """Streams chunks of a device-resident ensemble into a reservoir and trains.
+
+    inputs: (S, tau, x_dim) fp32 device tensor; fields: (S, tau, D) fp32 device
+    tensor, D a multiple of 4.  Chunk c holds time step (c mod tau) of the
+    `wave` simulations of wave c // tau.
+    """
+
+    def __init__(self, widths, batch: int, capacity: int, threshold: int, wave: int, tau: int,
+                 inputs: torch.Tensor, fields: torch.Tensor, reservoir_seed: int, init_seed: int,
+                 precision: int = OT_FP32, lr: float = 1e-3, stream: Optional[torch.cuda.Stream] = None,
+                 record_steps: int = 0):
+        self.stream = stream if stream is not None else torch.cuda.current_stream()
+        self.widths = tuple(widths)
+        self.batch, self.wave, self.tau = batch, wave, tau
+        self.inputs, self.fields = inputs, fields
+        self.n_sims = inputs.shape[0]
+        self.n_chunks = (self.n_sims // wave) * tau
+        x_dim, d = inputs.shape[-1], fields.shape[-1]
+        self.res = Reservoir(capacity, threshold, x_dim, d, reservoir_seed, order_stream=self.stream)
+        self.sur = Surrogate(widths, precision=precision, lr=lr, seed=init_seed, max_batch=batch)
+        dev = inputs.device
+        self.xb = torch.empty(batch, _round_up(x_dim, 4), device=dev)[:, :x_dim]
+        self.ub = torch.empty(batch, _round_up(d, 4), device=dev)[:, :d]
+        self.slots = torch.empty(batch, dtype=torch.int32, device=dev)
+        self.record_steps = record_steps
+        self.slot_log = torch.empty((max(record_steps, 1), batch), dtype=torch.int32, device=dev)
+        self.loss_log = torch.zeros(max(record_steps, 1), device=dev)
+        self.loss = torch.zeros(1, device=dev)
+        self.accepted = torch.zeros(1, dtype=torch.int64, device=dev)
+        self.iteration = 0
+        self.steps_done = 0
+        self.chunk_cursor = 0
+
+    def chunk_views(self, c: int):
+        w, k = divmod(c % self.n_chunks, self.tau)
+        s0 = w * self.wave
+        return self.inputs[s0:s0 + self.wave, k, :], self.fields[s0:s0 + self.wave, k, :]
+
+    def put_next(self, wrap: bool = False) -> bool:
+        """Put the next chunk; after the last chunk, wrap around only if asked."""
+        if self.chunk_cursor >= self.n_chunks and not wrap:
+            return False
+        x, u = self.chunk_views(self.chunk_cursor)
+        self.res.put(x, u, stream=self.stream, accepted=self.accepted)
+        self.chunk_cursor += 1
+        return True
+
+    def sample_and_train(self) -> bool:
+        rec = self.steps_done < self.record_steps
+        slots = self.slot_log[self.steps_done] if rec else self.slots
+        st, n, _ = self.res.sample_batch(self.batch, slots, x_out=self.xb, u_out=self.ub, stream=self.stream)
+        if st != OT_OK:
+            return False
+        loss = self.loss_log[self.steps_done:self.steps_done + 1] if rec else self.loss
+        self.sur.train_step(self.xb, self.ub, stream=self.stream, loss=loss)
+        self.steps_done += 1
+        return True
+
+    def iterate(self, wrap: bool = False) -> bool:
+        """One iteration of the schedule; returns whether a train step ran."""
+        self.put_next(wrap)
+        trained = self.sample_and_train()
+        self.iteration += 1
+        return trained
+
+    def run(self, n_steps: int, wrap: bool = False) -> None:
+        target = self.steps_done + n_steps
+        while self.steps_done < target:
+            if self.chunk_cursor >= self.n_chunks and not wrap and self.res.stats()["n"] <= self.res.threshold:
+                raise RuntimeError("schedule ran out of data before the buffer became ready")
+            self.iterate(wrap)
+
+    def close(self):
+        self.res.close()
+        self.sur.close()

@@ -1,0 +1,195 @@
+"""GPU reservoir against the oracle reservoir: bit-exact slots, seen counts,
+sample ids, eviction histogram and gathered rows, over seeded operation
+sequences that fill, evict and drain the buffer; statuses; concurrent
+producers replayed in ticket order."""
+import threading
+
+import numpy as np
+import pytest
+import torch
+
+from fixtures.synthetic import hash_inputs, hash_rows
+from oracle import reservoir as orv
+
+pytestmark = pytest.mark.gpu
+
+DEV = torch.device("cuda:0")
+
+
+def padded(rows, d):
+    """Device tensor (rows, d) whose leading dimension is a multiple of 4."""
+    ld = (d + 3) // 4 * 4
+    return torch.zeros(rows, ld, device=DEV)[:, :d]
+
+
+def compare_meta(gres, ores, hist_len):
+    seen, ids, hist = gres.read_meta()
+    o_seen = np.where(ores.occupied, ores.seen_count, -1)
+    o_ids = np.where(ores.occupied, ores.sample_id, -1)
+    assert np.array_equal(seen, o_seen)
+    assert np.array_equal(ids, o_ids)
+    oh = np.zeros(hist_len, np.int64)
+    for k, c in ores.evict_hist.items():
+        oh[min(k, hist_len - 1)] += c
+    assert np.array_equal(hist, oh)
+    st = gres.stats()
+    assert (st["n"], st["unseen"], st["seen"]) == (ores.N, ores.U, ores.S)
+    assert st["total_put"] == ores.total_put and st["total_evicted"] == ores.total_evicted
+    assert st["total_draws"] == ores.total_draws and st["next_ticket"] == ores.next_ticket
+
+
+@pytest.mark.parametrize("C,T,d,seed,ops", [
+    (64, 32, 256, 0, 60),        # the 16x16 workload's reservoir
+    (97, 10, 1003, 5, 80),       # ragged row length, prime capacity
+    (300, 50, 4099, 9, 60),      # rows longer than one copy segment
+])
+def test_sequence_bit_exact(C, T, d, seed, ops):
+    from paper_2309_16743_amd import OT_NOT_READY, OT_OK, Reservoir
+    print(f"reservoir sequence C={C} T={T} d={d} seed={seed}", flush=True)
+    rng = np.random.default_rng(seed)
+    g = Reservoir(C, T, 6, d, seed)
+    o = orv.Reservoir(C, T, 6, d, seed)
+    key = 0
+    acc = torch.zeros(1, dtype=torch.int64, device=DEV)
+    for step in range(ops):
+        if rng.random() < 0.5:
+            k = int(rng.integers(0, 40))
+            keys = np.arange(key, key + k)
+            u = hash_rows(keys, d)
+            x = hash_inputs(keys)
+            ud = padded(k, d)
+            xd = padded(k, 6)
+            if k:
+                ud.copy_(torch.from_numpy(u))
+                xd.copy_(torch.from_numpy(x))
+            t = g.put(xd if k else None, ud if k else None, accepted=acc)
+            _, a, ot_, _ = o.put(x, u, k=k)
+            assert t == ot_
+            torch.cuda.synchronize()
+            assert int(acc.item()) == a
+            key += a
+        else:
+            b = int(rng.integers(1, 70))
+            slots = torch.empty(b, dtype=torch.int32, device=DEV)
+            ub = padded(b, d)
+            xb = padded(b, 6)
+            st, n, t = g.sample_batch(b, slots, x_out=xb, u_out=ub)
+            ost, oslots, ox, ou, ot_ = o.sample_batch(b)
+            assert st == ost
+            if st == OT_OK:
+                assert t == ot_
+                torch.cuda.synchronize()
+                assert np.array_equal(slots.cpu().numpy(), np.array(oslots))
+                assert np.array_equal(ub.cpu().numpy(), ou)
+                assert np.array_equal(xb.cpu().numpy(), ox)
+            else:
+                assert st == OT_NOT_READY
+        if step % 10 == 9:
+            compare_meta(g, o, 64)
+    compare_meta(g, o, 64)
+    assert o.total_evicted > 0
+    # drain after reception ends
+    g.end_reception()
+    o.end_reception()
+    while True:
+        b = int(rng.integers(1, 40))
+        slots = torch.empty(b, dtype=torch.int32, device=DEV)
+        ub = padded(b, d)
+        st, n, t = g.sample_batch(b, slots, u_out=ub)
+        ost, oslots, _, ou, _ = o.sample_batch(b)
+        assert st == ost
+        if st != OT_OK:
+            break
+        torch.cuda.synchronize()
+        assert n == len(oslots)
+        assert np.array_equal(slots[:n].cpu().numpy(), np.array(oslots))
+        assert np.array_equal(ub[:n].cpu().numpy(), ou)
+        compare_meta(g, o, 64)
+    assert o.N == 0
+    g.close()
+
+
+def test_statuses():
+    from paper_2309_16743_amd import OT_EMPTY, OT_NOT_READY, OT_OK, OTError, Reservoir
+    g = Reservoir(8, 4, 6, 16, 1)
+    slots = torch.empty(4, dtype=torch.int32, device=DEV)
+    assert g.sample_batch(4, slots)[0] == OT_NOT_READY
+    u = padded(5, 16)
+    g.put(None, u)
+    assert g.sample_batch(4, slots)[0] == OT_OK
+    assert g.stats()["next_ticket"] == 2
+    g.end_reception()
+    with pytest.raises(OTError):
+        g.put(None, u)
+    while g.sample_batch(4, slots)[0] == OT_OK:
+        pass
+    assert g.sample_batch(4, slots)[0] == OT_EMPTY
+    with pytest.raises(OTError):
+        g.sample_batch(0, slots)
+    g.close()
+
+
+def test_full_of_unseen_accepts_nothing():
+    from paper_2309_16743_amd import Reservoir
+    g = Reservoir(16, 0, 6, 8, 2)
+    acc = torch.zeros(1, dtype=torch.int64, device=DEV)
+    g.put(None, padded(16, 8), accepted=acc)
+    g.put(None, padded(5, 8), accepted=acc)
+    torch.cuda.synchronize()
+    assert acc.item() == 0
+    st = g.stats()
+    assert st["n"] == 16 and st["unseen"] == 16 and st["total_put"] == 16
+    g.close()
+
+
+def test_concurrent_producers_replay_in_ticket_order():
+    """Several host threads put on their own streams while the consumer draws;
+    replaying the recorded ticket order in the oracle gives identical state."""
+    from paper_2309_16743_amd import OT_OK, Reservoir
+    C, T, d, seed = 200, 40, 512, 11
+    g = Reservoir(C, T, 6, d, seed)
+    log = []
+    lock = threading.Lock()
+    n_prod, puts_each, k = 4, 12, 16
+
+    def producer(p):
+        s = torch.cuda.Stream()
+        for i in range(puts_each):
+            keys = np.arange((p * puts_each + i) * k, (p * puts_each + i + 1) * k)
+            with torch.cuda.stream(s):
+                ud = padded(k, d)
+                ud.copy_(torch.from_numpy(hash_rows(keys, d)), non_blocking=False)
+                t = g.put(None, ud, stream=s)
+            s.synchronize()
+            with lock:
+                log.append((t, "put", keys))
+
+    threads = [threading.Thread(target=producer, args=(p,)) for p in range(n_prod)]
+    for th in threads:
+        th.start()
+    cons = []
+    for _ in range(40):
+        slots = torch.empty(32, dtype=torch.int32, device=DEV)
+        ub = padded(32, d)
+        st, n, t = g.sample_batch(32, slots, u_out=ub)
+        if st == OT_OK:
+            torch.cuda.synchronize()
+            cons.append((t, slots.cpu().numpy(), ub.cpu().numpy()))
+    for th in threads:
+        th.join()
+    o = orv.Reservoir(C, T, 6, d, seed)
+    events = sorted([(t, "put", keys) for t, _, keys in log] + [(t, "sample", None) for t, _, _ in cons],
+                    key=lambda e: e[0])
+    by_ticket = {t: (s, u) for t, s, u in cons}
+    for t, kind, keys in events:
+        if kind == "put":
+            _, _, ot_, _ = o.put(None, hash_rows(keys, d), k=len(keys))
+            assert ot_ == t
+        else:
+            ost, oslots, _, ou, ot_ = o.sample_batch(32)
+            assert ost == OT_OK and ot_ == t
+            s, u = by_ticket[t]
+            assert np.array_equal(s, np.array(oslots))
+            assert np.array_equal(u, ou)
+    compare_meta(g, o, 64)
+    g.close()

@@ -1,0 +1,144 @@
+"""GPU surrogate against the fp64 oracle: initialisation (bit-exact), one train
+step (loss, every gradient, parameters after Adam) over shapes that span
+several tiles, ragged edges, split-K and the small-K first layer; prediction;
+and 100 online steps on the 16x16 workload (slots bit-exact, loss, gradients
+and parameters within 1e-3 relative L2)."""
+import numpy as np
+import pytest
+import torch
+
+from fixtures import configs, heat
+from oracle import mlp, runner
+
+pytestmark = pytest.mark.gpu
+
+DEV = torch.device("cuda:0")
+
+
+def rel(a, b):
+    a = np.asarray(a, dtype=np.float64)
+    b = np.asarray(b, dtype=np.float64)
+    return float(np.linalg.norm(a - b) / max(np.linalg.norm(b), 1e-30))
+
+
+def padded_from(arr):
+    rows, d = arr.shape
+    ld = (d + 3) // 4 * 4
+    t = torch.zeros(rows, ld, device=DEV)[:, :d]
+    t.copy_(torch.from_numpy(np.ascontiguousarray(arr, dtype=np.float32)))
+    return t
+
+
+def problem(widths, B, seed):
+    rng = np.random.default_rng(seed)
+    params = []
+    for l in range(len(widths) - 1):
+        fi, fo = widths[l], widths[l + 1]
+        bound = 1 / np.sqrt(fi)
+        params.append((rng.uniform(-bound, bound, (fo, fi)).astype(np.float32).astype(np.float64),
+                       rng.uniform(-bound, bound, fo).astype(np.float32).astype(np.float64)))
+    if widths[0] == 6:
+        X = np.concatenate([rng.uniform(100, 500, (B, 5)), rng.uniform(0.01, 1.0, (B, 1))], axis=1)
+        U = rng.uniform(100, 500, (B, widths[-1]))
+    else:
+        X = rng.normal(size=(B, widths[0]))
+        U = rng.normal(size=(B, widths[-1]))
+    return params, X.astype(np.float32), U.astype(np.float32)
+
+
+def make_gpu(widths, params, B):
+    from paper_2309_16743_amd import Surrogate
+    s = Surrogate(widths, max_batch=B, seed=0)
+    for l, (W, b) in enumerate(params):
+        s.set_params(l, W.astype(np.float32), b.astype(np.float32))
+    return s
+
+
+SHAPES = [
+    ((6, 64, 64, 256), 32),          # the 16x16 workload's net
+    ((6, 37, 50, 123), 45),          # ragged widths and batch
+    ((6, 256, 256, 1000), 300),      # several tiles, split-K output input-gradient
+    ((6, 128, 4000), 64),            # two layers, wide output
+    ((20, 48, 30), 17),              # first layer through the GEMM path
+    ((6, 10), 9),                    # single layer
+    ((6, 256, 256, 10000), 1024),    # the 100x100 workload's net at its batch
+]
+
+
+@pytest.mark.parametrize("widths,B", SHAPES)
+def test_one_train_step(widths, B):
+    print(f"one train step widths={widths} B={B}", flush=True)
+    params, X, U = problem(widths, B, seed=sum(widths) + B)
+    s = make_gpu(widths, params, B)
+    loss = torch.zeros(1, device=DEV)
+    s.train_step(padded_from(X), padded_from(U), loss=loss)
+    torch.cuda.synchronize()
+    o_loss, o_grads = mlp.loss_and_grads(params, X.astype(np.float64), U.astype(np.float64))
+    o_new = mlp.Adam(lr=1e-3).step(params, o_grads)
+    assert abs(loss.item() - o_loss) / o_loss < 1e-5
+    for l in range(len(widths) - 1):
+        gW, gb = s.get_grads(l)
+        assert rel(gW, o_grads[l][0]) < 1e-4, (l, rel(gW, o_grads[l][0]))
+        assert rel(gb, o_grads[l][1]) < 1e-4, (l, rel(gb, o_grads[l][1]))
+        W, b = s.get_params(l)
+        assert rel(W, o_new[l][0]) < 1e-4 and rel(b, o_new[l][1]) < 1e-4
+    s.close()
+
+
+@pytest.mark.parametrize("widths,n", [((6, 64, 64, 256), 50), ((6, 37, 50, 123), 77), ((20, 48, 30), 5)])
+def test_predict(widths, n):
+    params, X, _ = problem(widths, n, seed=3)
+    s = make_gpu(widths, params, 32)          # n above max_batch exercises the row chunking
+    Y = padded_from(np.zeros((n, widths[-1]), np.float32))
+    s.predict(padded_from(X), Y)
+    torch.cuda.synchronize()
+    ref = mlp.predict(params, X.astype(np.float64))
+    assert rel(Y.cpu().numpy(), ref) < 1e-5
+    s.close()
+
+
+@pytest.mark.parametrize("widths,seed", [((6, 64, 64, 256), 1), ((6, 37, 50, 123), 7)])
+def test_init_matches_oracle_bit_exact(widths, seed):
+    from paper_2309_16743_amd import Surrogate
+    s = Surrogate(widths, seed=seed, max_batch=8)
+    ref = mlp.init_params(widths, seed)
+    for l in range(len(widths) - 1):
+        W, b = s.get_params(l)
+        assert np.array_equal(W.astype(np.float64), ref[l][0])
+        assert np.array_equal(b.astype(np.float64), ref[l][1])
+    s.close()
+
+
+def test_tiny_workload_100_steps():
+    """16x16 heat fields, 6-64-64-256, batch 32, C 64, T 32: the schedule of the
+    first workload; gradients compared at steps 1 and 100."""
+    from paper_2309_16743_amd.online import OnlineTrainer
+    w = configs.TINY
+    X = heat.sample_parameters(w.n_sims, w.data_seed)
+    inputs = heat.inputs_for(X, w.tau)
+    fields = heat.heat_fields(X, w.grid, w.tau)
+    ref = runner.run(w, inputs, fields, n_steps=100, keep_grads=(1, 100))
+    tr = OnlineTrainer(w.widths, w.batch, w.capacity, w.threshold, w.wave, w.tau,
+                       torch.from_numpy(inputs).to(DEV), torch.from_numpy(fields).to(DEV),
+                       w.reservoir_seed, w.init_seed, lr=w.lr, record_steps=100)
+    grads1 = None
+    while tr.steps_done < 100:
+        tr.iterate()
+        if tr.steps_done == 1 and grads1 is None:
+            grads1 = [tr.sur.get_grads(l) for l in range(3)]
+    torch.cuda.synchronize()
+    slots = tr.slot_log.cpu().numpy()
+    for i in range(100):
+        assert np.array_equal(slots[i], ref["slots"][i]), i
+    losses = tr.loss_log.cpu().numpy()
+    assert rel(losses, ref["losses"]) < 1e-3
+    grads100 = [tr.sur.get_grads(l) for l in range(3)]
+    for l in range(3):
+        for i in range(2):
+            assert rel(grads1[l][i], ref["grads"][1][l][i]) < 1e-3
+            assert rel(grads100[l][i], ref["grads"][100][l][i]) < 1e-3
+        W, b = tr.sur.get_params(l)
+        assert rel(W, ref["params"][l][0]) < 1e-3 and rel(b, ref["params"][l][1]) < 1e-3
+    st = tr.res.stats()
+    assert st["total_evicted"] == ref["reservoir"].total_evicted == 16
+    tr.close()
