@@ -66,20 +66,33 @@ def ftcs_run(u0: np.ndarray, bc: np.ndarray, r: float, n_steps: int) -> np.ndarr
 
 
 def heat_fields(X: np.ndarray, n: int, tau: int, r: float = R_DEFAULT,
-                sims_per_block: int = 256) -> np.ndarray:
+                sims_per_block: int = 32, threads: int = 0) -> np.ndarray:
     """Fields u_X^k for k = 1..tau of every simulation, fp32, shape (S, tau, n*n).
 
     X rows are (T_IC, T_x1, T_y1, T_x2, T_y2); the initial field is T_IC
-    everywhere.  Simulations are advanced in blocks to bound memory.
+    everywhere.  Simulations are advanced in independent blocks (bounded
+    memory), on `threads` worker threads (0: one per available core).
     """
+    import concurrent.futures as cf
+    import os
     X = np.asarray(X, dtype=np.float64)
     s = X.shape[0]
     out = np.empty((s, tau, n * n), dtype=np.float32)
-    for b0 in range(0, s, sims_per_block):
+
+    def block(b0):
         xb = X[b0:b0 + sims_per_block]
         u0 = np.broadcast_to(xb[:, 0, None, None], (xb.shape[0], n, n))
         states = ftcs_run(u0, xb[:, 1:5], r, tau)             # (tau, sb, n, n)
         out[b0:b0 + xb.shape[0]] = states.transpose(1, 0, 2, 3).reshape(xb.shape[0], tau, n * n)
+
+    starts = list(range(0, s, sims_per_block))
+    workers = threads or min(16, len(os.sched_getaffinity(0)))
+    if workers <= 1 or len(starts) == 1:
+        for b0 in starts:
+            block(b0)
+    else:
+        with cf.ThreadPoolExecutor(max_workers=workers) as ex:
+            list(ex.map(block, starts))
     return out
 
 

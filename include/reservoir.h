@@ -128,6 +128,24 @@ int reservoir_read_meta(ot_reservoir* r, int32_t* seen_count, int64_t* sample_id
 int reservoir_read_rows(ot_reservoir* r, const int32_t* slots_host, int64_t n,
                         float* x_host, float* u_host);
 
+/* Kernel phases of the reservoir calls, for the timing hook below. */
+enum ot_reservoir_phase {
+  OT_PH_PUT_ASSIGN = 0,  /* put: slot assignment and eviction draws */
+  OT_PH_PUT_COPY = 1,    /* put: row copies into the slabs */
+  OT_PH_SELECT = 2,      /* sample: batch draws and seen-count update */
+  OT_PH_GATHER = 3,      /* sample: row copies into the batch buffers */
+  OT_RESERVOIR_PHASES = 4
+};
+
+/* Profiling hook: record HIP events on the ordering stream around the
+ * kernels of every phase in phase_mask for the next max_calls put or sample
+ * calls.  Allocates 2 events per phase and call. */
+int reservoir_timing_begin(ot_reservoir* r, uint32_t phase_mask, int64_t max_calls);
+
+/* Wait for the recorded events and return summed milliseconds and counts per
+ * phase (arrays of OT_RESERVOIR_PHASES, each nullable). */
+int reservoir_timing_end(ot_reservoir* r, double* ms_total, int64_t* count);
+
 /* Synchronise and free everything the reservoir owns. */
 int reservoir_destroy(ot_reservoir* r);
 

@@ -83,6 +83,29 @@ int surrogate_train_step(ot_surrogate* s, const float* x, int64_t ldx, const flo
 int surrogate_predict(ot_surrogate* s, const float* x, int64_t ldx, int64_t n, float* y,
                       int64_t ldy, void* stream);
 
+/* Kernel phases of one train step, for the timing hook below. */
+enum ot_surrogate_phase {
+  OT_PH_FWD_HIDDEN = 0,    /* hidden-layer forward GEMMs (bias + ReLU epilogue) */
+  OT_PH_FWD_OUTPUT = 1,    /* output-layer forward GEMM with the fused MSE epilogue */
+  OT_PH_LOSS = 2,          /* loss reduction */
+  OT_PH_WGRAD_OUTPUT = 3,  /* output-layer weight-gradient GEMM (with bias gradient) */
+  OT_PH_IGRAD_OUTPUT = 4,  /* output-layer input-gradient GEMM */
+  OT_PH_IGRAD_REDUCE = 5,  /* split-K reduction + ReLU mask of that gradient */
+  OT_PH_BWD_HIDDEN = 6,    /* hidden-layer backward */
+  OT_PH_ADAM = 7,          /* Adam over all parameters */
+  OT_SURROGATE_PHASES = 8
+};
+
+/* Profiling hook: record HIP events around the kernels of every phase in
+ * phase_mask (bit p = phase p) for the next max_steps train steps, on the
+ * stream each step runs on.  Allocates 2 events per phase and step. */
+int surrogate_timing_begin(ot_surrogate* s, uint32_t phase_mask, int64_t max_steps);
+
+/* Wait for the recorded events; ms_total[p] receives the summed duration of
+ * phase p in milliseconds and count[p] the number of steps it covers
+ * (arrays of OT_SURROGATE_PHASES, each nullable).  Releases the events. */
+int surrogate_timing_end(ot_surrogate* s, double* ms_total, int64_t* count);
+
 /* Synchronise and free everything the surrogate owns. */
 int surrogate_destroy(ot_surrogate* s);
 

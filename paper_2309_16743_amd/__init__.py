@@ -115,6 +115,18 @@ class Reservoir:
                                                                  x.ctypes.data, u.ctypes.data))
         return x, u
 
+    def timing_begin(self, phases, max_calls: int) -> None:
+        mask = sum(1 << _abi.RESERVOIR_PHASES.index(p) for p in phases)
+        check("reservoir_timing_begin", load().reservoir_timing_begin(self._h, mask, max_calls))
+
+    def timing_end(self) -> dict:
+        """{phase: (total ms, calls)} for the phases being timed."""
+        n = len(_abi.RESERVOIR_PHASES)
+        ms = np.zeros(n, np.float64)
+        cnt = np.zeros(n, np.int64)
+        check("reservoir_timing_end", load().reservoir_timing_end(self._h, ms.ctypes.data, cnt.ctypes.data))
+        return {p: (float(ms[i]), int(cnt[i])) for i, p in enumerate(_abi.RESERVOIR_PHASES) if cnt[i]}
+
     def close(self) -> None:
         if getattr(self, "_h", None) is not None and self._h.value:
             check("reservoir_destroy", load().reservoir_destroy(self._h))
@@ -193,6 +205,18 @@ class Surrogate:
         yp, ldy = _rows(y, "y")
         check("surrogate_predict", load().surrogate_predict(self._h, xp, ldx, x.shape[0], yp, ldy,
                                                             _stream_handle(stream)))
+
+    def timing_begin(self, phases, max_steps: int) -> None:
+        mask = sum(1 << _abi.SURROGATE_PHASES.index(p) for p in phases)
+        check("surrogate_timing_begin", load().surrogate_timing_begin(self._h, mask, max_steps))
+
+    def timing_end(self) -> dict:
+        """{phase: (total ms, steps)} for the phases being timed."""
+        n = len(_abi.SURROGATE_PHASES)
+        ms = np.zeros(n, np.float64)
+        cnt = np.zeros(n, np.int64)
+        check("surrogate_timing_end", load().surrogate_timing_end(self._h, ms.ctypes.data, cnt.ctypes.data))
+        return {p: (float(ms[i]), int(cnt[i])) for i, p in enumerate(_abi.SURROGATE_PHASES) if cnt[i]}
 
     def close(self) -> None:
         if getattr(self, "_h", None) is not None and self._h.value:

@@ -22,6 +22,10 @@ OT_E_STATE = -5
 OT_FP32 = 0
 OT_BF16 = 1
 
+SURROGATE_PHASES = ("fwd_hidden", "fwd_output", "loss", "wgrad_output", "igrad_output", "igrad_reduce",
+                    "bwd_hidden", "adam")
+RESERVOIR_PHASES = ("put_assign", "put_copy", "select", "gather")
+
 
 class ReservoirStats(C.Structure):
     _fields_ = [(name, C.c_int64) for name in (
@@ -47,6 +51,8 @@ SIGNATURES = {
     "reservoir_stats": (C.c_int, [vp, C.POINTER(ReservoirStats)]),
     "reservoir_read_meta": (C.c_int, [vp, vp, vp, vp]),
     "reservoir_read_rows": (C.c_int, [vp, vp, i64, vp, vp]),
+    "reservoir_timing_begin": (C.c_int, [vp, u32, i64]),
+    "reservoir_timing_end": (C.c_int, [vp, vp, vp]),
     "reservoir_destroy": (C.c_int, [vp]),
     "surrogate_create": (C.c_int, [C.POINTER(vp), C.POINTER(i64), i32, i32, f32, f32, f32, f32, u64, i64, u32]),
     "surrogate_set_params": (C.c_int, [vp, i32, vp, vp]),
@@ -56,6 +62,8 @@ SIGNATURES = {
     "surrogate_set_lr": (C.c_int, [vp, f32]),
     "surrogate_train_step": (C.c_int, [vp, vp, i64, vp, i64, i64, vp, vp]),
     "surrogate_predict": (C.c_int, [vp, vp, i64, i64, vp, i64, vp]),
+    "surrogate_timing_begin": (C.c_int, [vp, u32, i64]),
+    "surrogate_timing_end": (C.c_int, [vp, vp, vp]),
     "surrogate_destroy": (C.c_int, [vp]),
 }
 

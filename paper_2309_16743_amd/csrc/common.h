@@ -7,6 +7,7 @@
 
 #include <cstdarg>
 #include <string>
+#include <vector>
 
 #include "ot_status.h"
 
@@ -17,6 +18,32 @@ int set_error(int code, const char* fmt, ...) __attribute__((format(printf, 2, 3
 void clear_error();
 
 inline int64_t round_up(int64_t v, int64_t m) { return (v + m - 1) / m * m; }
+
+// Per-phase HIP-event timing of the kernels one call enqueues (profiling
+// hook).  begin() creates start/end events for max_calls calls of every phase
+// in `mask`; mark() records them on the stream the phase's kernels use;
+// end() waits for the events and returns the summed milliseconds per phase.
+struct PhaseTimer {
+  uint32_t mask = 0;
+  int nph = 0;
+  int64_t max_calls = 0;
+  int64_t call = 0;
+  std::vector<hipEvent_t> ev;
+  std::vector<char> rec;
+
+  bool on(int phase) const { return mask && ((mask >> phase) & 1u) && call < max_calls; }
+  void mark(hipStream_t st, int phase, int which) {
+    if (!on(phase)) return;
+    const size_t i = (size_t)((call * nph + phase) * 2 + which);
+    if (hipEventRecord(ev[i], st) == hipSuccess) rec[i] = 1;
+  }
+  void next_call() {
+    if (mask) ++call;
+  }
+  int begin(uint32_t m, int phases, int64_t calls);
+  int end(double* ms, int64_t* counts);
+  void release();
+};
 inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
 }  // namespace ot

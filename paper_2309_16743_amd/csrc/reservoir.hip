@@ -365,6 +365,7 @@ struct ot_reservoir {
   int64_t n_host = 0;      // N, known from the call sequence
   int64_t occ_base = 0;    // drain order offset
   bool reception_over = false;
+  ot::PhaseTimer timer;
 };
 
 namespace {
@@ -372,6 +373,7 @@ namespace {
 void free_reservoir(ot_reservoir* r) {
   if (!r) return;
   if (r->stream) (void)hipStreamSynchronize(r->stream);
+  r->timer.release();
   (void)hipFree(r->xslab);
   (void)hipFree(r->uslab);
   (void)hipFree(r->seen);
@@ -490,18 +492,24 @@ extern "C" int reservoir_put(ot_reservoir* r, const float* x, int64_t ldx, const
   if (ticket_out) *ticket_out = ticket;
   int rc = enter(r, cs);
   if (rc) return rc;
+  ot::PhaseTimer& tm = r->timer;
+  tm.mark(r->stream, OT_PH_PUT_ASSIGN, 0);
   hipLaunchKernelGGL(ot::put_assign_kernel, dim3(1), dim3(ot::kAssignThreads), 0, r->stream, k, ticket,
                      r->seed, r->C, r->seen, r->sample_id, r->sarr, r->put_slots, r->hist, r->ctr,
                      reinterpret_cast<long long*>(accepted_dev));
   OT_LAUNCHED("put_assign_kernel");
+  tm.mark(r->stream, OT_PH_PUT_ASSIGN, 1);
   if (k > 0) {
+    tm.mark(r->stream, OT_PH_PUT_COPY, 0);
     const int vec_ok = aligned16(u) && (ldu % 4 == 0);
     const int64_t segs = ot::ceil_div(r->u_dim, ot::kCopySeg);
     hipLaunchKernelGGL(ot::put_copy_kernel, dim3((unsigned)(segs * k)), dim3(ot::kCopyThreads), 0, r->stream,
                        x, ldx, u, ldu, r->put_slots, r->ctr, r->xslab, r->ldxs, r->uslab, r->ldus, r->x_dim,
                        r->u_dim, segs, vec_ok);
     OT_LAUNCHED("put_copy_kernel");
+    tm.mark(r->stream, OT_PH_PUT_COPY, 1);
   }
+  tm.next_call();
   r->n_host = std::min<int64_t>(r->C, r->n_host + k);
   return leave(r, cs);
 }
@@ -532,6 +540,8 @@ extern "C" int reservoir_sample_batch(ot_reservoir* r, int64_t b, void* stream, 
   if (ticket_out) *ticket_out = ticket;
   int rc = enter(r, cs);
   if (rc) return rc;
+  ot::PhaseTimer& tm = r->timer;
+  tm.mark(r->stream, OT_PH_SELECT, 0);
   if (!r->reception_over) {
     hipLaunchKernelGGL(ot::select_kernel, dim3((unsigned)ot::ceil_div(b, 256)), dim3(256), 0, r->stream,
                        r->seed, ticket, r->n_host, b, slots, r->seen, r->ctr);
@@ -544,14 +554,18 @@ extern "C" int reservoir_sample_batch(ot_reservoir* r, int64_t b, void* stream, 
     r->occ_base += drawn;
     r->n_host -= drawn;
   }
+  tm.mark(r->stream, OT_PH_SELECT, 1);
   if (u_out || x_out) {
+    tm.mark(r->stream, OT_PH_GATHER, 0);
     const int vec_ok = (u_out == nullptr) || (aligned16(u_out) && (lduo % 4 == 0));
     const int64_t segs = ot::ceil_div(r->u_dim, ot::kCopySeg);
     hipLaunchKernelGGL(ot::gather_kernel, dim3((unsigned)(segs * drawn)), dim3(ot::kCopyThreads), 0, r->stream,
                        slots, r->xslab, r->ldxs, r->uslab, r->ldus, x_out, ldxo, u_out, lduo, r->x_dim,
                        r->u_dim, segs, vec_ok);
     OT_LAUNCHED("gather_kernel");
+    tm.mark(r->stream, OT_PH_GATHER, 1);
   }
+  tm.next_call();
   if (count_out) *count_out = drawn;
   return leave(r, cs);
 }
@@ -634,4 +648,19 @@ extern "C" int reservoir_destroy(ot_reservoir* r) {
   if (!r) return OT_OK;
   free_reservoir(r);
   return OT_OK;
+}
+
+extern "C" int reservoir_timing_begin(ot_reservoir* r, uint32_t phase_mask, int64_t max_calls) {
+  ot::clear_error();
+  OT_REQUIRE(r != nullptr, "reservoir_timing_begin: NULL reservoir");
+  OT_REQUIRE(phase_mask != 0 && phase_mask < (1u << OT_RESERVOIR_PHASES), "reservoir_timing_begin: bad mask");
+  std::lock_guard<std::mutex> lock(r->mu);
+  return r->timer.begin(phase_mask, OT_RESERVOIR_PHASES, max_calls);
+}
+
+extern "C" int reservoir_timing_end(ot_reservoir* r, double* ms_total, int64_t* count) {
+  ot::clear_error();
+  OT_REQUIRE(r != nullptr, "reservoir_timing_end: NULL reservoir");
+  std::lock_guard<std::mutex> lock(r->mu);
+  return r->timer.end(ms_total, count);
 }

@@ -226,6 +226,7 @@ struct ot_surrogate {
   float* l1_part = nullptr;
   int64_t l1_part_elems = 0;
   float* loss_last = nullptr;
+  ot::PhaseTimer timer;
 };
 
 namespace {
@@ -262,6 +263,7 @@ void free_surrogate(ot_surrogate* s) {
   if (!s) return;
   (void)hipDeviceSynchronize();
   free_workspace(s);
+  s->timer.release();
   (void)hipFree(s->params);
   (void)hipFree(s->grads);
   (void)hipFree(s->m);
@@ -519,8 +521,11 @@ extern "C" int surrogate_train_step(ot_surrogate* s, const float* x, int64_t ldx
   if ((rc = ensure_workspace(s, b))) return rc;
   hipStream_t st = static_cast<hipStream_t>(stream);
 
+  ot::PhaseTimer& tm = s->timer;
   // ---- forward: hidden layers
+  tm.mark(st, OT_PH_FWD_HIDDEN, 0);
   if ((rc = forward_hidden(s, x, ldx, b, st))) return rc;
+  tm.mark(st, OT_PH_FWD_HIDDEN, 1);
   // ---- output layer with fused bias + MSE: dY = 2 (Y - U) / (B D), loss partials
   const Layer& lo = s->layers[L - 1];
   int64_t n_partials = 0;
@@ -545,20 +550,27 @@ extern "C" int surrogate_train_step(ot_surrogate* s, const float* x, int64_t ldx
       OT_REQUIRE(aligned16(x) && ldx % 4 == 0, "single-layer nets need 16-byte aligned x, ldx %% 4 == 0");
     n_partials = gemm_blocks<Lay::KMajor, Lay::KMajor, Epi::Mse>(g, 1);
     if (n_partials > s->n_partials_cap) return ot::set_error(OT_E_STATE, "loss partial buffer too small");
+    tm.mark(st, OT_PH_FWD_OUTPUT, 0);
     if ((rc = gemm<Lay::KMajor, Lay::KMajor, Epi::Mse>(g, 1, st, "output forward+MSE"))) return rc;
+    tm.mark(st, OT_PH_FWD_OUTPUT, 1);
   }
+  tm.mark(st, OT_PH_LOSS, 0);
   hipLaunchKernelGGL(ot::loss_finalize_kernel, dim3(1), dim3(256), 0, st, s->loss_partials, n_partials,
                      1.0 / ((double)b * (double)D), loss_dev, s->loss_last);
   OT_LAUNCHED("loss_finalize_kernel");
+  tm.mark(st, OT_PH_LOSS, 1);
 
   // ---- backward, layer by layer from the output
   for (int l = L; l >= 1; --l) {
+    if (l == L - 1) tm.mark(st, OT_PH_BWD_HIDDEN, 0);
+    const int ph_w = (l == L) ? OT_PH_WGRAD_OUTPUT : -1;
     const Layer& ly = s->layers[l - 1];
     const float* A_in = (l == 1) ? x : s->act[l - 1];
     const int64_t ld_in = (l == 1) ? ldx : s->ld[l - 1];
     float* dW = s->grads + ly.w_off;
     float* db = s->grads + ly.b_off;
     // weight and bias gradient: dW = dZ^T A_in, db = column sums of dZ
+    if (ph_w >= 0) tm.mark(st, ph_w, 0);
     if (l == 1 && ly.in <= ot::kMaxSmallK) {
       const int64_t rows_per = ot::ceil_div(b, kL1Parts);
       const int64_t P = ot::ceil_div(b, rows_per);
@@ -584,6 +596,7 @@ extern "C" int surrogate_train_step(ot_surrogate* s, const float* x, int64_t ldx
       g.rowsum = db;
       if ((rc = gemm<Lay::MNMajor, Lay::MNMajor, Epi::Store>(g, 1, st, "weight gradient"))) return rc;
     }
+    if (ph_w >= 0) tm.mark(st, ph_w, 1);
     if (l == 1) break;
     // input gradient dA_{l-1} = dZ_l W_l, then the ReLU mask of layer l-1
     GemmArgs g = args0();
@@ -602,21 +615,28 @@ extern "C" int surrogate_train_step(ot_surrogate* s, const float* x, int64_t ldx
       g.C = s->splitws;
       g.ldc = s->ld[l - 1];
       g.split_stride = b * s->ld[l - 1];
+      if (l == L) tm.mark(st, OT_PH_IGRAD_OUTPUT, 0);
       if ((rc = gemm<Lay::KMajor, Lay::MNMajor, Epi::SplitK>(g, used, st, "input gradient (split)"))) return rc;
+      if (l == L) tm.mark(st, OT_PH_IGRAD_OUTPUT, 1);
+      if (l == L) tm.mark(st, OT_PH_IGRAD_REDUCE, 0);
       const int64_t work = b * ot::ceil_div(ly.in, 4);
       hipLaunchKernelGGL(ot::splitk_reduce_mask_kernel, dim3((unsigned)ot::ceil_div(work, 256)), dim3(256), 0, st,
                          s->splitws, used, g.split_stride, b, ly.in, s->ld[l - 1], s->act[l - 1], s->ld[l - 1],
                          s->dz[l - 1], s->ld[l - 1]);
       OT_LAUNCHED("splitk_reduce_mask_kernel");
+      if (l == L) tm.mark(st, OT_PH_IGRAD_REDUCE, 1);
     } else {
       g.k_chunk = ly.out;
       g.C = s->dz[l - 1];
       g.ldc = s->ld[l - 1];
       g.mask = s->act[l - 1];
       g.ldmask = s->ld[l - 1];
+      if (l == L) tm.mark(st, OT_PH_IGRAD_OUTPUT, 0);
       if ((rc = gemm<Lay::KMajor, Lay::MNMajor, Epi::Mask>(g, 1, st, "input gradient"))) return rc;
+      if (l == L) tm.mark(st, OT_PH_IGRAD_OUTPUT, 1);
     }
   }
+  if (L >= 2) tm.mark(st, OT_PH_BWD_HIDDEN, 1);
 
   // ---- Adam over every parameter
   s->t += 1;
@@ -624,10 +644,26 @@ extern "C" int surrogate_train_step(ot_surrogate* s, const float* x, int64_t ldx
   const double c2 = 1.0 - std::pow((double)s->beta2, (double)s->t);
   const int64_t n4 = s->n_flat / 4;
   const int64_t blocks = std::min<int64_t>(ot::ceil_div(n4, 256), 8192);
+  tm.mark(st, OT_PH_ADAM, 0);
   hipLaunchKernelGGL(ot::adam_kernel, dim3((unsigned)blocks), dim3(256), 0, st, s->params, s->grads, s->m, s->v, n4,
                      s->lr, s->beta1, s->beta2, s->eps, (float)c1, (float)c2);
   OT_LAUNCHED("adam_kernel");
+  tm.mark(st, OT_PH_ADAM, 1);
+  tm.next_call();
   return OT_OK;
+}
+
+extern "C" int surrogate_timing_begin(ot_surrogate* s, uint32_t phase_mask, int64_t max_steps) {
+  ot::clear_error();
+  OT_REQUIRE(s != nullptr, "surrogate_timing_begin: NULL surrogate");
+  OT_REQUIRE(phase_mask != 0 && phase_mask < (1u << OT_SURROGATE_PHASES), "surrogate_timing_begin: bad mask");
+  return s->timer.begin(phase_mask, OT_SURROGATE_PHASES, max_steps);
+}
+
+extern "C" int surrogate_timing_end(ot_surrogate* s, double* ms_total, int64_t* count) {
+  ot::clear_error();
+  OT_REQUIRE(s != nullptr, "surrogate_timing_end: NULL surrogate");
+  return s->timer.end(ms_total, count);
 }
 
 extern "C" int surrogate_predict(ot_surrogate* s, const float* x, int64_t ldx, int64_t n, float* y, int64_t ldy,
