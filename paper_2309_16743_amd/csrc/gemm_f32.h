@@ -56,6 +56,7 @@ struct GemmArgs {
   const float* mask;        // Mask
   int64_t ldmask;
   float* rowsum;            // optional: sum_k A(m, k) for m of the block's rows (n tile 0 only)
+  int64_t rowsum_stride;    // SplitK: elements between consecutive split slices of rowsum
 };
 
 constexpr int kNumXcd = 8;
@@ -248,7 +249,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_f32_kernel(GemmArgs g) {
     if (kt + 1 < nk) store_tile(buf ^ 1);
     __syncthreads();
   }
-  if (do_rowsum && tid < BM && m0 + tid < g.M) g.rowsum[m0 + tid] = rsum;
+  if (do_rowsum && tid < BM && m0 + tid < g.M) g.rowsum[split * g.rowsum_stride + m0 + tid] = rsum;
 
   // ---------------------------------------------------------------- epilogue
   double lsum = 0.0;
@@ -294,6 +295,8 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_f32_kernel(GemmArgs g) {
       float* cp = Cb + m * g.ldc + col_base;
       if (FN == 4 && full) {
         *reinterpret_cast<f32x4*>(cp) = f32x4{v[0], v[FN > 1 ? 1 : 0], v[FN > 2 ? 2 : 0], v[FN > 3 ? 3 : 0]};
+      } else if (FN == 2 && full) {
+        *reinterpret_cast<f32x2*>(cp) = f32x2{v[0], v[FN > 1 ? 1 : 0]};
       } else {
 #pragma unroll
         for (int h = 0; h < FN; ++h)

@@ -25,6 +25,7 @@
 namespace ot {
 
 constexpr int kHistLen = 64;           // eviction histogram buckets (last = overflow)
+constexpr int kTile = 1024;            // slots per tile of the seen-count index
 constexpr int64_t kMaxPut = 4096;      // rows per put (bounded LDS of the assign kernel)
 constexpr int64_t kMaxDrainBatch = 4096;
 constexpr int64_t kMaxBatch = 65536;
@@ -32,8 +33,11 @@ constexpr int kAssignThreads = 1024;
 
 struct ResCounters {
   long long U, S, N, total_put, total_evicted, total_deleted, total_draws, next_sample_id;
-  long long last_accepted;
-  long long pad[7];
+  long long last_accepted;   // a of the last put
+  long long last_free;       // F of the last put
+  long long last_evicted;    // E of the last put
+  long long last_base_id;    // first sample id of the last put
+  long long pad[4];
 };
 
 // ------------------------------------------------------------------ device helpers
@@ -79,6 +83,7 @@ __device__ int block_exclusive_scan(int v, int* wave_tot, int* total) {
 // the pre_j chains are resolved by pointer jumping.  Inputs: r[0..E) in LDS.
 // Outputs: pre[0..E), taken[0..E) in LDS; last_writer[j] = 1 when no later
 // step writes position r_j (used by the drain to persist the shuffle).
+// base == nullptr stands for the identity array (A[p] = p).
 __device__ void resolve_partial_shuffle(int E, const int* r, const int* base, int* par, int* par2,
                                         int* lv, int* pre, int* taken, int* last_writer) {
   const int nt = blockDim.x;
@@ -106,11 +111,11 @@ __device__ void resolve_partial_shuffle(int E, const int* r, const int* base, in
     __syncthreads();
     int* t = src; src = dst; dst = t;
   }
-  for (int j = threadIdx.x; j < E; j += nt) pre[j] = base[src[j]];
+  for (int j = threadIdx.x; j < E; j += nt) pre[j] = base ? base[src[j]] : src[j];
   __syncthreads();
   for (int j = threadIdx.x; j < E; j += nt) {
     const int rj = r[j];
-    taken[j] = (rj == j) ? pre[j] : (lv[j] >= 0 ? pre[lv[j]] : base[rj]);
+    taken[j] = (rj == j) ? pre[j] : (lv[j] >= 0 ? pre[lv[j]] : (base ? base[rj] : rj));
   }
   __syncthreads();
 }
@@ -128,15 +133,37 @@ __global__ void init_meta_kernel(int32_t* seen, long long* sample_id, int64_t C,
     reinterpret_cast<long long*>(ctr)[i] = 0;
 }
 
-// Put, metadata half.  One block.  a = min(k, C - U) rows are accepted; the
-// first F = min(a, C - N) go to free slots N.., the other E = a - F replace
-// seen samples chosen by a partial Fisher-Yates over the ascending list of
-// seen slots (Philox kind 2, j = replacement index, range S - j).
+// Seen slots per tile of kTile slots: tile_cnt[t] = #{s in tile t : seen[s] >= 1}.
+// grid = number of tiles, 256 threads x 4 slots.
+__global__ __launch_bounds__(256) void seen_tile_count_kernel(const int32_t* __restrict__ seen, int64_t C,
+                                                              int32_t* __restrict__ tile_cnt) {
+  __shared__ int red[4];
+  const int64_t s0 = (int64_t)blockIdx.x * kTile + threadIdx.x * 4;
+  int c = 0;
+  if (s0 + 3 < C) {
+    const int4 v = *reinterpret_cast<const int4*>(seen + s0);
+    c = (v.x >= 1) + (v.y >= 1) + (v.z >= 1) + (v.w >= 1);
+  } else {
+    for (int i = 0; i < 4; ++i) c += (s0 + i < C) && seen[s0 + i] >= 1;
+  }
+  for (int off = 32; off > 0; off >>= 1) c += __shfl_xor(c, off, 64);
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = c;
+  __syncthreads();
+  if (threadIdx.x == 0) tile_cnt[blockIdx.x] = red[0] + red[1] + red[2] + red[3];
+}
+
+// Put, metadata decisions.  One block.  a = min(k, C - U) rows are accepted;
+// the first F = min(a, C - N) go to free slots N.., the other E = a - F
+// replace seen samples chosen by a partial Fisher-Yates over the ascending
+// list of seen slots (Philox kind 2, j = replacement index, range S - j).
+// This kernel resolves the shuffle on *positions* of that list; the slots
+// are found by put_victim_kernel from the tile prefix sums written here, and
+// the per-slot metadata is written by put_copy_kernel.  `may_evict` is 0 when
+// the host knows N + k <= C (then E = 0 and the tile counts were not made).
 __global__ __launch_bounds__(kAssignThreads) void put_assign_kernel(
-    int64_t k, uint64_t ticket, uint64_t seed, int64_t C, int32_t* __restrict__ seen,
-    long long* __restrict__ sample_id, int32_t* __restrict__ sarr, int32_t* __restrict__ put_slots,
-    unsigned long long* __restrict__ hist, ResCounters* __restrict__ ctr,
-    long long* __restrict__ accepted_out) {
+    int64_t k, uint64_t ticket, uint64_t seed, int64_t C, int may_evict, const int32_t* __restrict__ tile_cnt,
+    int64_t ntiles, int32_t* __restrict__ tile_off, int32_t* __restrict__ victim_pos,
+    int32_t* __restrict__ put_slots, ResCounters* __restrict__ ctr, long long* __restrict__ accepted_out) {
   __shared__ int s_r[kMaxPut];
   __shared__ int s_par[kMaxPut];
   __shared__ int s_par2[kMaxPut];
@@ -150,41 +177,31 @@ __global__ __launch_bounds__(kAssignThreads) void put_assign_kernel(
   const long long U = ctr->U, S = ctr->S, N = ctr->N, base_id = ctr->next_sample_id;
   const long long a = min((long long)k, (long long)C - U);
   const long long F = min(a, (long long)C - N);
-  const long long E = a - F;
+  const long long E = may_evict ? a - F : 0;
   const int tid = threadIdx.x, nt = blockDim.x;
 
-  for (long long i = tid; i < F; i += nt) {
-    const long long slot = N + i;
-    put_slots[i] = (int32_t)slot;
-    seen[slot] = 0;
-    sample_id[slot] = base_id + i;
-  }
+  for (long long i = tid; i < F; i += nt) put_slots[i] = (int32_t)(N + i);
+  for (long long j = tid; j < E; j += nt) put_slots[F + j] = -1;   // filled by put_victim_kernel
 
   if (E > 0) {
-    // E > 0 implies the buffer is full (N + F == C); list seen slots of [0, N).
-    const long long chunk = (N + nt - 1) / nt;
-    const long long lo = min((long long)tid * chunk, N), hi = min(lo + chunk, N);
-    int cnt = 0;
-    for (long long s = lo; s < hi; ++s) cnt += seen[s] >= 1;
-    int off = block_exclusive_scan<kAssignThreads>(cnt, s_wave, &s_total);
-    for (long long s = lo; s < hi; ++s)
-      if (seen[s] >= 1) sarr[off++] = (int32_t)s;
-    __syncthreads();
-    // s_total == S here (every occupied slot is unseen or seen).
+    // exclusive prefix sums of the tile counts (tile_off[ntiles] = S)
+    int carry = 0;
+    for (int64_t t0 = 0; t0 < ntiles; t0 += nt) {
+      const int64_t t = t0 + tid;
+      const int c = t < ntiles ? tile_cnt[t] : 0;
+      const int off = block_exclusive_scan<kAssignThreads>(c, s_wave, &s_total);
+      if (t < ntiles) tile_off[t] = carry + off;
+      carry += s_total;
+      __syncthreads();
+    }
+    if (tid == 0) tile_off[ntiles] = carry;
     for (long long j = tid; j < E; j += nt) {
       const uint64_t w = draw_word(seed, (uint64_t)j, ticket, kKindEvict);
       s_r[j] = (int)(j + (long long)range_map(w, (uint64_t)(S - j)));
     }
     __syncthreads();
-    resolve_partial_shuffle((int)E, s_r, sarr, s_par, s_par2, s_lv, s_pre, s_taken, s_last);
-    for (long long j = tid; j < E; j += nt) {
-      const int victim = s_taken[j];
-      const int c = seen[victim];
-      atomicAdd(&hist[min(c, kHistLen - 1)], 1ull);
-      seen[victim] = 0;
-      sample_id[victim] = base_id + F + j;
-      put_slots[F + j] = victim;
-    }
+    resolve_partial_shuffle((int)E, s_r, nullptr, s_par, s_par2, s_lv, s_pre, s_taken, s_last);
+    for (long long j = tid; j < E; j += nt) victim_pos[j] = s_taken[j];
   }
   __syncthreads();
   if (tid == 0) {
@@ -195,7 +212,57 @@ __global__ __launch_bounds__(kAssignThreads) void put_assign_kernel(
     ctr->total_evicted += E;
     ctr->next_sample_id = base_id + a;
     ctr->last_accepted = a;
+    ctr->last_free = F;
+    ctr->last_evicted = E;
+    ctr->last_base_id = base_id;
     if (accepted_out) *accepted_out = a;
+  }
+}
+
+// Slot of each victim: position p of the ascending list of seen slots lies in
+// the tile t with tile_off[t] <= p < tile_off[t + 1]; the rank p - tile_off[t]
+// is found by one wavefront over the tile's seen counts.  Reads metadata only.
+// grid = k blocks of 64 threads (block j handles victim j < E).
+__global__ __launch_bounds__(64) void put_victim_kernel(const int32_t* __restrict__ seen, int64_t C,
+                                                        const int32_t* __restrict__ tile_off, int64_t ntiles,
+                                                        const int32_t* __restrict__ victim_pos,
+                                                        int32_t* __restrict__ put_slots,
+                                                        const ResCounters* __restrict__ ctr) {
+  const int64_t j = blockIdx.x;
+  if (j >= ctr->last_evicted) return;
+  const int lane = threadIdx.x;
+  const int p = victim_pos[j];
+  // last tile whose offset is <= p (offsets are non-decreasing)
+  int64_t tile = 0;
+  for (int64_t b0 = 0; b0 < ntiles; b0 += 64) {
+    const int64_t t = b0 + lane;
+    const int v = t < ntiles ? tile_off[t] : 0x7fffffff;
+    const uint64_t m = __ballot(v <= p);
+    if (m == 0) break;
+    tile = b0 + 63 - __clzll((long long)m);
+    if (m != ~0ull) break;
+  }
+  const int rank = p - tile_off[tile];
+  const int64_t s0 = tile * kTile + (int64_t)lane * (kTile / 64);
+  int c = 0;
+  for (int i = 0; i < kTile / 64; ++i) c += (s0 + i < C) && seen[s0 + i] >= 1;
+  int incl = c;
+  for (int off = 1; off < 64; off <<= 1) {
+    const int t = __shfl_up(incl, off, 64);
+    if (lane >= off) incl += t;
+  }
+  const int excl = incl - c;
+  if (rank >= excl && rank < incl) {
+    int want = rank - excl;
+    for (int i = 0; i < kTile / 64; ++i) {
+      if ((s0 + i < C) && seen[s0 + i] >= 1) {
+        if (want == 0) {
+          put_slots[ctr->last_free + j] = (int32_t)(s0 + i);
+          break;
+        }
+        --want;
+      }
+    }
   }
 }
 
@@ -238,10 +305,18 @@ __global__ __launch_bounds__(kCopyThreads) void put_copy_kernel(
     const float* __restrict__ x, int64_t ldx, const float* __restrict__ u, int64_t ldu,
     const int32_t* __restrict__ put_slots, const ResCounters* __restrict__ ctr,
     float* __restrict__ xslab, int64_t ldxs, float* __restrict__ uslab, int64_t ldus, int64_t x_dim,
-    int64_t u_dim, int64_t segs, int vec_ok) {
+    int64_t u_dim, int64_t segs, int vec_ok, int32_t* __restrict__ seen, long long* __restrict__ sample_id,
+    unsigned long long* __restrict__ hist, int64_t C) {
   const int64_t row = (int64_t)blockIdx.x / segs, seg = (int64_t)blockIdx.x % segs;
   if (row >= ctr->last_accepted) return;
   const int64_t slot = put_slots[row];
+  if (slot < 0 || slot >= C) return;   // never expected: every accepted row has a slot
+  if (seg == 0 && threadIdx.x == 0) {
+    // the slot's new sample: unseen, next id; a replaced seen sample is counted
+    if (row >= ctr->last_free) atomicAdd(&hist[min(seen[slot], kHistLen - 1)], 1ull);
+    seen[slot] = 0;
+    sample_id[slot] = ctr->last_base_id + row;
+  }
   const int64_t seg0 = seg * kCopySeg;
   const int64_t n = min(kCopySeg, u_dim - seg0);
   copy_segment<true, true>(uslab + slot * ldus + seg0, u + row * ldu + seg0, n, vec_ok != 0);
@@ -353,8 +428,11 @@ struct ot_reservoir {
   int32_t* seen = nullptr;
   long long* sample_id = nullptr;
   int32_t* occ = nullptr;
-  int32_t* sarr = nullptr;
   int32_t* put_slots = nullptr;
+  int32_t* tile_cnt = nullptr;
+  int32_t* tile_off = nullptr;
+  int32_t* victim_pos = nullptr;
+  int64_t ntiles = 0;
   unsigned long long* hist = nullptr;
   ResCounters* ctr = nullptr;
   hipStream_t stream = nullptr;
@@ -379,8 +457,10 @@ void free_reservoir(ot_reservoir* r) {
   (void)hipFree(r->seen);
   (void)hipFree(r->sample_id);
   (void)hipFree(r->occ);
-  (void)hipFree(r->sarr);
   (void)hipFree(r->put_slots);
+  (void)hipFree(r->tile_cnt);
+  (void)hipFree(r->tile_off);
+  (void)hipFree(r->victim_pos);
   (void)hipFree(r->hist);
   (void)hipFree(r->ctr);
   if (r->ev_in) (void)hipEventDestroy(r->ev_in);
@@ -449,8 +529,11 @@ extern "C" int reservoir_create(ot_reservoir** out, int64_t capacity, int64_t th
   if ((rc = dev_alloc(&r->seen, (size_t)capacity))) return fail(rc);
   if ((rc = dev_alloc(&r->sample_id, (size_t)capacity))) return fail(rc);
   if ((rc = dev_alloc(&r->occ, (size_t)capacity))) return fail(rc);
-  if ((rc = dev_alloc(&r->sarr, (size_t)capacity))) return fail(rc);
   if ((rc = dev_alloc(&r->put_slots, (size_t)ot::kMaxPut))) return fail(rc);
+  r->ntiles = ot::ceil_div(capacity, ot::kTile);
+  if ((rc = dev_alloc(&r->tile_cnt, (size_t)r->ntiles))) return fail(rc);
+  if ((rc = dev_alloc(&r->tile_off, (size_t)r->ntiles + 1))) return fail(rc);
+  if ((rc = dev_alloc(&r->victim_pos, (size_t)ot::kMaxPut))) return fail(rc);
   if ((rc = dev_alloc(&r->hist, (size_t)ot::kHistLen))) return fail(rc);
   if ((rc = dev_alloc(&r->ctr, 1))) return fail(rc);
   if (order_stream) {
@@ -494,10 +577,23 @@ extern "C" int reservoir_put(ot_reservoir* r, const float* x, int64_t ldx, const
   if (rc) return rc;
   ot::PhaseTimer& tm = r->timer;
   tm.mark(r->stream, OT_PH_PUT_ASSIGN, 0);
-  hipLaunchKernelGGL(ot::put_assign_kernel, dim3(1), dim3(ot::kAssignThreads), 0, r->stream, k, ticket,
-                     r->seed, r->C, r->seen, r->sample_id, r->sarr, r->put_slots, r->hist, r->ctr,
+  // Replacement is possible only if N + k > C (host-known N); only then are
+  // the seen slots indexed.
+  const int may_evict = (r->n_host + k > r->C) ? 1 : 0;
+  if (may_evict) {
+    hipLaunchKernelGGL(ot::seen_tile_count_kernel, dim3((unsigned)r->ntiles), dim3(256), 0, r->stream, r->seen,
+                       r->C, r->tile_cnt);
+    OT_LAUNCHED("seen_tile_count_kernel");
+  }
+  hipLaunchKernelGGL(ot::put_assign_kernel, dim3(1), dim3(ot::kAssignThreads), 0, r->stream, k, ticket, r->seed,
+                     r->C, may_evict, r->tile_cnt, r->ntiles, r->tile_off, r->victim_pos, r->put_slots, r->ctr,
                      reinterpret_cast<long long*>(accepted_dev));
   OT_LAUNCHED("put_assign_kernel");
+  if (may_evict && k > 0) {
+    hipLaunchKernelGGL(ot::put_victim_kernel, dim3((unsigned)k), dim3(64), 0, r->stream, r->seen, r->C,
+                       r->tile_off, r->ntiles, r->victim_pos, r->put_slots, r->ctr);
+    OT_LAUNCHED("put_victim_kernel");
+  }
   tm.mark(r->stream, OT_PH_PUT_ASSIGN, 1);
   if (k > 0) {
     tm.mark(r->stream, OT_PH_PUT_COPY, 0);
@@ -505,7 +601,7 @@ extern "C" int reservoir_put(ot_reservoir* r, const float* x, int64_t ldx, const
     const int64_t segs = ot::ceil_div(r->u_dim, ot::kCopySeg);
     hipLaunchKernelGGL(ot::put_copy_kernel, dim3((unsigned)(segs * k)), dim3(ot::kCopyThreads), 0, r->stream,
                        x, ldx, u, ldu, r->put_slots, r->ctr, r->xslab, r->ldxs, r->uslab, r->ldus, r->x_dim,
-                       r->u_dim, segs, vec_ok);
+                       r->u_dim, segs, vec_ok, r->seen, r->sample_id, r->hist, r->C);
     OT_LAUNCHED("put_copy_kernel");
     tm.mark(r->stream, OT_PH_PUT_COPY, 1);
   }

@@ -115,30 +115,48 @@ __global__ void small_k_wgrad_reduce_kernel(const float* __restrict__ part, int6
   else db[n] = s;
 }
 
-// dZ[m][n] = (sum_s ws[s][m][n]) * (mask[m][n] > 0), splits summed in order.
-__global__ void splitk_reduce_mask_kernel(const float* __restrict__ ws, int64_t splits,
-                                          int64_t split_stride, int64_t M, int64_t N, int64_t ldw_s,
-                                          const float* __restrict__ mask, int64_t ldm,
-                                          float* __restrict__ out, int64_t ldo) {
+// Split-K epilogue: out[m][n] = epi(sum_s ws[s][m][n]) with the splits summed
+// in order; epi adds bias[n] (if given), applies ReLU (if relu) and the mask
+// (mask[m][n] > 0, if given).  Threads of column group 0 also reduce the
+// split row sums rs[s][m] into rowsum_out[m] (if given).
+__global__ void splitk_epilogue_kernel(const float* __restrict__ ws, int64_t splits, int64_t split_stride,
+                                       int64_t M, int64_t N, int64_t ldws, const float* __restrict__ bias, int relu,
+                                       const float* __restrict__ mask, int64_t ldm, float* __restrict__ out,
+                                       int64_t ldo, const float* __restrict__ rs, int64_t rs_stride,
+                                       float* __restrict__ rowsum_out) {
   const int64_t groups = (N + 3) / 4;
   const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (t >= M * groups) return;
   const int64_t m = t / groups, n = (t % groups) * 4;
-  if (n + 3 < N) {
-    f32x4 s = *reinterpret_cast<const f32x4*>(ws + m * ldw_s + n);
-    for (int64_t p = 1; p < splits; ++p) s += *reinterpret_cast<const f32x4*>(ws + p * split_stride + m * ldw_s + n);
-    if (mask) {
-      const f32x4 mk = *reinterpret_cast<const f32x4*>(mask + m * ldm + n);
-      for (int c = 0; c < 4; ++c) s[c] = mk[c] > 0.f ? s[c] : 0.f;
-    }
-    *reinterpret_cast<f32x4*>(out + m * ldo + n) = s;
+  if (rowsum_out && n == 0) {
+    float r = rs[m];
+    for (int64_t p = 1; p < splits; ++p) r += rs[p * rs_stride + m];
+    rowsum_out[m] = r;
+  }
+  float v[4];
+  const int cnt = (int)min((int64_t)4, N - n);
+  if (cnt == 4) {
+    f32x4 acc = *reinterpret_cast<const f32x4*>(ws + m * ldws + n);
+    for (int64_t p = 1; p < splits; ++p) acc += *reinterpret_cast<const f32x4*>(ws + p * split_stride + m * ldws + n);
+    for (int c = 0; c < 4; ++c) v[c] = acc[c];
   } else {
-    for (int64_t c = n; c < N; ++c) {
-      float s = ws[m * ldw_s + c];
-      for (int64_t p = 1; p < splits; ++p) s += ws[p * split_stride + m * ldw_s + c];
-      if (mask) s = mask[m * ldm + c] > 0.f ? s : 0.f;
-      out[m * ldo + c] = s;
+    for (int c = 0; c < cnt; ++c) {
+      float a = ws[m * ldws + n + c];
+      for (int64_t p = 1; p < splits; ++p) a += ws[p * split_stride + m * ldws + n + c];
+      v[c] = a;
     }
+  }
+  for (int c = 0; c < cnt; ++c) {
+    float x = v[c];
+    if (bias) x += bias[n + c];
+    if (relu) x = x > 0.f ? x : 0.f;
+    if (mask) x = mask[m * ldm + n + c] > 0.f ? x : 0.f;
+    v[c] = x;
+  }
+  if (cnt == 4 && ((ldo & 3) == 0) && ((reinterpret_cast<uintptr_t>(out) & 15) == 0)) {
+    *reinterpret_cast<f32x4*>(out + m * ldo + n) = f32x4{v[0], v[1], v[2], v[3]};
+  } else {
+    for (int c = 0; c < cnt; ++c) out[m * ldo + n + c] = v[c];
   }
 }
 
@@ -219,8 +237,10 @@ struct ot_surrogate {
   std::vector<float*> act;   // act[l] = A_l, l = 1..L-1 (index 0 unused)
   std::vector<float*> dz;    // dz[l] = dZ_l, l = 1..L (dz[L] = dY)
   std::vector<int64_t> ld;   // ld[l] = round_up(widths[l], 4)
-  float* splitws = nullptr;
+  float* splitws = nullptr;     // split-K partial products
   int64_t splitws_elems = 0;
+  float* rsws = nullptr;        // split-K partial row sums (bias gradients)
+  int64_t rsws_elems = 0;
   double* loss_partials = nullptr;
   int64_t n_partials_cap = 0;
   float* l1_part = nullptr;
@@ -251,9 +271,13 @@ void free_workspace(ot_surrogate* s) {
   s->act.assign(s->L + 1, nullptr);
   s->dz.assign(s->L + 1, nullptr);
   (void)hipFree(s->splitws);
+  (void)hipFree(s->rsws);
   (void)hipFree(s->loss_partials);
   (void)hipFree(s->l1_part);
   s->splitws = nullptr;
+  s->splitws_elems = 0;
+  s->rsws = nullptr;
+  s->rsws_elems = 0;
   s->loss_partials = nullptr;
   s->l1_part = nullptr;
   s->ws_rows = 0;
@@ -272,14 +296,6 @@ void free_surrogate(ot_surrogate* s) {
   delete s;
 }
 
-// Split count for the output-layer input-gradient GEMM (K = D can be large).
-int64_t choose_splits(int64_t tiles, int64_t K) {
-  int64_t splits = 1;
-  while (tiles * splits < 512 && K / (splits * 2) >= 256) splits *= 2;
-  return splits;
-}
-
-constexpr int64_t kSplitCap = 64;
 constexpr int64_t kL1Parts = 32;
 
 int ensure_workspace(ot_surrogate* s, int64_t rows) {
@@ -292,11 +308,6 @@ int ensure_workspace(ot_surrogate* s, int64_t rows) {
     if ((rc = salloc((void**)&s->act[l], (size_t)rows * s->ld[l] * sizeof(float)))) return rc;
   for (int l = 1; l <= L; ++l)
     if ((rc = salloc((void**)&s->dz[l], (size_t)rows * s->ld[l] * sizeof(float)))) return rc;
-  // split-K partials of an input gradient: splits x rows x (widest hidden ld)
-  int64_t hl = 4;
-  for (int l = 1; l < L; ++l) hl = std::max(hl, s->ld[l]);
-  s->splitws_elems = kSplitCap * rows * hl;
-  if ((rc = salloc((void**)&s->splitws, (size_t)s->splitws_elems * sizeof(float)))) return rc;
   // one loss partial per block of the output GEMM (64 x 64 tiles bound the count)
   s->n_partials_cap = ot::ceil_div(rows, 64) * ot::ceil_div(s->widths[L], 64) + 64;
   if ((rc = salloc((void**)&s->loss_partials, (size_t)s->n_partials_cap * sizeof(double)))) return rc;
@@ -306,22 +317,148 @@ int ensure_workspace(ot_surrogate* s, int64_t rows) {
   return OT_OK;
 }
 
-// Dispatch one fp32 GEMM: 128 x 128 tiles when that fills the chip, else 64 x 64.
-template <Lay LA, Lay LB, Epi EPI>
-int gemm(const GemmArgs& g, int64_t splits, hipStream_t st, const char* what) {
-  hipError_t e;
-  const int64_t big = ot::gemm_tiles<2, 2, 4, 4>(g.M, g.N);
-  if (big * splits >= 240) e = ot::launch_gemm_f32<2, 2, 4, 4, LA, LB, EPI>(g, splits, st);
-  else e = ot::launch_gemm_f32<2, 2, 2, 2, LA, LB, EPI>(g, splits, st);
-  if (e != hipSuccess) return ot::set_error(OT_E_HIP, "launch of %s GEMM failed: %s", what, hipGetErrorString(e));
-  return OT_OK;
+// Tile shapes: 128 x 128 (4 waves, 64 x 64 each), 128 x 64, 64 x 64.
+enum Cfg : int { kC128x128 = 0, kC128x64 = 1, kC64x64 = 2 };
+
+int64_t tiles_of(int cfg, int64_t M, int64_t N) {
+  switch (cfg) {
+    case kC128x128: return ot::gemm_tiles<2, 2, 4, 4>(M, N);
+    case kC128x64: return ot::gemm_tiles<2, 2, 4, 2>(M, N);
+    default: return ot::gemm_tiles<2, 2, 2, 2>(M, N);
+  }
+}
+
+struct Plan {
+  int cfg = kC64x64;
+  int64_t splits = 1;     // k ranges actually launched
+  int64_t k_chunk = 0;
+  int64_t blocks = 0;
+};
+
+// Largest tile whose tile count alone gives about one block per CU; else the
+// largest tile that reaches it by splitting the k range (at least 256 deep per
+// split); else 64 x 64 tiles split down to 32-deep k ranges.
+Plan make_plan(int64_t M, int64_t N, int64_t K, bool allow_split) {
+  constexpr int64_t kFill = 240;
+  Plan p;
+  bool done = false;
+  for (int cfg : {kC128x128, kC128x64, kC64x64}) {
+    if (tiles_of(cfg, M, N) >= kFill) {
+      p.cfg = cfg;
+      done = true;
+      break;
+    }
+  }
+  if (!done && allow_split) {
+    for (int cfg : {kC128x128, kC128x64, kC64x64}) {
+      const int64_t t = tiles_of(cfg, M, N);
+      int64_t sp = 1;
+      while (t * sp < 2 * kFill && K / (2 * sp) >= 256) sp *= 2;
+      if (t * sp >= kFill) {
+        p.cfg = cfg;
+        p.splits = sp;
+        done = true;
+        break;
+      }
+    }
+  }
+  if (!done) {
+    p.cfg = kC64x64;
+    const int64_t t = tiles_of(kC64x64, M, N);
+    p.splits = 1;
+    if (allow_split)
+      while (t * p.splits < 256 && K / (2 * p.splits) >= 32) p.splits *= 2;
+  }
+  p.k_chunk = ot::round_up(ot::ceil_div(K, p.splits), 16);
+  p.splits = std::max<int64_t>(1, ot::ceil_div(K, p.k_chunk));
+  p.blocks = tiles_of(p.cfg, M, N) * p.splits;
+  return p;
 }
 
 template <Lay LA, Lay LB, Epi EPI>
-int64_t gemm_blocks(const GemmArgs& g, int64_t splits) {
-  const int64_t big = ot::gemm_tiles<2, 2, 4, 4>(g.M, g.N);
-  if (big * splits >= 240) return big * splits;
-  return ot::gemm_tiles<2, 2, 2, 2>(g.M, g.N) * splits;
+hipError_t launch_cfg(int cfg, const GemmArgs& g, int64_t splits, hipStream_t st) {
+  switch (cfg) {
+    case kC128x128: return ot::launch_gemm_f32<2, 2, 4, 4, LA, LB, EPI>(g, splits, st);
+    case kC128x64: return ot::launch_gemm_f32<2, 2, 4, 2, LA, LB, EPI>(g, splits, st);
+    default: return ot::launch_gemm_f32<2, 2, 2, 2, LA, LB, EPI>(g, splits, st);
+  }
+}
+
+template <Lay LA, Lay LB>
+hipError_t launch_epi(Epi epi, int cfg, const GemmArgs& g, int64_t splits, hipStream_t st) {
+  switch (epi) {
+    case Epi::Store: return launch_cfg<LA, LB, Epi::Store>(cfg, g, splits, st);
+    case Epi::Bias: return launch_cfg<LA, LB, Epi::Bias>(cfg, g, splits, st);
+    case Epi::BiasRelu: return launch_cfg<LA, LB, Epi::BiasRelu>(cfg, g, splits, st);
+    case Epi::Mse: return launch_cfg<LA, LB, Epi::Mse>(cfg, g, splits, st);
+    case Epi::SplitK: return launch_cfg<LA, LB, Epi::SplitK>(cfg, g, splits, st);
+    default: return launch_cfg<LA, LB, Epi::Mask>(cfg, g, splits, st);
+  }
+}
+
+int ensure_split_ws(ot_surrogate* s, int64_t elems, int64_t rs_elems) {
+  if (elems > s->splitws_elems) {
+    OT_HIP(hipDeviceSynchronize());
+    (void)hipFree(s->splitws);
+    s->splitws = nullptr;
+    s->splitws_elems = 0;
+    int rc = salloc((void**)&s->splitws, (size_t)elems * sizeof(float));
+    if (rc) return rc;
+    s->splitws_elems = elems;
+  }
+  if (rs_elems > s->rsws_elems) {
+    OT_HIP(hipDeviceSynchronize());
+    (void)hipFree(s->rsws);
+    s->rsws = nullptr;
+    s->rsws_elems = 0;
+    int rc = salloc((void**)&s->rsws, (size_t)rs_elems * sizeof(float));
+    if (rc) return rc;
+    s->rsws_elems = rs_elems;
+  }
+  return OT_OK;
+}
+
+// C = epi(A B) with the plan's tile shape; split-K runs write partial sums to
+// the workspace and a second kernel applies the epilogue (fixed split order).
+// ph_gemm / ph_reduce: timing phases of the two halves (-1: not timed).
+template <Lay LA, Lay LB>
+int run_gemm(ot_surrogate* s, GemmArgs g, Epi epi, hipStream_t st, const char* what, bool allow_split,
+             int ph_gemm = -1, int ph_reduce = -1, int64_t* blocks_out = nullptr) {
+  const Plan p = make_plan(g.M, g.N, g.K, allow_split && epi != Epi::Mse);
+  if (blocks_out) *blocks_out = p.blocks;
+  ot::PhaseTimer& tm = s->timer;
+  if (p.splits == 1) {
+    g.k_chunk = g.K;
+    if (ph_gemm >= 0) tm.mark(st, ph_gemm, 0);
+    hipError_t e = launch_epi<LA, LB>(epi, p.cfg, g, 1, st);
+    if (e != hipSuccess) return ot::set_error(OT_E_HIP, "launch of %s GEMM failed: %s", what, hipGetErrorString(e));
+    if (ph_gemm >= 0) tm.mark(st, ph_gemm, 1);
+    return OT_OK;
+  }
+  const int64_t ldws = ot::round_up(g.N, 4);
+  int rc = ensure_split_ws(s, p.splits * g.M * ldws, g.rowsum ? p.splits * g.M : 0);
+  if (rc) return rc;
+  GemmArgs h = g;
+  h.C = s->splitws;
+  h.ldc = ldws;
+  h.split_stride = g.M * ldws;
+  h.k_chunk = p.k_chunk;
+  h.rowsum = g.rowsum ? s->rsws : nullptr;
+  h.rowsum_stride = g.M;
+  if (ph_gemm >= 0) tm.mark(st, ph_gemm, 0);
+  hipError_t e = launch_epi<LA, LB>(Epi::SplitK, p.cfg, h, p.splits, st);
+  if (e != hipSuccess) return ot::set_error(OT_E_HIP, "launch of %s GEMM failed: %s", what, hipGetErrorString(e));
+  if (ph_gemm >= 0) tm.mark(st, ph_gemm, 1);
+  if (ph_reduce >= 0) tm.mark(st, ph_reduce, 0);
+  const int64_t work = g.M * ot::ceil_div(g.N, 4);
+  const bool bias = (epi == Epi::Bias || epi == Epi::BiasRelu);
+  hipLaunchKernelGGL(ot::splitk_epilogue_kernel, dim3((unsigned)ot::ceil_div(work, 256)), dim3(256), 0, st,
+                     s->splitws, p.splits, h.split_stride, g.M, g.N, ldws, bias ? g.bias : nullptr,
+                     epi == Epi::BiasRelu ? 1 : 0, epi == Epi::Mask ? g.mask : nullptr, g.ldmask, g.C, g.ldc,
+                     h.rowsum, h.rowsum_stride, g.rowsum);
+  OT_LAUNCHED("splitk_epilogue_kernel");
+  if (ph_reduce >= 0) tm.mark(st, ph_reduce, 1);
+  return OT_OK;
 }
 
 GemmArgs args0() {
@@ -355,9 +492,8 @@ int forward_hidden(ot_surrogate* s, const float* X, int64_t ldx, int64_t rows, h
     g.M = rows;
     g.N = ly.out;
     g.K = ly.in;
-    g.k_chunk = ly.in;
     g.bias = b;
-    int rc = gemm<Lay::KMajor, Lay::KMajor, Epi::BiasRelu>(g, 1, st, "hidden forward");
+    int rc = run_gemm<Lay::KMajor, Lay::KMajor>(s, g, Epi::BiasRelu, st, "hidden forward", true);
     if (rc) return rc;
   }
   return OT_OK;
@@ -540,7 +676,6 @@ extern "C" int surrogate_train_step(ot_surrogate* s, const float* x, int64_t ldx
     g.M = b;
     g.N = D;
     g.K = lo.in;
-    g.k_chunk = lo.in;
     g.bias = s->params + lo.b_off;
     g.target = u;
     g.ldt = ldu;
@@ -548,11 +683,11 @@ extern "C" int surrogate_train_step(ot_surrogate* s, const float* x, int64_t ldx
     g.loss_partials = s->loss_partials;
     if (L == 1 && lo.in <= ot::kMaxSmallK)
       OT_REQUIRE(aligned16(x) && ldx % 4 == 0, "single-layer nets need 16-byte aligned x, ldx %% 4 == 0");
-    n_partials = gemm_blocks<Lay::KMajor, Lay::KMajor, Epi::Mse>(g, 1);
+    n_partials = make_plan(g.M, g.N, g.K, false).blocks;
     if (n_partials > s->n_partials_cap) return ot::set_error(OT_E_STATE, "loss partial buffer too small");
-    tm.mark(st, OT_PH_FWD_OUTPUT, 0);
-    if ((rc = gemm<Lay::KMajor, Lay::KMajor, Epi::Mse>(g, 1, st, "output forward+MSE"))) return rc;
-    tm.mark(st, OT_PH_FWD_OUTPUT, 1);
+    if ((rc = run_gemm<Lay::KMajor, Lay::KMajor>(s, g, Epi::Mse, st, "output forward+MSE", false,
+                                                 OT_PH_FWD_OUTPUT)))
+      return rc;
   }
   tm.mark(st, OT_PH_LOSS, 0);
   hipLaunchKernelGGL(ot::loss_finalize_kernel, dim3(1), dim3(256), 0, st, s->loss_partials, n_partials,
@@ -592,9 +727,8 @@ extern "C" int surrogate_train_step(ot_surrogate* s, const float* x, int64_t ldx
       g.M = ly.out;
       g.N = ly.in;
       g.K = b;
-      g.k_chunk = b;
       g.rowsum = db;
-      if ((rc = gemm<Lay::MNMajor, Lay::MNMajor, Epi::Store>(g, 1, st, "weight gradient"))) return rc;
+      if ((rc = run_gemm<Lay::MNMajor, Lay::MNMajor>(s, g, Epi::Store, st, "weight gradient", true))) return rc;
     }
     if (ph_w >= 0) tm.mark(st, ph_w, 1);
     if (l == 1) break;
@@ -607,34 +741,14 @@ extern "C" int surrogate_train_step(ot_surrogate* s, const float* x, int64_t ldx
     g.M = b;
     g.N = ly.in;
     g.K = ly.out;
-    const int64_t tiles = ot::gemm_tiles<2, 2, 4, 4>(b, ly.in);
-    const int64_t splits = std::min<int64_t>(kSplitCap, choose_splits(tiles, ly.out));
-    if (splits > 1) {
-      g.k_chunk = ot::round_up(ot::ceil_div(ly.out, splits), 16);
-      const int64_t used = ot::ceil_div(ly.out, g.k_chunk);
-      g.C = s->splitws;
-      g.ldc = s->ld[l - 1];
-      g.split_stride = b * s->ld[l - 1];
-      if (l == L) tm.mark(st, OT_PH_IGRAD_OUTPUT, 0);
-      if ((rc = gemm<Lay::KMajor, Lay::MNMajor, Epi::SplitK>(g, used, st, "input gradient (split)"))) return rc;
-      if (l == L) tm.mark(st, OT_PH_IGRAD_OUTPUT, 1);
-      if (l == L) tm.mark(st, OT_PH_IGRAD_REDUCE, 0);
-      const int64_t work = b * ot::ceil_div(ly.in, 4);
-      hipLaunchKernelGGL(ot::splitk_reduce_mask_kernel, dim3((unsigned)ot::ceil_div(work, 256)), dim3(256), 0, st,
-                         s->splitws, used, g.split_stride, b, ly.in, s->ld[l - 1], s->act[l - 1], s->ld[l - 1],
-                         s->dz[l - 1], s->ld[l - 1]);
-      OT_LAUNCHED("splitk_reduce_mask_kernel");
-      if (l == L) tm.mark(st, OT_PH_IGRAD_REDUCE, 1);
-    } else {
-      g.k_chunk = ly.out;
-      g.C = s->dz[l - 1];
-      g.ldc = s->ld[l - 1];
-      g.mask = s->act[l - 1];
-      g.ldmask = s->ld[l - 1];
-      if (l == L) tm.mark(st, OT_PH_IGRAD_OUTPUT, 0);
-      if ((rc = gemm<Lay::KMajor, Lay::MNMajor, Epi::Mask>(g, 1, st, "input gradient"))) return rc;
-      if (l == L) tm.mark(st, OT_PH_IGRAD_OUTPUT, 1);
-    }
+    g.C = s->dz[l - 1];
+    g.ldc = s->ld[l - 1];
+    g.mask = s->act[l - 1];
+    g.ldmask = s->ld[l - 1];
+    if ((rc = run_gemm<Lay::KMajor, Lay::MNMajor>(s, g, Epi::Mask, st, "input gradient", true,
+                                                  l == L ? OT_PH_IGRAD_OUTPUT : -1,
+                                                  l == L ? OT_PH_IGRAD_REDUCE : -1)))
+      return rc;
   }
   if (L >= 2) tm.mark(st, OT_PH_BWD_HIDDEN, 1);
 
@@ -697,9 +811,8 @@ extern "C" int surrogate_predict(ot_surrogate* s, const float* x, int64_t ldx, i
     g.M = rows;
     g.N = D;
     g.K = lo.in;
-    g.k_chunk = lo.in;
     g.bias = s->params + lo.b_off;
-    if ((rc = gemm<Lay::KMajor, Lay::KMajor, Epi::Bias>(g, 1, st, "output forward"))) return rc;
+    if ((rc = run_gemm<Lay::KMajor, Lay::KMajor>(s, g, Epi::Bias, st, "output forward", true))) return rc;
   }
   return OT_OK;
 }
