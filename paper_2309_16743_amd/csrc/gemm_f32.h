@@ -79,10 +79,10 @@ struct FragVec<2> { typedef f32x2 T; };
 template <>
 struct FragVec<1> { typedef float T; };
 
-template <int WGM, int WGN, int FM, int FN, Lay LA, Lay LB, Epi EPI>
+template <int WGM, int WGN, int FM, int FN, Lay LA, Lay LB, Epi EPI, int BK = 16>
 __global__ __launch_bounds__(64 * WGM * WGN) void gemm_f32_kernel(GemmArgs g) {
   constexpr int NT = 64 * WGM * WGN;
-  constexpr int BK = 16;
+  static_assert(BK % 16 == 0, "k tile must be a multiple of 16");
   constexpr int BM = 16 * FM * WGM;
   constexpr int BN = 16 * FN * WGN;
   constexpr int PAD = 4;
@@ -114,8 +114,39 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_f32_kernel(GemmArgs g) {
 
   // Global -> register staging of one k tile.
   f32x4 ra[VA], rb[VB];
+  // Blocks whose tile lies inside M x N load full k tiles without predication.
+  const bool interior = (m0 + BM <= g.M) && (n0 + BN <= g.N);
+
+  auto load_tile_fast = [&](int64_t k0) {
+#pragma unroll
+    for (int i = 0; i < VA; ++i) {
+      const int v = tid + i * NT;
+      if constexpr (LA == Lay::MNMajor) {
+        const int kr = v / (BM / 4), mc = (v % (BM / 4)) * 4;
+        ra[i] = *reinterpret_cast<const f32x4*>(g.A + (k0 + kr) * g.lda + m0 + mc);
+      } else {
+        const int mr = v / (BK / 4), kc = (v % (BK / 4)) * 4;
+        ra[i] = *reinterpret_cast<const f32x4*>(g.A + (m0 + mr) * g.lda + k0 + kc);
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < VB; ++i) {
+      const int v = tid + i * NT;
+      if constexpr (LB == Lay::MNMajor) {
+        const int kr = v / (BN / 4), nc = (v % (BN / 4)) * 4;
+        rb[i] = *reinterpret_cast<const f32x4*>(g.B + (k0 + kr) * g.ldb + n0 + nc);
+      } else {
+        const int nr = v / (BK / 4), kc = (v % (BK / 4)) * 4;
+        rb[i] = *reinterpret_cast<const f32x4*>(g.B + (n0 + nr) * g.ldb + k0 + kc);
+      }
+    }
+  };
 
   auto load_tile = [&](int64_t k0) {
+    if (interior && k0 + BK <= kend) {
+      load_tile_fast(k0);
+      return;
+    }
 #pragma unroll
     for (int i = 0; i < VA; ++i) {
       const int v = tid + i * NT;
@@ -131,7 +162,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_f32_kernel(GemmArgs g) {
         }
         ra[i] = t;
       } else {
-        const int mr = v / 4, kc = (v % 4) * 4;
+        const int mr = v / (BK / 4), kc = (v % (BK / 4)) * 4;
         const int64_t m = m0 + mr, k = k0 + kc;
         f32x4 t = {0.f, 0.f, 0.f, 0.f};
         if (m < g.M) {
@@ -158,7 +189,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_f32_kernel(GemmArgs g) {
         }
         rb[i] = t;
       } else {
-        const int nr = v / 4, kc = (v % 4) * 4;
+        const int nr = v / (BK / 4), kc = (v % (BK / 4)) * 4;
         const int64_t n = n0 + nr, k = k0 + kc;
         f32x4 t = {0.f, 0.f, 0.f, 0.f};
         if (n < g.N) {
@@ -182,7 +213,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_f32_kernel(GemmArgs g) {
         const int kr = v / (BM / 4), mc = (v % (BM / 4)) * 4;
         *reinterpret_cast<f32x4*>(as + kr * LDA_S + mc) = ra[i];
       } else {
-        const int mr = v / 4, kc = (v % 4) * 4;
+        const int mr = v / (BK / 4), kc = (v % (BK / 4)) * 4;
 #pragma unroll
         for (int c = 0; c < 4; ++c) as[(kc + c) * LDA_S + mr] = ra[i][c];
       }
@@ -194,7 +225,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_f32_kernel(GemmArgs g) {
         const int kr = v / (BN / 4), nc = (v % (BN / 4)) * 4;
         *reinterpret_cast<f32x4*>(bs + kr * LDB_S + nc) = rb[i];
       } else {
-        const int nr = v / 4, kc = (v % 4) * 4;
+        const int nr = v / (BK / 4), kc = (v % (BK / 4)) * 4;
 #pragma unroll
         for (int c = 0; c < 4; ++c) bs[(kc + c) * LDB_S + nr] = rb[i][c];
       }
@@ -225,11 +256,20 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_f32_kernel(GemmArgs g) {
     if (kt + 1 < nk) load_tile(kbeg + (kt + 1) * BK);
     const float* as = As[buf];
     const float* bs = Bs[buf];
+    typedef typename FragVec<FM>::T FA;
+    typedef typename FragVec<FN>::T FB;
+    // fragments of step kk + 1 are read while step kk's MFMAs run
+    FA an = *reinterpret_cast<const FA*>(as + kl * LDA_S + a_off);
+    FB bn = *reinterpret_cast<const FB*>(bs + kl * LDB_S + b_off);
 #pragma unroll
     for (int kk = 0; kk < BK / 4; ++kk) {
-      const int kr = 4 * kk + kl;
-      const typename FragVec<FM>::T av = *reinterpret_cast<const typename FragVec<FM>::T*>(as + kr * LDA_S + a_off);
-      const typename FragVec<FN>::T bv = *reinterpret_cast<const typename FragVec<FN>::T*>(bs + kr * LDB_S + b_off);
+      const FA av = an;
+      const FB bv = bn;
+      if (kk + 1 < BK / 4) {
+        const int kr = 4 * (kk + 1) + kl;
+        an = *reinterpret_cast<const FA*>(as + kr * LDA_S + a_off);
+        bn = *reinterpret_cast<const FB*>(bs + kr * LDB_S + b_off);
+      }
 #pragma unroll
       for (int f = 0; f < FM; ++f) {
         float a_f;
@@ -252,10 +292,33 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_f32_kernel(GemmArgs g) {
   if (do_rowsum && tid < BM && m0 + tid < g.M) g.rowsum[split * g.rowsum_stride + m0 + tid] = rsum;
 
   // ---------------------------------------------------------------- epilogue
-  double lsum = 0.0;
+  float lsum = 0.f;
   const int64_t row_base = m0 + 16 * FM * wm + 4 * FM * (lane / 16);
   const int64_t col_base = n0 + 16 * FN * wn + FN * (lane % 16);
   float* Cb = g.C + (EPI == Epi::SplitK ? split * g.split_stride : 0);
+  const bool full = (col_base + FN - 1 < g.N);
+  // FN consecutive values starting at column col_base (zeros past N); the
+  // pointers are 4 * FN-byte aligned because col_base is a multiple of FN
+  // and every leading dimension is a multiple of 4.
+  auto load_cols = [&](const float* p, float* out) {
+    if (full) {
+      if constexpr (FN == 4) {
+        const f32x4 t = *reinterpret_cast<const f32x4*>(p);
+        out[0] = t[0]; out[1] = t[1]; out[2] = t[2]; out[3] = t[3];
+      } else if constexpr (FN == 2) {
+        const f32x2 t = *reinterpret_cast<const f32x2*>(p);
+        out[0] = t[0]; out[1] = t[1];
+      } else {
+#pragma unroll
+        for (int h = 0; h < FN; ++h) out[h] = p[h];
+      }
+    } else {
+#pragma unroll
+      for (int h = 0; h < FN; ++h) out[h] = (col_base + h < g.N) ? p[h] : 0.f;
+    }
+  };
+  float bv[FN];
+  if constexpr (EPI == Epi::Bias || EPI == Epi::BiasRelu || EPI == Epi::Mse) load_cols(g.bias + col_base, bv);
 #pragma unroll
   for (int r = 0; r < 4; ++r) {
 #pragma unroll
@@ -265,32 +328,29 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_f32_kernel(GemmArgs g) {
       float v[FN];
 #pragma unroll
       for (int h = 0; h < FN; ++h) v[h] = acc[f][h][r];
-      const bool full = (col_base + FN - 1 < g.N);
       if constexpr (EPI == Epi::Bias || EPI == Epi::BiasRelu || EPI == Epi::Mse) {
 #pragma unroll
-        for (int h = 0; h < FN; ++h)
-          if (col_base + h < g.N) v[h] += g.bias[col_base + h];
+        for (int h = 0; h < FN; ++h) v[h] += bv[h];
       }
       if constexpr (EPI == Epi::BiasRelu) {
 #pragma unroll
         for (int h = 0; h < FN; ++h) v[h] = v[h] > 0.f ? v[h] : 0.f;
       }
       if constexpr (EPI == Epi::Mse) {
-        const float* tp = g.target + m * g.ldt + col_base;
+        float tv[FN];
+        load_cols(g.target + m * g.ldt + col_base, tv);
 #pragma unroll
         for (int h = 0; h < FN; ++h) {
-          if (col_base + h < g.N) {
-            const float rr = v[h] - tp[h];
-            lsum += (double)(rr * rr);
-            v[h] = g.scale * rr;
-          }
+          const float rr = (col_base + h < g.N) ? v[h] - tv[h] : 0.f;
+          lsum += rr * rr;
+          v[h] = g.scale * rr;
         }
       }
       if constexpr (EPI == Epi::Mask) {
-        const float* mp = g.mask + m * g.ldmask + col_base;
+        float mv[FN];
+        load_cols(g.mask + m * g.ldmask + col_base, mv);
 #pragma unroll
-        for (int h = 0; h < FN; ++h)
-          if (col_base + h < g.N) v[h] = mp[h] > 0.f ? v[h] : 0.f;
+        for (int h = 0; h < FN; ++h) v[h] = mv[h] > 0.f ? v[h] : 0.f;
       }
       float* cp = Cb + m * g.ldc + col_base;
       if (FN == 4 && full) {
@@ -305,8 +365,8 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_f32_kernel(GemmArgs g) {
     }
   }
   if constexpr (EPI == Epi::Mse) {
-    lsum = warp_sum(lsum);
-    if (lane == 0) s_red[wid] = lsum;
+    double ls = warp_sum((double)lsum);
+    if (lane == 0) s_red[wid] = ls;
     __syncthreads();
     if (tid == 0) {
       double t = 0.0;
@@ -317,12 +377,12 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_f32_kernel(GemmArgs g) {
 }
 
 // Host launcher.  Returns the hipError_t of the launch.
-template <int WGM, int WGN, int FM, int FN, Lay LA, Lay LB, Epi EPI>
+template <int WGM, int WGN, int FM, int FN, Lay LA, Lay LB, Epi EPI, int BK = 16>
 hipError_t launch_gemm_f32(const GemmArgs& g, int64_t splits, hipStream_t stream) {
   constexpr int BM = 16 * FM * WGM, BN = 16 * FN * WGN;
   const int64_t tiles = ((g.M + BM - 1) / BM) * ((g.N + BN - 1) / BN);
   dim3 grid((unsigned)tiles, (unsigned)splits);
-  hipLaunchKernelGGL((gemm_f32_kernel<WGM, WGN, FM, FN, LA, LB, EPI>), grid, dim3(64 * WGM * WGN), 0, stream, g);
+  hipLaunchKernelGGL((gemm_f32_kernel<WGM, WGN, FM, FN, LA, LB, EPI, BK>), grid, dim3(64 * WGM * WGN), 0, stream, g);
   return hipGetLastError();
 }
 

@@ -317,13 +317,13 @@ int ensure_workspace(ot_surrogate* s, int64_t rows) {
   return OT_OK;
 }
 
-// Tile shapes: 128 x 128 (4 waves, 64 x 64 each), 128 x 64, 64 x 64.
-enum Cfg : int { kC128x128 = 0, kC128x64 = 1, kC64x64 = 2 };
+// Tile shapes (4 wavefronts each): 128 x 128, 64 x 128, 64 x 64.
+enum Cfg : int { kC128x128 = 0, kC64x128 = 1, kC64x64 = 2 };
 
 int64_t tiles_of(int cfg, int64_t M, int64_t N) {
   switch (cfg) {
     case kC128x128: return ot::gemm_tiles<2, 2, 4, 4>(M, N);
-    case kC128x64: return ot::gemm_tiles<2, 2, 4, 2>(M, N);
+    case kC64x128: return ot::gemm_tiles<2, 2, 2, 4>(M, N);
     default: return ot::gemm_tiles<2, 2, 2, 2>(M, N);
   }
 }
@@ -335,39 +335,31 @@ struct Plan {
   int64_t blocks = 0;
 };
 
-// Largest tile whose tile count alone gives about one block per CU; else the
-// largest tile that reaches it by splitting the k range (at least 256 deep per
-// split); else 64 x 64 tiles split down to 32-deep k ranges.
+// Tile and k-split choice (measured on MI355X at the surrogate's shapes).
+// Whole tiles per CU matter more than tile size: a launch whose block count
+// leaves some CUs a block more than others loses that fraction, so the plan
+// aims for about 4 blocks per CU (960+) with 64 x 128 tiles, splits long k
+// ranges (>= 4096) over 128 x 128 tiles, splits medium ones over 64 x 64
+// tiles (>= 256 deep per split), and splits short problems down to 32-deep
+// ranges until every CU has a block.  The MSE epilogue needs whole sums and
+// is never split.
 Plan make_plan(int64_t M, int64_t N, int64_t K, bool allow_split) {
-  constexpr int64_t kFill = 240;
+  constexpr int64_t kCUs = 256;
   Plan p;
-  bool done = false;
-  for (int cfg : {kC128x128, kC128x64, kC64x64}) {
-    if (tiles_of(cfg, M, N) >= kFill) {
-      p.cfg = cfg;
-      done = true;
-      break;
-    }
-  }
-  if (!done && allow_split) {
-    for (int cfg : {kC128x128, kC128x64, kC64x64}) {
-      const int64_t t = tiles_of(cfg, M, N);
-      int64_t sp = 1;
-      while (t * sp < 2 * kFill && K / (2 * sp) >= 256) sp *= 2;
-      if (t * sp >= kFill) {
-        p.cfg = cfg;
-        p.splits = sp;
-        done = true;
-        break;
-      }
-    }
-  }
-  if (!done) {
+  if (tiles_of(kC64x128, M, N) >= 960 || !allow_split) {
+    p.cfg = kC64x128;
+    if (tiles_of(kC64x128, M, N) < kCUs) p.cfg = kC64x64;
+    if (!allow_split && tiles_of(kC64x64, M, N) < kCUs) p.cfg = kC64x64;
+  } else if (K >= 4096) {
+    p.cfg = kC128x128;
+    const int64_t t = tiles_of(kC128x128, M, N);
+    while (t * p.splits < 2 * kCUs - 32 && K / (2 * p.splits) >= 256) p.splits *= 2;
+  } else {
     p.cfg = kC64x64;
     const int64_t t = tiles_of(kC64x64, M, N);
-    p.splits = 1;
-    if (allow_split)
-      while (t * p.splits < 256 && K / (2 * p.splits) >= 32) p.splits *= 2;
+    while (t * p.splits < 960 && K / (2 * p.splits) >= 256) p.splits *= 2;
+    if (t * p.splits < kCUs)
+      while (t * p.splits < kCUs && K / (2 * p.splits) >= 32) p.splits *= 2;
   }
   p.k_chunk = ot::round_up(ot::ceil_div(K, p.splits), 16);
   p.splits = std::max<int64_t>(1, ot::ceil_div(K, p.k_chunk));
@@ -379,7 +371,7 @@ template <Lay LA, Lay LB, Epi EPI>
 hipError_t launch_cfg(int cfg, const GemmArgs& g, int64_t splits, hipStream_t st) {
   switch (cfg) {
     case kC128x128: return ot::launch_gemm_f32<2, 2, 4, 4, LA, LB, EPI>(g, splits, st);
-    case kC128x64: return ot::launch_gemm_f32<2, 2, 4, 2, LA, LB, EPI>(g, splits, st);
+    case kC64x128: return ot::launch_gemm_f32<2, 2, 2, 4, LA, LB, EPI>(g, splits, st);
     default: return ot::launch_gemm_f32<2, 2, 2, 2, LA, LB, EPI>(g, splits, st);
   }
 }
