@@ -93,7 +93,8 @@ enum ot_surrogate_phase {
   OT_PH_IGRAD_REDUCE = 5,  /* split-K reduction + ReLU mask of that gradient */
   OT_PH_BWD_HIDDEN = 6,    /* hidden-layer backward */
   OT_PH_ADAM = 7,          /* Adam over all parameters */
-  OT_SURROGATE_PHASES = 8
+  OT_PH_WGRAD_REDUCE = 8,  /* split-K reduction of the output-layer weight gradient */
+  OT_SURROGATE_PHASES = 9
 };
 
 /* Profiling hook: record HIP events around the kernels of every phase in

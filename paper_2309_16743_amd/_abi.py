@@ -23,7 +23,7 @@ OT_FP32 = 0
 OT_BF16 = 1
 
 SURROGATE_PHASES = ("fwd_hidden", "fwd_output", "loss", "wgrad_output", "igrad_output", "igrad_reduce",
-                    "bwd_hidden", "adam")
+                    "bwd_hidden", "adam", "wgrad_reduce")
 RESERVOIR_PHASES = ("put_assign", "put_copy", "select", "gather")
 
 

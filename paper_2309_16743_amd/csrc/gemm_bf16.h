@@ -1,0 +1,351 @@
+// bf16 GEMM on CDNA4 matrix cores (v_mfma_f32_16x16x32_bf16), fp32
+// accumulation, with fused epilogues for the mixed-precision surrogate.
+//
+//   C[m, n] = sum_k A(m, k) * B(n, k)      (A, B bf16; C fp32 or bf16)
+//
+// Operand storage as in the fp32 kernel: "KMajor" = k contiguous
+// (A[m * lda + k]), "MNMajor" = m (or n) contiguous (A[k * lda + m]).
+// Leading dimensions are multiples of 8 elements and bases 16-byte aligned.
+//
+// MFMA lane layout (16x16x32 bf16): lane l supplies A[i = l%16][k = 8(l/16)+e]
+// and B[k = 8(l/16)+e][j = l%16], e = 0..7; accumulator element r of lane l is
+// D[4(l/16)+r][l%16].
+//
+// LDS staging keeps each operand in its global layout, so every global load
+// and LDS write is a 16-byte vector:
+//   KMajor  -> tile [mn][BK + 8]: a lane's 8 k-values are one ds_read_b128;
+//   MNMajor -> tile [BK][mn + 16]: a lane's 8 k-values are two
+//              ds_read_b64_tr_b16 transpose reads (within each 16-lane group,
+//              lane c addresses row k0 + c/4, columns 4 (c%4)..+3, and lane i
+//              receives column i of those 4 rows).
+// Block: 4 wavefronts (2 x 2), wave tile (16 FM) x (16 FN), fragment f
+// covering rows 16 f .. 16 f + 15 of the wave tile.  The epilogue stages the
+// fp32 accumulators through LDS so that each lane then handles 4 consecutive
+// columns of a row: targets, bias and masks are read, and C written, with
+// 16-byte (fp32) or 8-byte (bf16) vector accesses.
+#pragma once
+
+#include "common.h"
+
+namespace ot {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef uint16_t u16x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+// fp32 -> bf16, round to nearest even (finite inputs).
+__device__ __forceinline__ uint16_t f2bf(float x) {
+  uint32_t u = __float_as_uint(x);
+  u += 0x7FFFu + ((u >> 16) & 1u);
+  return (uint16_t)(u >> 16);
+}
+__device__ __forceinline__ float bf2f(uint16_t h) { return __uint_as_float((uint32_t)h << 16); }
+
+enum class LayB : int { KMajor = 0, MNMajor = 1 };
+enum class EpiB : int {
+  StoreF32 = 0,   // C (fp32) = acc
+  SplitK = 1,     // C (fp32)[split] = acc
+  BiasF32 = 2,    // C (fp32) = acc + bias[n]
+  BiasReluBf = 3, // C (bf16) = bf16(max(acc + bias[n], 0))
+  MaskBf = 4,     // C (bf16) = bf16(acc * (mask[m, n] > 0)), mask bf16
+  MseBf = 5       // R = acc + bias[n] - T[m, n] (T fp32); C (bf16) = bf16(scale R); per-block sum of R^2
+};
+
+struct GemmBArgs {
+  const uint16_t* A;
+  int64_t lda;
+  const uint16_t* B;
+  int64_t ldb;
+  void* C;
+  int64_t ldc;
+  int64_t M, N, K;
+  int64_t k_chunk;          // per split, multiple of BK
+  int64_t split_stride;     // SplitK: elements between split slices
+  const float* bias;
+  const float* target;      // MseBf (fp32)
+  int64_t ldt;
+  float scale;
+  double* loss_partials;
+  const uint16_t* mask;     // MaskBf (bf16 activations)
+  int64_t ldmask;
+  float* rowsum;            // StoreF32 / SplitK with MNMajor A: sum_k A(m, k) (n tile 0)
+  int64_t rowsum_stride;
+};
+
+__device__ __forceinline__ int64_t xcd_remap_b(int64_t p, int64_t g) {
+  const int64_t xcd = p % 8, q = p / 8;
+  const int64_t per = g / 8, rem = g % 8;
+  return xcd * per + (xcd < rem ? xcd : rem) + q;
+}
+
+template <int FM, int FN, LayB LA, LayB LB, EpiB EPI, int BK>
+__global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmBArgs g) {
+  constexpr int NT = 256, WGM = 2, WGN = 2;
+  constexpr int WM = 16 * FM, WN = 16 * FN;
+  constexpr int BM = WGM * WM, BN = WGN * WN;
+  static_assert(BK % 32 == 0, "k tile must be a multiple of 32");
+  // LDS tile geometry (elements of 16 bits)
+  constexpr int A_ROWS = (LA == LayB::KMajor) ? BM : BK;
+  constexpr int A_PITCH = (LA == LayB::KMajor) ? BK + 8 : BM + 16;
+  constexpr int B_ROWS = (LB == LayB::KMajor) ? BN : BK;
+  constexpr int B_PITCH = (LB == LayB::KMajor) ? BK + 8 : BN + 16;
+  constexpr int A_ELEMS = A_ROWS * A_PITCH, B_ELEMS = B_ROWS * B_PITCH;
+  constexpr int VA = BM * BK / 8 / NT, VB = BN * BK / 8 / NT;   // 16-byte loads per thread
+  static_assert(VA >= 1 && VA * NT * 8 == BM * BK && VB >= 1 && VB * NT * 8 == BN * BK, "tile split");
+  constexpr int TILE_BYTES = 2 * 2 * (A_ELEMS + B_ELEMS);
+  constexpr int EPI_BYTES = 4 * (WM * (WN + 4)) * 4;            // per-wave fp32 staging
+  constexpr int LDS_BYTES = TILE_BYTES > EPI_BYTES ? TILE_BYTES : EPI_BYTES;
+  __shared__ __attribute__((aligned(16))) unsigned char smem[LDS_BYTES];
+  __shared__ double s_red[4];
+  uint16_t* const tiles16 = reinterpret_cast<uint16_t*>(smem);
+  auto As = [&](int buf) { return tiles16 + buf * A_ELEMS; };
+  auto Bs = [&](int buf) { return tiles16 + 2 * A_ELEMS + buf * B_ELEMS; };
+
+  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+  const int wm = wid % WGM, wn = wid / WGM;
+  const int64_t tiles_m = (g.M + BM - 1) / BM;
+  const int64_t logical = xcd_remap_b(blockIdx.x, (int64_t)gridDim.x);
+  const int64_t tm = logical % tiles_m, tn = logical / tiles_m;
+  const int64_t m0 = tm * BM, n0 = tn * BN;
+  const int64_t split = blockIdx.y;
+  const int64_t kbeg = split * g.k_chunk;
+  const int64_t kend = (kbeg + g.k_chunk < g.K) ? kbeg + g.k_chunk : g.K;
+  const int64_t nk = (kend > kbeg) ? (kend - kbeg + BK - 1) / BK : 0;
+  const bool interior = (m0 + BM <= g.M) && (n0 + BN <= g.N);
+
+  u32x4 ra[VA], rb[VB];
+
+  // 8 consecutive elements at p, zero where the predicate fails
+  auto load8 = [&](const uint16_t* p, bool all, int valid) -> u32x4 {
+    if (all) return *reinterpret_cast<const u32x4*>(p);
+    uint16_t t[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) t[e] = e < valid ? p[e] : (uint16_t)0;
+    u32x4 r;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) r[e] = (uint32_t)t[2 * e] | ((uint32_t)t[2 * e + 1] << 16);
+    return r;
+  };
+
+  auto load_tile = [&](int64_t k0) {
+    const bool fast = interior && (k0 + BK <= kend);
+#pragma unroll
+    for (int i = 0; i < VA; ++i) {
+      const int v = tid + i * NT;
+      if constexpr (LA == LayB::KMajor) {
+        const int r = v / (BK / 8), c = (v % (BK / 8)) * 8;
+        const int64_t m = m0 + r, k = k0 + c;
+        if (fast) ra[i] = *reinterpret_cast<const u32x4*>(g.A + m * g.lda + k);
+        else if (m < g.M && k < kend) ra[i] = load8(g.A + m * g.lda + k, k + 8 <= kend, (int)(kend - k));
+        else ra[i] = u32x4{0, 0, 0, 0};
+      } else {
+        const int r = v / (BM / 8), c = (v % (BM / 8)) * 8;
+        const int64_t k = k0 + r, m = m0 + c;
+        if (fast) ra[i] = *reinterpret_cast<const u32x4*>(g.A + k * g.lda + m);
+        else if (k < kend && m < g.M) ra[i] = load8(g.A + k * g.lda + m, m + 8 <= g.M, (int)(g.M - m));
+        else ra[i] = u32x4{0, 0, 0, 0};
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < VB; ++i) {
+      const int v = tid + i * NT;
+      if constexpr (LB == LayB::KMajor) {
+        const int r = v / (BK / 8), c = (v % (BK / 8)) * 8;
+        const int64_t n = n0 + r, k = k0 + c;
+        if (fast) rb[i] = *reinterpret_cast<const u32x4*>(g.B + n * g.ldb + k);
+        else if (n < g.N && k < kend) rb[i] = load8(g.B + n * g.ldb + k, k + 8 <= kend, (int)(kend - k));
+        else rb[i] = u32x4{0, 0, 0, 0};
+      } else {
+        const int r = v / (BN / 8), c = (v % (BN / 8)) * 8;
+        const int64_t k = k0 + r, n = n0 + c;
+        if (fast) rb[i] = *reinterpret_cast<const u32x4*>(g.B + k * g.ldb + n);
+        else if (k < kend && n < g.N) rb[i] = load8(g.B + k * g.ldb + n, n + 8 <= g.N, (int)(g.N - n));
+        else rb[i] = u32x4{0, 0, 0, 0};
+      }
+    }
+  };
+
+  auto store_tile = [&](int buf) {
+#pragma unroll
+    for (int i = 0; i < VA; ++i) {
+      const int v = tid + i * NT;
+      int r, c;
+      if constexpr (LA == LayB::KMajor) { r = v / (BK / 8); c = (v % (BK / 8)) * 8; }
+      else { r = v / (BM / 8); c = (v % (BM / 8)) * 8; }
+      *reinterpret_cast<u32x4*>(As(buf) + r * A_PITCH + c) = ra[i];
+    }
+#pragma unroll
+    for (int i = 0; i < VB; ++i) {
+      const int v = tid + i * NT;
+      int r, c;
+      if constexpr (LB == LayB::KMajor) { r = v / (BK / 8); c = (v % (BK / 8)) * 8; }
+      else { r = v / (BN / 8); c = (v % (BN / 8)) * 8; }
+      *reinterpret_cast<u32x4*>(Bs(buf) + r * B_PITCH + c) = rb[i];
+    }
+  };
+
+  // Operand fragment (8 k-values for this lane) from an LDS tile.
+  // KMajor: row `row`, k offset kofs.  MNMajor: k rows kofs.., column block col0.
+  auto frag_k = [&](const uint16_t* t, int pitch, int row, int kofs) -> bf16x8 {
+    return *reinterpret_cast<const bf16x8*>(t + row * pitch + kofs);
+  };
+  auto frag_mn = [&](const uint16_t* t, int pitch, int col0, int kofs) -> bf16x8 {
+    const int c = lane % 16;
+    typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
+    const uint16_t* p0 = t + (kofs + c / 4) * pitch + col0 + 4 * (c % 4);
+    const uint16_t* p1 = p0 + 4 * pitch;
+    bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)p0);
+    bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)p1);
+    return bf16x8{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+  };
+
+  f32x4 acc[FM][FN];
+#pragma unroll
+  for (int f = 0; f < FM; ++f)
+#pragma unroll
+    for (int h = 0; h < FN; ++h) acc[f][h] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  const bool do_rowsum = (g.rowsum != nullptr) && (tn == 0);
+  float rsum = 0.f;
+  const int kgrp = 8 * (lane / 16);
+
+  if (nk > 0) {
+    load_tile(kbeg);
+    store_tile(0);
+    __syncthreads();
+  }
+  for (int64_t kt = 0; kt < nk; ++kt) {
+    const int buf = (int)(kt & 1);
+    if (kt + 1 < nk) load_tile(kbeg + (kt + 1) * BK);
+    const uint16_t* as = As(buf);
+    const uint16_t* bs = Bs(buf);
+#pragma unroll
+    for (int ks = 0; ks < BK / 32; ++ks) {
+      bf16x8 af[FM], bfr[FN];
+#pragma unroll
+      for (int f = 0; f < FM; ++f) {
+        if constexpr (LA == LayB::KMajor) af[f] = frag_k(as, A_PITCH, WM * wm + 16 * f + lane % 16, 32 * ks + kgrp);
+        else af[f] = frag_mn(as, A_PITCH, WM * wm + 16 * f, 32 * ks + kgrp);
+      }
+#pragma unroll
+      for (int h = 0; h < FN; ++h) {
+        if constexpr (LB == LayB::KMajor) bfr[h] = frag_k(bs, B_PITCH, WN * wn + 16 * h + lane % 16, 32 * ks + kgrp);
+        else bfr[h] = frag_mn(bs, B_PITCH, WN * wn + 16 * h, 32 * ks + kgrp);
+      }
+#pragma unroll
+      for (int f = 0; f < FM; ++f)
+#pragma unroll
+        for (int h = 0; h < FN; ++h)
+          acc[f][h] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[f], bfr[h], acc[f][h], 0, 0, 0);
+    }
+    if (do_rowsum && tid < BM) {
+      static_assert(LA == LayB::MNMajor || EPI == EpiB::MaskBf || true, "");
+      if constexpr (LA == LayB::MNMajor) {
+#pragma unroll 8
+        for (int k = 0; k < BK; ++k) rsum += bf2f(as[k * A_PITCH + tid]);
+      }
+    }
+    if (kt + 1 < nk) store_tile(buf ^ 1);
+    __syncthreads();
+  }
+  if (do_rowsum && tid < BM && m0 + tid < g.M) g.rowsum[split * g.rowsum_stride + m0 + tid] = rsum;
+
+  // ---------------------------------------------------------------- epilogue
+  // Stage this wave's WM x WN accumulators (fp32) in LDS, pitch WN + 4.
+  constexpr int EP = WN + 4;
+  float* ep = reinterpret_cast<float*>(smem) + wid * (WM * EP);
+  // the main loop ended with a barrier, so the tile buffers are free
+#pragma unroll
+  for (int f = 0; f < FM; ++f)
+#pragma unroll
+    for (int h = 0; h < FN; ++h)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) ep[(16 * f + 4 * (lane / 16) + r) * EP + 16 * h + lane % 16] = acc[f][h][r];
+  __syncthreads();
+  float lsum = 0.f;
+  const int cg = lane % (WN / 4);                 // column group of 4
+  const int rl = lane / (WN / 4);                 // row within a pass
+  constexpr int ROWS_PER_PASS = 64 / (WN / 4);
+  const int64_t col = n0 + WN * wn + 4 * cg;
+  const bool cfull = col + 3 < g.N;
+  float bias4[4] = {0.f, 0.f, 0.f, 0.f};
+  if constexpr (EPI == EpiB::BiasF32 || EPI == EpiB::BiasReluBf || EPI == EpiB::MseBf) {
+    if (cfull) {
+      const f32x4 t = *reinterpret_cast<const f32x4*>(g.bias + col);
+      bias4[0] = t[0]; bias4[1] = t[1]; bias4[2] = t[2]; bias4[3] = t[3];
+    } else {
+      for (int c = 0; c < 4; ++c) bias4[c] = (col + c < g.N) ? g.bias[col + c] : 0.f;
+    }
+  }
+  for (int rr = rl; rr < WM; rr += ROWS_PER_PASS) {
+    const int64_t m = m0 + WM * wm + rr;
+    if (m >= g.M || col >= g.N) continue;
+    const f32x4 a4 = *reinterpret_cast<const f32x4*>(ep + rr * EP + 4 * cg);
+    float v[4] = {a4[0], a4[1], a4[2], a4[3]};
+    if constexpr (EPI == EpiB::StoreF32 || EPI == EpiB::SplitK || EPI == EpiB::BiasF32) {
+      if constexpr (EPI == EpiB::BiasF32)
+        for (int c = 0; c < 4; ++c) v[c] += bias4[c];
+      float* C = reinterpret_cast<float*>(g.C) + (EPI == EpiB::SplitK ? split * g.split_stride : 0) + m * g.ldc + col;
+      if (cfull) *reinterpret_cast<f32x4*>(C) = f32x4{v[0], v[1], v[2], v[3]};
+      else
+        for (int c = 0; c < 4; ++c)
+          if (col + c < g.N) C[c] = v[c];
+    } else {
+      if constexpr (EPI == EpiB::BiasReluBf) {
+        for (int c = 0; c < 4; ++c) { v[c] += bias4[c]; v[c] = v[c] > 0.f ? v[c] : 0.f; }
+      }
+      if constexpr (EPI == EpiB::MaskBf) {
+        const uint16_t* mp = g.mask + m * g.ldmask + col;
+        for (int c = 0; c < 4; ++c) {
+          const float mk = (col + c < g.N) ? bf2f(mp[c]) : 0.f;
+          v[c] = mk > 0.f ? v[c] : 0.f;
+        }
+      }
+      if constexpr (EPI == EpiB::MseBf) {
+        float t4[4];
+        const float* tp = g.target + m * g.ldt + col;
+        if (cfull) {
+          const f32x4 t = *reinterpret_cast<const f32x4*>(tp);
+          t4[0] = t[0]; t4[1] = t[1]; t4[2] = t[2]; t4[3] = t[3];
+        } else {
+          for (int c = 0; c < 4; ++c) t4[c] = (col + c < g.N) ? tp[c] : 0.f;
+        }
+        for (int c = 0; c < 4; ++c) {
+          const float r = (col + c < g.N) ? (v[c] + bias4[c]) - t4[c] : 0.f;
+          lsum += r * r;
+          v[c] = g.scale * r;
+        }
+      }
+      uint16_t* C = reinterpret_cast<uint16_t*>(g.C) + m * g.ldc + col;
+      if (cfull) {
+        *reinterpret_cast<u16x4*>(C) = u16x4{f2bf(v[0]), f2bf(v[1]), f2bf(v[2]), f2bf(v[3])};
+      } else {
+        for (int c = 0; c < 4; ++c)
+          if (col + c < g.N) C[c] = f2bf(v[c]);
+      }
+    }
+  }
+  if constexpr (EPI == EpiB::MseBf) {
+    const double ls = warp_sum((double)lsum);
+    if (lane == 0) s_red[wid] = ls;
+    __syncthreads();
+    if (tid == 0) g.loss_partials[blockIdx.y * gridDim.x + blockIdx.x] = ((s_red[0] + s_red[1]) + s_red[2]) + s_red[3];
+  }
+}
+
+template <int FM, int FN, LayB LA, LayB LB, EpiB EPI, int BK>
+hipError_t launch_gemm_bf16(const GemmBArgs& g, int64_t splits, hipStream_t stream) {
+  constexpr int BM = 32 * FM, BN = 32 * FN;
+  const int64_t tiles = ((g.M + BM - 1) / BM) * ((g.N + BN - 1) / BN);
+  hipLaunchKernelGGL((gemm_bf16_kernel<FM, FN, LA, LB, EPI, BK>), dim3((unsigned)tiles, (unsigned)splits), dim3(256), 0,
+                     stream, g);
+  return hipGetLastError();
+}
+
+template <int FM, int FN>
+constexpr int64_t gemm_bf16_tiles(int64_t M, int64_t N) {
+  return ((M + 32 * FM - 1) / (32 * FM)) * ((N + 32 * FN - 1) / (32 * FN));
+}
+
+}  // namespace ot

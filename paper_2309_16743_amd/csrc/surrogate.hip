@@ -12,6 +12,7 @@
 #include <vector>
 
 #include "common.h"
+#include "gemm_bf16.h"
 #include "gemm_f32.h"
 #include "philox.h"
 #include "surrogate.h"
@@ -48,7 +49,8 @@ __global__ void fill_kernel(float* __restrict__ p, int64_t n, float v) {
 __global__ void small_k_forward_kernel(const float* __restrict__ X, int64_t ldx,
                                        const float* __restrict__ W, int64_t ldw,
                                        const float* __restrict__ bias, float* __restrict__ out,
-                                       int64_t ldo, int64_t M, int64_t N, int64_t K, int relu) {
+                                       int64_t ldo, int64_t M, int64_t N, int64_t K, int relu,
+                                       uint16_t* __restrict__ out16) {
   const int64_t groups = (N + 3) / 4;
   const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (t >= M * groups) return;
@@ -64,7 +66,9 @@ __global__ void small_k_forward_kernel(const float* __restrict__ X, int64_t ldx,
     for (int k = 0; k < kMaxSmallK; ++k)
       if (k < K) acc = fmaf(x[k], W[n * ldw + k], acc);
     acc += bias[n];
-    out[m * ldo + n] = relu ? (acc > 0.f ? acc : 0.f) : acc;
+    const float y = relu ? (acc > 0.f ? acc : 0.f) : acc;
+    if (out16) out16[m * ldo + n] = f2bf(y);   // bf16 activations feed the bf16 GEMMs
+    else out[m * ldo + n] = y;
   }
 }
 
@@ -73,7 +77,8 @@ __global__ void small_k_forward_kernel(const float* __restrict__ X, int64_t ldx,
 // grid = (ceil(N / 64), P); 256 threads = 64 columns x 4 row groups.
 __global__ __launch_bounds__(256) void small_k_wgrad_partial_kernel(
     const float* __restrict__ dZ, int64_t ldz, const float* __restrict__ X, int64_t ldx,
-    float* __restrict__ part, int64_t M, int64_t N, int64_t K, int64_t rows_per_part) {
+    float* __restrict__ part, int64_t M, int64_t N, int64_t K, int64_t rows_per_part,
+    const uint16_t* __restrict__ dZ16) {
   __shared__ float red[4][64][kMaxSmallK + 1];
   const int cn = threadIdx.x % 64, grp = threadIdx.x / 64;
   const int64_t n = (int64_t)blockIdx.x * 64 + cn;
@@ -84,7 +89,7 @@ __global__ __launch_bounds__(256) void small_k_wgrad_partial_kernel(
   for (int k = 0; k <= kMaxSmallK; ++k) acc[k] = 0.f;
   if (n < N) {
     for (int64_t m = mb + grp; m < me; m += 4) {
-      const float d = dZ[m * ldz + n];
+      const float d = dZ16 ? bf2f(dZ16[m * ldz + n]) : dZ[m * ldz + n];
 #pragma unroll
       for (int k = 0; k < kMaxSmallK; ++k)
         if (k < K) acc[k] = fmaf(d, X[m * ldx + k], acc[k]);
@@ -136,8 +141,19 @@ __global__ void splitk_epilogue_kernel(const float* __restrict__ ws, int64_t spl
   float v[4];
   const int cnt = (int)min((int64_t)4, N - n);
   if (cnt == 4) {
-    f32x4 acc = *reinterpret_cast<const f32x4*>(ws + m * ldws + n);
-    for (int64_t p = 1; p < splits; ++p) acc += *reinterpret_cast<const f32x4*>(ws + p * split_stride + m * ldws + n);
+    const f32x4* src = reinterpret_cast<const f32x4*>(ws + m * ldws + n);
+    const int64_t st4 = split_stride / 4;
+    f32x4 acc = src[0];
+    int64_t p = 1;
+    // eight loads in flight, added in split order
+    for (; p + 8 <= splits; p += 8) {
+      f32x4 t[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) t[u] = src[(p + u) * st4];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) acc += t[u];
+    }
+    for (; p < splits; ++p) acc += src[p * st4];
     for (int c = 0; c < 4; ++c) v[c] = acc[c];
   } else {
     for (int c = 0; c < cnt; ++c) {
@@ -186,7 +202,7 @@ __global__ __launch_bounds__(256) void loss_finalize_kernel(const double* __rest
 __global__ __launch_bounds__(256) void adam_kernel(float* __restrict__ p, const float* __restrict__ g,
                                                    float* __restrict__ m, float* __restrict__ v,
                                                    int64_t n4, float lr, float b1, float b2, float eps,
-                                                   float c1, float c2) {
+                                                   float c1, float c2, uint16_t* __restrict__ pb) {
   const int64_t stride = (int64_t)gridDim.x * blockDim.x;
   for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n4; i += stride) {
     f32x4 pp = reinterpret_cast<f32x4*>(p)[i];
@@ -204,6 +220,60 @@ __global__ __launch_bounds__(256) void adam_kernel(float* __restrict__ p, const 
     reinterpret_cast<f32x4*>(p)[i] = pp;
     reinterpret_cast<f32x4*>(m)[i] = mm;
     reinterpret_cast<f32x4*>(v)[i] = vv;
+    if (pb)   // bf16 copy of the updated master weights
+      reinterpret_cast<u16x4*>(pb)[i] = u16x4{f2bf(pp[0]), f2bf(pp[1]), f2bf(pp[2]), f2bf(pp[3])};
+  }
+}
+
+}  // namespace ot
+
+namespace ot {
+
+// bf16 copy of fp32 values (round to nearest even).
+__global__ void to_bf16_kernel(const float* __restrict__ p, uint16_t* __restrict__ pb, int64_t n) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) pb[i] = f2bf(p[i]);
+}
+
+// Split-K epilogue with a bf16 result: out[m][n] = bf16(epi(sum_s ws[s][m][n])),
+// epi = + bias[n] then ReLU (if relu), or * (mask[m][n] > 0) with a bf16 mask.
+__global__ void splitk_epilogue_bf16_kernel(const float* __restrict__ ws, int64_t splits, int64_t split_stride,
+                                            int64_t M, int64_t N, int64_t ldws, const float* __restrict__ bias,
+                                            int relu, const uint16_t* __restrict__ mask, int64_t ldm,
+                                            uint16_t* __restrict__ out, int64_t ldo) {
+  const int64_t groups = (N + 3) / 4;
+  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (t >= M * groups) return;
+  const int64_t m = t / groups, n = (t % groups) * 4;
+  const int cnt = (int)min((int64_t)4, N - n);
+  float v[4] = {0.f, 0.f, 0.f, 0.f};
+  if (cnt == 4) {
+    const f32x4* src = reinterpret_cast<const f32x4*>(ws + m * ldws + n);
+    const int64_t st4 = split_stride / 4;
+    f32x4 acc = src[0];
+    int64_t p = 1;
+    for (; p + 8 <= splits; p += 8) {
+      f32x4 tt[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) tt[u] = src[(p + u) * st4];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) acc += tt[u];
+    }
+    for (; p < splits; ++p) acc += src[p * st4];
+    for (int c = 0; c < 4; ++c) v[c] = acc[c];
+  } else {
+    for (int c = 0; c < cnt; ++c) {
+      float a = ws[m * ldws + n + c];
+      for (int64_t p = 1; p < splits; ++p) a += ws[p * split_stride + m * ldws + n + c];
+      v[c] = a;
+    }
+  }
+  for (int c = 0; c < cnt; ++c) {
+    float x = v[c];
+    if (bias) x += bias[n + c];
+    if (relu) x = x > 0.f ? x : 0.f;
+    if (mask) x = bf2f(mask[m * ldm + n + c]) > 0.f ? x : 0.f;
+    out[m * ldo + n + c] = f2bf(x);
   }
 }
 
@@ -247,6 +317,10 @@ struct ot_surrogate {
   int64_t l1_part_elems = 0;
   float* loss_last = nullptr;
   ot::PhaseTimer timer;
+  // OT_BF16 only
+  uint16_t* pb = nullptr;                  // bf16 copy of the flat parameters
+  std::vector<uint16_t*> act16;            // act16[l] = bf16(A_l), l = 1..L-1
+  std::vector<uint16_t*> dz16;             // dz16[l] = bf16(dZ_l), l = 1..L (dz16[L] = dY)
 };
 
 namespace {
@@ -268,8 +342,12 @@ int salloc(void** p, size_t bytes) {
 void free_workspace(ot_surrogate* s) {
   for (float* p : s->act) (void)hipFree(p);
   for (float* p : s->dz) (void)hipFree(p);
+  for (uint16_t* p : s->act16) (void)hipFree(p);
+  for (uint16_t* p : s->dz16) (void)hipFree(p);
   s->act.assign(s->L + 1, nullptr);
   s->dz.assign(s->L + 1, nullptr);
+  s->act16.assign(s->L + 1, nullptr);
+  s->dz16.assign(s->L + 1, nullptr);
   (void)hipFree(s->splitws);
   (void)hipFree(s->rsws);
   (void)hipFree(s->loss_partials);
@@ -293,6 +371,7 @@ void free_surrogate(ot_surrogate* s) {
   (void)hipFree(s->m);
   (void)hipFree(s->v);
   (void)hipFree(s->loss_last);
+  (void)hipFree(s->pb);
   delete s;
 }
 
@@ -304,10 +383,17 @@ int ensure_workspace(ot_surrogate* s, int64_t rows) {
   free_workspace(s);
   const int L = s->L;
   int rc;
-  for (int l = 1; l < L; ++l)
-    if ((rc = salloc((void**)&s->act[l], (size_t)rows * s->ld[l] * sizeof(float)))) return rc;
-  for (int l = 1; l <= L; ++l)
-    if ((rc = salloc((void**)&s->dz[l], (size_t)rows * s->ld[l] * sizeof(float)))) return rc;
+  if (s->precision == OT_BF16) {
+    for (int l = 1; l < L; ++l)
+      if ((rc = salloc((void**)&s->act16[l], (size_t)rows * s->ld[l] * sizeof(uint16_t)))) return rc;
+    for (int l = 1; l <= L; ++l)
+      if ((rc = salloc((void**)&s->dz16[l], (size_t)rows * s->ld[l] * sizeof(uint16_t)))) return rc;
+  } else {
+    for (int l = 1; l < L; ++l)
+      if ((rc = salloc((void**)&s->act[l], (size_t)rows * s->ld[l] * sizeof(float)))) return rc;
+    for (int l = 1; l <= L; ++l)
+      if ((rc = salloc((void**)&s->dz[l], (size_t)rows * s->ld[l] * sizeof(float)))) return rc;
+  }
   // one loss partial per block of the output GEMM (64 x 64 tiles bound the count)
   s->n_partials_cap = ot::ceil_div(rows, 64) * ot::ceil_div(s->widths[L], 64) + 64;
   if ((rc = salloc((void**)&s->loss_partials, (size_t)s->n_partials_cap * sizeof(double)))) return rc;
@@ -444,7 +530,7 @@ int run_gemm(ot_surrogate* s, GemmArgs g, Epi epi, hipStream_t st, const char* w
   if (ph_reduce >= 0) tm.mark(st, ph_reduce, 0);
   const int64_t work = g.M * ot::ceil_div(g.N, 4);
   const bool bias = (epi == Epi::Bias || epi == Epi::BiasRelu);
-  hipLaunchKernelGGL(ot::splitk_epilogue_kernel, dim3((unsigned)ot::ceil_div(work, 256)), dim3(256), 0, st,
+  hipLaunchKernelGGL(ot::splitk_epilogue_kernel, dim3((unsigned)ot::ceil_div(work, 128)), dim3(128), 0, st,
                      s->splitws, p.splits, h.split_stride, g.M, g.N, ldws, bias ? g.bias : nullptr,
                      epi == Epi::BiasRelu ? 1 : 0, epi == Epi::Mask ? g.mask : nullptr, g.ldmask, g.C, g.ldc,
                      h.rowsum, h.rowsum_stride, g.rowsum);
@@ -470,7 +556,7 @@ int forward_hidden(ot_surrogate* s, const float* X, int64_t ldx, int64_t rows, h
     if (l == 1 && ly.in <= ot::kMaxSmallK) {
       const int64_t work = rows * ot::ceil_div(ly.out, 4);
       hipLaunchKernelGGL(ot::small_k_forward_kernel, dim3((unsigned)ot::ceil_div(work, 256)), dim3(256), 0, st, X,
-                         ldx, W, ly.ldw, b, s->act[1], s->ld[1], rows, ly.out, ly.in, 1);
+                         ldx, W, ly.ldw, b, s->act[1], s->ld[1], rows, ly.out, ly.in, 1, (uint16_t*)nullptr);
       OT_LAUNCHED("small_k_forward_kernel");
       continue;
     }
@@ -489,6 +575,251 @@ int forward_hidden(ot_surrogate* s, const float* X, int64_t ldx, int64_t rows, h
     if (rc) return rc;
   }
   return OT_OK;
+}
+
+// ------------------------------------------------------------------ bf16 path
+using ot::EpiB;
+using ot::GemmBArgs;
+using ot::LayB;
+
+// bf16 tiles: 128 x 128 (4 x 4 fragments per wave) and 64 x 64 (2 x 2), k tile 32.
+enum CfgB : int { kB128 = 0, kB64 = 1 };
+constexpr int kBK = 32;
+
+int64_t tiles_b(int cfg, int64_t M, int64_t N) {
+  return cfg == kB128 ? ot::gemm_bf16_tiles<4, 4>(M, N) : ot::gemm_bf16_tiles<2, 2>(M, N);
+}
+
+// 128 x 128 tiles when they give about two blocks per CU; long k ranges are
+// split over 128 x 128 tiles, shorter ones over 64 x 64 tiles.
+Plan make_plan_b(int64_t M, int64_t N, int64_t K, bool allow_split) {
+  constexpr int64_t kCUs = 256;
+  Plan p;
+  const int64_t t128 = tiles_b(kB128, M, N);
+  if (t128 >= 2 * kCUs - 32) {
+    p.cfg = kB128;
+  } else if (!allow_split) {
+    p.cfg = t128 >= kCUs - 16 ? kB128 : kB64;
+  } else {
+    p.cfg = K >= 4096 ? kB128 : kB64;
+    const int64_t t = tiles_b(p.cfg, M, N);
+    while (t * p.splits < 2 * kCUs - 32 && K / (2 * p.splits) >= 256) p.splits *= 2;
+    if (t * p.splits < kCUs)
+      while (t * p.splits < kCUs && K / (2 * p.splits) >= 64) p.splits *= 2;
+  }
+  p.k_chunk = ot::round_up(ot::ceil_div(K, p.splits), kBK);
+  p.splits = std::max<int64_t>(1, ot::ceil_div(K, p.k_chunk));
+  p.blocks = tiles_b(p.cfg, M, N) * p.splits;
+  return p;
+}
+
+template <LayB LA, LayB LB, EpiB E>
+hipError_t launch_cfg_b(int cfg, const GemmBArgs& g, int64_t splits, hipStream_t st) {
+  if (cfg == kB128) return ot::launch_gemm_bf16<4, 4, LA, LB, E, kBK>(g, splits, st);
+  return ot::launch_gemm_bf16<2, 2, LA, LB, E, kBK>(g, splits, st);
+}
+
+// C = epi(A B) on bf16 operands; split-K runs write fp32 partials and a
+// fixed-order pass applies the epilogue.
+template <LayB LA, LayB LB, EpiB E>
+int run_gemm_b(ot_surrogate* s, GemmBArgs g, hipStream_t st, const char* what, bool allow_split,
+               int ph_gemm = -1, int ph_reduce = -1, int64_t* blocks_out = nullptr) {
+  const Plan p = make_plan_b(g.M, g.N, g.K, allow_split && E != EpiB::MseBf);
+  if (blocks_out) *blocks_out = p.blocks;
+  ot::PhaseTimer& tm = s->timer;
+  if (p.splits == 1) {
+    g.k_chunk = p.k_chunk;
+    if (ph_gemm >= 0) tm.mark(st, ph_gemm, 0);
+    hipError_t e = launch_cfg_b<LA, LB, E>(p.cfg, g, 1, st);
+    if (e != hipSuccess) return ot::set_error(OT_E_HIP, "launch of %s GEMM failed: %s", what, hipGetErrorString(e));
+    if (ph_gemm >= 0) tm.mark(st, ph_gemm, 1);
+    return OT_OK;
+  }
+  if constexpr (E == EpiB::MseBf) {
+    return ot::set_error(OT_E_STATE, "%s: the MSE epilogue cannot be split", what);
+  } else {
+    const int64_t ldws = ot::round_up(g.N, 4);
+    int rc = ensure_split_ws(s, p.splits * g.M * ldws, g.rowsum ? p.splits * g.M : 0);
+    if (rc) return rc;
+    GemmBArgs h = g;
+    h.C = s->splitws;
+    h.ldc = ldws;
+    h.split_stride = g.M * ldws;
+    h.k_chunk = p.k_chunk;
+    h.rowsum = g.rowsum ? s->rsws : nullptr;
+    h.rowsum_stride = g.M;
+    if (ph_gemm >= 0) tm.mark(st, ph_gemm, 0);
+    hipError_t e = launch_cfg_b<LA, LB, EpiB::SplitK>(p.cfg, h, p.splits, st);
+    if (e != hipSuccess) return ot::set_error(OT_E_HIP, "launch of %s GEMM failed: %s", what, hipGetErrorString(e));
+    if (ph_gemm >= 0) tm.mark(st, ph_gemm, 1);
+    if (ph_reduce >= 0) tm.mark(st, ph_reduce, 0);
+    const int64_t work = g.M * ot::ceil_div(g.N, 4);
+    if constexpr (E == EpiB::StoreF32 || E == EpiB::BiasF32) {
+      hipLaunchKernelGGL(ot::splitk_epilogue_kernel, dim3((unsigned)ot::ceil_div(work, 128)), dim3(128), 0, st,
+                         s->splitws, p.splits, h.split_stride, g.M, g.N, ldws,
+                         E == EpiB::BiasF32 ? g.bias : nullptr, 0, (const float*)nullptr, (int64_t)0,
+                         reinterpret_cast<float*>(g.C), g.ldc, h.rowsum, h.rowsum_stride, g.rowsum);
+      OT_LAUNCHED("splitk_epilogue_kernel");
+    } else {
+      hipLaunchKernelGGL(ot::splitk_epilogue_bf16_kernel, dim3((unsigned)ot::ceil_div(work, 128)), dim3(128), 0, st,
+                         s->splitws, p.splits, h.split_stride, g.M, g.N, ldws,
+                         E == EpiB::BiasReluBf ? g.bias : nullptr, E == EpiB::BiasReluBf ? 1 : 0,
+                         E == EpiB::MaskBf ? g.mask : nullptr, g.ldmask, reinterpret_cast<uint16_t*>(g.C), g.ldc);
+      OT_LAUNCHED("splitk_epilogue_bf16_kernel");
+    }
+    if (ph_reduce >= 0) tm.mark(st, ph_reduce, 1);
+    return OT_OK;
+  }
+}
+
+GemmBArgs bargs0() {
+  GemmBArgs g{};
+  return g;
+}
+
+// bf16 forward of layers 1..L-1 into act16[]: layer 1 in fp32 (K = input width).
+int forward_hidden_bf16(ot_surrogate* s, const float* X, int64_t ldx, int64_t rows, hipStream_t st) {
+  const int L = s->L;
+  for (int l = 1; l < L; ++l) {
+    const Layer& ly = s->layers[l - 1];
+    if (l == 1) {
+      const int64_t work = rows * ot::ceil_div(ly.out, 4);
+      hipLaunchKernelGGL(ot::small_k_forward_kernel, dim3((unsigned)ot::ceil_div(work, 256)), dim3(256), 0, st, X,
+                         ldx, s->params + ly.w_off, ly.ldw, s->params + ly.b_off, (float*)nullptr, s->ld[1], rows,
+                         ly.out, ly.in, 1, s->act16[1]);
+      OT_LAUNCHED("small_k_forward_kernel");
+      continue;
+    }
+    GemmBArgs g = bargs0();
+    g.A = s->act16[l - 1];
+    g.lda = s->ld[l - 1];
+    g.B = s->pb + ly.w_off;
+    g.ldb = ly.ldw;
+    g.C = s->act16[l];
+    g.ldc = s->ld[l];
+    g.M = rows;
+    g.N = ly.out;
+    g.K = ly.in;
+    g.bias = s->params + ly.b_off;
+    int rc = run_gemm_b<LayB::KMajor, LayB::KMajor, EpiB::BiasReluBf>(s, g, st, "bf16 hidden forward", true);
+    if (rc) return rc;
+  }
+  return OT_OK;
+}
+
+int train_step_bf16(ot_surrogate* s, const float* x, int64_t ldx, const float* u, int64_t ldu, int64_t b,
+                    hipStream_t st, float* loss_dev) {
+  const int L = s->L;
+  const int64_t D = s->widths[L];
+  ot::PhaseTimer& tm = s->timer;
+  int rc;
+  tm.mark(st, OT_PH_FWD_HIDDEN, 0);
+  if ((rc = forward_hidden_bf16(s, x, ldx, b, st))) return rc;
+  tm.mark(st, OT_PH_FWD_HIDDEN, 1);
+  const Layer& lo = s->layers[L - 1];
+  int64_t n_partials = 0;
+  {
+    GemmBArgs g = bargs0();
+    g.A = s->act16[L - 1];
+    g.lda = s->ld[L - 1];
+    g.B = s->pb + lo.w_off;
+    g.ldb = lo.ldw;
+    g.C = s->dz16[L];
+    g.ldc = s->ld[L];
+    g.M = b;
+    g.N = D;
+    g.K = lo.in;
+    g.bias = s->params + lo.b_off;
+    g.target = u;
+    g.ldt = ldu;
+    g.scale = (float)(2.0 / ((double)b * (double)D));
+    g.loss_partials = s->loss_partials;
+    n_partials = make_plan_b(g.M, g.N, g.K, false).blocks;
+    if (n_partials > s->n_partials_cap) return ot::set_error(OT_E_STATE, "loss partial buffer too small");
+    if ((rc = run_gemm_b<LayB::KMajor, LayB::KMajor, EpiB::MseBf>(s, g, st, "bf16 output forward+MSE", false,
+                                                                  OT_PH_FWD_OUTPUT)))
+      return rc;
+  }
+  tm.mark(st, OT_PH_LOSS, 0);
+  hipLaunchKernelGGL(ot::loss_finalize_kernel, dim3(1), dim3(256), 0, st, s->loss_partials, n_partials,
+                     1.0 / ((double)b * (double)D), loss_dev, s->loss_last);
+  OT_LAUNCHED("loss_finalize_kernel");
+  tm.mark(st, OT_PH_LOSS, 1);
+
+  for (int l = L; l >= 1; --l) {
+    if (l == L - 1) tm.mark(st, OT_PH_BWD_HIDDEN, 0);
+    const Layer& ly = s->layers[l - 1];
+    float* dW = s->grads + ly.w_off;
+    float* db = s->grads + ly.b_off;
+    if (l == 1) {
+      const int64_t rows_per = ot::ceil_div(b, kL1Parts);
+      const int64_t P = ot::ceil_div(b, rows_per);
+      hipLaunchKernelGGL(ot::small_k_wgrad_partial_kernel, dim3((unsigned)ot::ceil_div(ly.out, 64), (unsigned)P),
+                         dim3(256), 0, st, (const float*)nullptr, s->ld[1], x, ldx, s->l1_part, b, ly.out, ly.in,
+                         rows_per, s->dz16[1]);
+      OT_LAUNCHED("small_k_wgrad_partial_kernel");
+      const int64_t n = ly.out * (ly.in + 1);
+      hipLaunchKernelGGL(ot::small_k_wgrad_reduce_kernel, dim3((unsigned)ot::ceil_div(n, 256)), dim3(256), 0, st,
+                         s->l1_part, P, ly.out, ly.in, dW, ly.ldw, db);
+      OT_LAUNCHED("small_k_wgrad_reduce_kernel");
+      break;
+    }
+    const int ph_w = (l == L) ? OT_PH_WGRAD_OUTPUT : -1;
+    {
+      GemmBArgs g = bargs0();
+      g.A = s->dz16[l];
+      g.lda = s->ld[l];
+      g.B = s->act16[l - 1];
+      g.ldb = s->ld[l - 1];
+      g.C = dW;
+      g.ldc = ly.ldw;
+      g.M = ly.out;
+      g.N = ly.in;
+      g.K = b;
+      g.rowsum = db;
+      if ((rc = run_gemm_b<LayB::MNMajor, LayB::MNMajor, EpiB::StoreF32>(s, g, st, "bf16 weight gradient", true, ph_w,
+                                                                         ph_w >= 0 ? OT_PH_WGRAD_REDUCE : -1)))
+        return rc;
+    }
+    GemmBArgs g = bargs0();
+    g.A = s->dz16[l];
+    g.lda = s->ld[l];
+    g.B = s->pb + ly.w_off;
+    g.ldb = ly.ldw;
+    g.C = s->dz16[l - 1];
+    g.ldc = s->ld[l - 1];
+    g.M = b;
+    g.N = ly.in;
+    g.K = ly.out;
+    g.mask = s->act16[l - 1];
+    g.ldmask = s->ld[l - 1];
+    if ((rc = run_gemm_b<LayB::KMajor, LayB::MNMajor, EpiB::MaskBf>(s, g, st, "bf16 input gradient", true,
+                                                                    l == L ? OT_PH_IGRAD_OUTPUT : -1,
+                                                                    l == L ? OT_PH_IGRAD_REDUCE : -1)))
+      return rc;
+  }
+  tm.mark(st, OT_PH_BWD_HIDDEN, 1);
+  return OT_OK;
+}
+
+int predict_bf16(ot_surrogate* s, const float* xr, int64_t ldx, int64_t rows, float* yr, int64_t ldy,
+                 hipStream_t st) {
+  int rc = forward_hidden_bf16(s, xr, ldx, rows, st);
+  if (rc) return rc;
+  const int L = s->L;
+  const Layer& lo = s->layers[L - 1];
+  GemmBArgs g = bargs0();
+  g.A = s->act16[L - 1];
+  g.lda = s->ld[L - 1];
+  g.B = s->pb + lo.w_off;
+  g.ldb = lo.ldw;
+  g.C = yr;
+  g.ldc = ldy;
+  g.M = rows;
+  g.N = s->widths[L];
+  g.K = lo.in;
+  g.bias = s->params + lo.b_off;
+  return run_gemm_b<LayB::KMajor, LayB::KMajor, EpiB::BiasF32>(s, g, st, "bf16 output forward", true);
 }
 
 int check_input(ot_surrogate* s, const float* X, int64_t ldx) {
@@ -511,7 +842,11 @@ extern "C" int surrogate_create(ot_surrogate** out, const int64_t* widths, int32
   OT_REQUIRE(n_widths >= 2 && n_widths <= 16, "surrogate_create: n_widths outside [2, 16]");
   for (int i = 0; i < n_widths; ++i)
     OT_REQUIRE(widths[i] >= 1 && widths[i] <= (1LL << 26), "surrogate_create: width %d outside [1, 2^26]", i);
-  OT_REQUIRE(precision == OT_FP32, "surrogate_create: precision %d not available", (int)precision);
+  OT_REQUIRE(precision == OT_FP32 || precision == OT_BF16, "surrogate_create: unknown precision %d",
+             (int)precision);
+  if (precision == OT_BF16)
+    OT_REQUIRE(n_widths >= 3 && widths[0] <= 16,
+               "surrogate_create: bf16 nets need >= 2 layers and an input width <= 16 (first layer runs in fp32)");
   OT_REQUIRE(flags == 0, "surrogate_create: flags must be 0");
   OT_REQUIRE(max_batch >= 1 && max_batch <= (1LL << 20), "surrogate_create: max_batch outside [1, 2^20]");
   OT_REQUIRE(lr >= 0.f && beta1 >= 0.f && beta1 < 1.f && beta2 >= 0.f && beta2 < 1.f && eps > 0.f,
@@ -525,13 +860,13 @@ extern "C" int surrogate_create(ot_surrogate** out, const int64_t* widths, int32
   s->beta2 = beta2;
   s->eps = eps;
   s->ld.resize(n_widths);
-  for (int i = 0; i < n_widths; ++i) s->ld[i] = ot::round_up(widths[i], 4);
+  for (int i = 0; i < n_widths; ++i) s->ld[i] = ot::round_up(widths[i], 8);
   int64_t off = 0;
   for (int l = 0; l < s->L; ++l) {
     Layer ly;
     ly.in = widths[l];
     ly.out = widths[l + 1];
-    ly.ldw = ot::round_up(ly.in, 4);
+    ly.ldw = ot::round_up(ly.in, 8);
     ly.w_off = off;
     off = ot::round_up(off + ly.out * ly.ldw, 64);
     ly.b_off = off;
@@ -541,6 +876,8 @@ extern "C" int surrogate_create(ot_surrogate** out, const int64_t* widths, int32
   s->n_flat = off;
   s->act.assign(s->L + 1, nullptr);
   s->dz.assign(s->L + 1, nullptr);
+  s->act16.assign(s->L + 1, nullptr);
+  s->dz16.assign(s->L + 1, nullptr);
   auto fail = [&](int code) {
     free_surrogate(s);
     return code;
@@ -563,6 +900,10 @@ extern "C" int surrogate_create(ot_surrogate** out, const int64_t* widths, int32
     hipLaunchKernelGGL(ot::init_layer_kernel, dim3((unsigned)ot::ceil_div(n, 256)), dim3(256), 0, 0,
                        s->params + ly.w_off, s->params + ly.b_off, ly.in, ly.out, ly.ldw, seed, (uint64_t)l,
                        1.0 / std::sqrt((double)ly.in));
+  }
+  if (precision == OT_BF16) {
+    if ((rc = salloc((void**)&s->pb, (size_t)s->n_flat * sizeof(uint16_t)))) return fail(rc);
+    hipLaunchKernelGGL(ot::to_bf16_kernel, dim3(fb), dim3(256), 0, 0, s->params, s->pb, s->n_flat);
   }
   if (hipGetLastError() != hipSuccess) return fail(ot::set_error(OT_E_HIP, "initialisation launch failed"));
   if ((rc = ensure_workspace(s, max_batch))) return fail(rc);
@@ -601,6 +942,12 @@ extern "C" int surrogate_set_params(ot_surrogate* s, int32_t layer, const float*
     OT_HIP(hipMemcpy2D(s->params + ly.w_off, ly.ldw * sizeof(float), W_host, ly.in * sizeof(float),
                        ly.in * sizeof(float), ly.out, hipMemcpyHostToDevice));
   if (b_host) OT_HIP(hipMemcpy(s->params + ly.b_off, b_host, ly.out * sizeof(float), hipMemcpyHostToDevice));
+  if (s->pb) {
+    hipLaunchKernelGGL(ot::to_bf16_kernel, dim3((unsigned)ot::ceil_div(s->n_flat, 256)), dim3(256), 0, 0, s->params,
+                       s->pb, s->n_flat);
+    OT_LAUNCHED("to_bf16_kernel");
+    OT_HIP(hipDeviceSynchronize());
+  }
   return OT_OK;
 }
 
@@ -635,6 +982,23 @@ extern "C" int surrogate_set_lr(ot_surrogate* s, float lr) {
   return OT_OK;
 }
 
+// Adam over every parameter (and the bf16 weight copy in OT_BF16 mode).
+static int adam_step(ot_surrogate* s, hipStream_t st) {
+  ot::PhaseTimer& tm = s->timer;
+  s->t += 1;
+  const double c1 = 1.0 - std::pow((double)s->beta1, (double)s->t);
+  const double c2 = 1.0 - std::pow((double)s->beta2, (double)s->t);
+  const int64_t n4 = s->n_flat / 4;
+  const int64_t blocks = std::min<int64_t>(ot::ceil_div(n4, 256), 8192);
+  tm.mark(st, OT_PH_ADAM, 0);
+  hipLaunchKernelGGL(ot::adam_kernel, dim3((unsigned)blocks), dim3(256), 0, st, s->params, s->grads, s->m, s->v, n4,
+                     s->lr, s->beta1, s->beta2, s->eps, (float)c1, (float)c2, s->pb);
+  OT_LAUNCHED("adam_kernel");
+  tm.mark(st, OT_PH_ADAM, 1);
+  tm.next_call();
+  return OT_OK;
+}
+
 extern "C" int surrogate_train_step(ot_surrogate* s, const float* x, int64_t ldx, const float* u, int64_t ldu,
                                     int64_t b, void* stream, float* loss_dev) {
   ot::clear_error();
@@ -649,6 +1013,10 @@ extern "C" int surrogate_train_step(ot_surrogate* s, const float* x, int64_t ldx
   if ((rc = ensure_workspace(s, b))) return rc;
   hipStream_t st = static_cast<hipStream_t>(stream);
 
+  if (s->precision == OT_BF16) {
+    if ((rc = train_step_bf16(s, x, ldx, u, ldu, b, st, loss_dev))) return rc;
+    return adam_step(s, st);
+  }
   ot::PhaseTimer& tm = s->timer;
   // ---- forward: hidden layers
   tm.mark(st, OT_PH_FWD_HIDDEN, 0);
@@ -697,17 +1065,19 @@ extern "C" int surrogate_train_step(ot_surrogate* s, const float* x, int64_t ldx
     float* dW = s->grads + ly.w_off;
     float* db = s->grads + ly.b_off;
     // weight and bias gradient: dW = dZ^T A_in, db = column sums of dZ
-    if (ph_w >= 0) tm.mark(st, ph_w, 0);
     if (l == 1 && ly.in <= ot::kMaxSmallK) {
+      if (ph_w >= 0) tm.mark(st, ph_w, 0);
       const int64_t rows_per = ot::ceil_div(b, kL1Parts);
       const int64_t P = ot::ceil_div(b, rows_per);
       hipLaunchKernelGGL(ot::small_k_wgrad_partial_kernel, dim3((unsigned)ot::ceil_div(ly.out, 64), (unsigned)P),
-                         dim3(256), 0, st, s->dz[1], s->ld[1], x, ldx, s->l1_part, b, ly.out, ly.in, rows_per);
+                         dim3(256), 0, st, s->dz[1], s->ld[1], x, ldx, s->l1_part, b, ly.out, ly.in, rows_per,
+                         (const uint16_t*)nullptr);
       OT_LAUNCHED("small_k_wgrad_partial_kernel");
       const int64_t n = ly.out * (ly.in + 1);
       hipLaunchKernelGGL(ot::small_k_wgrad_reduce_kernel, dim3((unsigned)ot::ceil_div(n, 256)), dim3(256), 0, st,
                          s->l1_part, P, ly.out, ly.in, dW, ly.ldw, db);
       OT_LAUNCHED("small_k_wgrad_reduce_kernel");
+      if (ph_w >= 0) tm.mark(st, ph_w, 1);
     } else {
       GemmArgs g = args0();
       g.A = s->dz[l];
@@ -720,9 +1090,10 @@ extern "C" int surrogate_train_step(ot_surrogate* s, const float* x, int64_t ldx
       g.N = ly.in;
       g.K = b;
       g.rowsum = db;
-      if ((rc = run_gemm<Lay::MNMajor, Lay::MNMajor>(s, g, Epi::Store, st, "weight gradient", true))) return rc;
+      if ((rc = run_gemm<Lay::MNMajor, Lay::MNMajor>(s, g, Epi::Store, st, "weight gradient", true, ph_w,
+                                                     ph_w >= 0 ? OT_PH_WGRAD_REDUCE : -1)))
+        return rc;
     }
-    if (ph_w >= 0) tm.mark(st, ph_w, 1);
     if (l == 1) break;
     // input gradient dA_{l-1} = dZ_l W_l, then the ReLU mask of layer l-1
     GemmArgs g = args0();
@@ -744,19 +1115,7 @@ extern "C" int surrogate_train_step(ot_surrogate* s, const float* x, int64_t ldx
   }
   if (L >= 2) tm.mark(st, OT_PH_BWD_HIDDEN, 1);
 
-  // ---- Adam over every parameter
-  s->t += 1;
-  const double c1 = 1.0 - std::pow((double)s->beta1, (double)s->t);
-  const double c2 = 1.0 - std::pow((double)s->beta2, (double)s->t);
-  const int64_t n4 = s->n_flat / 4;
-  const int64_t blocks = std::min<int64_t>(ot::ceil_div(n4, 256), 8192);
-  tm.mark(st, OT_PH_ADAM, 0);
-  hipLaunchKernelGGL(ot::adam_kernel, dim3((unsigned)blocks), dim3(256), 0, st, s->params, s->grads, s->m, s->v, n4,
-                     s->lr, s->beta1, s->beta2, s->eps, (float)c1, (float)c2);
-  OT_LAUNCHED("adam_kernel");
-  tm.mark(st, OT_PH_ADAM, 1);
-  tm.next_call();
-  return OT_OK;
+  return adam_step(s, st);
 }
 
 extern "C" int surrogate_timing_begin(ot_surrogate* s, uint32_t phase_mask, int64_t max_steps) {
@@ -792,6 +1151,10 @@ extern "C" int surrogate_predict(ot_surrogate* s, const float* x, int64_t ldx, i
   for (int64_t r0 = 0; r0 < n; r0 += chunk) {
     const int64_t rows = std::min(chunk, n - r0);
     const float* xr = x + r0 * ldx;
+    if (s->precision == OT_BF16) {
+      if ((rc = predict_bf16(s, xr, ldx, rows, y + r0 * ldy, ldy, st))) return rc;
+      continue;
+    }
     if ((rc = forward_hidden(s, xr, ldx, rows, st))) return rc;
     GemmArgs g = args0();
     g.A = (L == 1) ? xr : s->act[L - 1];
