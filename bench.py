@@ -2,20 +2,29 @@
 """Online surrogate-training throughput on one MI355X.
 
 One step is one pass of the whole hot path on one batch: a put of one chunk of
-streamed samples into the GPU reservoir (eviction of seen samples once full),
-a batch draw with replacement and its gather, and one train step of the MLP
-surrogate (forward, fused MSE, backward, Adam).  Workload: 100x100 heat fields
-from an FTCS solver, 1000 simulations x 100 steps, MLP 6-256-256-10000 fp32,
-batch 1024, reservoir of 100,000 samples (threshold 16,667), chunks of the
-100 concurrent simulations' current time step.  The whole ensemble is first
-streamed through the schedule (untimed), then the stream wraps around so
-every timed put replaces seen samples.
+streamed samples into the GPU reservoir (replacing seen samples once full), a
+batch draw with replacement and its gather, and one train step of the MLP
+surrogate (forward, fused MSE, backward, Adam).
+
+Default workload (--config heat-100x100): 100x100 heat fields from an FTCS
+solver, 1000 simulations x 100 steps, MLP 6-256-256-10000 fp32, batch 1024,
+reservoir of 100,000 samples (threshold 16,667), chunks of the 100 concurrent
+simulations' current time step.  The whole ensemble is first streamed through
+the schedule (untimed), then the stream wraps around so every timed put
+replaces seen samples.
+
+--config sine-1000x1000 / deep-sine-1000x1000: 1000x1000 fields (smooth
+sine-mode stand-ins for heat solutions, generated on the GPU), bf16 GEMMs with
+fp32 master weights and Adam, batch 512 / 1024, reservoirs of 20,000 / 30,000
+samples (80 / 120 GB).  The reservoir is filled with generated chunks
+(untimed); timed puts cycle through a pool of pre-generated chunks of 64
+samples.
 
 Prints one JSON line.  `value` is samples processed per second by the train
-step (batch size x steps / time), measured with HIP events on the work stream
-over the timed steps.  `roofline` reports the dominant kernel's algorithmic
-rate against MI355X's datasheet peak, from HIP events around that kernel in
-the same timed region.  `cpu_baseline` times the plain fp64 CPU oracle on a
+step (batch size x steps / time), from HIP events on the work stream over the
+timed steps.  `roofline` reports the dominant kernel's algorithmic rate
+against MI355X's datasheet peak, from HIP events around that kernel inside the
+same timed region.  `cpu_baseline` times the plain fp64 CPU oracle on a
 bounded sample of the same workload on this host.
 """
 from __future__ import annotations
@@ -33,16 +42,18 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 PEAK_FP32_MFMA = 157.3e12      # MI355X dense fp32 matrix peak, FLOP/s
+PEAK_BF16_MFMA = 2.5e15        # MI355X dense bf16 matrix peak, FLOP/s
 PEAK_HBM = 8.0e12              # MI355X HBM3E, bytes/s
+METRIC = "surrogate train samples/s at 1 MI355X; MFMA util of output layer; reservoir GB/s"
 
 
 def parse_args():
     p = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     p.add_argument("--gpus", type=int, default=1)
-    p.add_argument("--steps", type=int, default=2000)
-    p.add_argument("--warmup", type=int, default=50)
+    p.add_argument("--steps", type=int, default=None, help="timed steps (default 2000 fp32, 100 bf16)")
+    p.add_argument("--warmup", type=int, default=None, help="untimed steps before timing (default 50 / 5)")
     p.add_argument("--config", default="heat-100x100")
-    p.add_argument("--profile-steps", type=int, default=200,
+    p.add_argument("--profile-steps", type=int, default=None,
                    help="steps of the per-kernel breakdown pass (all phases timed)")
     p.add_argument("--cpu-seconds", type=float, default=15.0,
                    help="target duration of the CPU-oracle baseline sample (0 disables it)")
@@ -55,33 +66,59 @@ def gemm_flops(w) -> float:
     return 2.0 * w.batch * w.widths[-2] * w.widths[-1]
 
 
+def adam_bytes(w) -> float:
+    """Algorithmic bytes of one Adam launch: read p, g, m, v; write p, m, v
+    (+ the bf16 weight copy in mixed precision)."""
+    return (28.0 + (2.0 if w.precision == "bf16" else 0.0)) * w.n_params()
+
+
+def gather_bytes(w) -> float:
+    return 2.0 * w.batch * (w.widths[-1] + w.widths[0]) * 4
+
+
+def put_bytes(w) -> float:
+    return 2.0 * w.wave * (w.widths[-1] + w.widths[0]) * 4
+
+
 def kernel_table(w, phases_ms: dict, res_ms: dict) -> dict:
     """Average duration and algorithmic rate of each timed phase."""
+    peak_mfma = PEAK_BF16_MFMA if w.precision == "bf16" else PEAK_FP32_MFMA
     out = {}
-    D, B, H = w.widths[-1], w.batch, w.widths[-2]
-    n_params = w.n_params()
     for name, (ms, n) in phases_ms.items():
         avg = ms / max(n, 1)
         row = {"avg_us": round(avg * 1e3, 2), "launches": n}
         if name in ("fwd_output", "wgrad_output", "igrad_output"):
             rate = gemm_flops(w) / (avg * 1e-3)
-            row.update(achieved_tflops=round(rate / 1e12, 2), frac_fp32_mfma=round(rate / PEAK_FP32_MFMA, 4))
+            row.update(achieved_tflops=round(rate / 1e12, 2), frac_mfma=round(rate / peak_mfma, 4))
         if name == "adam":
-            rate = 28.0 * n_params / (avg * 1e-3)
+            rate = adam_bytes(w) / (avg * 1e-3)
             row.update(achieved_gbs=round(rate / 1e9, 1), frac_hbm=round(rate / PEAK_HBM, 4))
         out[name] = row
-    x_dim = w.widths[0]
     for name, (ms, n) in res_ms.items():
         avg = ms / max(n, 1)
         row = {"avg_us": round(avg * 1e3, 2), "launches": n}
-        if name == "gather":
-            byts = 2.0 * B * (D + x_dim) * 4
-            row.update(achieved_gbs=round(byts / (avg * 1e-3) / 1e9, 1), frac_hbm=round(byts / (avg * 1e-3) / PEAK_HBM, 4))
-        if name == "put_copy":
-            byts = 2.0 * w.wave * (D + x_dim) * 4
-            row.update(achieved_gbs=round(byts / (avg * 1e-3) / 1e9, 1), frac_hbm=round(byts / (avg * 1e-3) / PEAK_HBM, 4))
+        byts = {"gather": gather_bytes(w), "put_copy": put_bytes(w)}.get(name)
+        if byts:
+            rate = byts / (avg * 1e-3)
+            row.update(achieved_gbs=round(rate / 1e9, 1), frac_hbm=round(rate / PEAK_HBM, 4))
         out["reservoir_" + name] = row
     return out
+
+
+def roofline_entry(w, phase: str, avg_s: float) -> dict:
+    """Roofline object for the dominant kernel (per-launch algorithmic work / duration)."""
+    if phase in ("fwd_output", "wgrad_output", "igrad_output"):
+        peak = PEAK_BF16_MFMA if w.precision == "bf16" else PEAK_FP32_MFMA
+        work = gemm_flops(w)
+        return {"bound": "mfma", "kernel": f"gemm_{w.precision} ({phase})",
+                "achieved": round(work / avg_s / 1e12, 2), "peak": peak / 1e12, "unit": "TFLOP/s",
+                "frac": round(work / avg_s / peak, 4), "traffic": None, "per_launch_flops": work,
+                "avg_us": round(avg_s * 1e6, 2)}
+    work = {"adam": adam_bytes(w), "gather": gather_bytes(w)}[phase]
+    return {"bound": "hbm", "kernel": ("adam_kernel" if phase == "adam" else "gather_kernel"),
+            "achieved": round(work / avg_s / 1e9, 1), "peak": PEAK_HBM / 1e9, "unit": "GB/s",
+            "frac": round(work / avg_s / PEAK_HBM, 4), "traffic": None, "per_launch_bytes": work,
+            "avg_us": round(avg_s * 1e6, 2)}
 
 
 def cpu_baseline(w, inputs, fields, seconds: float) -> dict:
@@ -121,32 +158,113 @@ def cpu_baseline(w, inputs, fields, seconds: float) -> dict:
             "ms_per_step": round(dt / steps * 1e3, 1)}
 
 
-def main():
-    args = parse_args()
-    world = int(os.environ.get("WORLD_SIZE", "1"))
-    if args.gpus != 1 or world != 1:
-        print(f"bench.py measures one GPU only; --gpus {args.gpus} (WORLD_SIZE {world}) is not supported: "
-              "this build has no multi-GPU path.", file=sys.stderr)
-        sys.exit(2)
+def cpu_baseline_scaled(w, seconds: float) -> dict:
+    """The fp64 oracle's train step at the bf16 workload's hidden widths but a
+    1/f slice of the output layer (the full 1M-wide output layer does not fit
+    a CPU time budget), timed and scaled by f; reservoir ops excluded."""
+    from oracle import mlp
+    try:
+        import threadpoolctl
+        blas_threads = max((b.get("num_threads", 1) for b in threadpoolctl.threadpool_info()), default=1)
+    except Exception:  # pragma: no cover
+        blas_threads = 1
+    f = 200
+    widths = list(w.widths[:-1]) + [w.widths[-1] // f]
+    rng = np.random.default_rng(0)
+    params = mlp.init_params(widths, w.init_seed)
+    X = np.concatenate([rng.uniform(100, 500, (w.batch, 5)), rng.uniform(0.01, 1.0, (w.batch, 1))], axis=1)
+    U = rng.uniform(100, 500, (w.batch, widths[-1]))
+    opt = mlp.Adam(lr=w.lr)
+    steps = 0
+    t0 = time.perf_counter()
+    while steps < 1 or time.perf_counter() - t0 < seconds:
+        loss, grads = mlp.loss_and_grads(params, X, U, bf16=True)
+        params = opt.step(params, grads)
+        steps += 1
+    dt = (time.perf_counter() - t0) / steps * f
+    return {"value": round(w.batch / dt, 3), "unit": "samples/s", "cores": blas_threads, "kind": "oracle",
+            "sample": f"{steps} fp64 bf16-rounding train steps of {'-'.join(map(str, widths))} "
+                      f"(output layer 1/{f} of {w.widths[-1]}), step time scaled by {f}; reservoir ops excluded",
+            "ms_per_step": round(dt * 1e3, 1)}
 
+
+def timed_region(tr, w, K, profile_steps, stream, wrap_put):
+    """Breakdown pass (all phases), then K timed steps with events around the
+    dominant kernel and the gather."""
     import torch
 
-    from fixtures import configs, heat
     from paper_2309_16743_amd._abi import SURROGATE_PHASES
-    from paper_2309_16743_amd.online import OnlineTrainer
+    kp = max(profile_steps, 1)
+    tr.sur.timing_begin(list(SURROGATE_PHASES), kp)
+    tr.res.timing_begin(["put_assign", "put_copy", "select", "gather"], 2 * kp)
+    for _ in range(kp):
+        wrap_put()
+        assert tr.sample_and_train()
+    breakdown = kernel_table(w, tr.sur.timing_end(), tr.res.timing_end())
+    candidates = ("fwd_output", "wgrad_output", "igrad_output", "adam", "reservoir_gather")
+    dominant = max(candidates, key=lambda p: breakdown[p]["avg_us"])
+    dom_phase = "gather" if dominant == "reservoir_gather" else dominant
 
-    if args.config not in configs.ALL or configs.ALL[args.config].precision != "fp32":
-        print(f"unsupported config {args.config}", file=sys.stderr)
-        sys.exit(2)
-    w = configs.ALL[args.config]
+    if dom_phase != "gather":
+        tr.sur.timing_begin([dom_phase], K)
+    tr.res.timing_begin(["gather"], 2 * K)
+    n_win = K // 10
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(n_win + 2)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    ev[0].record(stream)
+    for i in range(K):
+        wrap_put()
+        assert tr.sample_and_train()
+        if (i + 1) % 10 == 0 and (i + 1) // 10 <= n_win:
+            ev[(i + 1) // 10].record(stream)
+    ev[-1].record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    gpu_ms = ev[0].elapsed_time(ev[-1])
+    windows = [ev[j].elapsed_time(ev[j + 1]) for j in range(n_win)]
+    g_ms, g_n = tr.res.timing_end()["gather"]
+    if dom_phase == "gather":
+        dom_avg_s = g_ms / g_n * 1e-3
+    else:
+        dom_ms, dom_n = tr.sur.timing_end()[dom_phase]
+        dom_avg_s = dom_ms / dom_n * 1e-3
+    return dict(gpu_ms=gpu_ms, wall=wall, windows=windows, breakdown=breakdown, dom_phase=dom_phase,
+                dom_avg_s=dom_avg_s, gather_avg_s=g_ms / g_n * 1e-3, loss=float(tr.loss.item()))
+
+
+def result_line(w, args, K, warmup, r, config: dict) -> dict:
+    value = w.batch * K / (r["gpu_ms"] * 1e-3)
+    win_sps = [10 * w.batch / (t * 1e-3) for t in r["windows"]] if r["windows"] else [value]
+    gather_rate = gather_bytes(w) / r["gather_avg_s"]
+    return {
+        "metric": METRIC, "value": round(value, 1), "unit": "samples/s", "n_gpus": 1, "steps": K,
+        "warmup": warmup, "ms_per_step": round(r["gpu_ms"] / K, 4), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "f32" if w.precision == "fp32" else "bf16",
+        "data": "synthetic", "config": config,
+        "roofline": roofline_entry(w, r["dom_phase"], r["dom_avg_s"]),
+        "reservoir_gather": {"achieved": round(gather_rate / 1e9, 1), "unit": "GB/s",
+                             "frac_hbm": round(gather_rate / PEAK_HBM, 4),
+                             "avg_us": round(r["gather_avg_s"] * 1e6, 2)},
+        "windows_of_10": {"median_samples_s": round(float(np.median(win_sps)), 1),
+                          "mean_samples_s": round(float(np.mean(win_sps)), 1), "n": len(win_sps)},
+        "wall_s": round(r["wall"], 3), "last_loss": r["loss"], "kernels": r["breakdown"], "cpu_baseline": None,
+    }
+
+
+def run_heat(args, w):
+    import torch
+
+    from fixtures import heat
+    from paper_2309_16743_amd.online import OnlineTrainer
+    K = args.steps or 2000
+    warmup = 50 if args.warmup is None else args.warmup
     t_gen = time.perf_counter()
     X = heat.sample_parameters(w.n_sims, w.data_seed)
     inputs = heat.inputs_for(X, w.tau)
     fields = heat.heat_fields(X, w.grid, w.tau)
-    t_gen = time.perf_counter() - t_gen
-    print(f"[bench] generated {fields.nbytes / 1e9:.1f} GB of {w.grid}x{w.grid} fields in {t_gen:.1f} s",
-          file=sys.stderr, flush=True)
-
+    print(f"[bench] generated {fields.nbytes / 1e9:.1f} GB of {w.grid}x{w.grid} fields in "
+          f"{time.perf_counter() - t_gen:.1f} s", file=sys.stderr, flush=True)
     dev = torch.device("cuda:0")
     inputs_d = torch.from_numpy(inputs).to(dev)
     fields_d = torch.from_numpy(fields).to(dev)
@@ -154,88 +272,101 @@ def main():
     with torch.cuda.stream(stream):
         tr = OnlineTrainer(w.widths, w.batch, w.capacity, w.threshold, w.wave, w.tau, inputs_d, fields_d,
                            w.reservoir_seed, w.init_seed, lr=w.lr, stream=stream)
-        # stream the whole ensemble through the schedule (untimed), then warm up
-        for _ in range(w.n_chunks):
+        for _ in range(w.n_chunks):             # stream the ensemble once (untimed)
             tr.iterate()
-        for _ in range(args.warmup):
+        for _ in range(warmup):
             assert tr.iterate(wrap=True)
         torch.cuda.synchronize()
         print(f"[bench] setup done: {tr.steps_done} train steps, reservoir {tr.res.stats()['n']} samples",
               file=sys.stderr, flush=True)
-
-        # per-kernel breakdown pass (every phase timed)
-        kp = max(args.profile_steps, 1)
-        tr.sur.timing_begin(list(SURROGATE_PHASES), kp)
-        tr.res.timing_begin(["put_assign", "put_copy", "select", "gather"], 2 * kp)
-        for _ in range(kp):
-            tr.iterate(wrap=True)
-        breakdown = kernel_table(w, tr.sur.timing_end(), tr.res.timing_end())
-        gemm_phases = ("fwd_output", "wgrad_output", "igrad_output")
-        dominant = max(gemm_phases, key=lambda p: breakdown[p]["avg_us"])
-
-        # timed region: K steps; HIP events around the dominant kernel and the gather
-        K = args.steps
-        tr.sur.timing_begin([dominant], K)
-        tr.res.timing_begin(["gather"], 2 * K)
-        n_win = K // 10
-        ev = [torch.cuda.Event(enable_timing=True) for _ in range(n_win + 2)]
-        torch.cuda.synchronize()
-        t0 = time.perf_counter()
-        ev[0].record(stream)
-        for i in range(K):
-            tr.iterate(wrap=True)
-            if (i + 1) % 10 == 0 and (i + 1) // 10 <= n_win:
-                ev[(i + 1) // 10].record(stream)
-        ev[-1].record(stream)
-        torch.cuda.synchronize()
-        wall = time.perf_counter() - t0
-        gpu_ms = ev[0].elapsed_time(ev[-1])
-        windows = [ev[j].elapsed_time(ev[j + 1]) for j in range(n_win)]
-        dom_ms, dom_n = tr.sur.timing_end()[dominant]
-        g_ms, g_n = tr.res.timing_end()["gather"]
-        loss = float(tr.loss.item())
-
-    ms_per_step = gpu_ms / K
-    value = w.batch * K / (gpu_ms * 1e-3)
-    win_sps = [10 * w.batch / (t * 1e-3) for t in windows] if windows else [value]
-    dom_avg_s = dom_ms / dom_n * 1e-3
-    achieved = gemm_flops(w) / dom_avg_s
-    gather_avg_s = g_ms / g_n * 1e-3
-    gather_rate = 2.0 * w.batch * (w.widths[-1] + w.widths[0]) * 4 / gather_avg_s
-
-    line = {
-        "metric": "surrogate train samples/s at 1 MI355X; MFMA util of output layer; reservoir GB/s",
-        "value": round(value, 1),
-        "unit": "samples/s",
-        "n_gpus": 1,
-        "steps": K,
-        "warmup": args.warmup,
-        "ms_per_step": round(ms_per_step, 4),
-        "higher_is_better": True,
-        "scaling": "weak",
-        "vs_baseline": None,
-        "dtype": "f32",
-        "data": "synthetic",
-        "config": {"workload": w.name, "fields": f"FTCS heat {w.grid}x{w.grid}, {w.n_sims} sims x {w.tau} steps",
-                   "widths": list(w.widths), "batch": w.batch, "capacity": w.capacity,
-                   "threshold": w.threshold, "put_rows_per_step": w.wave},
-        "roofline": {"bound": "mfma", "kernel": f"gemm_f32 ({dominant})", "achieved": round(achieved / 1e12, 2),
-                     "peak": PEAK_FP32_MFMA / 1e12, "unit": "TFLOP/s", "frac": round(achieved / PEAK_FP32_MFMA, 4),
-                     "traffic": None, "per_launch_flops": gemm_flops(w), "avg_us": round(dom_avg_s * 1e6, 2)},
-        "reservoir_gather": {"achieved": round(gather_rate / 1e9, 1), "unit": "GB/s",
-                             "frac_hbm": round(gather_rate / PEAK_HBM, 4), "avg_us": round(gather_avg_s * 1e6, 2)},
-        "windows_of_10": {"median_samples_s": round(float(np.median(win_sps)), 1),
-                          "mean_samples_s": round(float(np.mean(win_sps)), 1), "n": len(win_sps)},
-        "wall_s": round(wall, 3),
-        "last_loss": loss,
-        "kernels": breakdown,
-        "cpu_baseline": None,
-    }
+        r = timed_region(tr, w, K, args.profile_steps or 200, stream, lambda: tr.put_next(wrap=True))
+    config = {"workload": w.name, "fields": f"FTCS heat {w.grid}x{w.grid}, {w.n_sims} sims x {w.tau} steps",
+              "widths": list(w.widths), "batch": w.batch, "capacity": w.capacity, "threshold": w.threshold,
+              "put_rows_per_step": w.wave, "precision": w.precision}
+    line = result_line(w, args, K, warmup, r, config)
     tr.close()
     del inputs_d, fields_d
     torch.cuda.empty_cache()
     if args.cpu_seconds > 0:
         line["cpu_baseline"] = cpu_baseline(w, inputs, fields, args.cpu_seconds)
+    return line
+
+
+def run_field(args, w):
+    import torch
+
+    from fixtures import heat, synthetic
+    from paper_2309_16743_amd import OT_BF16
+    from paper_2309_16743_amd.online import OnlineTrainer
+    K = args.steps or 100
+    warmup = 5 if args.warmup is None else args.warmup
+    dev = torch.device("cuda:0")
+    n, D = w.grid, w.widths[-1]
+    X = torch.from_numpy(heat.sample_parameters(w.n_sims, w.data_seed)).to(dev)
+    basis = synthetic.sine_mode_basis_torch(n, w.data_seed, dev)
+    stream = torch.cuda.Stream(device=dev)
+
+    def gen_chunk(c, xbuf, ubuf):
+        wv, k = divmod(c % w.n_chunks, w.tau)
+        sims = X[wv * w.wave:(wv + 1) * w.wave]
+        t = torch.full((w.wave,), 0.01 * (k + 1), device=dev, dtype=torch.float64)
+        synthetic.sine_mode_fields_torch(sims, t, w.data_seed, basis, out=ubuf)
+        xbuf[:, :5] = sims.to(torch.float32)
+        xbuf[:, 5] = t.to(torch.float32)
+
+    with torch.cuda.stream(stream):
+        pool = 8
+        pool_x = [torch.empty(w.wave, 8, device=dev)[:, :6] for _ in range(pool)]
+        pool_u = [torch.empty(w.wave, D, device=dev) for _ in range(pool)]
+        first_pool_chunk = w.n_chunks // 2
+        for i in range(pool):
+            gen_chunk(first_pool_chunk + i, pool_x[i], pool_u[i])
+        tr = OnlineTrainer(w.widths, w.batch, w.capacity, w.threshold, w.wave, w.tau, None, None,
+                           w.reservoir_seed, w.init_seed, precision=OT_BF16, lr=w.lr, stream=stream,
+                           chunk_fn=lambda c: (pool_x[c % pool], pool_u[c % pool]), n_chunks=1 << 40, device=dev)
+        fx = torch.empty(w.wave, 8, device=dev)[:, :6]
+        fu = torch.empty(w.wave, D, device=dev)
+        t_fill = time.perf_counter()
+        n_stored, c = 0, 0
+        while n_stored < w.capacity:            # fill with generated chunks (untimed), drawing once past T
+            gen_chunk(c, fx, fu)
+            tr.res.put(fx, fu, stream=stream)
+            n_stored = min(w.capacity, n_stored + w.wave)
+            c += 1
+            if n_stored > w.threshold:
+                tr.sample_only()
+        for _ in range(warmup):
+            tr.put_next(wrap=True)
+            assert tr.sample_and_train()
+        torch.cuda.synchronize()
+        print(f"[bench] filled {n_stored} samples ({n_stored * D * 4 / 1e9:.0f} GB) in "
+              f"{time.perf_counter() - t_fill:.1f} s; {tr.steps_done} warm-up steps",
+              file=sys.stderr, flush=True)
+        r = timed_region(tr, w, K, args.profile_steps or 20, stream, lambda: tr.put_next(wrap=True))
+    config = {"workload": w.name, "fields": f"sine-mode {n}x{n}, {w.n_sims} sims x {w.tau} steps",
+              "widths": list(w.widths), "batch": w.batch, "capacity": w.capacity, "threshold": w.threshold,
+              "put_rows_per_step": w.wave, "precision": w.precision}
+    line = result_line(w, args, K, warmup, r, config)
+    tr.close()
+    torch.cuda.empty_cache()
+    if args.cpu_seconds > 0:
+        line["cpu_baseline"] = cpu_baseline_scaled(w, args.cpu_seconds)
+    return line
+
+
+def main():
+    args = parse_args()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print(f"bench.py measures one GPU only; --gpus {args.gpus} (WORLD_SIZE {world}) is not supported: "
+              "this build has no multi-GPU path.", file=sys.stderr)
+        sys.exit(2)
+    from fixtures import configs
+    if args.config not in configs.ALL:
+        print(f"unknown config {args.config}; choose from {sorted(configs.ALL)}", file=sys.stderr)
+        sys.exit(2)
+    w = configs.ALL[args.config]
+    line = run_heat(args, w) if w.fields == "ftcs" else run_field(args, w)
     text = json.dumps(line)
     print(text, flush=True)
     if args.out:

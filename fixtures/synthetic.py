@@ -73,3 +73,36 @@ def hash_inputs(keys: np.ndarray, x_dim: int = 6) -> np.ndarray:
     if x_dim > 1:
         out[:, 1] = (keys >> 24).astype(np.float32)
     return out
+
+
+def sine_mode_basis_torch(n: int, seed: int, device):
+    """(8, n*n) fp32 device tensor of the separable modes sin(p pi x) sin(q pi y)."""
+    import torch
+    p, q, _, _ = sine_mode_table(seed)
+    xs = torch.arange(1, n + 1, device=device, dtype=torch.float32) / (n + 1)
+    pt = torch.tensor(p, device=device, dtype=torch.float32)
+    qt = torch.tensor(q, device=device, dtype=torch.float32)
+    sx = torch.sin(torch.pi * pt[:, None] * xs[None, :])
+    sy = torch.sin(torch.pi * qt[:, None] * xs[None, :])
+    return (sx[:, :, None] * sy[:, None, :]).reshape(N_MODES, n * n)
+
+
+def sine_mode_fields_torch(X, t, seed: int, basis, out=None):
+    """sine_mode_fields on the GPU with torch (fp32 arithmetic): same formula,
+    values agree with the numpy version to fp32 rounding.  Benchmark inputs
+    only; parity tests use the numpy version.  X: (S, 5), t: (S,) device
+    tensors; basis from sine_mode_basis_torch."""
+    import torch
+    p, q, sgn, col = sine_mode_table(seed)
+    dev = X.device
+    pt = torch.tensor(p, device=dev, dtype=torch.float32)
+    qt = torch.tensor(q, device=dev, dtype=torch.float32)
+    Xf = X.to(torch.float32)
+    m = Xf.mean(dim=1)
+    amp = torch.minimum(m - 100.0, 500.0 - m)
+    a = amp[:, None] * torch.tensor(sgn, device=dev, dtype=torch.float32)[None, :] \
+        * (Xf[:, torch.tensor(col, device=dev)] - 100.0) / 400.0 / N_MODES
+    a = a * torch.exp(-(torch.pi ** 2) * (pt ** 2 + qt ** 2)[None, :] * t.to(torch.float32)[:, None])
+    res = torch.addmm(m[:, None].expand(-1, basis.shape[1]), a, basis) if out is None else \
+        torch.addmm(m[:, None].expand(-1, basis.shape[1]), a, basis, out=out)
+    return res

@@ -71,12 +71,114 @@ struct GemmBArgs {
   int64_t ldmask;
   float* rowsum;            // StoreF32 / SplitK with MNMajor A: sum_k A(m, k) (n tile 0)
   int64_t rowsum_stride;
+  float* colsum;            // MseBf: per m-tile column sums of the bf16 dY, colsum[tm * colsum_ld + n]
+  int64_t colsum_ld;
 };
 
 __device__ __forceinline__ int64_t xcd_remap_b(int64_t p, int64_t g) {
   const int64_t xcd = p % 8, q = p / 8;
   const int64_t per = g / 8, rem = g % 8;
   return xcd * per + (xcd < rem ? xcd : rem) + q;
+}
+
+// Epilogue shared by the bf16 kernels.  `ep` holds this wavefront's WM x WN
+// fp32 accumulators (pitch WN + 4) for output rows mw.., columns nw..; each
+// lane then handles 4 consecutive columns of a row, so targets, bias and masks
+// are read, and C written, with vector accesses.  MseBf also writes, per
+// m-tile, the column sums of the rounded dY (the output bias gradient) when
+// g.colsum is set.  s_red: >= 8 doubles + 4 * WN floats of LDS.
+template <int WM, int WN, EpiB EPI>
+__device__ __forceinline__ void bf16_epilogue(const GemmBArgs& g, const float* ep, int64_t mw, int64_t nw,
+                                              int64_t tm, int64_t split, double* s_red) {
+  constexpr int EP = WN + 4;
+  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+  float lsum = 0.f;
+  float csum[4] = {0.f, 0.f, 0.f, 0.f};
+  const int cg = lane % (WN / 4);                 // column group of 4
+  const int rl = lane / (WN / 4);                 // row within a pass
+  constexpr int ROWS_PER_PASS = 64 / (WN / 4);
+  const int64_t col = nw + 4 * cg;
+  const bool cfull = col + 3 < g.N;
+  float bias4[4] = {0.f, 0.f, 0.f, 0.f};
+  if constexpr (EPI == EpiB::BiasF32 || EPI == EpiB::BiasReluBf || EPI == EpiB::MseBf) {
+    if (cfull) {
+      const f32x4 t = *reinterpret_cast<const f32x4*>(g.bias + col);
+      bias4[0] = t[0]; bias4[1] = t[1]; bias4[2] = t[2]; bias4[3] = t[3];
+    } else {
+      for (int c = 0; c < 4; ++c) bias4[c] = (col + c < g.N) ? g.bias[col + c] : 0.f;
+    }
+  }
+  for (int rr = rl; rr < WM; rr += ROWS_PER_PASS) {
+    const int64_t m = mw + rr;
+    if (m >= g.M || col >= g.N) continue;
+    const f32x4 a4 = *reinterpret_cast<const f32x4*>(ep + rr * EP + 4 * cg);
+    float v[4] = {a4[0], a4[1], a4[2], a4[3]};
+    if constexpr (EPI == EpiB::StoreF32 || EPI == EpiB::SplitK || EPI == EpiB::BiasF32) {
+      if constexpr (EPI == EpiB::BiasF32)
+        for (int c = 0; c < 4; ++c) v[c] += bias4[c];
+      float* C = reinterpret_cast<float*>(g.C) + (EPI == EpiB::SplitK ? split * g.split_stride : 0) + m * g.ldc + col;
+      if (cfull) *reinterpret_cast<f32x4*>(C) = f32x4{v[0], v[1], v[2], v[3]};
+      else
+        for (int c = 0; c < 4; ++c)
+          if (col + c < g.N) C[c] = v[c];
+    } else {
+      if constexpr (EPI == EpiB::BiasReluBf) {
+        for (int c = 0; c < 4; ++c) { v[c] += bias4[c]; v[c] = v[c] > 0.f ? v[c] : 0.f; }
+      }
+      if constexpr (EPI == EpiB::MaskBf) {
+        const uint16_t* mp = g.mask + m * g.ldmask + col;
+        for (int c = 0; c < 4; ++c) {
+          const float mk = (col + c < g.N) ? bf2f(mp[c]) : 0.f;
+          v[c] = mk > 0.f ? v[c] : 0.f;
+        }
+      }
+      if constexpr (EPI == EpiB::MseBf) {
+        float t4[4];
+        const float* tp = g.target + m * g.ldt + col;
+        if (cfull) {
+          const f32x4 t = *reinterpret_cast<const f32x4*>(tp);
+          t4[0] = t[0]; t4[1] = t[1]; t4[2] = t[2]; t4[3] = t[3];
+        } else {
+          for (int c = 0; c < 4; ++c) t4[c] = (col + c < g.N) ? tp[c] : 0.f;
+        }
+        for (int c = 0; c < 4; ++c) {
+          const float r = (col + c < g.N) ? (v[c] + bias4[c]) - t4[c] : 0.f;
+          lsum += r * r;
+          v[c] = g.scale * r;
+        }
+      }
+      const uint16_t h4[4] = {f2bf(v[0]), f2bf(v[1]), f2bf(v[2]), f2bf(v[3])};
+      if constexpr (EPI == EpiB::MseBf)
+        for (int c = 0; c < 4; ++c) csum[c] += (col + c < g.N) ? bf2f(h4[c]) : 0.f;
+      uint16_t* C = reinterpret_cast<uint16_t*>(g.C) + m * g.ldc + col;
+      if (cfull) {
+        *reinterpret_cast<u16x4*>(C) = u16x4{h4[0], h4[1], h4[2], h4[3]};
+      } else {
+        for (int c = 0; c < 4; ++c)
+          if (col + c < g.N) C[c] = h4[c];
+      }
+    }
+  }
+  if constexpr (EPI == EpiB::MseBf) {
+    const double ls = warp_sum((double)lsum);
+    if (lane == 0) s_red[wid] = ls;
+    // lanes with the same lane % (WN/4) hold the same 4 columns: fold the
+    // ROWS_PER_PASS lanes, then the two wavefronts of each column half
+    for (int c = 0; c < 4; ++c)
+      for (int off = WN / 4; off < 64; off <<= 1) csum[c] += __shfl_xor(csum[c], off, 64);
+    float* xs = reinterpret_cast<float*>(s_red + 8);   // 4 waves x WN floats
+    if (rl == 0)
+      for (int c = 0; c < 4; ++c) xs[wid * WN + 4 * cg + c] = csum[c];
+    __syncthreads();
+    if (tid == 0) g.loss_partials[blockIdx.y * gridDim.x + blockIdx.x] = ((s_red[0] + s_red[1]) + s_red[2]) + s_red[3];
+    // waves (0, 1) share column half wn = 0, waves (2, 3) wn = 1
+    if (g.colsum && (wid & 1) == 0 && rl == 0) {
+      for (int c = 0; c < 4; ++c) {
+        const int64_t n = col + c;
+        if (n < g.N) g.colsum[tm * g.colsum_ld + n] = xs[wid * WN + 4 * cg + c] + xs[(wid + 1) * WN + 4 * cg + c];
+      }
+    }
+  }
 }
 
 template <int FM, int FN, LayB LA, LayB LB, EpiB EPI, int BK>
@@ -97,7 +199,7 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmBArgs g) {
   constexpr int EPI_BYTES = 4 * (WM * (WN + 4)) * 4;            // per-wave fp32 staging
   constexpr int LDS_BYTES = TILE_BYTES > EPI_BYTES ? TILE_BYTES : EPI_BYTES;
   __shared__ __attribute__((aligned(16))) unsigned char smem[LDS_BYTES];
-  __shared__ double s_red[4];
+  __shared__ double s_red[8 + 2 * WN];   // loss partials + column-sum exchange (4 waves x WN floats)
   uint16_t* const tiles16 = reinterpret_cast<uint16_t*>(smem);
   auto As = [&](int buf) { return tiles16 + buf * A_ELEMS; };
   auto Bs = [&](int buf) { return tiles16 + 2 * A_ELEMS + buf * B_ELEMS; };
@@ -263,75 +365,7 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmBArgs g) {
 #pragma unroll
       for (int r = 0; r < 4; ++r) ep[(16 * f + 4 * (lane / 16) + r) * EP + 16 * h + lane % 16] = acc[f][h][r];
   __syncthreads();
-  float lsum = 0.f;
-  const int cg = lane % (WN / 4);                 // column group of 4
-  const int rl = lane / (WN / 4);                 // row within a pass
-  constexpr int ROWS_PER_PASS = 64 / (WN / 4);
-  const int64_t col = n0 + WN * wn + 4 * cg;
-  const bool cfull = col + 3 < g.N;
-  float bias4[4] = {0.f, 0.f, 0.f, 0.f};
-  if constexpr (EPI == EpiB::BiasF32 || EPI == EpiB::BiasReluBf || EPI == EpiB::MseBf) {
-    if (cfull) {
-      const f32x4 t = *reinterpret_cast<const f32x4*>(g.bias + col);
-      bias4[0] = t[0]; bias4[1] = t[1]; bias4[2] = t[2]; bias4[3] = t[3];
-    } else {
-      for (int c = 0; c < 4; ++c) bias4[c] = (col + c < g.N) ? g.bias[col + c] : 0.f;
-    }
-  }
-  for (int rr = rl; rr < WM; rr += ROWS_PER_PASS) {
-    const int64_t m = m0 + WM * wm + rr;
-    if (m >= g.M || col >= g.N) continue;
-    const f32x4 a4 = *reinterpret_cast<const f32x4*>(ep + rr * EP + 4 * cg);
-    float v[4] = {a4[0], a4[1], a4[2], a4[3]};
-    if constexpr (EPI == EpiB::StoreF32 || EPI == EpiB::SplitK || EPI == EpiB::BiasF32) {
-      if constexpr (EPI == EpiB::BiasF32)
-        for (int c = 0; c < 4; ++c) v[c] += bias4[c];
-      float* C = reinterpret_cast<float*>(g.C) + (EPI == EpiB::SplitK ? split * g.split_stride : 0) + m * g.ldc + col;
-      if (cfull) *reinterpret_cast<f32x4*>(C) = f32x4{v[0], v[1], v[2], v[3]};
-      else
-        for (int c = 0; c < 4; ++c)
-          if (col + c < g.N) C[c] = v[c];
-    } else {
-      if constexpr (EPI == EpiB::BiasReluBf) {
-        for (int c = 0; c < 4; ++c) { v[c] += bias4[c]; v[c] = v[c] > 0.f ? v[c] : 0.f; }
-      }
-      if constexpr (EPI == EpiB::MaskBf) {
-        const uint16_t* mp = g.mask + m * g.ldmask + col;
-        for (int c = 0; c < 4; ++c) {
-          const float mk = (col + c < g.N) ? bf2f(mp[c]) : 0.f;
-          v[c] = mk > 0.f ? v[c] : 0.f;
-        }
-      }
-      if constexpr (EPI == EpiB::MseBf) {
-        float t4[4];
-        const float* tp = g.target + m * g.ldt + col;
-        if (cfull) {
-          const f32x4 t = *reinterpret_cast<const f32x4*>(tp);
-          t4[0] = t[0]; t4[1] = t[1]; t4[2] = t[2]; t4[3] = t[3];
-        } else {
-          for (int c = 0; c < 4; ++c) t4[c] = (col + c < g.N) ? tp[c] : 0.f;
-        }
-        for (int c = 0; c < 4; ++c) {
-          const float r = (col + c < g.N) ? (v[c] + bias4[c]) - t4[c] : 0.f;
-          lsum += r * r;
-          v[c] = g.scale * r;
-        }
-      }
-      uint16_t* C = reinterpret_cast<uint16_t*>(g.C) + m * g.ldc + col;
-      if (cfull) {
-        *reinterpret_cast<u16x4*>(C) = u16x4{f2bf(v[0]), f2bf(v[1]), f2bf(v[2]), f2bf(v[3])};
-      } else {
-        for (int c = 0; c < 4; ++c)
-          if (col + c < g.N) C[c] = f2bf(v[c]);
-      }
-    }
-  }
-  if constexpr (EPI == EpiB::MseBf) {
-    const double ls = warp_sum((double)lsum);
-    if (lane == 0) s_red[wid] = ls;
-    __syncthreads();
-    if (tid == 0) g.loss_partials[blockIdx.y * gridDim.x + blockIdx.x] = ((s_red[0] + s_red[1]) + s_red[2]) + s_red[3];
-  }
+  bf16_epilogue<WM, WN, EPI>(g, ep, m0 + WM * wm, n0 + WN * wn, tm, split, s_red);
 }
 
 template <int FM, int FN, LayB LA, LayB LB, EpiB EPI, int BK>
@@ -346,6 +380,182 @@ hipError_t launch_gemm_bf16(const GemmBArgs& g, int64_t splits, hipStream_t stre
 template <int FM, int FN>
 constexpr int64_t gemm_bf16_tiles(int64_t M, int64_t N) {
   return ((M + 32 * FM - 1) / (32 * FM)) * ((N + 32 * FN - 1) / (32 * FN));
+}
+
+
+// ---------------------------------------------------------------------------
+// Pipelined bf16 GEMM for the large output-layer products.
+//
+// Block tile BM x BN (256 x 128 or 128 x 256), 4 wavefronts of (BM/2) x (BN/2)
+// built from v_mfma_f32_32x32x16_bf16 (lane l supplies A[i = l%32][k =
+// 8 (l/32) + e], B[k = 8 (l/32) + e][j = l%32]; accumulator element r of
+// lane l is D[8 (r/4) + 4 (l/32) + r%4][l%32]), k tile 64, and a ring of 3 LDS
+// stages filled by direct global -> LDS loads
+// (global_load_lds_dwordx4: each lane's 16 bytes land at the wave's LDS base +
+// 16 * lane), so two k tiles are always in flight while the MFMAs consume the
+// third.  LDS rows are unpadded; instead the eight 16-byte chunks of each
+// aligned group are permuted by XOR with (row mod 8), so the MFMA operand reads
+// of 8 consecutive rows hit 8 different bank groups.
+//   KMajor operand: stage tile [mn][64] (8 chunks per row);
+//   MNMajor operand: stage tile [64][mn] (mn / 8 chunks per row), read with
+//   ds_read_b64_tr_b16 as in gemm_bf16_kernel.
+// Requirements: K (and the split size) a multiple of 64.  Rows / columns past
+// M or N are read from clamped addresses and their results are not stored.
+template <int BM, int BN, LayB LA, LayB LB, EpiB EPI>
+__global__ __launch_bounds__(256, 1) void gemm_bf16_pipe_kernel(GemmBArgs g) {
+  constexpr int NT = 256, BK = 64, S = 3;
+  constexpr int WM = BM / 2, WN = BN / 2, FM = WM / 32, FN = WN / 32;
+  constexpr int A_CH = BM * BK / 8, B_CH = BN * BK / 8;          // 16-byte chunks per stage
+  constexpr int LA_N = A_CH / NT, LB_N = B_CH / NT;               // loads per thread per k tile
+  static_assert(A_CH % NT == 0 && B_CH % NT == 0, "tile split");
+  constexpr int STAGE_BYTES = (A_CH + B_CH) * 16;
+  constexpr int EP_BYTES = 4 * WM * (WN + 4) * 4;
+  constexpr int LDS_BYTES = S * STAGE_BYTES > EP_BYTES ? S * STAGE_BYTES : EP_BYTES;
+  __shared__ __attribute__((aligned(16))) unsigned char smem[LDS_BYTES];
+  __shared__ double s_red[8 + 2 * WN];
+
+  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+  const int wm = wid % 2, wn = wid / 2;
+  const int64_t tiles_m = (g.M + BM - 1) / BM;
+  const int64_t logical = xcd_remap_b(blockIdx.x, (int64_t)gridDim.x);
+  const int64_t tm = logical % tiles_m, tn = logical / tiles_m;
+  const int64_t m0 = tm * BM, n0 = tn * BN;
+  const int64_t split = blockIdx.y;
+  const int64_t kbeg = split * g.k_chunk;
+  const int64_t kend = (kbeg + g.k_chunk < g.K) ? kbeg + g.k_chunk : g.K;
+  const int nk = (int)((kend - kbeg) / BK);
+
+  // Per-thread global offsets (elements) of its chunks, relative to the k tile start.
+  // Chunk ci = (i * 4 + wid) * 64 + lane of operand X sits in LDS slot ci.
+  int64_t a_off[LA_N], b_off[LB_N];
+#pragma unroll
+  for (int i = 0; i < LA_N; ++i) {
+    const int ci = (i * 4 + wid) * 64 + lane;
+    if constexpr (LA == LayB::KMajor) {
+      const int row = ci / 8, pc = ci % 8, lc = pc ^ (row & 7);
+      const int64_t m = min(m0 + row, g.M - 1);
+      a_off[i] = m * g.lda + 8 * lc;
+    } else {
+      constexpr int CPR = BM / 8;
+      const int row = ci / CPR, pc = ci % CPR, lc = pc ^ (row & 7);
+      const int64_t m = min(m0 + 8 * lc, (g.M - 1) / 8 * 8);
+      a_off[i] = (int64_t)row * g.lda + m;
+    }
+  }
+#pragma unroll
+  for (int i = 0; i < LB_N; ++i) {
+    const int ci = (i * 4 + wid) * 64 + lane;
+    if constexpr (LB == LayB::KMajor) {
+      const int row = ci / 8, pc = ci % 8, lc = pc ^ (row & 7);
+      const int64_t n = min(n0 + row, g.N - 1);
+      b_off[i] = n * g.ldb + 8 * lc;
+    } else {
+      constexpr int CPR = BN / 8;
+      const int row = ci / CPR, pc = ci % CPR, lc = pc ^ (row & 7);
+      const int64_t n = min(n0 + 8 * lc, (g.N - 1) / 8 * 8);
+      b_off[i] = (int64_t)row * g.ldb + n;
+    }
+  }
+  typedef __attribute__((address_space(3))) void lds_void;
+  // k tile kt into stage st
+  auto issue = [&](int kt, int st) {
+    const int64_t k0 = kbeg + (int64_t)kt * BK;
+    unsigned char* sa = smem + st * STAGE_BYTES;
+    unsigned char* sb = sa + A_CH * 16;
+#pragma unroll
+    for (int i = 0; i < LA_N; ++i) {
+      const uint16_t* src = (LA == LayB::KMajor) ? g.A + a_off[i] + k0 : g.A + a_off[i] + k0 * g.lda;
+      __builtin_amdgcn_global_load_lds(src, (lds_void*)(sa + (i * 4 + wid) * 1024), 16, 0, 0);
+    }
+#pragma unroll
+    for (int i = 0; i < LB_N; ++i) {
+      const uint16_t* src = (LB == LayB::KMajor) ? g.B + b_off[i] + k0 : g.B + b_off[i] + k0 * g.ldb;
+      __builtin_amdgcn_global_load_lds(src, (lds_void*)(sb + (i * 4 + wid) * 1024), 16, 0, 0);
+    }
+  };
+
+  typedef float f32x16 __attribute__((ext_vector_type(16)));
+  typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
+  // Operand of one 16-deep k step (kk) for the 32-wide fragment at `base`.
+  // KMajor: lane l reads row base + l%32, 8 k-values at 16 kk + 8 (l/32).
+  // MNMajor: 16-lane group q covers columns base + 16 (q%2) .. +15 and k rows
+  // 16 kk + 8 (q/2) .. +7, read as two transposed 4-row blocks.
+  auto frag = [&](const unsigned char* st, int cpr, bool kmajor, int base, int kk) -> bf16x8 {
+    if (kmajor) {
+      const int row = base + lane % 32;
+      const int lc = 2 * kk + lane / 32;
+      return *reinterpret_cast<const bf16x8*>(st + (row * 8 + (lc ^ (row & 7))) * 16);
+    }
+    const int c = lane % 16, q = lane / 16;
+    const int col = base + 16 * (q & 1) + 4 * (c % 4);
+    const int r0 = 16 * kk + 8 * (q >> 1) + c / 4, r1 = r0 + 4;
+    const int ch = col / 8, half = (col / 4) & 1;
+    bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(st + (r0 * cpr + (ch ^ (r0 & 7))) * 16 + half * 8));
+    bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(st + (r1 * cpr + (ch ^ (r1 & 7))) * 16 + half * 8));
+    return bf16x8{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+  };
+
+  f32x16 acc[FM][FN];
+#pragma unroll
+  for (int f = 0; f < FM; ++f)
+#pragma unroll
+    for (int h = 0; h < FN; ++h) acc[f][h] = f32x16{};
+
+  // vmcnt wait with lgkm / exp counters left unconstrained (gfx9 encoding)
+#define OT_WAIT_VM(n) __builtin_amdgcn_s_waitcnt(((n) & 0xF) | (0x7 << 4) | (0xF << 8) | (((n) >> 4) << 14))
+  constexpr int PER_TILE = LA_N + LB_N;
+  for (int s = 0; s < S - 1; ++s)
+    if (s < nk) issue(s, s);
+  for (int kt = 0; kt < nk; ++kt) {
+    // tile kt's loads are the oldest outstanding ones; later tiles may stay in flight
+    const int ahead = min(S - 2, nk - 1 - kt);
+    if (ahead >= 1) OT_WAIT_VM(PER_TILE);
+    else OT_WAIT_VM(0);
+    __syncthreads();
+    if (kt + S - 1 < nk) issue(kt + S - 1, (kt + S - 1) % S);
+    const unsigned char* sa = smem + (kt % S) * STAGE_BYTES;
+    const unsigned char* sb = sa + A_CH * 16;
+#pragma unroll
+    for (int kk = 0; kk < BK / 16; ++kk) {
+      bf16x8 af[FM], bfr[FN];
+#pragma unroll
+      for (int f = 0; f < FM; ++f) af[f] = frag(sa, BM / 8, LA == LayB::KMajor, WM * wm + 32 * f, kk);
+#pragma unroll
+      for (int h = 0; h < FN; ++h) bfr[h] = frag(sb, BN / 8, LB == LayB::KMajor, WN * wn + 32 * h, kk);
+#pragma unroll
+      for (int f = 0; f < FM; ++f)
+#pragma unroll
+        for (int h = 0; h < FN; ++h)
+          acc[f][h] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[f], bfr[h], acc[f][h], 0, 0, 0);
+    }
+  }
+#undef OT_WAIT_VM
+  __syncthreads();
+
+  constexpr int EP = WN + 4;
+  float* ep = reinterpret_cast<float*>(smem) + wid * (WM * EP);
+#pragma unroll
+  for (int f = 0; f < FM; ++f)
+#pragma unroll
+    for (int h = 0; h < FN; ++h)
+#pragma unroll
+      for (int r = 0; r < 16; ++r)
+        ep[(32 * f + 8 * (r / 4) + 4 * (lane / 32) + r % 4) * EP + 32 * h + lane % 32] = acc[f][h][r];
+  __syncthreads();
+  bf16_epilogue<WM, WN, EPI>(g, ep, m0 + WM * wm, n0 + WN * wn, tm, split, s_red);
+}
+
+template <int BM, int BN, LayB LA, LayB LB, EpiB EPI>
+hipError_t launch_gemm_bf16_pipe(const GemmBArgs& g, int64_t splits, hipStream_t stream) {
+  const int64_t tiles = ((g.M + BM - 1) / BM) * ((g.N + BN - 1) / BN);
+  hipLaunchKernelGGL((gemm_bf16_pipe_kernel<BM, BN, LA, LB, EPI>), dim3((unsigned)tiles, (unsigned)splits), dim3(256),
+                     0, stream, g);
+  return hipGetLastError();
+}
+
+template <int BM, int BN>
+constexpr int64_t gemm_bf16_pipe_tiles(int64_t M, int64_t N) {
+  return ((M + BM - 1) / BM) * ((N + BN - 1) / BN);
 }
 
 }  // namespace ot

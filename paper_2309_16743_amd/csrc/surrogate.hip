@@ -229,6 +229,16 @@ __global__ __launch_bounds__(256) void adam_kernel(float* __restrict__ p, const 
 
 namespace ot {
 
+// db[n] = sum over m-tiles t (in order) of colsum[t * ld + n].
+__global__ void colsum_reduce_kernel(const float* __restrict__ colsum, int64_t tiles, int64_t N, int64_t ld,
+                                     float* __restrict__ db) {
+  const int64_t n = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (n >= N) return;
+  float acc = 0.f;
+  for (int64_t t = 0; t < tiles; ++t) acc += colsum[t * ld + n];
+  db[n] = acc;
+}
+
 // bf16 copy of fp32 values (round to nearest even).
 __global__ void to_bf16_kernel(const float* __restrict__ p, uint16_t* __restrict__ pb, int64_t n) {
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
@@ -321,6 +331,8 @@ struct ot_surrogate {
   uint16_t* pb = nullptr;                  // bf16 copy of the flat parameters
   std::vector<uint16_t*> act16;            // act16[l] = bf16(A_l), l = 1..L-1
   std::vector<uint16_t*> dz16;             // dz16[l] = bf16(dZ_l), l = 1..L (dz16[L] = dY)
+  float* colsum = nullptr;                 // per m-tile column sums of dY (output bias gradient)
+  int64_t colsum_elems = 0;
 };
 
 namespace {
@@ -372,6 +384,7 @@ void free_surrogate(ot_surrogate* s) {
   (void)hipFree(s->v);
   (void)hipFree(s->loss_last);
   (void)hipFree(s->pb);
+  (void)hipFree(s->colsum);
   delete s;
 }
 
@@ -472,6 +485,18 @@ hipError_t launch_epi(Epi epi, int cfg, const GemmArgs& g, int64_t splits, hipSt
     case Epi::SplitK: return launch_cfg<LA, LB, Epi::SplitK>(cfg, g, splits, st);
     default: return launch_cfg<LA, LB, Epi::Mask>(cfg, g, splits, st);
   }
+}
+
+int ensure_colsum(ot_surrogate* s, int64_t elems) {
+  if (elems <= s->colsum_elems) return OT_OK;
+  OT_HIP(hipDeviceSynchronize());
+  (void)hipFree(s->colsum);
+  s->colsum = nullptr;
+  s->colsum_elems = 0;
+  int rc = salloc((void**)&s->colsum, (size_t)elems * sizeof(float));
+  if (rc) return rc;
+  s->colsum_elems = elems;
+  return OT_OK;
 }
 
 int ensure_split_ws(ot_surrogate* s, int64_t elems, int64_t rs_elems) {
@@ -582,19 +607,38 @@ using ot::EpiB;
 using ot::GemmBArgs;
 using ot::LayB;
 
-// bf16 tiles: 128 x 128 (4 x 4 fragments per wave) and 64 x 64 (2 x 2), k tile 32.
-enum CfgB : int { kB128 = 0, kB64 = 1 };
+// bf16 tiles: the pipelined 256 x 128 kernel (k tile 64, direct-to-LDS loads)
+// for large products; 128 x 128 (4 x 4 fragments per wave) and 64 x 64 (2 x 2)
+// with a k tile of 32 otherwise.
+enum CfgB : int { kB128 = 0, kB64 = 1, kBPipe = 2 };
 constexpr int kBK = 32;
+constexpr int kPipeBK = 64;
 
 int64_t tiles_b(int cfg, int64_t M, int64_t N) {
+  if (cfg == kBPipe) return ot::gemm_bf16_pipe_tiles<256, 128>(M, N);
   return cfg == kB128 ? ot::gemm_bf16_tiles<4, 4>(M, N) : ot::gemm_bf16_tiles<2, 2>(M, N);
 }
 
-// 128 x 128 tiles when they give about two blocks per CU; long k ranges are
-// split over 128 x 128 tiles, shorter ones over 64 x 64 tiles.
+// The pipelined kernel when k is a multiple of its 64-deep k tile and its
+// tiles (split over k when needed, at least 16 k tiles per split) give about
+// one block per CU; else 128 x 128 tiles when they give about two blocks per
+// CU; long k ranges are split over 128 x 128 tiles, shorter ones over 64 x 64.
 Plan make_plan_b(int64_t M, int64_t N, int64_t K, bool allow_split) {
   constexpr int64_t kCUs = 256;
   Plan p;
+  if (K % kPipeBK == 0 && M >= 256 && N >= 128) {
+    const int64_t t = tiles_b(kBPipe, M, N);
+    int64_t sp = 1;
+    if (allow_split)
+      while (t * sp < 2 * kCUs - 32 && K / (2 * sp) >= 16 * kPipeBK) sp *= 2;
+    if (t * sp >= kCUs - 16) {
+      p.cfg = kBPipe;
+      p.k_chunk = ot::round_up(ot::ceil_div(K, sp), kPipeBK);
+      p.splits = std::max<int64_t>(1, ot::ceil_div(K, p.k_chunk));
+      p.blocks = t * p.splits;
+      return p;
+    }
+  }
   const int64_t t128 = tiles_b(kB128, M, N);
   if (t128 >= 2 * kCUs - 32) {
     p.cfg = kB128;
@@ -615,6 +659,7 @@ Plan make_plan_b(int64_t M, int64_t N, int64_t K, bool allow_split) {
 
 template <LayB LA, LayB LB, EpiB E>
 hipError_t launch_cfg_b(int cfg, const GemmBArgs& g, int64_t splits, hipStream_t st) {
+  if (cfg == kBPipe) return ot::launch_gemm_bf16_pipe<256, 128, LA, LB, E>(g, splits, st);
   if (cfg == kB128) return ot::launch_gemm_bf16<4, 4, LA, LB, E, kBK>(g, splits, st);
   return ot::launch_gemm_bf16<2, 2, LA, LB, E, kBK>(g, splits, st);
 }
@@ -734,11 +779,21 @@ int train_step_bf16(ot_surrogate* s, const float* x, int64_t ldx, const float* u
     g.ldt = ldu;
     g.scale = (float)(2.0 / ((double)b * (double)D));
     g.loss_partials = s->loss_partials;
+    // output bias gradient: per m-tile column sums of the rounded dY
+    const int64_t mtiles = ot::ceil_div(b, 64);
+    if ((rc = ensure_colsum(s, mtiles * s->ld[L]))) return rc;
+    g.colsum = s->colsum;
+    g.colsum_ld = s->ld[L];
     n_partials = make_plan_b(g.M, g.N, g.K, false).blocks;
     if (n_partials > s->n_partials_cap) return ot::set_error(OT_E_STATE, "loss partial buffer too small");
+    const Plan pf = make_plan_b(g.M, g.N, g.K, false);
     if ((rc = run_gemm_b<LayB::KMajor, LayB::KMajor, EpiB::MseBf>(s, g, st, "bf16 output forward+MSE", false,
                                                                   OT_PH_FWD_OUTPUT)))
       return rc;
+    const int64_t used_mtiles = ot::ceil_div(b, pf.cfg == kBPipe ? 256 : (pf.cfg == kB128 ? 128 : 64));
+    hipLaunchKernelGGL(ot::colsum_reduce_kernel, dim3((unsigned)ot::ceil_div(D, 256)), dim3(256), 0, st, s->colsum,
+                       used_mtiles, D, s->ld[L], s->grads + lo.b_off);
+    OT_LAUNCHED("colsum_reduce_kernel");
   }
   tm.mark(st, OT_PH_LOSS, 0);
   hipLaunchKernelGGL(ot::loss_finalize_kernel, dim3(1), dim3(256), 0, st, s->loss_partials, n_partials,
@@ -776,7 +831,7 @@ int train_step_bf16(ot_surrogate* s, const float* x, int64_t ldx, const float* u
       g.M = ly.out;
       g.N = ly.in;
       g.K = b;
-      g.rowsum = db;
+      g.rowsum = (l == L) ? nullptr : db;   // the output bias gradient came from the forward epilogue
       if ((rc = run_gemm_b<LayB::MNMajor, LayB::MNMajor, EpiB::StoreF32>(s, g, st, "bf16 weight gradient", true, ph_w,
                                                                          ph_w >= 0 ? OT_PH_WGRAD_REDUCE : -1)))
         return rc;

@@ -4,7 +4,7 @@ training threads (Sec. 3.1); all work is enqueued on one HIP stream.
 """
 from __future__ import annotations
 
-from typing import Optional
+from typing import Callable, Optional
 
 import torch
 
@@ -16,27 +16,35 @@ def _round_up(v: int, m: int) -> int:
 
 
 class OnlineTrainer:
-    """Streams chunks of a device-resident ensemble into a reservoir and trains.
+    """Streams chunks of an ensemble into a reservoir and trains.
 
-    inputs: (S, tau, x_dim) fp32 device tensor; fields: (S, tau, D) fp32 device
-    tensor, D a multiple of 4.  Chunk c holds time step (c mod tau) of the
-    `wave` simulations of wave c // tau.
+    Either inputs: (S, tau, x_dim) and fields: (S, tau, D) fp32 device tensors
+    (chunk c holds time step (c mod tau) of the `wave` simulations of wave
+    c // tau), or chunk_fn(c) -> (x rows, u rows) device tensors for chunks
+    0 .. n_chunks - 1 (rows with unit column stride, leading dimension a
+    multiple of 4).
     """
 
     def __init__(self, widths, batch: int, capacity: int, threshold: int, wave: int, tau: int,
-                 inputs: torch.Tensor, fields: torch.Tensor, reservoir_seed: int, init_seed: int,
-                 precision: int = OT_FP32, lr: float = 1e-3, stream: Optional[torch.cuda.Stream] = None,
-                 record_steps: int = 0):
+                 inputs: Optional[torch.Tensor], fields: Optional[torch.Tensor], reservoir_seed: int,
+                 init_seed: int, precision: int = OT_FP32, lr: float = 1e-3,
+                 stream: Optional[torch.cuda.Stream] = None, record_steps: int = 0,
+                 chunk_fn: Optional[Callable] = None, n_chunks: int = 0, device=None):
         self.stream = stream if stream is not None else torch.cuda.current_stream()
         self.widths = tuple(widths)
         self.batch, self.wave, self.tau = batch, wave, tau
         self.inputs, self.fields = inputs, fields
-        self.n_sims = inputs.shape[0]
-        self.n_chunks = (self.n_sims // wave) * tau
-        x_dim, d = inputs.shape[-1], fields.shape[-1]
+        self.chunk_fn = chunk_fn
+        if chunk_fn is None:
+            self.n_sims = inputs.shape[0]
+            self.n_chunks = (self.n_sims // wave) * tau
+            dev = inputs.device
+        else:
+            self.n_chunks = n_chunks
+            dev = device
+        x_dim, d = widths[0], widths[-1]
         self.res = Reservoir(capacity, threshold, x_dim, d, reservoir_seed, order_stream=self.stream)
         self.sur = Surrogate(widths, precision=precision, lr=lr, seed=init_seed, max_batch=batch)
-        dev = inputs.device
         self.xb = torch.empty(batch, _round_up(x_dim, 4), device=dev)[:, :x_dim]
         self.ub = torch.empty(batch, _round_up(d, 4), device=dev)[:, :d]
         self.slots = torch.empty(batch, dtype=torch.int32, device=dev)
@@ -50,6 +58,8 @@ class OnlineTrainer:
         self.chunk_cursor = 0
 
     def chunk_views(self, c: int):
+        if self.chunk_fn is not None:
+            return self.chunk_fn(c)
         w, k = divmod(c % self.n_chunks, self.tau)
         s0 = w * self.wave
         return self.inputs[s0:s0 + self.wave, k, :], self.fields[s0:s0 + self.wave, k, :]
@@ -62,6 +72,11 @@ class OnlineTrainer:
         self.res.put(x, u, stream=self.stream, accepted=self.accepted)
         self.chunk_cursor += 1
         return True
+
+    def sample_only(self) -> bool:
+        """Draw a batch without gathering or training (marks samples seen)."""
+        st, _, _ = self.res.sample_batch(self.batch, self.slots, stream=self.stream)
+        return st == OT_OK
 
     def sample_and_train(self) -> bool:
         rec = self.steps_done < self.record_steps

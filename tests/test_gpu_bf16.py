@@ -55,7 +55,8 @@ SHAPES = [
     ((6, 100, 77, 1001), 50),          # ragged widths, 64 x 64 tiles, partial tiles
     ((6, 256, 256, 4000), 128),        # split-K input gradient
     ((6, 128, 128, 128, 300), 64),     # three hidden layers
-    ((6, 512, 512, 20000), 512),       # 128 x 128 tiles, the bf16 workloads' batch
+    ((6, 512, 512, 20000), 512),       # pipelined 256 x 128 kernel, the bf16 workloads' batch
+    ((6, 512, 512, 30001), 320),       # pipelined kernel with ragged M and N (clamped edges)
 ]
 
 
