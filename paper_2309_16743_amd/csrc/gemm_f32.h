@@ -79,7 +79,9 @@ struct FragVec<2> { typedef f32x2 T; };
 template <>
 struct FragVec<1> { typedef float T; };
 
-template <int WGM, int WGN, int FM, int FN, Lay LA, Lay LB, Epi EPI, int BK = 16>
+// ROLE only separates instantiations (0: hidden layers, 1: output layer) so
+// that profiles attribute the output-layer products to their own kernels.
+template <int WGM, int WGN, int FM, int FN, Lay LA, Lay LB, Epi EPI, int BK = 16, int ROLE = 0>
 __global__ __launch_bounds__(64 * WGM * WGN) void gemm_f32_kernel(GemmArgs g) {
   constexpr int NT = 64 * WGM * WGN;
   static_assert(BK % 16 == 0, "k tile must be a multiple of 16");
@@ -377,12 +379,13 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_f32_kernel(GemmArgs g) {
 }
 
 // Host launcher.  Returns the hipError_t of the launch.
-template <int WGM, int WGN, int FM, int FN, Lay LA, Lay LB, Epi EPI, int BK = 16>
+template <int WGM, int WGN, int FM, int FN, Lay LA, Lay LB, Epi EPI, int BK = 16, int ROLE = 0>
 hipError_t launch_gemm_f32(const GemmArgs& g, int64_t splits, hipStream_t stream) {
   constexpr int BM = 16 * FM * WGM, BN = 16 * FN * WGN;
   const int64_t tiles = ((g.M + BM - 1) / BM) * ((g.N + BN - 1) / BN);
   dim3 grid((unsigned)tiles, (unsigned)splits);
-  hipLaunchKernelGGL((gemm_f32_kernel<WGM, WGN, FM, FN, LA, LB, EPI, BK>), grid, dim3(64 * WGM * WGN), 0, stream, g);
+  hipLaunchKernelGGL((gemm_f32_kernel<WGM, WGN, FM, FN, LA, LB, EPI, BK, ROLE>), grid, dim3(64 * WGM * WGN), 0, stream,
+                     g);
   return hipGetLastError();
 }
 

@@ -466,24 +466,24 @@ Plan make_plan(int64_t M, int64_t N, int64_t K, bool allow_split) {
   return p;
 }
 
-template <Lay LA, Lay LB, Epi EPI>
+template <Lay LA, Lay LB, Epi EPI, int ROLE>
 hipError_t launch_cfg(int cfg, const GemmArgs& g, int64_t splits, hipStream_t st) {
   switch (cfg) {
-    case kC128x128: return ot::launch_gemm_f32<2, 2, 4, 4, LA, LB, EPI>(g, splits, st);
-    case kC64x128: return ot::launch_gemm_f32<2, 2, 2, 4, LA, LB, EPI>(g, splits, st);
-    default: return ot::launch_gemm_f32<2, 2, 2, 2, LA, LB, EPI>(g, splits, st);
+    case kC128x128: return ot::launch_gemm_f32<2, 2, 4, 4, LA, LB, EPI, 16, ROLE>(g, splits, st);
+    case kC64x128: return ot::launch_gemm_f32<2, 2, 2, 4, LA, LB, EPI, 16, ROLE>(g, splits, st);
+    default: return ot::launch_gemm_f32<2, 2, 2, 2, LA, LB, EPI, 16, ROLE>(g, splits, st);
   }
 }
 
-template <Lay LA, Lay LB>
+template <Lay LA, Lay LB, int ROLE>
 hipError_t launch_epi(Epi epi, int cfg, const GemmArgs& g, int64_t splits, hipStream_t st) {
   switch (epi) {
-    case Epi::Store: return launch_cfg<LA, LB, Epi::Store>(cfg, g, splits, st);
-    case Epi::Bias: return launch_cfg<LA, LB, Epi::Bias>(cfg, g, splits, st);
-    case Epi::BiasRelu: return launch_cfg<LA, LB, Epi::BiasRelu>(cfg, g, splits, st);
-    case Epi::Mse: return launch_cfg<LA, LB, Epi::Mse>(cfg, g, splits, st);
-    case Epi::SplitK: return launch_cfg<LA, LB, Epi::SplitK>(cfg, g, splits, st);
-    default: return launch_cfg<LA, LB, Epi::Mask>(cfg, g, splits, st);
+    case Epi::Store: return launch_cfg<LA, LB, Epi::Store, ROLE>(cfg, g, splits, st);
+    case Epi::Bias: return launch_cfg<LA, LB, Epi::Bias, ROLE>(cfg, g, splits, st);
+    case Epi::BiasRelu: return launch_cfg<LA, LB, Epi::BiasRelu, ROLE>(cfg, g, splits, st);
+    case Epi::Mse: return launch_cfg<LA, LB, Epi::Mse, ROLE>(cfg, g, splits, st);
+    case Epi::SplitK: return launch_cfg<LA, LB, Epi::SplitK, ROLE>(cfg, g, splits, st);
+    default: return launch_cfg<LA, LB, Epi::Mask, ROLE>(cfg, g, splits, st);
   }
 }
 
@@ -524,7 +524,7 @@ int ensure_split_ws(ot_surrogate* s, int64_t elems, int64_t rs_elems) {
 // C = epi(A B) with the plan's tile shape; split-K runs write partial sums to
 // the workspace and a second kernel applies the epilogue (fixed split order).
 // ph_gemm / ph_reduce: timing phases of the two halves (-1: not timed).
-template <Lay LA, Lay LB>
+template <Lay LA, Lay LB, int ROLE = 0>
 int run_gemm(ot_surrogate* s, GemmArgs g, Epi epi, hipStream_t st, const char* what, bool allow_split,
              int ph_gemm = -1, int ph_reduce = -1, int64_t* blocks_out = nullptr) {
   const Plan p = make_plan(g.M, g.N, g.K, allow_split && epi != Epi::Mse);
@@ -533,7 +533,7 @@ int run_gemm(ot_surrogate* s, GemmArgs g, Epi epi, hipStream_t st, const char* w
   if (p.splits == 1) {
     g.k_chunk = g.K;
     if (ph_gemm >= 0) tm.mark(st, ph_gemm, 0);
-    hipError_t e = launch_epi<LA, LB>(epi, p.cfg, g, 1, st);
+    hipError_t e = launch_epi<LA, LB, ROLE>(epi, p.cfg, g, 1, st);
     if (e != hipSuccess) return ot::set_error(OT_E_HIP, "launch of %s GEMM failed: %s", what, hipGetErrorString(e));
     if (ph_gemm >= 0) tm.mark(st, ph_gemm, 1);
     return OT_OK;
@@ -549,7 +549,7 @@ int run_gemm(ot_surrogate* s, GemmArgs g, Epi epi, hipStream_t st, const char* w
   h.rowsum = g.rowsum ? s->rsws : nullptr;
   h.rowsum_stride = g.M;
   if (ph_gemm >= 0) tm.mark(st, ph_gemm, 0);
-  hipError_t e = launch_epi<LA, LB>(Epi::SplitK, p.cfg, h, p.splits, st);
+  hipError_t e = launch_epi<LA, LB, ROLE>(Epi::SplitK, p.cfg, h, p.splits, st);
   if (e != hipSuccess) return ot::set_error(OT_E_HIP, "launch of %s GEMM failed: %s", what, hipGetErrorString(e));
   if (ph_gemm >= 0) tm.mark(st, ph_gemm, 1);
   if (ph_reduce >= 0) tm.mark(st, ph_reduce, 0);
@@ -1100,8 +1100,8 @@ extern "C" int surrogate_train_step(ot_surrogate* s, const float* x, int64_t ldx
       OT_REQUIRE(aligned16(x) && ldx % 4 == 0, "single-layer nets need 16-byte aligned x, ldx %% 4 == 0");
     n_partials = make_plan(g.M, g.N, g.K, false).blocks;
     if (n_partials > s->n_partials_cap) return ot::set_error(OT_E_STATE, "loss partial buffer too small");
-    if ((rc = run_gemm<Lay::KMajor, Lay::KMajor>(s, g, Epi::Mse, st, "output forward+MSE", false,
-                                                 OT_PH_FWD_OUTPUT)))
+    if ((rc = run_gemm<Lay::KMajor, Lay::KMajor, 1>(s, g, Epi::Mse, st, "output forward+MSE", false,
+                                                    OT_PH_FWD_OUTPUT)))
       return rc;
   }
   tm.mark(st, OT_PH_LOSS, 0);
@@ -1145,9 +1145,10 @@ extern "C" int surrogate_train_step(ot_surrogate* s, const float* x, int64_t ldx
       g.N = ly.in;
       g.K = b;
       g.rowsum = db;
-      if ((rc = run_gemm<Lay::MNMajor, Lay::MNMajor>(s, g, Epi::Store, st, "weight gradient", true, ph_w,
-                                                     ph_w >= 0 ? OT_PH_WGRAD_REDUCE : -1)))
-        return rc;
+      rc = (l == L) ? run_gemm<Lay::MNMajor, Lay::MNMajor, 1>(s, g, Epi::Store, st, "weight gradient", true, ph_w,
+                                                              OT_PH_WGRAD_REDUCE)
+                    : run_gemm<Lay::MNMajor, Lay::MNMajor, 0>(s, g, Epi::Store, st, "weight gradient", true);
+      if (rc) return rc;
     }
     if (l == 1) break;
     // input gradient dA_{l-1} = dZ_l W_l, then the ReLU mask of layer l-1
@@ -1163,10 +1164,10 @@ extern "C" int surrogate_train_step(ot_surrogate* s, const float* x, int64_t ldx
     g.ldc = s->ld[l - 1];
     g.mask = s->act[l - 1];
     g.ldmask = s->ld[l - 1];
-    if ((rc = run_gemm<Lay::KMajor, Lay::MNMajor>(s, g, Epi::Mask, st, "input gradient", true,
-                                                  l == L ? OT_PH_IGRAD_OUTPUT : -1,
-                                                  l == L ? OT_PH_IGRAD_REDUCE : -1)))
-      return rc;
+    rc = (l == L) ? run_gemm<Lay::KMajor, Lay::MNMajor, 1>(s, g, Epi::Mask, st, "input gradient", true,
+                                                           OT_PH_IGRAD_OUTPUT, OT_PH_IGRAD_REDUCE)
+                  : run_gemm<Lay::KMajor, Lay::MNMajor, 0>(s, g, Epi::Mask, st, "input gradient", true);
+    if (rc) return rc;
   }
   if (L >= 2) tm.mark(st, OT_PH_BWD_HIDDEN, 1);
 
@@ -1222,7 +1223,7 @@ extern "C" int surrogate_predict(ot_surrogate* s, const float* x, int64_t ldx, i
     g.N = D;
     g.K = lo.in;
     g.bias = s->params + lo.b_off;
-    if ((rc = run_gemm<Lay::KMajor, Lay::KMajor>(s, g, Epi::Bias, st, "output forward", true))) return rc;
+    if ((rc = run_gemm<Lay::KMajor, Lay::KMajor, 1>(s, g, Epi::Bias, st, "output forward", true))) return rc;
   }
   return OT_OK;
 }
