@@ -42,6 +42,13 @@ __device__ __forceinline__ uint16_t f2bf(float x) {
 }
 __device__ __forceinline__ float bf2f(uint16_t h) { return __uint_as_float((uint32_t)h << 16); }
 
+// Workgroup barrier that orders LDS accesses only.  __syncthreads() also
+// waits for every outstanding global memory access (vmcnt(0)), which would
+// drain loads that are meant to stay in flight across the barrier (k tiles of
+// the pipelined loop, prefetched epilogue operands); code that needs a global
+// load's data waits for it with its own vmcnt before this barrier.
+__device__ __forceinline__ void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
+
 enum class LayB : int { KMajor = 0, MNMajor = 1 };
 enum class EpiB : int {
   StoreF32 = 0,   // C (fp32) = acc
@@ -81,105 +88,149 @@ __device__ __forceinline__ int64_t xcd_remap_b(int64_t p, int64_t g) {
   return xcd * per + (xcd < rem ? xcd : rem) + q;
 }
 
-// Epilogue shared by the bf16 kernels.  `ep` holds this wavefront's WM x WN
-// fp32 accumulators (pitch WN + 4) for output rows mw.., columns nw..; each
-// lane then handles 4 consecutive columns of a row, so targets, bias and masks
-// are read, and C written, with vector accesses.  MseBf also writes, per
-// m-tile, the column sums of the rounded dY (the output bias gradient) when
-// g.colsum is set.  s_red: >= 8 doubles + 4 * WN floats of LDS.
-template <int WM, int WN, EpiB EPI>
-__device__ __forceinline__ void bf16_epilogue(const GemmBArgs& g, const float* ep, int64_t mw, int64_t nw,
-                                              int64_t tm, int64_t split, double* s_red) {
-  constexpr int EP = WN + 4;
-  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+// Epilogue shared by the bf16 kernels.  A wavefront stages its fp32
+// accumulators in LDS (`ep`, pitch WN + 4) for output rows mw.., columns nw..,
+// in chunks of ROWS rows; each lane then handles 4 consecutive columns of a
+// row, so targets, bias and masks are read, and C written, with vector
+// accesses.  The reads of a chunk's targets / masks are issued before the chunk
+// is staged, so their latency overlaps the staging.  MseBf also accumulates the
+// loss partial of the block and, per m-tile, the column sums of the rounded dY
+// (the output bias gradient) when g.colsum is set (finish()).
+template <int WN, EpiB EPI>
+struct BEpi {
+  static constexpr int EP = WN + 4;
+  static constexpr int CG = WN / 4;               // column groups of 4
+  static constexpr int RPP = 64 / CG;             // rows per pass of a wavefront
+  int cg, rl;
+  int64_t col;
+  bool cfull;
   float lsum = 0.f;
   float csum[4] = {0.f, 0.f, 0.f, 0.f};
-  const int cg = lane % (WN / 4);                 // column group of 4
-  const int rl = lane / (WN / 4);                 // row within a pass
-  constexpr int ROWS_PER_PASS = 64 / (WN / 4);
-  const int64_t col = nw + 4 * cg;
-  const bool cfull = col + 3 < g.N;
   float bias4[4] = {0.f, 0.f, 0.f, 0.f};
-  if constexpr (EPI == EpiB::BiasF32 || EPI == EpiB::BiasReluBf || EPI == EpiB::MseBf) {
-    if (cfull) {
-      const f32x4 t = *reinterpret_cast<const f32x4*>(g.bias + col);
-      bias4[0] = t[0]; bias4[1] = t[1]; bias4[2] = t[2]; bias4[3] = t[3];
-    } else {
-      for (int c = 0; c < 4; ++c) bias4[c] = (col + c < g.N) ? g.bias[col + c] : 0.f;
-    }
-  }
-  for (int rr = rl; rr < WM; rr += ROWS_PER_PASS) {
-    const int64_t m = mw + rr;
-    if (m >= g.M || col >= g.N) continue;
-    const f32x4 a4 = *reinterpret_cast<const f32x4*>(ep + rr * EP + 4 * cg);
-    float v[4] = {a4[0], a4[1], a4[2], a4[3]};
-    if constexpr (EPI == EpiB::StoreF32 || EPI == EpiB::SplitK || EPI == EpiB::BiasF32) {
-      if constexpr (EPI == EpiB::BiasF32)
-        for (int c = 0; c < 4; ++c) v[c] += bias4[c];
-      float* C = reinterpret_cast<float*>(g.C) + (EPI == EpiB::SplitK ? split * g.split_stride : 0) + m * g.ldc + col;
-      if (cfull) *reinterpret_cast<f32x4*>(C) = f32x4{v[0], v[1], v[2], v[3]};
-      else
-        for (int c = 0; c < 4; ++c)
-          if (col + c < g.N) C[c] = v[c];
-    } else {
-      if constexpr (EPI == EpiB::BiasReluBf) {
-        for (int c = 0; c < 4; ++c) { v[c] += bias4[c]; v[c] = v[c] > 0.f ? v[c] : 0.f; }
-      }
-      if constexpr (EPI == EpiB::MaskBf) {
-        const uint16_t* mp = g.mask + m * g.ldmask + col;
-        for (int c = 0; c < 4; ++c) {
-          const float mk = (col + c < g.N) ? bf2f(mp[c]) : 0.f;
-          v[c] = mk > 0.f ? v[c] : 0.f;
-        }
-      }
-      if constexpr (EPI == EpiB::MseBf) {
-        float t4[4];
-        const float* tp = g.target + m * g.ldt + col;
-        if (cfull) {
-          const f32x4 t = *reinterpret_cast<const f32x4*>(tp);
-          t4[0] = t[0]; t4[1] = t[1]; t4[2] = t[2]; t4[3] = t[3];
-        } else {
-          for (int c = 0; c < 4; ++c) t4[c] = (col + c < g.N) ? tp[c] : 0.f;
-        }
-        for (int c = 0; c < 4; ++c) {
-          const float r = (col + c < g.N) ? (v[c] + bias4[c]) - t4[c] : 0.f;
-          lsum += r * r;
-          v[c] = g.scale * r;
-        }
-      }
-      const uint16_t h4[4] = {f2bf(v[0]), f2bf(v[1]), f2bf(v[2]), f2bf(v[3])};
-      if constexpr (EPI == EpiB::MseBf)
-        for (int c = 0; c < 4; ++c) csum[c] += (col + c < g.N) ? bf2f(h4[c]) : 0.f;
-      uint16_t* C = reinterpret_cast<uint16_t*>(g.C) + m * g.ldc + col;
+
+  __device__ __forceinline__ BEpi(const GemmBArgs& g, int64_t nw) {
+    const int lane = threadIdx.x & 63;
+    cg = lane % CG;
+    rl = lane / CG;
+    col = nw + 4 * cg;
+    cfull = col + 3 < g.N;
+    if constexpr (EPI == EpiB::BiasF32 || EPI == EpiB::BiasReluBf || EPI == EpiB::MseBf) {
       if (cfull) {
-        *reinterpret_cast<u16x4*>(C) = u16x4{h4[0], h4[1], h4[2], h4[3]};
+        const f32x4 t = *reinterpret_cast<const f32x4*>(g.bias + col);
+        bias4[0] = t[0]; bias4[1] = t[1]; bias4[2] = t[2]; bias4[3] = t[3];
       } else {
-        for (int c = 0; c < 4; ++c)
-          if (col + c < g.N) C[c] = h4[c];
+        for (int c = 0; c < 4; ++c) bias4[c] = (col + c < g.N) ? g.bias[col + c] : 0.f;
       }
     }
   }
-  if constexpr (EPI == EpiB::MseBf) {
-    const double ls = warp_sum((double)lsum);
-    if (lane == 0) s_red[wid] = ls;
-    // lanes with the same lane % (WN/4) hold the same 4 columns: fold the
-    // ROWS_PER_PASS lanes, then the two wavefronts of each column half
-    for (int c = 0; c < 4; ++c)
-      for (int off = WN / 4; off < 64; off <<= 1) csum[c] += __shfl_xor(csum[c], off, 64);
-    float* xs = reinterpret_cast<float*>(s_red + 8);   // 4 waves x WN floats
-    if (rl == 0)
-      for (int c = 0; c < 4; ++c) xs[wid * WN + 4 * cg + c] = csum[c];
-    __syncthreads();
-    if (tid == 0) g.loss_partials[blockIdx.y * gridDim.x + blockIdx.x] = ((s_red[0] + s_red[1]) + s_red[2]) + s_red[3];
-    // waves (0, 1) share column half wn = 0, waves (2, 3) wn = 1
-    if (g.colsum && (wid & 1) == 0 && rl == 0) {
-      for (int c = 0; c < 4; ++c) {
-        const int64_t n = col + c;
-        if (n < g.N) g.colsum[tm * g.colsum_ld + n] = xs[wid * WN + 4 * cg + c] + xs[(wid + 1) * WN + 4 * cg + c];
+
+  // Rows m0 .. m0 + ROWS - 1 (ep row 0 = row m0).  stage() writes the chunk's
+  // accumulators into ep and makes them visible to the wavefront.
+  template <int ROWS, class Stage>
+  __device__ __forceinline__ void rows(const GemmBArgs& g, const float* ep, int64_t m0, int64_t split, Stage stage) {
+    static_assert(ROWS % RPP == 0, "chunk rows");
+    constexpr int NP = ROWS / RPP;
+    // targets (MseBf) or mask (MaskBf) of each pass; one branch around all
+    // the loads of the chunk, so that they are all in flight together
+    f32x4 pre[NP];
+    if constexpr (EPI == EpiB::MseBf || EPI == EpiB::MaskBf) {
+      if (cfull) {
+#pragma unroll
+        for (int i = 0; i < NP; ++i) {
+          const int64_t m = min(m0 + rl + RPP * i, g.M - 1);
+          if constexpr (EPI == EpiB::MseBf) {
+            pre[i] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(g.target + m * g.ldt + col));
+          } else {
+            const u16x4 h = *reinterpret_cast<const u16x4*>(g.mask + m * g.ldmask + col);
+            pre[i] = f32x4{bf2f(h[0]), bf2f(h[1]), bf2f(h[2]), bf2f(h[3])};
+          }
+        }
+      } else {
+#pragma unroll
+        for (int i = 0; i < NP; ++i) {
+          const int64_t m = min(m0 + rl + RPP * i, g.M - 1);
+          for (int c = 0; c < 4; ++c) {
+            if constexpr (EPI == EpiB::MseBf) pre[i][c] = (col + c < g.N) ? g.target[m * g.ldt + col + c] : 0.f;
+            else pre[i][c] = (col + c < g.N) ? bf2f(g.mask[m * g.ldmask + col + c]) : 0.f;
+          }
+        }
+      }
+    }
+    stage();
+    // every prefetched operand of the chunk has landed (one wait here rather
+    // than per row, where the row stores would be waited for too)
+    if constexpr (EPI == EpiB::MseBf || EPI == EpiB::MaskBf)
+      __builtin_amdgcn_s_waitcnt((0x7 << 4) | (0xF << 8));            // vmcnt(0)
+#pragma unroll
+    for (int i = 0; i < NP; ++i) {
+      const int rr = rl + RPP * i;
+      const int64_t m = m0 + rr;
+      if (m >= g.M || col >= g.N) continue;
+      const f32x4 a4 = *reinterpret_cast<const f32x4*>(ep + rr * EP + 4 * cg);
+      float v[4] = {a4[0], a4[1], a4[2], a4[3]};
+      if constexpr (EPI == EpiB::StoreF32 || EPI == EpiB::SplitK || EPI == EpiB::BiasF32) {
+        if constexpr (EPI == EpiB::BiasF32)
+          for (int c = 0; c < 4; ++c) v[c] += bias4[c];
+        float* C = reinterpret_cast<float*>(g.C) + (EPI == EpiB::SplitK ? split * g.split_stride : 0) + m * g.ldc + col;
+        if (cfull) *reinterpret_cast<f32x4*>(C) = f32x4{v[0], v[1], v[2], v[3]};
+        else
+          for (int c = 0; c < 4; ++c)
+            if (col + c < g.N) C[c] = v[c];
+      } else {
+        if constexpr (EPI == EpiB::BiasReluBf) {
+          for (int c = 0; c < 4; ++c) { v[c] += bias4[c]; v[c] = v[c] > 0.f ? v[c] : 0.f; }
+        }
+        if constexpr (EPI == EpiB::MaskBf) {
+          for (int c = 0; c < 4; ++c) v[c] = pre[i][c] > 0.f ? v[c] : 0.f;
+        }
+        if constexpr (EPI == EpiB::MseBf) {
+          for (int c = 0; c < 4; ++c) {
+            const float r = (col + c < g.N) ? (v[c] + bias4[c]) - pre[i][c] : 0.f;
+            lsum += r * r;
+            v[c] = g.scale * r;
+          }
+        }
+        const uint16_t h4[4] = {f2bf(v[0]), f2bf(v[1]), f2bf(v[2]), f2bf(v[3])};
+        if constexpr (EPI == EpiB::MseBf)
+          for (int c = 0; c < 4; ++c) csum[c] += (col + c < g.N) ? bf2f(h4[c]) : 0.f;
+        uint16_t* C = reinterpret_cast<uint16_t*>(g.C) + m * g.ldc + col;
+        if (cfull) {
+          *reinterpret_cast<u16x4*>(C) = u16x4{h4[0], h4[1], h4[2], h4[3]};
+        } else {
+          for (int c = 0; c < 4; ++c)
+            if (col + c < g.N) C[c] = h4[c];
+        }
       }
     }
   }
-}
+
+  // Block-level reductions of MseBf (loss partial, per-m-tile column sums).
+  // Waves with the same wn share a column half; wave w's column half is w / 2.
+  // s_red: >= 8 doubles + 4 * WN floats of LDS.
+  __device__ __forceinline__ void finish(const GemmBArgs& g, int64_t tm, double* s_red) {
+    if constexpr (EPI == EpiB::MseBf) {
+      const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+      const double ls = warp_sum((double)lsum);
+      if (lane == 0) s_red[wid] = ls;
+      // lanes with the same lane % CG hold the same 4 columns: fold the RPP
+      // lanes, then the two wavefronts of each column half
+      for (int c = 0; c < 4; ++c)
+        for (int off = CG; off < 64; off <<= 1) csum[c] += __shfl_xor(csum[c], off, 64);
+      float* xs = reinterpret_cast<float*>(s_red + 8);   // 4 waves x WN floats
+      if (rl == 0)
+        for (int c = 0; c < 4; ++c) xs[wid * WN + 4 * cg + c] = csum[c];
+      lds_barrier();
+      if (tid == 0)
+        g.loss_partials[blockIdx.y * gridDim.x + blockIdx.x] = ((s_red[0] + s_red[1]) + s_red[2]) + s_red[3];
+      if (g.colsum && (wid & 1) == 0 && rl == 0) {
+        for (int c = 0; c < 4; ++c) {
+          const int64_t n = col + c;
+          if (n < g.N) g.colsum[tm * g.colsum_ld + n] = xs[wid * WN + 4 * cg + c] + xs[(wid + 1) * WN + 4 * cg + c];
+        }
+      }
+    }
+  }
+};
 
 template <int FM, int FN, LayB LA, LayB LB, EpiB EPI, int BK>
 __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmBArgs g) {
@@ -358,14 +409,17 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmBArgs g) {
   constexpr int EP = WN + 4;
   float* ep = reinterpret_cast<float*>(smem) + wid * (WM * EP);
   // the main loop ended with a barrier, so the tile buffers are free
+  BEpi<WN, EPI> e(g, n0 + WN * wn);
+  e.template rows<WM>(g, ep, m0 + WM * wm, split, [&] {
 #pragma unroll
-  for (int f = 0; f < FM; ++f)
+    for (int f = 0; f < FM; ++f)
 #pragma unroll
-    for (int h = 0; h < FN; ++h)
+      for (int h = 0; h < FN; ++h)
 #pragma unroll
-      for (int r = 0; r < 4; ++r) ep[(16 * f + 4 * (lane / 16) + r) * EP + 16 * h + lane % 16] = acc[f][h][r];
-  __syncthreads();
-  bf16_epilogue<WM, WN, EPI>(g, ep, m0 + WM * wm, n0 + WN * wn, tm, split, s_red);
+        for (int r = 0; r < 4; ++r) ep[(16 * f + 4 * (lane / 16) + r) * EP + 16 * h + lane % 16] = acc[f][h][r];
+    lds_barrier();
+  });
+  e.finish(g, tm, s_red);
 }
 
 template <int FM, int FN, LayB LA, LayB LB, EpiB EPI, int BK>
@@ -389,38 +443,71 @@ constexpr int64_t gemm_bf16_tiles(int64_t M, int64_t N) {
 // Block tile BM x BN (256 x 128 or 128 x 256), 4 wavefronts of (BM/2) x (BN/2)
 // built from v_mfma_f32_32x32x16_bf16 (lane l supplies A[i = l%32][k =
 // 8 (l/32) + e], B[k = 8 (l/32) + e][j = l%32]; accumulator element r of
-// lane l is D[8 (r/4) + 4 (l/32) + r%4][l%32]), k tile 64, and a ring of 3 LDS
-// stages filled by direct global -> LDS loads
+// lane l is D[8 (r/4) + 4 (l/32) + r%4][l%32]), k tile BK (32 or 64), and a
+// ring of S LDS stages filled by direct global -> LDS loads
 // (global_load_lds_dwordx4: each lane's 16 bytes land at the wave's LDS base +
-// 16 * lane), so two k tiles are always in flight while the MFMAs consume the
-// third.  LDS rows are unpadded; instead the eight 16-byte chunks of each
-// aligned group are permuted by XOR with (row mod 8), so the MFMA operand reads
-// of 8 consecutive rows hit 8 different bank groups.
-//   KMajor operand: stage tile [mn][64] (8 chunks per row);
-//   MNMajor operand: stage tile [64][mn] (mn / 8 chunks per row), read with
-//   ds_read_b64_tr_b16 as in gemm_bf16_kernel.
-// Requirements: K (and the split size) a multiple of 64.  Rows / columns past
+// 16 * lane), so S - 1 k tiles are in flight while the MFMAs consume one.
+// OCC blocks share a CU (BK 32, 3 stages: 72 KB of LDS per block), so one
+// block's prologue and epilogue overlap another's main loop.
+//
+// LDS rows are unpadded; the 16-byte chunks of a row are permuted by XOR with a
+// function of the row (kswz / mswz), so that the operand reads of a quarter
+// wavefront (16 lanes) touch 16 different 16-byte bank groups:
+//   KMajor operand: stage tile [mn][BK] (BK / 8 chunks per row); lanes read 16
+//     consecutive rows at one chunk;
+//   MNMajor operand: stage tile [BK][mn] (mn / 8 chunks per row), read with
+//     ds_read_b64_tr_b16 (within each 16-lane group, lane c addresses row
+//     k0 + c/4, columns 4 (c%4)..+3 of a 16-column block, and lane i receives
+//     column i of those 4 rows): 4 rows x 4 chunks per half wavefront.
+//
+// Tile order: consecutive blocks walk the dimension with fewer tiles first, so
+// the blocks that share the large operand's tile run together (and, through
+// the XCD remap, on one XCD's L2).  With M <= N that is the m tiles sharing a
+// B tile; otherwise the n tiles sharing an A tile.  Split-K grids keep all
+// tiles of one split together.
+//
+// The loss partial of an MseBf block is stored at its hardware index
+// (blockIdx.y * gridDim.x + blockIdx.x); any fixed slot per block gives the
+// same fixed-order sum.
+//
+// Requirements: K (and the split size) a multiple of BK.  Rows / columns past
 // M or N are read from clamped addresses and their results are not stored.
-template <int BM, int BN, LayB LA, LayB LB, EpiB EPI>
-__global__ __launch_bounds__(256, 1) void gemm_bf16_pipe_kernel(GemmBArgs g) {
-  constexpr int NT = 256, BK = 64, S = 3;
+template <int BK>
+__device__ __forceinline__ int kswz(int row) {
+  return BK == 64 ? ((row >> 1) & 7) : ((row >> 2) & 3);
+}
+__device__ __forceinline__ int mswz(int row) { return 4 * (row & 3); }
+
+template <int BM, int BN, int BK, int S, int OCC, LayB LA, LayB LB, EpiB EPI>
+__global__ __launch_bounds__(256, OCC) void gemm_bf16_pipe_kernel(GemmBArgs g) {
+  constexpr int NT = 256;
   constexpr int WM = BM / 2, WN = BN / 2, FM = WM / 32, FN = WN / 32;
+  constexpr int KC = BK / 8;                                      // chunks per KMajor row
   constexpr int A_CH = BM * BK / 8, B_CH = BN * BK / 8;          // 16-byte chunks per stage
   constexpr int LA_N = A_CH / NT, LB_N = B_CH / NT;               // loads per thread per k tile
   static_assert(A_CH % NT == 0 && B_CH % NT == 0, "tile split");
+  static_assert(BK == 32 || BK == 64, "k tile");
+  static_assert((LA == LayB::KMajor || BM >= 128) && (LB == LayB::KMajor || BN >= 128), "MNMajor swizzle needs >= 16 chunks per row");
   constexpr int STAGE_BYTES = (A_CH + B_CH) * 16;
-  constexpr int EP_BYTES = 4 * WM * (WN + 4) * 4;
-  constexpr int LDS_BYTES = S * STAGE_BYTES > EP_BYTES ? S * STAGE_BYTES : EP_BYTES;
-  __shared__ __attribute__((aligned(16))) unsigned char smem[LDS_BYTES];
+  // epilogue chunk: CH_F fragments (32 CH_F rows) of each wave staged at once
+  constexpr int EP = WN + 4;
+  constexpr int CH_F = (4 * FM * 32 * EP * 4 <= S * STAGE_BYTES) ? FM : FM / 2;
+  static_assert(CH_F >= 1 && 4 * CH_F * 32 * EP * 4 <= S * STAGE_BYTES, "epilogue staging");
+  __shared__ __attribute__((aligned(16))) unsigned char smem[S * STAGE_BYTES];
   __shared__ double s_red[8 + 2 * WN];
 
   const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
   const int wm = wid % 2, wn = wid / 2;
-  const int64_t tiles_m = (g.M + BM - 1) / BM;
-  const int64_t logical = xcd_remap_b(blockIdx.x, (int64_t)gridDim.x);
-  const int64_t tm = logical % tiles_m, tn = logical / tiles_m;
+  const int64_t tiles_m = (g.M + BM - 1) / BM, tiles_n = (g.N + BN - 1) / BN;
+  // XCD remap over the whole grid, tiles fastest: the blocks of one k split
+  // run on one XCD and share its L2.
+  const int64_t lin = (int64_t)blockIdx.y * gridDim.x + blockIdx.x;
+  const int64_t l2 = xcd_remap_b(lin, (int64_t)gridDim.x * gridDim.y);
+  const int64_t logical = l2 % gridDim.x, split = l2 / gridDim.x;
+  int64_t tm, tn;
+  if (tiles_m <= tiles_n) { tm = logical % tiles_m; tn = logical / tiles_m; }
+  else { tn = logical % tiles_n; tm = logical / tiles_n; }
   const int64_t m0 = tm * BM, n0 = tn * BN;
-  const int64_t split = blockIdx.y;
   const int64_t kbeg = split * g.k_chunk;
   const int64_t kend = (kbeg + g.k_chunk < g.K) ? kbeg + g.k_chunk : g.K;
   const int nk = (int)((kend - kbeg) / BK);
@@ -432,12 +519,12 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_pipe_kernel(GemmBArgs g) {
   for (int i = 0; i < LA_N; ++i) {
     const int ci = (i * 4 + wid) * 64 + lane;
     if constexpr (LA == LayB::KMajor) {
-      const int row = ci / 8, pc = ci % 8, lc = pc ^ (row & 7);
+      const int row = ci / KC, pc = ci % KC, lc = pc ^ kswz<BK>(row);
       const int64_t m = min(m0 + row, g.M - 1);
       a_off[i] = m * g.lda + 8 * lc;
     } else {
       constexpr int CPR = BM / 8;
-      const int row = ci / CPR, pc = ci % CPR, lc = pc ^ (row & 7);
+      const int row = ci / CPR, pc = ci % CPR, lc = pc ^ mswz(row);
       const int64_t m = min(m0 + 8 * lc, (g.M - 1) / 8 * 8);
       a_off[i] = (int64_t)row * g.lda + m;
     }
@@ -446,12 +533,12 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_pipe_kernel(GemmBArgs g) {
   for (int i = 0; i < LB_N; ++i) {
     const int ci = (i * 4 + wid) * 64 + lane;
     if constexpr (LB == LayB::KMajor) {
-      const int row = ci / 8, pc = ci % 8, lc = pc ^ (row & 7);
+      const int row = ci / KC, pc = ci % KC, lc = pc ^ kswz<BK>(row);
       const int64_t n = min(n0 + row, g.N - 1);
       b_off[i] = n * g.ldb + 8 * lc;
     } else {
       constexpr int CPR = BN / 8;
-      const int row = ci / CPR, pc = ci % CPR, lc = pc ^ (row & 7);
+      const int row = ci / CPR, pc = ci % CPR, lc = pc ^ mswz(row);
       const int64_t n = min(n0 + 8 * lc, (g.N - 1) / 8 * 8);
       b_off[i] = (int64_t)row * g.ldb + n;
     }
@@ -484,14 +571,14 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_pipe_kernel(GemmBArgs g) {
     if (kmajor) {
       const int row = base + lane % 32;
       const int lc = 2 * kk + lane / 32;
-      return *reinterpret_cast<const bf16x8*>(st + (row * 8 + (lc ^ (row & 7))) * 16);
+      return *reinterpret_cast<const bf16x8*>(st + (row * KC + (lc ^ kswz<BK>(row))) * 16);
     }
     const int c = lane % 16, q = lane / 16;
     const int col = base + 16 * (q & 1) + 4 * (c % 4);
     const int r0 = 16 * kk + 8 * (q >> 1) + c / 4, r1 = r0 + 4;
     const int ch = col / 8, half = (col / 4) & 1;
-    bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(st + (r0 * cpr + (ch ^ (r0 & 7))) * 16 + half * 8));
-    bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(st + (r1 * cpr + (ch ^ (r1 & 7))) * 16 + half * 8));
+    bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(st + (r0 * cpr + (ch ^ mswz(r0))) * 16 + half * 8));
+    bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(st + (r1 * cpr + (ch ^ mswz(r1))) * 16 + half * 8));
     return bf16x8{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
   };
 
@@ -504,14 +591,16 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_pipe_kernel(GemmBArgs g) {
   // vmcnt wait with lgkm / exp counters left unconstrained (gfx9 encoding)
 #define OT_WAIT_VM(n) __builtin_amdgcn_s_waitcnt(((n) & 0xF) | (0x7 << 4) | (0xF << 8) | (((n) >> 4) << 14))
   constexpr int PER_TILE = LA_N + LB_N;
+  static_assert((S - 2) * PER_TILE <= 63, "vmcnt range");
   for (int s = 0; s < S - 1; ++s)
     if (s < nk) issue(s, s);
   for (int kt = 0; kt < nk; ++kt) {
-    // tile kt's loads are the oldest outstanding ones; later tiles may stay in flight
+    // tile kt's loads are the oldest outstanding ones; up to S - 2 later tiles may stay in flight
     const int ahead = min(S - 2, nk - 1 - kt);
-    if (ahead >= 1) OT_WAIT_VM(PER_TILE);
+    if (ahead >= 2) OT_WAIT_VM(2 * PER_TILE);
+    else if (ahead == 1) OT_WAIT_VM(PER_TILE);
     else OT_WAIT_VM(0);
-    __syncthreads();
+    lds_barrier();
     if (kt + S - 1 < nk) issue(kt + S - 1, (kt + S - 1) % S);
     const unsigned char* sa = smem + (kt % S) * STAGE_BYTES;
     const unsigned char* sb = sa + A_CH * 16;
@@ -530,26 +619,34 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_pipe_kernel(GemmBArgs g) {
     }
   }
 #undef OT_WAIT_VM
-  __syncthreads();
+  static_assert(S <= 4, "wait depth");
 
-  constexpr int EP = WN + 4;
-  float* ep = reinterpret_cast<float*>(smem) + wid * (WM * EP);
+  // Epilogue in FM / CH_F chunks of 32 CH_F rows per wave, staged through the
+  // (now free) stage buffers.
+  float* ep = reinterpret_cast<float*>(smem) + wid * (CH_F * 32 * EP);
+  BEpi<WN, EPI> e(g, n0 + WN * wn);
 #pragma unroll
-  for (int f = 0; f < FM; ++f)
+  for (int c0 = 0; c0 < FM; c0 += CH_F) {
+    e.template rows<CH_F * 32>(g, ep, m0 + WM * wm + 32 * c0, split, [&] {
+      lds_barrier();                  // other waves are done with the stage buffers / previous chunk
 #pragma unroll
-    for (int h = 0; h < FN; ++h)
+      for (int f = 0; f < CH_F; ++f)
 #pragma unroll
-      for (int r = 0; r < 16; ++r)
-        ep[(32 * f + 8 * (r / 4) + 4 * (lane / 32) + r % 4) * EP + 32 * h + lane % 32] = acc[f][h][r];
-  __syncthreads();
-  bf16_epilogue<WM, WN, EPI>(g, ep, m0 + WM * wm, n0 + WN * wn, tm, split, s_red);
+        for (int h = 0; h < FN; ++h)
+#pragma unroll
+          for (int r = 0; r < 16; ++r)
+            ep[(32 * f + 8 * (r / 4) + 4 * (lane / 32) + r % 4) * EP + 32 * h + lane % 32] = acc[c0 + f][h][r];
+      lds_barrier();
+    });
+  }
+  e.finish(g, tm, s_red);
 }
 
-template <int BM, int BN, LayB LA, LayB LB, EpiB EPI>
+template <int BM, int BN, int BK, int S, int OCC, LayB LA, LayB LB, EpiB EPI>
 hipError_t launch_gemm_bf16_pipe(const GemmBArgs& g, int64_t splits, hipStream_t stream) {
   const int64_t tiles = ((g.M + BM - 1) / BM) * ((g.N + BN - 1) / BN);
-  hipLaunchKernelGGL((gemm_bf16_pipe_kernel<BM, BN, LA, LB, EPI>), dim3((unsigned)tiles, (unsigned)splits), dim3(256),
-                     0, stream, g);
+  hipLaunchKernelGGL((gemm_bf16_pipe_kernel<BM, BN, BK, S, OCC, LA, LB, EPI>), dim3((unsigned)tiles, (unsigned)splits),
+                     dim3(256), 0, stream, g);
   return hipGetLastError();
 }
 

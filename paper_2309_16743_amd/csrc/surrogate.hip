@@ -199,29 +199,59 @@ __global__ __launch_bounds__(256) void loss_finalize_kernel(const double* __rest
 // Adam (Kingma and Ba, 2015, Algorithm 1) over the flat parameter buffer, fp32:
 //   m = b1 m + (1 - b1) g;  v = b2 v + (1 - b2) g^2;
 //   p = p - lr * (m / c1) / (sqrt(v / c2) + eps),  c1 = 1 - b1^t, c2 = 1 - b2^t.
+__device__ __forceinline__ void adam4(f32x4& pp, const f32x4 gg, f32x4& mm, f32x4& vv, float lr, float b1, float b2,
+                                      float eps, float c1, float c2) {
+#pragma unroll
+  for (int c = 0; c < 4; ++c) {
+    mm[c] = b1 * mm[c] + (1.0f - b1) * gg[c];
+    vv[c] = b2 * vv[c] + (1.0f - b2) * (gg[c] * gg[c]);
+    const float mhat = mm[c] / c1;
+    const float vhat = vv[c] / c2;
+    pp[c] = pp[c] - lr * mhat / (sqrtf(vhat) + eps);
+  }
+}
+
+// Streaming kernel: two 16-byte groups per thread and pass (eight loads in
+// flight), non-temporal accesses (the state is touched once per step).
 __global__ __launch_bounds__(256) void adam_kernel(float* __restrict__ p, const float* __restrict__ g,
                                                    float* __restrict__ m, float* __restrict__ v,
                                                    int64_t n4, float lr, float b1, float b2, float eps,
                                                    float c1, float c2, uint16_t* __restrict__ pb) {
+  f32x4* P = reinterpret_cast<f32x4*>(p);
+  const f32x4* G = reinterpret_cast<const f32x4*>(g);
+  f32x4* Mv = reinterpret_cast<f32x4*>(m);
+  f32x4* V = reinterpret_cast<f32x4*>(v);
+  u16x4* PB = reinterpret_cast<u16x4*>(pb);
   const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n4; i += stride) {
-    f32x4 pp = reinterpret_cast<f32x4*>(p)[i];
-    const f32x4 gg = reinterpret_cast<const f32x4*>(g)[i];
-    f32x4 mm = reinterpret_cast<f32x4*>(m)[i];
-    f32x4 vv = reinterpret_cast<f32x4*>(v)[i];
+  int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  for (; i + stride < n4; i += 2 * stride) {
+    f32x4 pp[2], gg[2], mm[2], vv[2];
 #pragma unroll
-    for (int c = 0; c < 4; ++c) {
-      mm[c] = b1 * mm[c] + (1.0f - b1) * gg[c];
-      vv[c] = b2 * vv[c] + (1.0f - b2) * (gg[c] * gg[c]);
-      const float mhat = mm[c] / c1;
-      const float vhat = vv[c] / c2;
-      pp[c] = pp[c] - lr * mhat / (sqrtf(vhat) + eps);
+    for (int u = 0; u < 2; ++u) {
+      const int64_t j = i + u * stride;
+      pp[u] = __builtin_nontemporal_load(P + j);
+      gg[u] = __builtin_nontemporal_load(G + j);
+      mm[u] = __builtin_nontemporal_load(Mv + j);
+      vv[u] = __builtin_nontemporal_load(V + j);
     }
-    reinterpret_cast<f32x4*>(p)[i] = pp;
-    reinterpret_cast<f32x4*>(m)[i] = mm;
-    reinterpret_cast<f32x4*>(v)[i] = vv;
-    if (pb)   // bf16 copy of the updated master weights
-      reinterpret_cast<u16x4*>(pb)[i] = u16x4{f2bf(pp[0]), f2bf(pp[1]), f2bf(pp[2]), f2bf(pp[3])};
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      const int64_t j = i + u * stride;
+      adam4(pp[u], gg[u], mm[u], vv[u], lr, b1, b2, eps, c1, c2);
+      __builtin_nontemporal_store(pp[u], P + j);
+      __builtin_nontemporal_store(mm[u], Mv + j);
+      __builtin_nontemporal_store(vv[u], V + j);
+      if (pb)   // bf16 copy of the updated master weights
+        __builtin_nontemporal_store(u16x4{f2bf(pp[u][0]), f2bf(pp[u][1]), f2bf(pp[u][2]), f2bf(pp[u][3])}, PB + j);
+    }
+  }
+  if (i < n4) {
+    f32x4 pp = P[i], mm = Mv[i], vv = V[i];
+    adam4(pp, G[i], mm, vv, lr, b1, b2, eps, c1, c2);
+    P[i] = pp;
+    Mv[i] = mm;
+    V[i] = vv;
+    if (pb) PB[i] = u16x4{f2bf(pp[0]), f2bf(pp[1]), f2bf(pp[2]), f2bf(pp[3])};
   }
 }
 
@@ -607,30 +637,32 @@ using ot::EpiB;
 using ot::GemmBArgs;
 using ot::LayB;
 
-// bf16 tiles: the pipelined 256 x 128 kernel (k tile 64, direct-to-LDS loads)
-// for large products; 128 x 128 (4 x 4 fragments per wave) and 64 x 64 (2 x 2)
-// with a k tile of 32 otherwise.
+// bf16 tiles: the pipelined 256 x 128 kernel (k tile 32, direct-to-LDS loads,
+// two blocks per CU) for large products; 128 x 128 (4 x 4 fragments per wave)
+// and 64 x 64 (2 x 2) with a k tile of 32 otherwise.
 enum CfgB : int { kB128 = 0, kB64 = 1, kBPipe = 2 };
 constexpr int kBK = 32;
-constexpr int kPipeBK = 64;
+constexpr int kPipeBK = 32;
 
 int64_t tiles_b(int cfg, int64_t M, int64_t N) {
   if (cfg == kBPipe) return ot::gemm_bf16_pipe_tiles<256, 128>(M, N);
   return cfg == kB128 ? ot::gemm_bf16_tiles<4, 4>(M, N) : ot::gemm_bf16_tiles<2, 2>(M, N);
 }
 
-// The pipelined kernel when k is a multiple of its 64-deep k tile and its
-// tiles (split over k when needed, at least 16 k tiles per split) give about
-// one block per CU; else 128 x 128 tiles when they give about two blocks per
-// CU; long k ranges are split over 128 x 128 tiles, shorter ones over 64 x 64.
-Plan make_plan_b(int64_t M, int64_t N, int64_t K, bool allow_split) {
+// The pipelined kernel when k is a multiple of its 32-deep k tile and its
+// tiles give about one block per CU or more (long k ranges split until about
+// four blocks per CU, keeping at least 32 k tiles per split); else 128 x 128
+// tiles when they give about two blocks per CU; long k ranges are split over
+// 128 x 128 tiles, shorter ones over 64 x 64.
+// pipe_ok: the pipelined kernel may be used (it has no row-sum output).
+Plan make_plan_b(int64_t M, int64_t N, int64_t K, bool allow_split, bool pipe_ok = true) {
   constexpr int64_t kCUs = 256;
   Plan p;
-  if (K % kPipeBK == 0 && M >= 256 && N >= 128) {
+  if (pipe_ok && K % kPipeBK == 0 && M >= 256 && N >= 128) {
     const int64_t t = tiles_b(kBPipe, M, N);
     int64_t sp = 1;
     if (allow_split)
-      while (t * sp < 2 * kCUs - 32 && K / (2 * sp) >= 16 * kPipeBK) sp *= 2;
+      while (t * sp < 4 * kCUs - 64 && K / (2 * sp) >= 32 * kPipeBK) sp *= 2;
     if (t * sp >= kCUs - 16) {
       p.cfg = kBPipe;
       p.k_chunk = ot::round_up(ot::ceil_div(K, sp), kPipeBK);
@@ -659,7 +691,8 @@ Plan make_plan_b(int64_t M, int64_t N, int64_t K, bool allow_split) {
 
 template <LayB LA, LayB LB, EpiB E>
 hipError_t launch_cfg_b(int cfg, const GemmBArgs& g, int64_t splits, hipStream_t st) {
-  if (cfg == kBPipe) return ot::launch_gemm_bf16_pipe<256, 128, LA, LB, E>(g, splits, st);
+  // 256 x 128 tile, k tile 32, 3 stages, 2 blocks per CU
+  if (cfg == kBPipe) return ot::launch_gemm_bf16_pipe<256, 128, kPipeBK, 3, 2, LA, LB, E>(g, splits, st);
   if (cfg == kB128) return ot::launch_gemm_bf16<4, 4, LA, LB, E, kBK>(g, splits, st);
   return ot::launch_gemm_bf16<2, 2, LA, LB, E, kBK>(g, splits, st);
 }
@@ -669,7 +702,7 @@ hipError_t launch_cfg_b(int cfg, const GemmBArgs& g, int64_t splits, hipStream_t
 template <LayB LA, LayB LB, EpiB E>
 int run_gemm_b(ot_surrogate* s, GemmBArgs g, hipStream_t st, const char* what, bool allow_split,
                int ph_gemm = -1, int ph_reduce = -1, int64_t* blocks_out = nullptr) {
-  const Plan p = make_plan_b(g.M, g.N, g.K, allow_split && E != EpiB::MseBf);
+  const Plan p = make_plan_b(g.M, g.N, g.K, allow_split && E != EpiB::MseBf, g.rowsum == nullptr);
   if (blocks_out) *blocks_out = p.blocks;
   ot::PhaseTimer& tm = s->timer;
   if (p.splits == 1) {
@@ -1044,7 +1077,7 @@ static int adam_step(ot_surrogate* s, hipStream_t st) {
   const double c1 = 1.0 - std::pow((double)s->beta1, (double)s->t);
   const double c2 = 1.0 - std::pow((double)s->beta2, (double)s->t);
   const int64_t n4 = s->n_flat / 4;
-  const int64_t blocks = std::min<int64_t>(ot::ceil_div(n4, 256), 8192);
+  const int64_t blocks = std::min<int64_t>(ot::ceil_div(n4, 256), 32768);
   tm.mark(st, OT_PH_ADAM, 0);
   hipLaunchKernelGGL(ot::adam_kernel, dim3((unsigned)blocks), dim3(256), 0, st, s->params, s->grads, s->m, s->v, n4,
                      s->lr, s->beta1, s->beta2, s->eps, (float)c1, (float)c2, s->pb);

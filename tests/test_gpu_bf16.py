@@ -57,6 +57,7 @@ SHAPES = [
     ((6, 128, 128, 128, 300), 64),     # three hidden layers
     ((6, 512, 512, 20000), 512),       # pipelined 256 x 128 kernel, the bf16 workloads' batch
     ((6, 512, 512, 30001), 320),       # pipelined kernel with ragged M and N (clamped edges)
+    ((6, 1024, 1024, 69984), 512),     # split-K pipelined input gradient (63 splits, ragged last split)
 ]
 
 
