@@ -20,6 +20,13 @@ samples (80 / 120 GB).  The reservoir is filled with generated chunks
 (untimed); timed puts cycle through a pool of pre-generated chunks of 64
 samples.
 
+--config stress-100k-rows: the reservoir alone with rows of 100,000 floats,
+capacity 50,000 (20 GB slab), threshold 10,000, 64 producer streams putting
+chunks of 256 rows and one consumer drawing batches of 256 into a batch
+buffer; `value` is then the reservoir's data rate in GB/s (rows accepted by
+puts plus rows gathered, each moved once in and once out) over the timed
+iterations (one put and one draw each).
+
 Prints one JSON line.  `value` is samples processed per second by the train
 step (batch size x steps / time), from HIP events on the work stream over the
 timed steps.  `roofline` reports the dominant kernel's algorithmic rate
@@ -354,6 +361,162 @@ def run_field(args, w):
     return line
 
 
+def cpu_baseline_stress(w, seconds: float) -> dict:
+    """The oracle reservoir (put + draw + gather of 100,000-float rows) on this
+    host at a reduced capacity of 5,000 rows (2 GB slab), timed in steady state."""
+    from fixtures import synthetic
+    from oracle.reservoir import OK, Reservoir
+    C, T, D, k, B = 5000, 1000, w.row_len, w.chunk, w.batch
+    res = Reservoir(C, T, 6, D, w.reservoir_seed)
+    pool = [(synthetic.hash_inputs(np.arange(i * k, (i + 1) * k)), synthetic.hash_rows(np.arange(i * k, (i + 1) * k), D))
+            for i in range(2)]
+    i = 0
+    while res.N < C:                                 # fill (untimed), drawing once past the threshold
+        res.put(*pool[i % 2])
+        if res.N > T:
+            res.sample_batch(B)
+        i += 1
+    rows_in = rows_out = steps = 0
+    t0 = time.perf_counter()
+    while steps < 2 or time.perf_counter() - t0 < seconds:
+        _, a, _, _ = res.put(*pool[i % 2])
+        st, slots, _, _, _ = res.sample_batch(B)
+        assert st == OK
+        rows_in += a
+        rows_out += len(slots)
+        i += 1
+        steps += 1
+    dt = time.perf_counter() - t0
+    row_bytes = 2 * (D + 6) * 4
+    return {"value": round((rows_in + rows_out) * row_bytes / dt / 1e9, 3), "unit": "GB/s", "cores": 1,
+            "kind": "oracle",
+            "sample": f"{steps} iterations of put {k} rows + draw {B} rows (with gather) on a host reservoir of "
+                      f"capacity {C} (reduced from {w.capacity}; 2 GB slab) in steady state; numpy row copies, "
+                      f"one thread; {rows_in} rows accepted, {rows_out} drawn"}
+
+
+def run_stress(args):
+    """Reservoir-only workload: 100,000-float rows, 64 producer streams, one consumer."""
+    import torch
+
+    from fixtures import configs, synthetic
+    from paper_2309_16743_amd import OT_OK, Reservoir
+    w = configs.STRESS
+    K = args.steps or 2000
+    warmup = 20 if args.warmup is None else args.warmup
+    dev = torch.device("cuda:0")
+    D, k, B, P = w.row_len, w.chunk, w.batch, w.producers
+    order = torch.cuda.Stream(device=dev)
+    cons = torch.cuda.Stream(device=dev)
+    streams = [torch.cuda.Stream(device=dev) for _ in range(P)]
+    res = Reservoir(w.capacity, w.threshold, 6, D, w.reservoir_seed, order_stream=order)
+    xs, us = [], []
+    for p, s in enumerate(streams):                  # one chunk per producer stream (hash rows; untimed)
+        with torch.cuda.stream(s):
+            keys = torch.arange(p * k, (p + 1) * k, device=dev, dtype=torch.int64)
+            u = torch.empty(k, D, device=dev)
+            synthetic.hash_rows_torch(keys, D, out=u)
+            x = torch.empty(k, 8, device=dev)[:, :6]
+            x.copy_(synthetic.hash_inputs_torch(keys, 6))
+        xs.append(x)
+        us.append(u)
+    slots = torch.empty(B, dtype=torch.int32, device=dev)
+    xb = torch.empty(B, 8, device=dev)[:, :6]
+    ub = torch.empty(B, D, device=dev)
+    torch.cuda.synchronize()
+    row_bytes = 2 * (D + 6) * 4                      # read the source row + write the slab row (u and x)
+
+    # fill: 195 whole chunks from the producer streams, every row accepted
+    n_fill = w.capacity // k
+    res.timing_begin(["put_copy"], n_fill)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(order)
+    for i in range(n_fill):
+        res.put(xs[i % P], us[i % P], stream=streams[i % P])
+    e1.record(order)
+    torch.cuda.synchronize()
+    fill_ms = e0.elapsed_time(e1)
+    fill_copy_ms, fill_copies = res.timing_end()["put_copy"]
+    fill_rate = n_fill * k * row_bytes / (fill_ms * 1e-3)
+
+    # steady state: each iteration, one producer stream puts a chunk (replacing seen rows once full)
+    # and the consumer draws a batch with its gather
+    def iteration(i, direct=False):
+        res.put(xs[i % P], us[i % P], stream=order if direct else streams[i % P], accepted=acc[i:i + 1])
+        st, _, _ = res.sample_batch(B, slots, x_out=xb, u_out=ub, stream=order if direct else cons)
+        assert st == OT_OK
+
+    def timed(first, direct, timing):
+        torch.cuda.synchronize()
+        s0 = res.stats()
+        if timing:
+            res.timing_begin(["put_copy", "gather"], 2 * K + 8)
+        t_wall = time.perf_counter()
+        e0.record(order)
+        for i in range(first, first + K):
+            iteration(i, direct)
+        e1.record(order)
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - t_wall
+        tim = res.timing_end() if timing else None
+        s1 = res.stats()
+        rows_in = int(acc[first:first + K].sum().item())
+        assert s1["total_put"] - s0["total_put"] == rows_in and s1["total_draws"] - s0["total_draws"] == B * K
+        return e0.elapsed_time(e1), wall, rows_in, tim
+
+    acc = torch.zeros(2 * K + warmup, dtype=torch.int64, device=dev)
+    for i in range(warmup):
+        iteration(i)
+    gpu_ms, wall, rows_in, tim = timed(warmup, False, True)
+    d_ms, d_wall, d_rows_in, _ = timed(warmup + K, True, False)
+    rows_out = B * K
+    total_bytes = (rows_in + rows_out) * row_bytes
+    value = total_bytes / (gpu_ms * 1e-3) / 1e9
+    direct_rate = (d_rows_in + rows_out) * row_bytes / (d_ms * 1e-3) / 1e9
+    g_ms, g_n = tim["gather"]
+    c_ms, c_n = tim["put_copy"]
+    assert g_n == K and c_n == K
+    g_avg = g_ms * 1e-3 / g_n
+    g_rate = B * row_bytes / g_avg
+    put_rate = rows_in * row_bytes / (c_ms * 1e-3)
+    dom = "gather" if g_ms >= c_ms else "put_copy"
+    if dom == "gather":
+        roof = {"bound": "hbm", "kernel": "gather_kernel", "achieved": round(g_rate / 1e9, 1), "peak": PEAK_HBM / 1e9,
+                "unit": "GB/s", "frac": round(g_rate / PEAK_HBM, 4), "traffic": None,
+                "per_launch_bytes": B * row_bytes, "avg_us": round(g_avg * 1e6, 2)}
+    else:
+        c_avg = c_ms * 1e-3 / c_n
+        roof = {"bound": "hbm", "kernel": "put_copy_kernel", "achieved": round(put_rate / 1e9, 1),
+                "peak": PEAK_HBM / 1e9, "unit": "GB/s", "frac": round(put_rate / PEAK_HBM, 4), "traffic": None,
+                "per_launch_bytes": round(rows_in * row_bytes / c_n), "avg_us": round(c_avg * 1e6, 2)}
+    line = {
+        "metric": METRIC, "value": round(value, 1), "unit": "GB/s", "n_gpus": 1, "steps": K, "warmup": warmup,
+        "ms_per_step": round(gpu_ms / K, 4), "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "f32", "data": "synthetic",
+        "config": {"workload": w.name, "row_floats": D, "capacity": w.capacity, "threshold": w.threshold,
+                   "producer_streams": P, "chunk": k, "batch": B,
+                   "rows": "hash rows (value = hash of the row key, exact in fp32)"},
+        "roofline": roof,
+        "put": {"achieved": round(put_rate / 1e9, 1), "unit": "GB/s", "frac_hbm": round(put_rate / PEAK_HBM, 4),
+                "rows_accepted": rows_in, "rows_offered": k * K, "copy_ms": round(c_ms, 3)},
+        "gather": {"achieved": round(g_rate / 1e9, 1), "unit": "GB/s", "frac_hbm": round(g_rate / PEAK_HBM, 4),
+                   "rows": rows_out, "avg_us": round(g_avg * 1e6, 2)},
+        "same_stream": {"achieved": round(direct_rate, 1), "unit": "GB/s", "ms_per_step": round(d_ms / K, 4),
+                        "note": "the same iterations issued on the reservoir's ordering stream (no cross-stream "
+                                "events)"},
+        "host_s_per_step": round(wall / K, 6),
+        "fill": {"achieved": round(fill_rate / 1e9, 1), "unit": "GB/s", "puts": n_fill,
+                 "copy_avg_us": round(fill_copy_ms * 1e3 / fill_copies, 2), "ms": round(fill_ms, 3)},
+        "wall_s": round(wall, 3), "cpu_baseline": None,
+    }
+    res.close()
+    del xs, us, ub
+    torch.cuda.empty_cache()
+    if args.cpu_seconds > 0:
+        line["cpu_baseline"] = cpu_baseline_stress(w, args.cpu_seconds)
+    return line
+
+
 def main():
     args = parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -362,11 +525,15 @@ def main():
               "this build has no multi-GPU path.", file=sys.stderr)
         sys.exit(2)
     from fixtures import configs
-    if args.config not in configs.ALL:
-        print(f"unknown config {args.config}; choose from {sorted(configs.ALL)}", file=sys.stderr)
-        sys.exit(2)
-    w = configs.ALL[args.config]
-    line = run_heat(args, w) if w.fields == "ftcs" else run_field(args, w)
+    if args.config == configs.STRESS.name:
+        line = run_stress(args)
+    else:
+        if args.config not in configs.ALL:
+            print(f"unknown config {args.config}; choose from {sorted(configs.ALL) + [configs.STRESS.name]}",
+                  file=sys.stderr)
+            sys.exit(2)
+        w = configs.ALL[args.config]
+        line = run_heat(args, w) if w.fields == "ftcs" else run_field(args, w)
     text = json.dumps(line)
     print(text, flush=True)
     if args.out:

@@ -57,12 +57,17 @@ HASH_MUL_COL = 40503
 HASH_MOD = 1 << 24
 
 
-def hash_rows(keys: np.ndarray, d: int) -> np.ndarray:
-    """u[c] = float((key * 2654435761 + c * 40503) mod 2^24), fp32, shape (len(keys), d)."""
+def hash_values(keys: np.ndarray, cols: np.ndarray) -> np.ndarray:
+    """Columns `cols` of the hash rows of `keys`: fp32, shape (len(keys), len(cols))."""
     keys = np.asarray(keys, dtype=np.uint64)
-    c = np.arange(d, dtype=np.uint64)
+    c = np.asarray(cols, dtype=np.uint64)
     v = (keys[:, None] * np.uint64(HASH_MUL_KEY) + c[None, :] * np.uint64(HASH_MUL_COL)) % np.uint64(HASH_MOD)
     return v.astype(np.float32)
+
+
+def hash_rows(keys: np.ndarray, d: int) -> np.ndarray:
+    """u[c] = float((key * 2654435761 + c * 40503) mod 2^24), fp32, shape (len(keys), d)."""
+    return hash_values(keys, np.arange(d))
 
 
 def hash_inputs(keys: np.ndarray, x_dim: int = 6) -> np.ndarray:
@@ -106,3 +111,28 @@ def sine_mode_fields_torch(X, t, seed: int, basis, out=None):
     res = torch.addmm(m[:, None].expand(-1, basis.shape[1]), a, basis) if out is None else \
         torch.addmm(m[:, None].expand(-1, basis.shape[1]), a, basis, out=out)
     return res
+
+
+def hash_rows_torch(keys, d: int, out=None):
+    """hash_rows on the GPU with torch int64 arithmetic (exact for keys < 2^31):
+    (len(keys), d) fp32.  keys: int64 device tensor; out: optional (len(keys), >= d)
+    fp32 view whose first d columns are written."""
+    import torch
+    keys = keys.to(torch.int64)
+    c = torch.arange(d, device=keys.device, dtype=torch.int64)
+    v = ((keys[:, None] * HASH_MUL_KEY) % HASH_MOD + (c[None, :] * HASH_MUL_COL) % HASH_MOD) % HASH_MOD
+    if out is None:
+        return v.to(torch.float32)
+    out[:, :d].copy_(v)
+    return out
+
+
+def hash_inputs_torch(keys, x_dim: int = 6):
+    """hash_inputs on the GPU: (len(keys), x_dim) fp32."""
+    import torch
+    keys = keys.to(torch.int64)
+    out = torch.zeros(keys.shape[0], x_dim, device=keys.device, dtype=torch.float32)
+    out[:, 0] = (keys % HASH_MOD).to(torch.float32)
+    if x_dim > 1:
+        out[:, 1] = (keys >> 24).to(torch.float32)
+    return out

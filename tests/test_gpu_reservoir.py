@@ -10,6 +10,7 @@ import torch
 
 from fixtures.synthetic import hash_inputs, hash_rows
 from oracle import reservoir as orv
+from tests.reservoir_checks import compare_meta
 
 pytestmark = pytest.mark.gpu
 
@@ -20,22 +21,6 @@ def padded(rows, d):
     """Device tensor (rows, d) whose leading dimension is a multiple of 4."""
     ld = (d + 3) // 4 * 4
     return torch.zeros(rows, ld, device=DEV)[:, :d]
-
-
-def compare_meta(gres, ores, hist_len):
-    seen, ids, hist = gres.read_meta()
-    o_seen = np.where(ores.occupied, ores.seen_count, -1)
-    o_ids = np.where(ores.occupied, ores.sample_id, -1)
-    assert np.array_equal(seen, o_seen)
-    assert np.array_equal(ids, o_ids)
-    oh = np.zeros(hist_len, np.int64)
-    for k, c in ores.evict_hist.items():
-        oh[min(k, hist_len - 1)] += c
-    assert np.array_equal(hist, oh)
-    st = gres.stats()
-    assert (st["n"], st["unseen"], st["seen"]) == (ores.N, ores.U, ores.S)
-    assert st["total_put"] == ores.total_put and st["total_evicted"] == ores.total_evicted
-    assert st["total_draws"] == ores.total_draws and st["next_ticket"] == ores.next_ticket
 
 
 @pytest.mark.parametrize("C,T,d,seed,ops", [
