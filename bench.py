@@ -65,7 +65,134 @@ def parse_args():
     p.add_argument("--cpu-seconds", type=float, default=15.0,
                    help="target duration of the CPU-oracle baseline sample (0 disables it)")
     p.add_argument("--out", default=None, help="also write the JSON line to this file")
+    p.add_argument("--pmc-calibration", action="store_true",
+                   help="first run a reference elementwise kernel of known traffic (1 GiB read, 1 GiB written) "
+                        "for scaling rocprofv3 FETCH_SIZE / WRITE_SIZE")
+    p.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"), default=None,
+                   help="no GPU work: turn the counter CSVs of two rocprofv3 --pmc runs (FETCH_SIZE, WRITE_SIZE) of "
+                        "this workload with --pmc-calibration into per-launch HBM bytes of its dominant kernel "
+                        "(--kernel) and record them in profiles/hbm_traffic.json")
+    p.add_argument("--kernel", default=None, help="roofline kernel label for --summarize-pmc")
+    p.add_argument("--pmc-command", default="", help="command line recorded with --summarize-pmc")
     return p.parse_args()
+
+
+# ---------------------------------------------------------------- HBM traffic from PMC counters
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic.json")
+CAL_FLOATS = 1 << 28                                 # reference kernel: 1 GiB read + 1 GiB written
+
+
+def pmc_calibration():
+    """Elementwise negation of 2^28 floats, three launches: it moves exactly
+    the bytes of a copy, so its counter readings scale the others."""
+    import torch
+    a = torch.ones(CAL_FLOATS, device="cuda:0")
+    b = torch.empty_like(a)
+    for _ in range(3):
+        torch.neg(a, out=b)
+    torch.cuda.synchronize()
+    del a, b
+    torch.cuda.empty_cache()
+
+
+def kernel_sources(label: str):
+    csrc = os.path.join(ROOT, "paper_2309_16743_amd", "csrc")
+    files = ["common.h"]
+    if label.startswith("gemm_fp32"):
+        files += ["gemm_f32.h", "surrogate.hip"]
+    elif label.startswith("gemm_bf16"):
+        files += ["gemm_bf16.h", "surrogate.hip"]
+    elif label == "adam_kernel":
+        files += ["surrogate.hip"]
+    else:
+        files += ["reservoir.hip", "philox.h"]
+    return [os.path.join(csrc, f) for f in files]
+
+
+def sources_hash(label: str) -> str:
+    import hashlib
+    h = hashlib.sha256()
+    for f in kernel_sources(label):
+        with open(f, "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def kernel_matches(label: str, name: str) -> bool:
+    """Whether a rocprofv3 kernel name is the kernel behind a roofline label."""
+    if label in ("adam_kernel", "gather_kernel", "put_copy_kernel"):
+        return f"ot::{label}(" in name
+    phase = label.split("(")[1].rstrip(")")
+    if label.startswith("gemm_fp32"):
+        lay = {"fwd_output": "(ot::Lay)0, (ot::Lay)0", "wgrad_output": "(ot::Lay)1, (ot::Lay)1",
+               "igrad_output": "(ot::Lay)0, (ot::Lay)1"}[phase]
+        return "gemm_f32_kernel<" in name and lay in name and name.split(">(")[0].endswith(", 1")
+    lay = {"fwd_output": "(ot::LayB)0, (ot::LayB)0", "wgrad_output": "(ot::LayB)1, (ot::LayB)1",
+           "igrad_output": "(ot::LayB)0, (ot::LayB)1"}[phase]
+    return "gemm_bf16_pipe_kernel<" in name and lay in name
+
+
+def traffic_for(workload: str, label: str):
+    """Recorded HBM bytes per launch, or None if absent or the kernel's sources changed since."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            db = json.load(f)
+    except (OSError, ValueError):
+        return None
+    e = db.get(f"{workload} / {label}")
+    if not e or e.get("sources_sha256") != sources_hash(label):
+        return None
+    return e["bytes_per_launch"]
+
+
+def summarize_pmc(fetch_dir: str, write_dir: str, workload: str, label: str, command: str) -> dict:
+    import csv
+    import glob
+
+    def rows(d, counter):
+        files = glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True)
+        if not files:
+            raise SystemExit(f"no counter_collection.csv under {d}")
+        out = []
+        for fn in files:
+            with open(fn) as f:
+                for r in csv.DictReader(f):
+                    if r["Counter_Name"] == counter:
+                        out.append((r["Kernel_Name"], float(r["Counter_Value"])))
+        return out
+
+    def per_dispatch_kb(rs, pred):
+        v = [x for n, x in rs if pred(n)]
+        if not v:
+            raise SystemExit("no matching dispatches")
+        return float(np.median(v)), len(v)
+
+    fr, wr = rows(fetch_dir, "FETCH_SIZE"), rows(write_dir, "WRITE_SIZE")
+    cal = lambda n: "neg_kernel" in n
+    cal_f, n_cf = per_dispatch_kb(fr, cal)
+    cal_w, n_cw = per_dispatch_kb(wr, cal)
+    cal_bytes = CAL_FLOATS * 4
+    sf, sw = cal_bytes / (cal_f * 1024), cal_bytes / (cal_w * 1024)
+    k_f, n_f = per_dispatch_kb(fr, lambda n: kernel_matches(label, n))
+    k_w, n_w = per_dispatch_kb(wr, lambda n: kernel_matches(label, n))
+    entry = {"workload": workload, "kernel": label,
+             "fetch_kib_per_launch": round(k_f, 1), "write_kib_per_launch": round(k_w, 1),
+             "launches": [n_f, n_w],
+             "calibration": {"kernel": "elementwise negation of 2^28 fp32 (1 GiB read, 1 GiB written)",
+                             "fetch_kib": round(cal_f, 1), "write_kib": round(cal_w, 1),
+                             "fetch_scale": round(sf, 4), "write_scale": round(sw, 4)},
+             "bytes_per_launch": round(k_f * 1024 * sf + k_w * 1024 * sw),
+             "sources_sha256": sources_hash(label), "command": command}
+    try:
+        with open(TRAFFIC_FILE) as f:
+            db = json.load(f)
+    except (OSError, ValueError):
+        db = {}
+    db[f"{workload} / {label}"] = entry
+    with open(TRAFFIC_FILE, "w") as f:
+        json.dump(db, f, indent=1, sort_keys=True)
+        f.write("\n")
+    return entry
 
 
 def gemm_flops(w) -> float:
@@ -113,19 +240,23 @@ def kernel_table(w, phases_ms: dict, res_ms: dict) -> dict:
 
 
 def roofline_entry(w, phase: str, avg_s: float) -> dict:
-    """Roofline object for the dominant kernel (per-launch algorithmic work / duration)."""
+    """Roofline object for the dominant kernel (per-launch algorithmic work / duration).
+    traffic: HBM bytes per launch from rocprofv3 counters (profiles/hbm_traffic.json),
+    None when not measured for this kernel as it now stands."""
     if phase in ("fwd_output", "wgrad_output", "igrad_output"):
         peak = PEAK_BF16_MFMA if w.precision == "bf16" else PEAK_FP32_MFMA
         work = gemm_flops(w)
-        return {"bound": "mfma", "kernel": f"gemm_{w.precision} ({phase})",
+        label = f"gemm_{w.precision} ({phase})"
+        return {"bound": "mfma", "kernel": label,
                 "achieved": round(work / avg_s / 1e12, 2), "peak": peak / 1e12, "unit": "TFLOP/s",
-                "frac": round(work / avg_s / peak, 4), "traffic": None, "per_launch_flops": work,
-                "avg_us": round(avg_s * 1e6, 2)}
+                "frac": round(work / avg_s / peak, 4), "traffic": traffic_for(w.name, label),
+                "per_launch_flops": work, "avg_us": round(avg_s * 1e6, 2)}
     work = {"adam": adam_bytes(w), "gather": gather_bytes(w)}[phase]
-    return {"bound": "hbm", "kernel": ("adam_kernel" if phase == "adam" else "gather_kernel"),
+    label = "adam_kernel" if phase == "adam" else "gather_kernel"
+    return {"bound": "hbm", "kernel": label,
             "achieved": round(work / avg_s / 1e9, 1), "peak": PEAK_HBM / 1e9, "unit": "GB/s",
-            "frac": round(work / avg_s / PEAK_HBM, 4), "traffic": None, "per_launch_bytes": work,
-            "avg_us": round(avg_s * 1e6, 2)}
+            "frac": round(work / avg_s / PEAK_HBM, 4), "traffic": traffic_for(w.name, label),
+            "per_launch_bytes": work, "avg_us": round(avg_s * 1e6, 2)}
 
 
 def cpu_baseline(w, inputs, fields, seconds: float) -> dict:
@@ -482,12 +613,13 @@ def run_stress(args):
     dom = "gather" if g_ms >= c_ms else "put_copy"
     if dom == "gather":
         roof = {"bound": "hbm", "kernel": "gather_kernel", "achieved": round(g_rate / 1e9, 1), "peak": PEAK_HBM / 1e9,
-                "unit": "GB/s", "frac": round(g_rate / PEAK_HBM, 4), "traffic": None,
+                "unit": "GB/s", "frac": round(g_rate / PEAK_HBM, 4), "traffic": traffic_for(w.name, "gather_kernel"),
                 "per_launch_bytes": B * row_bytes, "avg_us": round(g_avg * 1e6, 2)}
     else:
         c_avg = c_ms * 1e-3 / c_n
         roof = {"bound": "hbm", "kernel": "put_copy_kernel", "achieved": round(put_rate / 1e9, 1),
-                "peak": PEAK_HBM / 1e9, "unit": "GB/s", "frac": round(put_rate / PEAK_HBM, 4), "traffic": None,
+                "peak": PEAK_HBM / 1e9, "unit": "GB/s", "frac": round(put_rate / PEAK_HBM, 4),
+                "traffic": traffic_for(w.name, "put_copy_kernel"),
                 "per_launch_bytes": round(rows_in * row_bytes / c_n), "avg_us": round(c_avg * 1e6, 2)}
     line = {
         "metric": METRIC, "value": round(value, 1), "unit": "GB/s", "n_gpus": 1, "steps": K, "warmup": warmup,
@@ -519,12 +651,20 @@ def run_stress(args):
 
 def main():
     args = parse_args()
+    if args.summarize_pmc:
+        if not args.kernel:
+            raise SystemExit("--summarize-pmc needs --kernel")
+        e = summarize_pmc(args.summarize_pmc[0], args.summarize_pmc[1], args.config, args.kernel, args.pmc_command)
+        print(json.dumps(e))
+        return
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print(f"bench.py measures one GPU only; --gpus {args.gpus} (WORLD_SIZE {world}) is not supported: "
               "this build has no multi-GPU path.", file=sys.stderr)
         sys.exit(2)
     from fixtures import configs
+    if args.pmc_calibration:
+        pmc_calibration()
     if args.config == configs.STRESS.name:
         line = run_stress(args)
     else:

@@ -103,13 +103,18 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_f32_kernel(GemmArgs g) {
   const int lane = tid & 63, wid = tid >> 6;
   const int wm = wid % WGM, wn = wid / WGM;
 
+  // Tile order: XCD remap over the whole grid (the blocks of one k split stay
+  // on one XCD), and consecutive tiles walk the dimension with fewer tiles
+  // first, so the blocks sharing the larger operand's tile run together.
   const int64_t tiles_m = (g.M + BM - 1) / BM;
   const int64_t tiles_n = (g.N + BN - 1) / BN;
-  const int64_t logical = xcd_remap(blockIdx.x, (int64_t)gridDim.x);
-  const int64_t tm = logical % tiles_m, tn = logical / tiles_m;
-  (void)tiles_n;
+  const int64_t lin = (int64_t)blockIdx.y * gridDim.x + blockIdx.x;
+  const int64_t l2 = xcd_remap(lin, (int64_t)gridDim.x * gridDim.y);
+  const int64_t logical = l2 % gridDim.x, split = l2 / gridDim.x;
+  int64_t tm, tn;
+  if (tiles_m <= tiles_n) { tm = logical % tiles_m; tn = logical / tiles_m; }
+  else { tn = logical % tiles_n; tm = logical / tiles_n; }
   const int64_t m0 = tm * BM, n0 = tn * BN;
-  const int64_t split = blockIdx.y;
   const int64_t kbeg = split * g.k_chunk;
   const int64_t kend = (kbeg + g.k_chunk < g.K) ? kbeg + g.k_chunk : g.K;
   const int64_t nk = (kend > kbeg) ? (kend - kbeg + BK - 1) / BK : 0;
