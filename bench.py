@@ -60,6 +60,9 @@ def parse_args():
     p.add_argument("--steps", type=int, default=None, help="timed steps (default 2000 fp32, 100 bf16)")
     p.add_argument("--warmup", type=int, default=None, help="untimed steps before timing (default 50 / 5)")
     p.add_argument("--config", default="heat-100x100")
+    p.add_argument("--one-stream", action="store_true",
+                   help="run the reservoir and the train step on one stream (default: the reservoir's put, draw "
+                        "and gather of the next batch overlap the current train step on a second stream)")
     p.add_argument("--profile-steps", type=int, default=None,
                    help="steps of the per-kernel breakdown pass (all phases timed)")
     p.add_argument("--cpu-seconds", type=float, default=15.0,
@@ -200,10 +203,26 @@ def gemm_flops(w) -> float:
     return 2.0 * w.batch * w.widths[-2] * w.widths[-1]
 
 
+def out_weights(w) -> int:
+    """Weights of the output layer (H x D), whose Adam update is fused into the
+    weight-gradient GEMM (bf16) or its split-K reduction (fp32)."""
+    return w.widths[-2] * w.widths[-1]
+
+
 def adam_bytes(w) -> float:
-    """Algorithmic bytes of one Adam launch: read p, g, m, v; write p, m, v
-    (+ the bf16 weight copy in mixed precision)."""
-    return (28.0 + (2.0 if w.precision == "bf16" else 0.0)) * w.n_params()
+    """Algorithmic bytes of the standalone Adam launch over every parameter
+    except the output-layer weights: read p, g, m, v; write p, m, v (+ the
+    bf16 weight copy in mixed precision)."""
+    return (28.0 + (2.0 if w.precision == "bf16" else 0.0)) * (w.n_params() - out_weights(w))
+
+
+def fused_adam_bytes(w) -> float:
+    """Algorithmic bytes of the output layer's fused weight update: read p, m,
+    v and write p, m, v (+ the bf16 copy) of its H x D weights, and read its
+    operands dY (B x D) and A (B x H) once."""
+    e = 2.0 if w.precision == "bf16" else 4.0
+    per = 24.0 + (2.0 if w.precision == "bf16" else 0.0)
+    return per * out_weights(w) + e * w.batch * (w.widths[-1] + w.widths[-2])
 
 
 def gather_bytes(w) -> float:
@@ -224,6 +243,9 @@ def kernel_table(w, phases_ms: dict, res_ms: dict) -> dict:
         if name in ("fwd_output", "wgrad_output", "igrad_output"):
             rate = gemm_flops(w) / (avg * 1e-3)
             row.update(achieved_tflops=round(rate / 1e12, 2), frac_mfma=round(rate / peak_mfma, 4))
+        if (name == "wgrad_output" and w.precision == "bf16") or (name == "wgrad_reduce" and w.precision == "fp32"):
+            rate = fused_adam_bytes(w) / (avg * 1e-3)     # the phase that applies the fused Adam update
+            row.update(fused_adam=True, achieved_gbs=round(rate / 1e9, 1), frac_hbm=round(rate / PEAK_HBM, 4))
         if name == "adam":
             rate = adam_bytes(w) / (avg * 1e-3)
             row.update(achieved_gbs=round(rate / 1e9, 1), frac_hbm=round(rate / PEAK_HBM, 4))
@@ -243,6 +265,15 @@ def roofline_entry(w, phase: str, avg_s: float) -> dict:
     """Roofline object for the dominant kernel (per-launch algorithmic work / duration).
     traffic: HBM bytes per launch from rocprofv3 counters (profiles/hbm_traffic.json),
     None when not measured for this kernel as it now stands."""
+    if phase == "wgrad_output" and w.precision == "bf16":
+        # weight gradient with Adam in its epilogue: 26 B per output weight against 2 B H D flop
+        work = fused_adam_bytes(w)
+        label = "gemm_bf16 (wgrad_output + fused Adam)"
+        return {"bound": "hbm", "kernel": label,
+                "achieved": round(work / avg_s / 1e9, 1), "peak": PEAK_HBM / 1e9, "unit": "GB/s",
+                "frac": round(work / avg_s / PEAK_HBM, 4), "traffic": traffic_for(w.name, label),
+                "per_launch_bytes": work, "per_launch_flops": gemm_flops(w),
+                "mfma_frac": round(gemm_flops(w) / avg_s / PEAK_BF16_MFMA, 4), "avg_us": round(avg_s * 1e6, 2)}
     if phase in ("fwd_output", "wgrad_output", "igrad_output"):
         peak = PEAK_BF16_MFMA if w.precision == "bf16" else PEAK_FP32_MFMA
         work = gemm_flops(w)
@@ -351,6 +382,8 @@ def timed_region(tr, w, K, profile_steps, stream, wrap_put):
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     ev[0].record(stream)
+    if tr.overlap:
+        tr.res_stream.wait_event(ev[0])     # reservoir work of the timed steps starts after the first event
     for i in range(K):
         wrap_put()
         assert tr.sample_and_train()
@@ -409,7 +442,7 @@ def run_heat(args, w):
     stream = torch.cuda.Stream(device=dev)
     with torch.cuda.stream(stream):
         tr = OnlineTrainer(w.widths, w.batch, w.capacity, w.threshold, w.wave, w.tau, inputs_d, fields_d,
-                           w.reservoir_seed, w.init_seed, lr=w.lr, stream=stream)
+                           w.reservoir_seed, w.init_seed, lr=w.lr, stream=stream, overlap=not args.one_stream)
         for _ in range(w.n_chunks):             # stream the ensemble once (untimed)
             tr.iterate()
         for _ in range(warmup):
@@ -420,7 +453,8 @@ def run_heat(args, w):
         r = timed_region(tr, w, K, args.profile_steps or 200, stream, lambda: tr.put_next(wrap=True))
     config = {"workload": w.name, "fields": f"FTCS heat {w.grid}x{w.grid}, {w.n_sims} sims x {w.tau} steps",
               "widths": list(w.widths), "batch": w.batch, "capacity": w.capacity, "threshold": w.threshold,
-              "put_rows_per_step": w.wave, "precision": w.precision}
+              "put_rows_per_step": w.wave, "precision": w.precision,
+              "reservoir_stream": "one stream" if args.one_stream else "overlapped with the train step"}
     line = result_line(w, args, K, warmup, r, config)
     tr.close()
     del inputs_d, fields_d
@@ -461,7 +495,8 @@ def run_field(args, w):
             gen_chunk(first_pool_chunk + i, pool_x[i], pool_u[i])
         tr = OnlineTrainer(w.widths, w.batch, w.capacity, w.threshold, w.wave, w.tau, None, None,
                            w.reservoir_seed, w.init_seed, precision=OT_BF16, lr=w.lr, stream=stream,
-                           chunk_fn=lambda c: (pool_x[c % pool], pool_u[c % pool]), n_chunks=1 << 40, device=dev)
+                           chunk_fn=lambda c: (pool_x[c % pool], pool_u[c % pool]), n_chunks=1 << 40, device=dev,
+                           overlap=not args.one_stream)
         fx = torch.empty(w.wave, 8, device=dev)[:, :6]
         fu = torch.empty(w.wave, D, device=dev)
         t_fill = time.perf_counter()
@@ -483,7 +518,8 @@ def run_field(args, w):
         r = timed_region(tr, w, K, args.profile_steps or 20, stream, lambda: tr.put_next(wrap=True))
     config = {"workload": w.name, "fields": f"sine-mode {n}x{n}, {w.n_sims} sims x {w.tau} steps",
               "widths": list(w.widths), "batch": w.batch, "capacity": w.capacity, "threshold": w.threshold,
-              "put_rows_per_step": w.wave, "precision": w.precision}
+              "put_rows_per_step": w.wave, "precision": w.precision,
+              "reservoir_stream": "one stream" if args.one_stream else "overlapped with the train step"}
     line = result_line(w, args, K, warmup, r, config)
     tr.close()
     torch.cuda.empty_cache()

@@ -7,7 +7,10 @@
  * and b_l of widths[l]; Z_l = A_{l-1} W_l^T + b_l, A_l = ReLU(Z_l) for l < L,
  * Y = Z_L.  Loss = mean over the B x D batch of (Y - U)^2.  Adam (Kingma and
  * Ba, 2015): beta1, beta2, eps as given, bias-corrected, no weight decay, step
- * counter t from 1.  ReLU'(0) = 0.
+ * counter t from 1, in the operation order
+ *   m = b1 m + (1 - b1) g;  v = b2 v + (1 - b2) g^2;
+ *   p = p - lr (m / (1 - b1^t)) / (sqrt(v / (1 - b2^t)) + eps).
+ * ReLU'(0) = 0.
  *
  * Precision OT_FP32: every GEMM on fp32 operands with fp32 accumulation.
  * Precision OT_BF16: layer 1 (K = widths[0]) in fp32; every other GEMM takes
@@ -42,10 +45,21 @@ typedef struct ot_surrogate ot_surrogate;
 
 enum ot_precision { OT_FP32 = 0, OT_BF16 = 1 };
 
+/* Creation flags.
+ * OT_SURROGATE_KEEP_GRADS: store every gradient of a train step, then run
+ *   Adam over all parameters in one pass.  Without it (the default) the
+ *   output layer's weights are updated by Adam inside the epilogue of their
+ *   weight-gradient GEMM (or of its split-K reduction), which runs after the
+ *   output layer's input gradient has read the old weights: that gradient
+ *   (widths[L] x widths[L-1] fp32, the largest array of the step) is never
+ *   written or read back, and surrogate_get_grads refuses it.  Both modes
+ *   apply the same Adam arithmetic to the same gradient sums. */
+enum ot_surrogate_flags { OT_SURROGATE_KEEP_GRADS = 1 };
+
 /* Create an MLP with n_widths - 1 layers (2 <= n_widths <= 16, every width in
  * [1, 2^26]), parameters initialised from `seed` as above, Adam state zero.
  * max_batch: rows the train / predict workspaces are first sized for (grown
- * on demand).  flags must be 0.
+ * on demand).  flags: 0 or OT_SURROGATE_KEEP_GRADS.
  * Errors: OT_E_INVAL, OT_E_NOMEM, OT_E_HIP. */
 int surrogate_create(ot_surrogate** out, const int64_t* widths, int32_t n_widths,
                      int32_t precision, float lr, float beta1, float beta2, float eps,
@@ -59,7 +73,9 @@ int surrogate_set_params(ot_surrogate* s, int32_t layer, const float* W_host, co
 /* Copy layer parameters (fp32 master) to dense host arrays.  Synchronous. */
 int surrogate_get_params(ot_surrogate* s, int32_t layer, float* W_host, float* b_host);
 
-/* Copy the gradients of the last train step of one layer.  Synchronous. */
+/* Copy the gradients of the last train step of one layer.  Synchronous.
+ * OT_E_STATE for the output layer's dW_host (non-NULL) when that step fused
+ * the output layer's Adam update (no OT_SURROGATE_KEEP_GRADS). */
 int surrogate_get_grads(ot_surrogate* s, int32_t layer, float* dW_host, float* db_host);
 
 /* Copy Adam moments of one layer and the step counter t (each nullable). */

@@ -15,7 +15,7 @@ import numpy as np
 
 from . import _abi
 from ._abi import (OT_BF16, OT_E_CLOSED, OT_E_INVAL, OT_E_STATE, OT_EMPTY, OT_FP32, OT_NOT_READY, OT_OK,
-                   OTError, check, last_error, load)
+                   OT_SURROGATE_KEEP_GRADS, OTError, check, last_error, load)
 
 __all__ = [
     "Reservoir", "Surrogate", "reservoir_create", "reservoir_put", "reservoir_sample_batch",
@@ -24,6 +24,7 @@ __all__ = [
     "surrogate_get_grads", "surrogate_get_adam_state", "surrogate_set_lr", "surrogate_train_step",
     "surrogate_predict", "surrogate_destroy", "load", "last_error", "OTError",
     "OT_OK", "OT_NOT_READY", "OT_EMPTY", "OT_E_INVAL", "OT_E_CLOSED", "OT_E_STATE", "OT_FP32", "OT_BF16",
+    "OT_SURROGATE_KEEP_GRADS",
 ]
 
 
@@ -178,10 +179,13 @@ class Surrogate:
         check("surrogate_get_params", load().surrogate_get_params(self._h, layer, W.ctypes.data, b.ctypes.data))
         return W, b
 
-    def get_grads(self, layer: int):
+    def get_grads(self, layer: int, weights: bool = True):
+        """(dW, db) of the last step; dW is None when weights=False (the output
+        layer's dW is not stored when its Adam update is fused)."""
         W, b = self._layer_arrays(layer)
-        check("surrogate_get_grads", load().surrogate_get_grads(self._h, layer, W.ctypes.data, b.ctypes.data))
-        return W, b
+        check("surrogate_get_grads", load().surrogate_get_grads(self._h, layer, W.ctypes.data if weights else None,
+                                                                b.ctypes.data))
+        return (W if weights else None), b
 
     def get_adam_state(self, layer: int):
         mW, mb = self._layer_arrays(layer)

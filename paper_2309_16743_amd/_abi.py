@@ -21,6 +21,7 @@ OT_E_CLOSED = -4
 OT_E_STATE = -5
 OT_FP32 = 0
 OT_BF16 = 1
+OT_SURROGATE_KEEP_GRADS = 1
 
 SURROGATE_PHASES = ("fwd_hidden", "fwd_output", "loss", "wgrad_output", "igrad_output", "igrad_reduce",
                     "bwd_hidden", "adam", "wgrad_reduce")

@@ -25,6 +25,7 @@
 // 16-byte (fp32) or 8-byte (bf16) vector accesses.
 #pragma once
 
+#include "adam.h"
 #include "common.h"
 
 namespace ot {
@@ -56,7 +57,9 @@ enum class EpiB : int {
   BiasF32 = 2,    // C (fp32) = acc + bias[n]
   BiasReluBf = 3, // C (bf16) = bf16(max(acc + bias[n], 0))
   MaskBf = 4,     // C (bf16) = bf16(acc * (mask[m, n] > 0)), mask bf16
-  MseBf = 5       // R = acc + bias[n] - T[m, n] (T fp32); C (bf16) = bf16(scale R); per-block sum of R^2
+  MseBf = 5,      // R = acc + bias[n] - T[m, n] (T fp32); C (bf16) = bf16(scale R); per-block sum of R^2
+  AdamF32 = 6     // acc is the gradient of the fp32 master weights C: Adam updates C, adam_m, adam_v
+                  // (same layout as C) and writes bf16(C) to adam_pb; no gradient is stored
 };
 
 struct GemmBArgs {
@@ -80,6 +83,10 @@ struct GemmBArgs {
   int64_t rowsum_stride;
   float* colsum;            // MseBf: per m-tile column sums of the bf16 dY, colsum[tm * colsum_ld + n]
   int64_t colsum_ld;
+  float* adam_m;            // AdamF32: first and second moments, bf16 weight copy, all at C's offsets
+  float* adam_v;
+  uint16_t* adam_pb;
+  AdamArgs adam;
 };
 
 __device__ __forceinline__ int64_t xcd_remap_b(int64_t p, int64_t g) {
@@ -130,6 +137,11 @@ struct BEpi {
   __device__ __forceinline__ void rows(const GemmBArgs& g, const float* ep, int64_t m0, int64_t split, Stage stage) {
     static_assert(ROWS % RPP == 0, "chunk rows");
     constexpr int NP = ROWS / RPP;
+    if constexpr (EPI == EpiB::AdamF32) {
+      stage();
+      adam_rows<NP>(g, ep, m0);
+      return;
+    }
     // targets (MseBf) or mask (MaskBf) of each pass; one branch around all
     // the loads of the chunk, so that they are all in flight together
     f32x4 pre[NP];
@@ -199,6 +211,63 @@ struct BEpi {
         } else {
           for (int c = 0; c < 4; ++c)
             if (col + c < g.N) C[c] = h4[c];
+        }
+      }
+    }
+  }
+
+  // AdamF32: the chunk's gradients are staged in ep; each lane updates 4
+  // consecutive parameters of a row per pass.  The master weights and both
+  // moments of G passes are loaded together (non-temporal: every parameter is
+  // touched once per step), then updated and stored.
+  template <int NP>
+  __device__ __forceinline__ void adam_rows(const GemmBArgs& g, const float* ep, int64_t m0) {
+    constexpr int G = NP < 4 ? NP : 4;
+    static_assert(NP % G == 0, "pass groups");
+    if (col >= g.N) return;
+    float* const P = reinterpret_cast<float*>(g.C);
+#pragma unroll
+    for (int i0 = 0; i0 < NP; i0 += G) {
+      if (cfull) {
+        f32x4 pp[G], mm[G], vv[G];
+#pragma unroll
+        for (int u = 0; u < G; ++u) {
+          const int64_t m = min(m0 + rl + RPP * (i0 + u), g.M - 1);   // clamped rows are not stored
+          const int64_t o = m * g.ldc + col;
+          pp[u] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(P + o));
+          mm[u] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(g.adam_m + o));
+          vv[u] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(g.adam_v + o));
+        }
+#pragma unroll
+        for (int u = 0; u < G; ++u) {
+          const int rr = rl + RPP * (i0 + u);
+          const int64_t m = m0 + rr;
+          if (m >= g.M) continue;
+          const f32x4 gr = *reinterpret_cast<const f32x4*>(ep + rr * EP + 4 * cg);
+          adam4(pp[u], gr, mm[u], vv[u], g.adam);
+          const int64_t o = m * g.ldc + col;
+          __builtin_nontemporal_store(pp[u], reinterpret_cast<f32x4*>(P + o));
+          __builtin_nontemporal_store(mm[u], reinterpret_cast<f32x4*>(g.adam_m + o));
+          __builtin_nontemporal_store(vv[u], reinterpret_cast<f32x4*>(g.adam_v + o));
+          __builtin_nontemporal_store(u16x4{f2bf(pp[u][0]), f2bf(pp[u][1]), f2bf(pp[u][2]), f2bf(pp[u][3])},
+                                      reinterpret_cast<u16x4*>(g.adam_pb + o));
+        }
+      } else {
+#pragma unroll
+        for (int u = 0; u < G; ++u) {
+          const int rr = rl + RPP * (i0 + u);
+          const int64_t m = m0 + rr;
+          if (m >= g.M) continue;
+          for (int c = 0; c < 4; ++c) {
+            if (col + c >= g.N) break;
+            const int64_t o = m * g.ldc + col + c;
+            float p = P[o], mo = g.adam_m[o], vo = g.adam_v[o];
+            adam1(p, ep[rr * EP + 4 * cg + c], mo, vo, g.adam);
+            P[o] = p;
+            g.adam_m[o] = mo;
+            g.adam_v[o] = vo;
+            g.adam_pb[o] = f2bf(p);
+          }
         }
       }
     }

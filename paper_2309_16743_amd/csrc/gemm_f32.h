@@ -24,6 +24,7 @@
 // are consecutive and land on the same XCD (L2) of the 8 on the chip.
 #pragma once
 
+#include "adam.h"
 #include "common.h"
 
 namespace ot {
@@ -35,7 +36,8 @@ enum class Epi : int {
   BiasRelu = 2,  // C = max(acc + bias[n], 0)
   Mse = 3,       // Y = acc + bias[n]; R = Y - T; C = scale * R; partial sum of R^2 per block
   SplitK = 4,    // C[split] = acc (partial sums, reduced by a separate pass)
-  Mask = 5       // C = acc * (mask[m, n] > 0)
+  Mask = 5,      // C = acc * (mask[m, n] > 0)
+  Adam = 6       // acc is the gradient of the weights C: Adam updates C, adam_m, adam_v (same layout as C)
 };
 
 struct GemmArgs {
@@ -57,6 +59,9 @@ struct GemmArgs {
   int64_t ldmask;
   float* rowsum;            // optional: sum_k A(m, k) for m of the block's rows (n tile 0 only)
   int64_t rowsum_stride;    // SplitK: elements between consecutive split slices of rowsum
+  float* adam_m;            // Adam: moments at C's offsets
+  float* adam_v;
+  AdamArgs adam;
 };
 
 constexpr int kNumXcd = 8;
@@ -360,6 +365,29 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_f32_kernel(GemmArgs g) {
         for (int h = 0; h < FN; ++h) v[h] = mv[h] > 0.f ? v[h] : 0.f;
       }
       float* cp = Cb + m * g.ldc + col_base;
+      if constexpr (EPI == Epi::Adam) {
+        float* mp = g.adam_m + m * g.ldc + col_base;
+        float* vp = g.adam_v + m * g.ldc + col_base;
+        if (FN == 4 && full) {
+          f32x4 P = *reinterpret_cast<const f32x4*>(cp), Mo = *reinterpret_cast<const f32x4*>(mp),
+                V = *reinterpret_cast<const f32x4*>(vp);
+          adam4(P, f32x4{v[0], v[FN > 1 ? 1 : 0], v[FN > 2 ? 2 : 0], v[FN > 3 ? 3 : 0]}, Mo, V, g.adam);
+          *reinterpret_cast<f32x4*>(cp) = P;
+          *reinterpret_cast<f32x4*>(mp) = Mo;
+          *reinterpret_cast<f32x4*>(vp) = V;
+        } else {
+#pragma unroll
+          for (int h = 0; h < FN; ++h) {
+            if (col_base + h >= g.N) continue;
+            float P = cp[h], Mo = mp[h], V = vp[h];
+            adam1(P, v[h], Mo, V, g.adam);
+            cp[h] = P;
+            mp[h] = Mo;
+            vp[h] = V;
+          }
+        }
+        continue;
+      }
       if (FN == 4 && full) {
         *reinterpret_cast<f32x4*>(cp) = f32x4{v[0], v[FN > 1 ? 1 : 0], v[FN > 2 ? 2 : 0], v[FN > 3 ? 3 : 0]};
       } else if (FN == 2 && full) {

@@ -1,10 +1,13 @@
 // Surrogate MLP train step and prediction (the paper's deep surrogate of the
 // heat equation, Sec. 4.1): forward through ReLU hidden layers and an
 // identity output layer whose GEMM epilogue forms the mean-squared-error
-// residual, back-propagation, and one fused Adam update over all parameters.
+// residual, back-propagation, and Adam.  By default the output layer's weights
+// are updated inside the epilogue of their weight-gradient GEMM (or of its
+// split-K reduction), so that gradient is never stored; one elementwise pass
+// updates every other parameter.
 //
 // Parameter layout (device, fp32): one flat buffer; layer l holds W_l as
-// out x ldw (ldw = round_up(in, 4), pad columns stay 0) followed by b_l, each
+// out x ldw (ldw = round_up(in, 8), pad columns stay 0) followed by b_l, each
 // segment starting on a 64-float boundary.  Gradients and the Adam moments
 // use the same layout, so Adam is a single elementwise pass.
 #include <algorithm>
@@ -196,39 +199,29 @@ __global__ __launch_bounds__(256) void loss_finalize_kernel(const double* __rest
   }
 }
 
-// Adam (Kingma and Ba, 2015, Algorithm 1) over the flat parameter buffer, fp32:
-//   m = b1 m + (1 - b1) g;  v = b2 v + (1 - b2) g^2;
-//   p = p - lr * (m / c1) / (sqrt(v / c2) + eps),  c1 = 1 - b1^t, c2 = 1 - b2^t.
-__device__ __forceinline__ void adam4(f32x4& pp, const f32x4 gg, f32x4& mm, f32x4& vv, float lr, float b1, float b2,
-                                      float eps, float c1, float c2) {
-#pragma unroll
-  for (int c = 0; c < 4; ++c) {
-    mm[c] = b1 * mm[c] + (1.0f - b1) * gg[c];
-    vv[c] = b2 * vv[c] + (1.0f - b2) * (gg[c] * gg[c]);
-    const float mhat = mm[c] / c1;
-    const float vhat = vv[c] / c2;
-    pp[c] = pp[c] - lr * mhat / (sqrtf(vhat) + eps);
-  }
-}
-
-// Streaming kernel: two 16-byte groups per thread and pass (eight loads in
-// flight), non-temporal accesses (the state is touched once per step).
+// Adam over the flat parameter buffer (adam1 in adam.h), except the 16-byte
+// groups [hole, hole + hole_len) (the output-layer weights when their update
+// is fused into the weight-gradient GEMM).  Streaming kernel: two 16-byte
+// groups per thread and pass (eight loads in flight), non-temporal accesses
+// (the state is touched once per step).
 __global__ __launch_bounds__(256) void adam_kernel(float* __restrict__ p, const float* __restrict__ g,
-                                                   float* __restrict__ m, float* __restrict__ v,
-                                                   int64_t n4, float lr, float b1, float b2, float eps,
-                                                   float c1, float c2, uint16_t* __restrict__ pb) {
+                                                   float* __restrict__ m, float* __restrict__ v, int64_t n4,
+                                                   int64_t hole, int64_t hole_len, AdamArgs a,
+                                                   uint16_t* __restrict__ pb) {
   f32x4* P = reinterpret_cast<f32x4*>(p);
   const f32x4* G = reinterpret_cast<const f32x4*>(g);
   f32x4* Mv = reinterpret_cast<f32x4*>(m);
   f32x4* V = reinterpret_cast<f32x4*>(v);
   u16x4* PB = reinterpret_cast<u16x4*>(pb);
   const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  const int64_t n = n4 - hole_len;   // groups to update
+  auto at = [&](int64_t i) { return i < hole ? i : i + hole_len; };
   int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  for (; i + stride < n4; i += 2 * stride) {
+  for (; i + stride < n; i += 2 * stride) {
     f32x4 pp[2], gg[2], mm[2], vv[2];
 #pragma unroll
     for (int u = 0; u < 2; ++u) {
-      const int64_t j = i + u * stride;
+      const int64_t j = at(i + u * stride);
       pp[u] = __builtin_nontemporal_load(P + j);
       gg[u] = __builtin_nontemporal_load(G + j);
       mm[u] = __builtin_nontemporal_load(Mv + j);
@@ -236,8 +229,8 @@ __global__ __launch_bounds__(256) void adam_kernel(float* __restrict__ p, const 
     }
 #pragma unroll
     for (int u = 0; u < 2; ++u) {
-      const int64_t j = i + u * stride;
-      adam4(pp[u], gg[u], mm[u], vv[u], lr, b1, b2, eps, c1, c2);
+      const int64_t j = at(i + u * stride);
+      adam4(pp[u], gg[u], mm[u], vv[u], a);
       __builtin_nontemporal_store(pp[u], P + j);
       __builtin_nontemporal_store(mm[u], Mv + j);
       __builtin_nontemporal_store(vv[u], V + j);
@@ -245,13 +238,60 @@ __global__ __launch_bounds__(256) void adam_kernel(float* __restrict__ p, const 
         __builtin_nontemporal_store(u16x4{f2bf(pp[u][0]), f2bf(pp[u][1]), f2bf(pp[u][2]), f2bf(pp[u][3])}, PB + j);
     }
   }
-  if (i < n4) {
-    f32x4 pp = P[i], mm = Mv[i], vv = V[i];
-    adam4(pp, G[i], mm, vv, lr, b1, b2, eps, c1, c2);
-    P[i] = pp;
-    Mv[i] = mm;
-    V[i] = vv;
-    if (pb) PB[i] = u16x4{f2bf(pp[0]), f2bf(pp[1]), f2bf(pp[2]), f2bf(pp[3])};
+  if (i < n) {
+    const int64_t j = at(i);
+    f32x4 pp = P[j], mm = Mv[j], vv = V[j];
+    adam4(pp, G[j], mm, vv, a);
+    P[j] = pp;
+    Mv[j] = mm;
+    V[j] = vv;
+    if (pb) PB[j] = u16x4{f2bf(pp[0]), f2bf(pp[1]), f2bf(pp[2]), f2bf(pp[3])};
+  }
+}
+
+// Split-K reduction fused with Adam (fp32 output layer): the weight gradient
+// of element (m, n) is sum_s ws[s][m][n] in split order, exactly as the
+// split-K epilogue would store it; Adam then updates p, mo, vo at
+// m * ldp + n.  Threads of column group 0 also reduce the split row sums
+// rs[s][m] into rowsum_out[m] (the bias gradient; its Adam update is part of
+// the standalone pass).
+__global__ void splitk_adam_kernel(const float* __restrict__ ws, int64_t splits, int64_t split_stride, int64_t M,
+                                   int64_t N, int64_t ldws, float* __restrict__ p, float* __restrict__ mo,
+                                   float* __restrict__ vo, int64_t ldp, AdamArgs a, const float* __restrict__ rs,
+                                   int64_t rs_stride, float* __restrict__ rowsum_out) {
+  const int64_t groups = (N + 3) / 4;
+  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (t >= M * groups) return;
+  const int64_t m = t / groups, n = (t % groups) * 4;
+  if (rowsum_out && n == 0) {
+    float r = rs[m];
+    for (int64_t q = 1; q < splits; ++q) r += rs[q * rs_stride + m];
+    rowsum_out[m] = r;
+  }
+  const int cnt = (int)min((int64_t)4, N - n);
+  const int64_t o = m * ldp + n;
+  if (cnt == 4) {
+    const f32x4* src = reinterpret_cast<const f32x4*>(ws + m * ldws + n);
+    const int64_t st4 = split_stride / 4;
+    f32x4 pp = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(p + o));
+    f32x4 mm = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(mo + o));
+    f32x4 vv = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(vo + o));
+    f32x4 acc = src[0];
+    for (int64_t q = 1; q < splits; ++q) acc += src[q * st4];
+    adam4(pp, acc, mm, vv, a);
+    __builtin_nontemporal_store(pp, reinterpret_cast<f32x4*>(p + o));
+    __builtin_nontemporal_store(mm, reinterpret_cast<f32x4*>(mo + o));
+    __builtin_nontemporal_store(vv, reinterpret_cast<f32x4*>(vo + o));
+  } else {
+    for (int c = 0; c < cnt; ++c) {
+      float gsum = ws[m * ldws + n + c];
+      for (int64_t q = 1; q < splits; ++q) gsum += ws[q * split_stride + m * ldws + n + c];
+      float pc = p[o + c], mc = mo[o + c], vc = vo[o + c];
+      adam1(pc, gsum, mc, vc, a);
+      p[o + c] = pc;
+      mo[o + c] = mc;
+      vo[o + c] = vc;
+    }
   }
 }
 
@@ -342,6 +382,9 @@ struct ot_surrogate {
   float* v = nullptr;
   float lr = 1e-3f, beta1 = 0.9f, beta2 = 0.999f, eps = 1e-8f;
   int64_t t = 0;
+  bool fuse_out = false;      // output-layer Adam fused into its weight-gradient epilogue
+  bool fused_step = false;    // ... and the current step took that path
+  ot::AdamArgs step_adam{};   // Adam scalars of the current step
   // Workspaces, sized for ws_rows batch rows.
   int64_t ws_rows = 0;
   std::vector<float*> act;   // act[l] = A_l, l = 1..L-1 (index 0 unused)
@@ -513,6 +556,7 @@ hipError_t launch_epi(Epi epi, int cfg, const GemmArgs& g, int64_t splits, hipSt
     case Epi::BiasRelu: return launch_cfg<LA, LB, Epi::BiasRelu, ROLE>(cfg, g, splits, st);
     case Epi::Mse: return launch_cfg<LA, LB, Epi::Mse, ROLE>(cfg, g, splits, st);
     case Epi::SplitK: return launch_cfg<LA, LB, Epi::SplitK, ROLE>(cfg, g, splits, st);
+    case Epi::Adam: return launch_cfg<LA, LB, Epi::Adam, ROLE>(cfg, g, splits, st);
     default: return launch_cfg<LA, LB, Epi::Mask, ROLE>(cfg, g, splits, st);
   }
 }
@@ -584,6 +628,14 @@ int run_gemm(ot_surrogate* s, GemmArgs g, Epi epi, hipStream_t st, const char* w
   if (ph_gemm >= 0) tm.mark(st, ph_gemm, 1);
   if (ph_reduce >= 0) tm.mark(st, ph_reduce, 0);
   const int64_t work = g.M * ot::ceil_div(g.N, 4);
+  if (epi == Epi::Adam) {
+    hipLaunchKernelGGL(ot::splitk_adam_kernel, dim3((unsigned)ot::ceil_div(work, 128)), dim3(128), 0, st, s->splitws,
+                       p.splits, h.split_stride, g.M, g.N, ldws, g.C, g.adam_m, g.adam_v, g.ldc, g.adam, h.rowsum,
+                       h.rowsum_stride, g.rowsum);
+    OT_LAUNCHED("splitk_adam_kernel");
+    if (ph_reduce >= 0) tm.mark(st, ph_reduce, 1);
+    return OT_OK;
+  }
   const bool bias = (epi == Epi::Bias || epi == Epi::BiasRelu);
   hipLaunchKernelGGL(ot::splitk_epilogue_kernel, dim3((unsigned)ot::ceil_div(work, 128)), dim3(128), 0, st,
                      s->splitws, p.splits, h.split_stride, g.M, g.N, ldws, bias ? g.bias : nullptr,
@@ -702,7 +754,7 @@ hipError_t launch_cfg_b(int cfg, const GemmBArgs& g, int64_t splits, hipStream_t
 template <LayB LA, LayB LB, EpiB E>
 int run_gemm_b(ot_surrogate* s, GemmBArgs g, hipStream_t st, const char* what, bool allow_split,
                int ph_gemm = -1, int ph_reduce = -1, int64_t* blocks_out = nullptr) {
-  const Plan p = make_plan_b(g.M, g.N, g.K, allow_split && E != EpiB::MseBf, g.rowsum == nullptr);
+  const Plan p = make_plan_b(g.M, g.N, g.K, allow_split && E != EpiB::MseBf && E != EpiB::AdamF32, g.rowsum == nullptr);
   if (blocks_out) *blocks_out = p.blocks;
   ot::PhaseTimer& tm = s->timer;
   if (p.splits == 1) {
@@ -713,8 +765,8 @@ int run_gemm_b(ot_surrogate* s, GemmBArgs g, hipStream_t st, const char* what, b
     if (ph_gemm >= 0) tm.mark(st, ph_gemm, 1);
     return OT_OK;
   }
-  if constexpr (E == EpiB::MseBf) {
-    return ot::set_error(OT_E_STATE, "%s: the MSE epilogue cannot be split", what);
+  if constexpr (E == EpiB::MseBf || E == EpiB::AdamF32) {
+    return ot::set_error(OT_E_STATE, "%s: the MSE and Adam epilogues cannot be split", what);
   } else {
     const int64_t ldws = ot::round_up(g.N, 4);
     int rc = ensure_split_ws(s, p.splits * g.M * ldws, g.rowsum ? p.splits * g.M : 0);
@@ -853,38 +905,57 @@ int train_step_bf16(ot_surrogate* s, const float* x, int64_t ldx, const float* u
       break;
     }
     const int ph_w = (l == L) ? OT_PH_WGRAD_OUTPUT : -1;
-    {
+    const bool fused = (l == L) && s->fused_step;
+    // weight gradient dW = dZ^T A (the output bias gradient came from the
+    // forward epilogue); fused: Adam on W_L in the epilogue instead of a store
+    auto wgrad = [&]() -> int {
       GemmBArgs g = bargs0();
       g.A = s->dz16[l];
       g.lda = s->ld[l];
       g.B = s->act16[l - 1];
       g.ldb = s->ld[l - 1];
-      g.C = dW;
       g.ldc = ly.ldw;
       g.M = ly.out;
       g.N = ly.in;
       g.K = b;
-      g.rowsum = (l == L) ? nullptr : db;   // the output bias gradient came from the forward epilogue
-      if ((rc = run_gemm_b<LayB::MNMajor, LayB::MNMajor, EpiB::StoreF32>(s, g, st, "bf16 weight gradient", true, ph_w,
-                                                                         ph_w >= 0 ? OT_PH_WGRAD_REDUCE : -1)))
-        return rc;
+      if (fused) {
+        g.C = s->params + ly.w_off;
+        g.adam_m = s->m + ly.w_off;
+        g.adam_v = s->v + ly.w_off;
+        g.adam_pb = s->pb + ly.w_off;
+        g.adam = s->step_adam;
+        return run_gemm_b<LayB::MNMajor, LayB::MNMajor, EpiB::AdamF32>(s, g, st, "bf16 weight gradient + Adam",
+                                                                       false, ph_w);
+      }
+      g.C = dW;
+      g.rowsum = (l == L) ? nullptr : db;
+      return run_gemm_b<LayB::MNMajor, LayB::MNMajor, EpiB::StoreF32>(s, g, st, "bf16 weight gradient", true, ph_w,
+                                                                      ph_w >= 0 ? OT_PH_WGRAD_REDUCE : -1);
+    };
+    // input gradient dA_{l-1} = dZ_l W_l (bf16 copy of W), then the ReLU mask
+    auto igrad = [&]() -> int {
+      GemmBArgs g = bargs0();
+      g.A = s->dz16[l];
+      g.lda = s->ld[l];
+      g.B = s->pb + ly.w_off;
+      g.ldb = ly.ldw;
+      g.C = s->dz16[l - 1];
+      g.ldc = s->ld[l - 1];
+      g.M = b;
+      g.N = ly.in;
+      g.K = ly.out;
+      g.mask = s->act16[l - 1];
+      g.ldmask = s->ld[l - 1];
+      return run_gemm_b<LayB::KMajor, LayB::MNMajor, EpiB::MaskBf>(s, g, st, "bf16 input gradient", true,
+                                                                   l == L ? OT_PH_IGRAD_OUTPUT : -1,
+                                                                   l == L ? OT_PH_IGRAD_REDUCE : -1);
+    };
+    // the fused update rewrites W_L, which the input gradient reads first
+    if (fused) {
+      if ((rc = igrad()) || (rc = wgrad())) return rc;
+    } else {
+      if ((rc = wgrad()) || (rc = igrad())) return rc;
     }
-    GemmBArgs g = bargs0();
-    g.A = s->dz16[l];
-    g.lda = s->ld[l];
-    g.B = s->pb + ly.w_off;
-    g.ldb = ly.ldw;
-    g.C = s->dz16[l - 1];
-    g.ldc = s->ld[l - 1];
-    g.M = b;
-    g.N = ly.in;
-    g.K = ly.out;
-    g.mask = s->act16[l - 1];
-    g.ldmask = s->ld[l - 1];
-    if ((rc = run_gemm_b<LayB::KMajor, LayB::MNMajor, EpiB::MaskBf>(s, g, st, "bf16 input gradient", true,
-                                                                    l == L ? OT_PH_IGRAD_OUTPUT : -1,
-                                                                    l == L ? OT_PH_IGRAD_REDUCE : -1)))
-      return rc;
   }
   tm.mark(st, OT_PH_BWD_HIDDEN, 1);
   return OT_OK;
@@ -935,7 +1006,8 @@ extern "C" int surrogate_create(ot_surrogate** out, const int64_t* widths, int32
   if (precision == OT_BF16)
     OT_REQUIRE(n_widths >= 3 && widths[0] <= 16,
                "surrogate_create: bf16 nets need >= 2 layers and an input width <= 16 (first layer runs in fp32)");
-  OT_REQUIRE(flags == 0, "surrogate_create: flags must be 0");
+  OT_REQUIRE((flags & ~(uint32_t)OT_SURROGATE_KEEP_GRADS) == 0, "surrogate_create: unknown flags 0x%x",
+             (unsigned)flags);
   OT_REQUIRE(max_batch >= 1 && max_batch <= (1LL << 20), "surrogate_create: max_batch outside [1, 2^20]");
   OT_REQUIRE(lr >= 0.f && beta1 >= 0.f && beta1 < 1.f && beta2 >= 0.f && beta2 < 1.f && eps > 0.f,
              "surrogate_create: bad Adam hyper-parameters");
@@ -947,6 +1019,7 @@ extern "C" int surrogate_create(ot_surrogate** out, const int64_t* widths, int32
   s->beta1 = beta1;
   s->beta2 = beta2;
   s->eps = eps;
+  s->fuse_out = (flags & OT_SURROGATE_KEEP_GRADS) == 0;
   s->ld.resize(n_widths);
   for (int i = 0; i < n_widths; ++i) s->ld[i] = ot::round_up(widths[i], 8);
   int64_t off = 0;
@@ -1048,6 +1121,10 @@ extern "C" int surrogate_get_params(ot_surrogate* s, int32_t layer, float* W_hos
 extern "C" int surrogate_get_grads(ot_surrogate* s, int32_t layer, float* dW_host, float* db_host) {
   ot::clear_error();
   OT_REQUIRE(s != nullptr, "surrogate_get_grads: NULL surrogate");
+  if (s->fused_step && layer == s->L - 1 && dW_host != nullptr)
+    return ot::set_error(OT_E_STATE,
+                         "surrogate_get_grads: the output-layer weight gradient is not stored when its Adam update "
+                         "is fused (create the surrogate with OT_SURROGATE_KEEP_GRADS)");
   return copy_layer(s, layer, s->grads, dW_host, db_host);
 }
 
@@ -1070,17 +1147,30 @@ extern "C" int surrogate_set_lr(ot_surrogate* s, float lr) {
   return OT_OK;
 }
 
-// Adam over every parameter (and the bf16 weight copy in OT_BF16 mode).
-static int adam_step(ot_surrogate* s, hipStream_t st) {
-  ot::PhaseTimer& tm = s->timer;
+// Adam scalars of the step about to run (t counts from 1).
+static void begin_step(ot_surrogate* s) {
   s->t += 1;
   const double c1 = 1.0 - std::pow((double)s->beta1, (double)s->t);
   const double c2 = 1.0 - std::pow((double)s->beta2, (double)s->t);
+  s->step_adam = ot::AdamArgs{s->lr, s->beta1, s->beta2, s->eps, (float)c1, (float)c2};
+  const Layer& lo = s->layers[s->L - 1];
+  // a single layer with a small input width takes the small-K gradient kernels, which store
+  s->fused_step = s->fuse_out && !(s->L == 1 && lo.in <= ot::kMaxSmallK);
+}
+
+// Adam over every parameter (and the bf16 weight copy in OT_BF16 mode)
+// except the output-layer weights when the step updated them in the fused
+// epilogue.
+static int adam_step(ot_surrogate* s, hipStream_t st) {
+  ot::PhaseTimer& tm = s->timer;
   const int64_t n4 = s->n_flat / 4;
-  const int64_t blocks = std::min<int64_t>(ot::ceil_div(n4, 256), 32768);
+  const Layer& lo = s->layers[s->L - 1];
+  const int64_t hole = s->fused_step ? lo.w_off / 4 : 0;
+  const int64_t hole_len = s->fused_step ? (lo.b_off - lo.w_off) / 4 : 0;
+  const int64_t blocks = std::max<int64_t>(1, std::min<int64_t>(ot::ceil_div(n4 - hole_len, 256), 32768));
   tm.mark(st, OT_PH_ADAM, 0);
   hipLaunchKernelGGL(ot::adam_kernel, dim3((unsigned)blocks), dim3(256), 0, st, s->params, s->grads, s->m, s->v, n4,
-                     s->lr, s->beta1, s->beta2, s->eps, (float)c1, (float)c2, s->pb);
+                     hole, hole_len, s->step_adam, s->pb);
   OT_LAUNCHED("adam_kernel");
   tm.mark(st, OT_PH_ADAM, 1);
   tm.next_call();
@@ -1100,6 +1190,7 @@ extern "C" int surrogate_train_step(ot_surrogate* s, const float* x, int64_t ldx
              "surrogate_train_step: targets need 16-byte alignment and ldu >= D, ldu %% 4 == 0");
   if ((rc = ensure_workspace(s, b))) return rc;
   hipStream_t st = static_cast<hipStream_t>(stream);
+  begin_step(s);
 
   if (s->precision == OT_BF16) {
     if ((rc = train_step_bf16(s, x, ldx, u, ldu, b, st, loss_dev))) return rc;
@@ -1152,21 +1243,25 @@ extern "C" int surrogate_train_step(ot_surrogate* s, const float* x, int64_t ldx
     const int64_t ld_in = (l == 1) ? ldx : s->ld[l - 1];
     float* dW = s->grads + ly.w_off;
     float* db = s->grads + ly.b_off;
-    // weight and bias gradient: dW = dZ^T A_in, db = column sums of dZ
-    if (l == 1 && ly.in <= ot::kMaxSmallK) {
-      if (ph_w >= 0) tm.mark(st, ph_w, 0);
-      const int64_t rows_per = ot::ceil_div(b, kL1Parts);
-      const int64_t P = ot::ceil_div(b, rows_per);
-      hipLaunchKernelGGL(ot::small_k_wgrad_partial_kernel, dim3((unsigned)ot::ceil_div(ly.out, 64), (unsigned)P),
-                         dim3(256), 0, st, s->dz[1], s->ld[1], x, ldx, s->l1_part, b, ly.out, ly.in, rows_per,
-                         (const uint16_t*)nullptr);
-      OT_LAUNCHED("small_k_wgrad_partial_kernel");
-      const int64_t n = ly.out * (ly.in + 1);
-      hipLaunchKernelGGL(ot::small_k_wgrad_reduce_kernel, dim3((unsigned)ot::ceil_div(n, 256)), dim3(256), 0, st,
-                         s->l1_part, P, ly.out, ly.in, dW, ly.ldw, db);
-      OT_LAUNCHED("small_k_wgrad_reduce_kernel");
-      if (ph_w >= 0) tm.mark(st, ph_w, 1);
-    } else {
+    const bool fused = (l == L) && s->fused_step;
+    // weight and bias gradient: dW = dZ^T A_in, db = column sums of dZ;
+    // fused: Adam on W_L in the epilogue (or split-K reduction) instead of a store
+    auto wgrad = [&]() -> int {
+      if (l == 1 && ly.in <= ot::kMaxSmallK) {
+        if (ph_w >= 0) tm.mark(st, ph_w, 0);
+        const int64_t rows_per = ot::ceil_div(b, kL1Parts);
+        const int64_t P = ot::ceil_div(b, rows_per);
+        hipLaunchKernelGGL(ot::small_k_wgrad_partial_kernel, dim3((unsigned)ot::ceil_div(ly.out, 64), (unsigned)P),
+                           dim3(256), 0, st, s->dz[1], s->ld[1], x, ldx, s->l1_part, b, ly.out, ly.in, rows_per,
+                           (const uint16_t*)nullptr);
+        OT_LAUNCHED("small_k_wgrad_partial_kernel");
+        const int64_t n = ly.out * (ly.in + 1);
+        hipLaunchKernelGGL(ot::small_k_wgrad_reduce_kernel, dim3((unsigned)ot::ceil_div(n, 256)), dim3(256), 0, st,
+                           s->l1_part, P, ly.out, ly.in, dW, ly.ldw, db);
+        OT_LAUNCHED("small_k_wgrad_reduce_kernel");
+        if (ph_w >= 0) tm.mark(st, ph_w, 1);
+        return OT_OK;
+      }
       GemmArgs g = args0();
       g.A = s->dz[l];
       g.lda = s->ld[l];
@@ -1178,29 +1273,46 @@ extern "C" int surrogate_train_step(ot_surrogate* s, const float* x, int64_t ldx
       g.N = ly.in;
       g.K = b;
       g.rowsum = db;
-      rc = (l == L) ? run_gemm<Lay::MNMajor, Lay::MNMajor, 1>(s, g, Epi::Store, st, "weight gradient", true, ph_w,
-                                                              OT_PH_WGRAD_REDUCE)
-                    : run_gemm<Lay::MNMajor, Lay::MNMajor, 0>(s, g, Epi::Store, st, "weight gradient", true);
-      if (rc) return rc;
-    }
-    if (l == 1) break;
+      Epi epi = Epi::Store;
+      if (fused) {
+        g.C = s->params + ly.w_off;
+        g.adam_m = s->m + ly.w_off;
+        g.adam_v = s->v + ly.w_off;
+        g.adam = s->step_adam;
+        epi = Epi::Adam;
+      }
+      return (l == L) ? run_gemm<Lay::MNMajor, Lay::MNMajor, 1>(s, g, epi, st, "weight gradient", true, ph_w,
+                                                                OT_PH_WGRAD_REDUCE)
+                      : run_gemm<Lay::MNMajor, Lay::MNMajor, 0>(s, g, epi, st, "weight gradient", true);
+    };
     // input gradient dA_{l-1} = dZ_l W_l, then the ReLU mask of layer l-1
-    GemmArgs g = args0();
-    g.A = s->dz[l];
-    g.lda = s->ld[l];
-    g.B = s->params + ly.w_off;
-    g.ldb = ly.ldw;
-    g.M = b;
-    g.N = ly.in;
-    g.K = ly.out;
-    g.C = s->dz[l - 1];
-    g.ldc = s->ld[l - 1];
-    g.mask = s->act[l - 1];
-    g.ldmask = s->ld[l - 1];
-    rc = (l == L) ? run_gemm<Lay::KMajor, Lay::MNMajor, 1>(s, g, Epi::Mask, st, "input gradient", true,
-                                                           OT_PH_IGRAD_OUTPUT, OT_PH_IGRAD_REDUCE)
-                  : run_gemm<Lay::KMajor, Lay::MNMajor, 0>(s, g, Epi::Mask, st, "input gradient", true);
-    if (rc) return rc;
+    auto igrad = [&]() -> int {
+      GemmArgs g = args0();
+      g.A = s->dz[l];
+      g.lda = s->ld[l];
+      g.B = s->params + ly.w_off;
+      g.ldb = ly.ldw;
+      g.M = b;
+      g.N = ly.in;
+      g.K = ly.out;
+      g.C = s->dz[l - 1];
+      g.ldc = s->ld[l - 1];
+      g.mask = s->act[l - 1];
+      g.ldmask = s->ld[l - 1];
+      return (l == L) ? run_gemm<Lay::KMajor, Lay::MNMajor, 1>(s, g, Epi::Mask, st, "input gradient", true,
+                                                               OT_PH_IGRAD_OUTPUT, OT_PH_IGRAD_REDUCE)
+                      : run_gemm<Lay::KMajor, Lay::MNMajor, 0>(s, g, Epi::Mask, st, "input gradient", true);
+    };
+    if (l == 1) {
+      if ((rc = wgrad())) return rc;
+      break;
+    }
+    // the fused update rewrites W_L, which the input gradient reads first
+    if (fused) {
+      if ((rc = igrad()) || (rc = wgrad())) return rc;
+    } else {
+      if ((rc = wgrad()) || (rc = igrad())) return rc;
+    }
   }
   if (L >= 2) tm.mark(st, OT_PH_BWD_HIDDEN, 1);
 

@@ -1,6 +1,14 @@
 """Online training loop over the library: one aggregator put and one training
-step per iteration, as the paper's server alternates its data-aggregator and
-training threads (Sec. 3.1); all work is enqueued on one HIP stream.
+step per iteration, as the paper's server runs a data-aggregator thread that
+fills the buffer and a training thread that draws batches from it (Sec. 3.1).
+
+By default all work is enqueued on one HIP stream.  With overlap=True the
+reservoir (put, draw, gather) runs on its own ordering stream and the train
+step on the trainer's stream, with two batch buffers: the draw and gather of
+batch i + 1 run while batch i trains, as the paper's two threads do.  Events
+order the streams: train step i waits for gather i, and gather i + 2 waits for
+train step i to release its buffer.  The sequence of reservoir operations (and
+so every drawn slot) is the same as on one stream.
 """
 from __future__ import annotations
 
@@ -29,7 +37,8 @@ class OnlineTrainer:
                  inputs: Optional[torch.Tensor], fields: Optional[torch.Tensor], reservoir_seed: int,
                  init_seed: int, precision: int = OT_FP32, lr: float = 1e-3,
                  stream: Optional[torch.cuda.Stream] = None, record_steps: int = 0,
-                 chunk_fn: Optional[Callable] = None, n_chunks: int = 0, device=None):
+                 chunk_fn: Optional[Callable] = None, n_chunks: int = 0, device=None, flags: int = 0,
+                 overlap: bool = False):
         self.stream = stream if stream is not None else torch.cuda.current_stream()
         self.widths = tuple(widths)
         self.batch, self.wave, self.tau = batch, wave, tau
@@ -43,10 +52,18 @@ class OnlineTrainer:
             self.n_chunks = n_chunks
             dev = device
         x_dim, d = widths[0], widths[-1]
-        self.res = Reservoir(capacity, threshold, x_dim, d, reservoir_seed, order_stream=self.stream)
-        self.sur = Surrogate(widths, precision=precision, lr=lr, seed=init_seed, max_batch=batch)
-        self.xb = torch.empty(batch, _round_up(x_dim, 4), device=dev)[:, :x_dim]
-        self.ub = torch.empty(batch, _round_up(d, 4), device=dev)[:, :d]
+        self.overlap = overlap
+        # default-priority stream of its own for the reservoir when overlapping
+        self.res_stream = torch.cuda.Stream(device=dev) if overlap else self.stream
+        self.res = Reservoir(capacity, threshold, x_dim, d, reservoir_seed, order_stream=self.res_stream)
+        self.sur = Surrogate(widths, precision=precision, lr=lr, seed=init_seed, max_batch=batch, flags=flags)
+        nbuf = 2 if overlap else 1
+        self.xbufs = [torch.empty(batch, _round_up(x_dim, 4), device=dev)[:, :x_dim] for _ in range(nbuf)]
+        self.ubufs = [torch.empty(batch, _round_up(d, 4), device=dev)[:, :d] for _ in range(nbuf)]
+        self.xb, self.ub = self.xbufs[0], self.ubufs[0]
+        self.ready = [torch.cuda.Event() for _ in range(nbuf)]      # gather into buffer j done
+        self.released = [torch.cuda.Event() for _ in range(nbuf)]   # train step on buffer j done
+        self.released_recorded = [False] * nbuf
         self.slots = torch.empty(batch, dtype=torch.int32, device=dev)
         self.record_steps = record_steps
         self.slot_log = torch.empty((max(record_steps, 1), batch), dtype=torch.int32, device=dev)
@@ -69,23 +86,33 @@ class OnlineTrainer:
         if self.chunk_cursor >= self.n_chunks and not wrap:
             return False
         x, u = self.chunk_views(self.chunk_cursor)
-        self.res.put(x, u, stream=self.stream, accepted=self.accepted)
+        self.res.put(x, u, stream=self.res_stream, accepted=self.accepted)
         self.chunk_cursor += 1
         return True
 
     def sample_only(self) -> bool:
         """Draw a batch without gathering or training (marks samples seen)."""
-        st, _, _ = self.res.sample_batch(self.batch, self.slots, stream=self.stream)
+        st, _, _ = self.res.sample_batch(self.batch, self.slots, stream=self.res_stream)
         return st == OT_OK
 
     def sample_and_train(self) -> bool:
         rec = self.steps_done < self.record_steps
         slots = self.slot_log[self.steps_done] if rec else self.slots
-        st, n, _ = self.res.sample_batch(self.batch, slots, x_out=self.xb, u_out=self.ub, stream=self.stream)
+        j = self.steps_done % len(self.xbufs)
+        xb, ub = self.xbufs[j], self.ubufs[j]
+        if self.overlap and self.released_recorded[j]:
+            self.res_stream.wait_event(self.released[j])    # the step two back has finished with buffer j
+        st, n, _ = self.res.sample_batch(self.batch, slots, x_out=xb, u_out=ub, stream=self.res_stream)
         if st != OT_OK:
             return False
+        if self.overlap:
+            self.ready[j].record(self.res_stream)
+            self.stream.wait_event(self.ready[j])
         loss = self.loss_log[self.steps_done:self.steps_done + 1] if rec else self.loss
-        self.sur.train_step(self.xb, self.ub, stream=self.stream, loss=loss)
+        self.sur.train_step(xb, ub, stream=self.stream, loss=loss)
+        if self.overlap:
+            self.released[j].record(self.stream)
+            self.released_recorded[j] = True
         self.steps_done += 1
         return True
 

@@ -42,9 +42,9 @@ def problem(widths, B, seed):
     return params, X.astype(np.float32), U.astype(np.float32)
 
 
-def make_gpu(widths, params, B):
+def make_gpu(widths, params, B, flags=0):
     from paper_2309_16743_amd import OT_BF16, Surrogate
-    s = Surrogate(widths, precision=OT_BF16, max_batch=B, seed=0)
+    s = Surrogate(widths, precision=OT_BF16, max_batch=B, seed=0, flags=flags)
     for l, (W, b) in enumerate(params):
         s.set_params(l, W.astype(np.float32), b.astype(np.float32))
     return s
@@ -63,22 +63,36 @@ SHAPES = [
 
 @pytest.mark.parametrize("widths,B", SHAPES)
 def test_one_train_step_bf16(widths, B):
+    """Kept gradients: loss, every gradient and every parameter after Adam
+    against the oracle.  Fused output-layer Adam (the default): every
+    parameter against the oracle, and against the kept-gradient step within
+    1e-5 (the fused GEMM never splits k, the stored one may, so the gradient
+    sums can differ in rounding order)."""
+    from paper_2309_16743_amd import OT_SURROGATE_KEEP_GRADS
     print(f"bf16 one train step widths={widths} B={B}", flush=True)
     params, X, U = problem(widths, B, seed=sum(widths) + B)
-    s = make_gpu(widths, params, B)
-    loss = torch.zeros(1, device=DEV)
-    s.train_step(padded_from(X), padded_from(U), loss=loss)
+    s = make_gpu(widths, params, B, flags=OT_SURROGATE_KEEP_GRADS)
+    f = make_gpu(widths, params, B)
+    Xd, Ud = padded_from(X), padded_from(U)
+    loss, loss_f = torch.zeros(1, device=DEV), torch.zeros(1, device=DEV)
+    s.train_step(Xd, Ud, loss=loss)
+    f.train_step(Xd, Ud, loss=loss_f)
     torch.cuda.synchronize()
     o_loss, o_grads = mlp.loss_and_grads(params, X.astype(np.float64), U.astype(np.float64), bf16=True)
     o_new = mlp.Adam(lr=1e-3).step(params, o_grads)
     assert abs(loss.item() - o_loss) / o_loss < 1e-3
+    assert loss_f.item() == loss.item()
     for l in range(len(widths) - 1):
         gW, gb = s.get_grads(l)
         assert rel(gW, o_grads[l][0]) < TOL, (l, rel(gW, o_grads[l][0]))
         assert rel(gb, o_grads[l][1]) < TOL, (l, rel(gb, o_grads[l][1]))
         W, b = s.get_params(l)
         assert rel(W, o_new[l][0]) < TOL and rel(b, o_new[l][1]) < TOL
+        Wf, bf = f.get_params(l)
+        assert rel(Wf, o_new[l][0]) < TOL and rel(bf, o_new[l][1]) < TOL
+        assert rel(Wf, W) < 1e-5 and rel(bf, b) < 1e-5, (l, rel(Wf, W))
     s.close()
+    f.close()
 
 
 @pytest.mark.parametrize("widths,n", [((6, 64, 64, 256), 40), ((6, 100, 77, 1001), 77)])
@@ -120,15 +134,18 @@ def test_full_width_output_rows_bf16():
     train step from the library's own Philox initialisation; the oracle
     recomputes, for sampled output units j, dY[:, j], dW_L[j, :], db_L[j] and the
     updated W_L[j, :] from its own initialisation of those rows."""
-    from paper_2309_16743_amd import OT_BF16, Surrogate
+    from paper_2309_16743_amd import OT_BF16, OT_SURROGATE_KEEP_GRADS, Surrogate
     widths, B, seed = (6, 1024, 1024, 1_000_000), 512, 5
     rng = np.random.default_rng(11)
     X = np.concatenate([rng.uniform(100, 500, (B, 5)), rng.uniform(0.01, 1.0, (B, 1))], axis=1).astype(np.float32)
     U = rng.uniform(100, 500, (B, widths[-1])).astype(np.float32)
-    s = Surrogate(widths, precision=OT_BF16, max_batch=B, seed=seed)
+    s = Surrogate(widths, precision=OT_BF16, max_batch=B, seed=seed, flags=OT_SURROGATE_KEEP_GRADS)
+    f = Surrogate(widths, precision=OT_BF16, max_batch=B, seed=seed)      # fused output-layer Adam
     Ud = torch.from_numpy(U).to(DEV)
+    Xd = padded_from(X)
     loss = torch.zeros(1, device=DEV)
-    s.train_step(padded_from(X), Ud, loss=loss)
+    s.train_step(Xd, Ud, loss=loss)
+    f.train_step(Xd, Ud)
     torch.cuda.synchronize()
     del Ud
     # hidden layers from the oracle's own initialisation
@@ -147,4 +164,9 @@ def test_full_width_output_rows_bf16():
     W, b = s.get_params(2)
     newW = Wj - 1e-3 * dWj / (np.abs(dWj) + 1e-8)
     assert rel(W[js], newW) < TOL
+    Wf, bf = f.get_params(2)
+    assert rel(Wf[js], newW) < TOL
+    # neither step splits the 512-deep k range here: same sums, same Adam
+    assert np.array_equal(Wf, W) and np.array_equal(bf, b)
     s.close()
+    f.close()

@@ -46,9 +46,9 @@ def problem(widths, B, seed):
     return params, X.astype(np.float32), U.astype(np.float32)
 
 
-def make_gpu(widths, params, B):
+def make_gpu(widths, params, B, flags=0):
     from paper_2309_16743_amd import Surrogate
-    s = Surrogate(widths, max_batch=B, seed=0)
+    s = Surrogate(widths, max_batch=B, seed=0, flags=flags)
     for l, (W, b) in enumerate(params):
         s.set_params(l, W.astype(np.float32), b.astype(np.float32))
     return s
@@ -67,22 +67,47 @@ SHAPES = [
 
 @pytest.mark.parametrize("widths,B", SHAPES)
 def test_one_train_step(widths, B):
+    """Kept gradients: loss, every gradient and every parameter after Adam
+    against the oracle.  Fused output-layer Adam (the default): the same
+    parameters and Adam moments bit for bit (same gradient sums, same Adam
+    arithmetic), the output bias gradient still readable, its weight gradient
+    refused."""
+    from paper_2309_16743_amd import OT_SURROGATE_KEEP_GRADS, OTError
     print(f"one train step widths={widths} B={B}", flush=True)
     params, X, U = problem(widths, B, seed=sum(widths) + B)
-    s = make_gpu(widths, params, B)
-    loss = torch.zeros(1, device=DEV)
-    s.train_step(padded_from(X), padded_from(U), loss=loss)
+    s = make_gpu(widths, params, B, flags=OT_SURROGATE_KEEP_GRADS)
+    f = make_gpu(widths, params, B)
+    Xd, Ud = padded_from(X), padded_from(U)
+    loss, loss_f = torch.zeros(1, device=DEV), torch.zeros(1, device=DEV)
+    s.train_step(Xd, Ud, loss=loss)
+    f.train_step(Xd, Ud, loss=loss_f)
     torch.cuda.synchronize()
     o_loss, o_grads = mlp.loss_and_grads(params, X.astype(np.float64), U.astype(np.float64))
     o_new = mlp.Adam(lr=1e-3).step(params, o_grads)
     assert abs(loss.item() - o_loss) / o_loss < 1e-5
-    for l in range(len(widths) - 1):
+    assert loss_f.item() == loss.item()
+    L = len(widths) - 1
+    for l in range(L):
         gW, gb = s.get_grads(l)
         assert rel(gW, o_grads[l][0]) < 1e-4, (l, rel(gW, o_grads[l][0]))
         assert rel(gb, o_grads[l][1]) < 1e-4, (l, rel(gb, o_grads[l][1]))
         W, b = s.get_params(l)
         assert rel(W, o_new[l][0]) < 1e-4 and rel(b, o_new[l][1]) < 1e-4
+        Wf, bf = f.get_params(l)
+        assert np.array_equal(Wf, W) and np.array_equal(bf, b), l
+        (mW, mb), (vW, vb), t = s.get_adam_state(l)
+        (mWf, mbf), (vWf, vbf), tf = f.get_adam_state(l)
+        assert t == tf == 1
+        for a, c in ((mWf, mW), (mbf, mb), (vWf, vW), (vbf, vb)):
+            assert np.array_equal(a, c), l
+    fused_out = not (L == 1 and widths[0] <= 16)   # a small-K single layer stores its gradient
+    if fused_out:
+        with pytest.raises(OTError):
+            f.get_grads(L - 1)
+    _, gb = s.get_grads(L - 1)
+    assert np.array_equal(f.get_grads(L - 1, weights=False)[1], gb)
     s.close()
+    f.close()
 
 
 @pytest.mark.parametrize("widths,n", [((6, 64, 64, 256), 50), ((6, 37, 50, 123), 77), ((20, 48, 30), 5)])
@@ -117,10 +142,11 @@ def test_tiny_workload_100_steps():
     X = heat.sample_parameters(w.n_sims, w.data_seed)
     inputs = heat.inputs_for(X, w.tau)
     fields = heat.heat_fields(X, w.grid, w.tau)
+    from paper_2309_16743_amd import OT_SURROGATE_KEEP_GRADS
     ref = runner.run(w, inputs, fields, n_steps=100, keep_grads=(1, 100))
     tr = OnlineTrainer(w.widths, w.batch, w.capacity, w.threshold, w.wave, w.tau,
                        torch.from_numpy(inputs).to(DEV), torch.from_numpy(fields).to(DEV),
-                       w.reservoir_seed, w.init_seed, lr=w.lr, record_steps=100)
+                       w.reservoir_seed, w.init_seed, lr=w.lr, record_steps=100, flags=OT_SURROGATE_KEEP_GRADS)
     grads1 = None
     while tr.steps_done < 100:
         tr.iterate()
@@ -141,4 +167,54 @@ def test_tiny_workload_100_steps():
         assert rel(W, ref["params"][l][0]) < 1e-3 and rel(b, ref["params"][l][1]) < 1e-3
     st = tr.res.stats()
     assert st["total_evicted"] == ref["reservoir"].total_evicted == 16
+    tr.close()
+
+
+def test_tiny_workload_100_steps_fused():
+    """The same schedule with the output layer's Adam fused into its gradient
+    GEMM (the default): slots bit-exact, loss series and final parameters
+    within 1e-3 relative L2 of the oracle."""
+    from paper_2309_16743_amd.online import OnlineTrainer
+    w = configs.TINY
+    X = heat.sample_parameters(w.n_sims, w.data_seed)
+    inputs = heat.inputs_for(X, w.tau)
+    fields = heat.heat_fields(X, w.grid, w.tau)
+    ref = runner.run(w, inputs, fields, n_steps=100)
+    tr = OnlineTrainer(w.widths, w.batch, w.capacity, w.threshold, w.wave, w.tau,
+                       torch.from_numpy(inputs).to(DEV), torch.from_numpy(fields).to(DEV),
+                       w.reservoir_seed, w.init_seed, lr=w.lr, record_steps=100)
+    tr.run(100)
+    torch.cuda.synchronize()
+    slots = tr.slot_log.cpu().numpy()
+    for i in range(100):
+        assert np.array_equal(slots[i], ref["slots"][i]), i
+    assert rel(tr.loss_log.cpu().numpy(), ref["losses"]) < 1e-3
+    for l in range(3):
+        W, b = tr.sur.get_params(l)
+        assert rel(W, ref["params"][l][0]) < 1e-3 and rel(b, ref["params"][l][1]) < 1e-3
+    tr.close()
+
+
+def test_tiny_workload_overlapped_streams():
+    """The 16x16 schedule with the reservoir on its own stream and two batch
+    buffers (the draw of batch i + 1 overlaps train step i): the same slots
+    bit for bit and the same losses as the oracle."""
+    from paper_2309_16743_amd.online import OnlineTrainer
+    w = configs.TINY
+    X = heat.sample_parameters(w.n_sims, w.data_seed)
+    inputs = heat.inputs_for(X, w.tau)
+    fields = heat.heat_fields(X, w.grid, w.tau)
+    ref = runner.run(w, inputs, fields, n_steps=100)
+    tr = OnlineTrainer(w.widths, w.batch, w.capacity, w.threshold, w.wave, w.tau,
+                       torch.from_numpy(inputs).to(DEV), torch.from_numpy(fields).to(DEV),
+                       w.reservoir_seed, w.init_seed, lr=w.lr, record_steps=100, overlap=True)
+    tr.run(100)
+    torch.cuda.synchronize()
+    slots = tr.slot_log.cpu().numpy()
+    for i in range(100):
+        assert np.array_equal(slots[i], ref["slots"][i]), i
+    assert rel(tr.loss_log.cpu().numpy(), ref["losses"]) < 1e-3
+    for l in range(3):
+        W, b = tr.sur.get_params(l)
+        assert rel(W, ref["params"][l][0]) < 1e-3 and rel(b, ref["params"][l][1]) < 1e-3
     tr.close()
