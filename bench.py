@@ -4,7 +4,10 @@
 One step is one pass of the whole hot path on one batch: a put of one chunk of
 streamed samples into the GPU reservoir (replacing seen samples once full), a
 batch draw with replacement and its gather, and one train step of the MLP
-surrogate (forward, fused MSE, backward, Adam).
+surrogate (forward, fused MSE, backward, Adam).  The reservoir's put, draw and
+gather for the next batch run on a second stream while the current batch
+trains (two batch buffers, ordered by events), as the paper's aggregator and
+training threads run concurrently; --one-stream runs everything on one stream.
 
 Default workload (--config heat-100x100): 100x100 heat fields from an FTCS
 solver, 1000 simulations x 100 steps, MLP 6-256-256-10000 fp32, batch 1024,
@@ -366,10 +369,12 @@ def timed_region(tr, w, K, profile_steps, stream, wrap_put):
     kp = max(profile_steps, 1)
     tr.sur.timing_begin(list(SURROGATE_PHASES), kp)
     tr.res.timing_begin(["put_assign", "put_copy", "select", "gather"], 2 * kp)
+    tr.serialize = True             # breakdown with the reservoir and train step one after the other
     for _ in range(kp):
         wrap_put()
         assert tr.sample_and_train()
     breakdown = kernel_table(w, tr.sur.timing_end(), tr.res.timing_end())
+    tr.serialize = False
     candidates = ("fwd_output", "wgrad_output", "igrad_output", "adam", "reservoir_gather")
     dominant = max(candidates, key=lambda p: breakdown[p]["avg_us"])
     dom_phase = "gather" if dominant == "reservoir_gather" else dominant

@@ -138,8 +138,7 @@ struct BEpi {
     static_assert(ROWS % RPP == 0, "chunk rows");
     constexpr int NP = ROWS / RPP;
     if constexpr (EPI == EpiB::AdamF32) {
-      stage();
-      adam_rows<NP>(g, ep, m0);
+      adam_rows<NP>(g, ep, m0, stage);
       return;
     }
     // targets (MseBf) or mask (MaskBf) of each pass; one branch around all
@@ -216,59 +215,69 @@ struct BEpi {
     }
   }
 
-  // AdamF32: the chunk's gradients are staged in ep; each lane updates 4
-  // consecutive parameters of a row per pass.  The master weights and both
-  // moments of G passes are loaded together (non-temporal: every parameter is
-  // touched once per step), then updated and stored.
-  template <int NP>
-  __device__ __forceinline__ void adam_rows(const GemmBArgs& g, const float* ep, int64_t m0) {
+  // AdamF32: each lane updates 4 consecutive parameters of a row per pass,
+  // passes taken in groups of G.  The master weights and both moments of a
+  // group are loaded together (non-temporal: every parameter is touched once
+  // per step), and the loads of group i + 1 are issued before group i is
+  // updated and stored, so two groups are in flight; group 0's loads are
+  // issued before the gradients are staged in LDS.
+  template <int NP, class Stage>
+  __device__ __forceinline__ void adam_rows(const GemmBArgs& g, const float* ep, int64_t m0, Stage stage) {
     constexpr int G = NP < 4 ? NP : 4;
+    constexpr int NG = NP / G;
     static_assert(NP % G == 0, "pass groups");
-    if (col >= g.N) return;
     float* const P = reinterpret_cast<float*>(g.C);
-#pragma unroll
-    for (int i0 = 0; i0 < NP; i0 += G) {
-      if (cfull) {
-        f32x4 pp[G], mm[G], vv[G];
-#pragma unroll
-        for (int u = 0; u < G; ++u) {
-          const int64_t m = min(m0 + rl + RPP * (i0 + u), g.M - 1);   // clamped rows are not stored
-          const int64_t o = m * g.ldc + col;
-          pp[u] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(P + o));
-          mm[u] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(g.adam_m + o));
-          vv[u] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(g.adam_v + o));
+    if (!cfull || col >= g.N) {
+      stage();
+      if (col >= g.N) return;
+      for (int i = 0; i < NP; ++i) {
+        const int rr = rl + RPP * i;
+        const int64_t m = m0 + rr;
+        if (m >= g.M) continue;
+        for (int c = 0; c < 4; ++c) {
+          if (col + c >= g.N) break;
+          const int64_t o = m * g.ldc + col + c;
+          float p = P[o], mo = g.adam_m[o], vo = g.adam_v[o];
+          adam1(p, ep[rr * EP + 4 * cg + c], mo, vo, g.adam);
+          P[o] = p;
+          g.adam_m[o] = mo;
+          g.adam_v[o] = vo;
+          g.adam_pb[o] = f2bf(p);
         }
+      }
+      return;
+    }
+    f32x4 pp[2][G], mm[2][G], vv[2][G];
+    auto load = [&](int grp, int buf) {
 #pragma unroll
-        for (int u = 0; u < G; ++u) {
-          const int rr = rl + RPP * (i0 + u);
-          const int64_t m = m0 + rr;
-          if (m >= g.M) continue;
-          const f32x4 gr = *reinterpret_cast<const f32x4*>(ep + rr * EP + 4 * cg);
-          adam4(pp[u], gr, mm[u], vv[u], g.adam);
-          const int64_t o = m * g.ldc + col;
-          __builtin_nontemporal_store(pp[u], reinterpret_cast<f32x4*>(P + o));
-          __builtin_nontemporal_store(mm[u], reinterpret_cast<f32x4*>(g.adam_m + o));
-          __builtin_nontemporal_store(vv[u], reinterpret_cast<f32x4*>(g.adam_v + o));
-          __builtin_nontemporal_store(u16x4{f2bf(pp[u][0]), f2bf(pp[u][1]), f2bf(pp[u][2]), f2bf(pp[u][3])},
-                                      reinterpret_cast<u16x4*>(g.adam_pb + o));
-        }
-      } else {
+      for (int u = 0; u < G; ++u) {
+        const int64_t m = min(m0 + rl + RPP * (grp * G + u), g.M - 1);   // clamped rows are not stored
+        const int64_t o = m * g.ldc + col;
+        pp[buf][u] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(P + o));
+        mm[buf][u] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(g.adam_m + o));
+        vv[buf][u] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(g.adam_v + o));
+      }
+    };
+    load(0, 0);
+    stage();
 #pragma unroll
-        for (int u = 0; u < G; ++u) {
-          const int rr = rl + RPP * (i0 + u);
-          const int64_t m = m0 + rr;
-          if (m >= g.M) continue;
-          for (int c = 0; c < 4; ++c) {
-            if (col + c >= g.N) break;
-            const int64_t o = m * g.ldc + col + c;
-            float p = P[o], mo = g.adam_m[o], vo = g.adam_v[o];
-            adam1(p, ep[rr * EP + 4 * cg + c], mo, vo, g.adam);
-            P[o] = p;
-            g.adam_m[o] = mo;
-            g.adam_v[o] = vo;
-            g.adam_pb[o] = f2bf(p);
-          }
-        }
+    for (int gi = 0; gi < NG; ++gi) {
+      const int buf = gi & 1;
+      if (gi + 1 < NG) load(gi + 1, buf ^ 1);
+#pragma unroll
+      for (int u = 0; u < G; ++u) {
+        const int rr = rl + RPP * (gi * G + u);
+        const int64_t m = m0 + rr;
+        if (m >= g.M) continue;
+        const f32x4 gr = *reinterpret_cast<const f32x4*>(ep + rr * EP + 4 * cg);
+        adam4(pp[buf][u], gr, mm[buf][u], vv[buf][u], g.adam);
+        const int64_t o = m * g.ldc + col;
+        __builtin_nontemporal_store(pp[buf][u], reinterpret_cast<f32x4*>(P + o));
+        __builtin_nontemporal_store(mm[buf][u], reinterpret_cast<f32x4*>(g.adam_m + o));
+        __builtin_nontemporal_store(vv[buf][u], reinterpret_cast<f32x4*>(g.adam_v + o));
+        __builtin_nontemporal_store(
+            u16x4{f2bf(pp[buf][u][0]), f2bf(pp[buf][u][1]), f2bf(pp[buf][u][2]), f2bf(pp[buf][u][3])},
+            reinterpret_cast<u16x4*>(g.adam_pb + o));
       }
     }
   }

@@ -64,6 +64,11 @@ class OnlineTrainer:
         self.ready = [torch.cuda.Event() for _ in range(nbuf)]      # gather into buffer j done
         self.released = [torch.cuda.Event() for _ in range(nbuf)]   # train step on buffer j done
         self.released_recorded = [False] * nbuf
+        # serialize=True (overlap mode only): each put waits for the train
+        # step before it, so per-kernel timings are not inflated by the other
+        # stream's kernels (used for breakdowns, not for throughput)
+        self.serialize = False
+        self._train_done = torch.cuda.Event() if overlap else None
         self.slots = torch.empty(batch, dtype=torch.int32, device=dev)
         self.record_steps = record_steps
         self.slot_log = torch.empty((max(record_steps, 1), batch), dtype=torch.int32, device=dev)
@@ -86,6 +91,9 @@ class OnlineTrainer:
         if self.chunk_cursor >= self.n_chunks and not wrap:
             return False
         x, u = self.chunk_views(self.chunk_cursor)
+        if self.overlap and self.serialize:
+            self._train_done.record(self.stream)
+            self.res_stream.wait_event(self._train_done)
         self.res.put(x, u, stream=self.res_stream, accepted=self.accepted)
         self.chunk_cursor += 1
         return True
