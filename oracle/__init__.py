@@ -11,6 +11,8 @@ Modules:
   philox     -- Philox4x64-10 and the integer range map used for every draw.
   reservoir  -- slot encoding of Algorithm 1 (put with eviction of seen items,
                 batch draw with replacement, threshold, drain after reception).
+  buffers    -- the FIFO and FIRO comparison buffers of Sec. 3.2.3 (samples
+                leave the buffer when read).
   mlp        -- fp64 MLP forward, mean-squared-error loss, backward, Adam, with
                 an optional bf16 operand-rounding mode.
   runner     -- the deterministic put / sample / train loop over a workload.
