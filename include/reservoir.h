@@ -1,5 +1,7 @@
-/* GPU-resident training reservoir (the paper's Algorithm 1 "Reservoir",
- * Sec. 3.2.3), one per device.
+/* GPU-resident training buffer (Sec. 3.2.3), one per device: the paper's
+ * Algorithm 1 "Reservoir" (the default policy), or one of its two comparison
+ * buffers, FIFO and FIRO, which evict a sample when it is read (see
+ * ot_reservoir_policy below).
  *
  * The buffer holds at most C samples, each an input row x (x_dim fp32: the
  * simulation parameters X and the time t, Sec. 4.1) and a field row u (u_dim
@@ -58,18 +60,44 @@ typedef struct ot_reservoir_stats {
   int64_t next_sample_id;
   int32_t reception_over;
   int32_t hist_len;       /* length of the eviction histogram (reservoir_read_meta) */
+  int32_t policy;         /* ot_reservoir_policy */
+  int32_t reserved;
 } ot_reservoir_stats;
 
+/* Buffer policies (Sec. 3.2.3).  Each answers put / sample_batch /
+ * end_reception over the same slabs, tickets, statuses and gather.
+ * OT_POLICY_RESERVOIR: Algorithm 1 as described below (evict seen samples on
+ *   write, draw with replacement while N > T, drain after reception).
+ * OT_POLICY_FIFO: first in, first out.  put accepts a = min(k, C - N) (the
+ *   paper suspends production while the buffer is full); a batch takes the b
+ *   oldest samples and removes them, and is refused (OT_NOT_READY) while
+ *   N < b -- a batch as soon as the buffer holds one; the threshold is not
+ *   used.  Every sample is used exactly once, in arrival order.
+ * OT_POLICY_FIRO: first in, random out.  put as FIFO (appends to the list of
+ *   stored samples); a batch is refused while N <= T or N < b, otherwise it
+ *   takes b distinct samples by partial Fisher-Yates over the list (Philox
+ *   kind 1, j = draw index, range N - j; the remaining list keeps the
+ *   shuffled order) and removes them.
+ * FIFO and FIRO: after end_reception the threshold is 0, the last batch may be
+ *   short (min(b, N)) and an empty buffer answers OT_EMPTY; b <= 4096; a freed
+ *   slot joins a queue of free slots and a stored row takes the queue's head
+ *   (initially slots 0 .. C-1 in order, so FIFO fills the slab as a ring);
+ *   nothing is evicted by a put, so total_evicted stays 0 and every sample
+ *   leaves with seen count 1. */
+enum ot_reservoir_policy { OT_POLICY_RESERVOIR = 0, OT_POLICY_FIFO = 1, OT_POLICY_FIRO = 2 };
+
 /* Create a reservoir of `capacity` samples of x_dim + u_dim fp32 values.
- * threshold: batches are refused while N <= threshold (Algorithm 1, get).
- * seed: Philox key word 0.  order_stream: hipStream_t to run the reservoir's
+ * threshold: batches are refused while N <= threshold (Algorithm 1, get;
+ * unused by FIFO).  seed: Philox key word 0.  policy: ot_reservoir_policy.
+ * order_stream: hipStream_t to run the reservoir's
  * work on, or NULL to let the reservoir create (and later destroy) its own.
  * Allocates C * (round_up(x_dim, 4) + round_up(u_dim, 64)) * 4 bytes of slab
- * plus 16 bytes per slot of metadata on the current device.
+ * plus 20 bytes per slot of metadata on the current device.
  * Errors: OT_E_INVAL (capacity < 1 or > 2^31-1, threshold < 0, x_dim or u_dim
- * < 1), OT_E_NOMEM, OT_E_HIP. */
+ * < 1, unknown policy), OT_E_NOMEM, OT_E_HIP. */
 int reservoir_create(ot_reservoir** out, int64_t capacity, int64_t threshold,
-                     int64_t x_dim, int64_t u_dim, uint64_t seed, void* order_stream);
+                     int64_t x_dim, int64_t u_dim, uint64_t seed, int32_t policy,
+                     void* order_stream);
 
 /* Store up to k samples (Algorithm 1, put; Sec. 3.2.3).
  * x: k rows of x_dim fp32 at stride ldx elements (may be NULL: x rows are
@@ -83,7 +111,8 @@ int reservoir_create(ot_reservoir** out, int64_t capacity, int64_t threshold,
  * the next sample id and a seen count of 0.
  * accepted_dev: device int64 that receives a when the work runs (nullable).
  * ticket_out: host uint64 that receives the call's ticket (nullable).
- * k may be 0 (takes a ticket, stores nothing).  1 <= k <= 65536 otherwise.
+ * FIFO / FIRO accept a = min(k, C - N) into the free slots (see above).
+ * k may be 0 (takes a ticket, stores nothing).  1 <= k <= 4096 otherwise.
  * Errors: OT_E_CLOSED after end_reception, OT_E_INVAL, OT_E_HIP. */
 int reservoir_put(ot_reservoir* r, const float* x, int64_t ldx, const float* u, int64_t ldu,
                   int64_t k, void* stream, int64_t* accepted_dev, uint64_t* ticket_out);
@@ -101,7 +130,9 @@ int reservoir_put(ot_reservoir* r, const float* x, int64_t ldx, const float* u, 
  * u_out: device fp32 b rows at stride lduo (nullable; lduo multiple of 4).
  * count_out: host int64 receiving the number of rows drawn (nullable).
  * The batch is atomic with respect to puts.
- * Errors: OT_E_INVAL (b < 1, b > 65536, null slots, bad ld), OT_E_HIP. */
+ * FIFO / FIRO: see ot_reservoir_policy.
+ * Errors: OT_E_INVAL (b < 1, b > 65536 (4096 for FIFO / FIRO and while
+ * draining), null slots, bad ld), OT_E_HIP. */
 int reservoir_sample_batch(ot_reservoir* r, int64_t b, void* stream, int32_t* slots,
                            float* x_out, int64_t ldxo, float* u_out, int64_t lduo,
                            int64_t* count_out, uint64_t* ticket_out);

@@ -15,7 +15,8 @@ import numpy as np
 
 from . import _abi
 from ._abi import (OT_BF16, OT_E_CLOSED, OT_E_INVAL, OT_E_STATE, OT_EMPTY, OT_FP32, OT_NOT_READY, OT_OK,
-                   OT_SURROGATE_KEEP_GRADS, OTError, check, last_error, load)
+                   OT_POLICY_FIFO, OT_POLICY_FIRO, OT_POLICY_RESERVOIR, OT_SURROGATE_KEEP_GRADS, OTError,
+                   check, last_error, load)
 
 __all__ = [
     "Reservoir", "Surrogate", "reservoir_create", "reservoir_put", "reservoir_sample_batch",
@@ -24,7 +25,7 @@ __all__ = [
     "surrogate_get_grads", "surrogate_get_adam_state", "surrogate_set_lr", "surrogate_train_step",
     "surrogate_predict", "surrogate_destroy", "load", "last_error", "OTError",
     "OT_OK", "OT_NOT_READY", "OT_EMPTY", "OT_E_INVAL", "OT_E_CLOSED", "OT_E_STATE", "OT_FP32", "OT_BF16",
-    "OT_SURROGATE_KEEP_GRADS",
+    "OT_SURROGATE_KEEP_GRADS", "OT_POLICY_RESERVOIR", "OT_POLICY_FIFO", "OT_POLICY_FIRO",
 ]
 
 
@@ -59,11 +60,13 @@ class Reservoir:
     """Handle of one GPU training reservoir (include/reservoir.h)."""
 
     def __init__(self, capacity: int, threshold: int, x_dim: int, u_dim: int, seed: int,
-                 order_stream=None):
+                 order_stream=None, policy: int = OT_POLICY_RESERVOIR):
         lib = load()
         h = C.c_void_p()
         st = None if order_stream is None else _stream_handle(order_stream)
-        check("reservoir_create", lib.reservoir_create(C.byref(h), capacity, threshold, x_dim, u_dim, seed, st))
+        check("reservoir_create", lib.reservoir_create(C.byref(h), capacity, threshold, x_dim, u_dim, seed, policy,
+                                                       st))
+        self.policy = policy
         self._h = h
         self.capacity, self.threshold, self.x_dim, self.u_dim = capacity, threshold, x_dim, u_dim
 
@@ -235,8 +238,9 @@ class Surrogate:
 
 
 # ---- C-named entry points (argument marshalling only) ----------------------------
-def reservoir_create(capacity, threshold, x_dim, u_dim, seed, order_stream=None) -> Reservoir:
-    return Reservoir(capacity, threshold, x_dim, u_dim, seed, order_stream)
+def reservoir_create(capacity, threshold, x_dim, u_dim, seed, policy=OT_POLICY_RESERVOIR,
+                     order_stream=None) -> Reservoir:
+    return Reservoir(capacity, threshold, x_dim, u_dim, seed, order_stream, policy)
 
 
 def reservoir_put(r: Reservoir, x, u, stream=None, accepted=None) -> int:

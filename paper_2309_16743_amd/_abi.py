@@ -22,6 +22,9 @@ OT_E_STATE = -5
 OT_FP32 = 0
 OT_BF16 = 1
 OT_SURROGATE_KEEP_GRADS = 1
+OT_POLICY_RESERVOIR = 0
+OT_POLICY_FIFO = 1
+OT_POLICY_FIRO = 2
 
 SURROGATE_PHASES = ("fwd_hidden", "fwd_output", "loss", "wgrad_output", "igrad_output", "igrad_reduce",
                     "bwd_hidden", "adam", "wgrad_reduce")
@@ -32,7 +35,7 @@ class ReservoirStats(C.Structure):
     _fields_ = [(name, C.c_int64) for name in (
         "capacity", "threshold", "n", "unseen", "seen", "total_put", "total_evicted",
         "total_deleted", "total_draws", "next_ticket", "next_sample_id")] + [
-        ("reception_over", C.c_int32), ("hist_len", C.c_int32)]
+        ("reception_over", C.c_int32), ("hist_len", C.c_int32), ("policy", C.c_int32), ("reserved", C.c_int32)]
 
 
 vp = C.c_void_p
@@ -45,7 +48,7 @@ f32 = C.c_float
 SIGNATURES = {
     "ot_last_error": (C.c_char_p, []),
     "ot_version": (C.c_char_p, []),
-    "reservoir_create": (C.c_int, [C.POINTER(vp), i64, i64, i64, i64, u64, vp]),
+    "reservoir_create": (C.c_int, [C.POINTER(vp), i64, i64, i64, i64, u64, i32, vp]),
     "reservoir_put": (C.c_int, [vp, vp, i64, vp, i64, i64, vp, vp, C.POINTER(u64)]),
     "reservoir_sample_batch": (C.c_int, [vp, i64, vp, vp, vp, i64, vp, i64, C.POINTER(i64), C.POINTER(u64)]),
     "reservoir_end_reception": (C.c_int, [vp]),

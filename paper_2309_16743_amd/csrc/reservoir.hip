@@ -1,6 +1,15 @@
-// GPU-resident training reservoir: the paper's Algorithm 1 ("Reservoir",
-// Sec. 3.2.3) as slot-encoded device state plus four kernels per operation
-// pair (put: assign + copy, sample: select + gather).
+// GPU-resident training buffers of Sec. 3.2.3: the paper's Algorithm 1
+// ("Reservoir") as slot-encoded device state plus four kernels per operation
+// pair (put: assign + copy, sample: select + gather), and the two comparison
+// buffers that evict a sample when it is read, FIFO and FIRO, over the same
+// slabs, gather and copy kernels.
+//
+// FIFO / FIRO state: the list of stored samples `occ` is a ring of C
+// positions starting at occ_base; free slots form a second ring `free_q`
+// (head free_head, C - N entries): a put takes slots from its head and
+// appends them to the list, a batch takes samples out of the list (FIFO: the
+// first B; FIRO: B positions by partial Fisher-Yates) and pushes their slots
+// at the free queue's tail.  All ring positions are known on the host.
 //
 // State on the device: an x slab (C x ldxs fp32) and a u slab (C x ldus fp32),
 // per-slot seen counts (int32, -1 = empty slot) and sample ids (int64), the
@@ -83,8 +92,9 @@ __device__ int block_exclusive_scan(int v, int* wave_tot, int* total) {
 // the pre_j chains are resolved by pointer jumping.  Inputs: r[0..E) in LDS.
 // Outputs: pre[0..E), taken[0..E) in LDS; last_writer[j] = 1 when no later
 // step writes position r_j (used by the drain to persist the shuffle).
-// base == nullptr stands for the identity array (A[p] = p).
-__device__ void resolve_partial_shuffle(int E, const int* r, const int* base, int* par, int* par2,
+// base(p) returns base[p] (the identity for the eviction list).
+template <class Base>
+__device__ void resolve_partial_shuffle(int E, const int* r, Base base, int* par, int* par2,
                                         int* lv, int* pre, int* taken, int* last_writer) {
   const int nt = blockDim.x;
   for (int j = threadIdx.x; j < E; j += nt) {
@@ -111,11 +121,11 @@ __device__ void resolve_partial_shuffle(int E, const int* r, const int* base, in
     __syncthreads();
     int* t = src; src = dst; dst = t;
   }
-  for (int j = threadIdx.x; j < E; j += nt) pre[j] = base ? base[src[j]] : src[j];
+  for (int j = threadIdx.x; j < E; j += nt) pre[j] = base(src[j]);
   __syncthreads();
   for (int j = threadIdx.x; j < E; j += nt) {
     const int rj = r[j];
-    taken[j] = (rj == j) ? pre[j] : (lv[j] >= 0 ? pre[lv[j]] : (base ? base[rj] : rj));
+    taken[j] = (rj == j) ? pre[j] : (lv[j] >= 0 ? pre[lv[j]] : base(rj));
   }
   __syncthreads();
 }
@@ -200,7 +210,7 @@ __global__ __launch_bounds__(kAssignThreads) void put_assign_kernel(
       s_r[j] = (int)(j + (long long)range_map(w, (uint64_t)(S - j)));
     }
     __syncthreads();
-    resolve_partial_shuffle((int)E, s_r, nullptr, s_par, s_par2, s_lv, s_pre, s_taken, s_last);
+    resolve_partial_shuffle((int)E, s_r, [](int p) { return p; }, s_par, s_par2, s_lv, s_pre, s_taken, s_last);
     for (long long j = tid; j < E; j += nt) victim_pos[j] = s_taken[j];
   }
   __syncthreads();
@@ -343,13 +353,18 @@ __global__ void select_kernel(uint64_t seed, uint64_t ticket, int64_t N, int64_t
   }
 }
 
-// Batch draw after reception ends: b' = min(b, N) distinct samples by
-// partial Fisher-Yates over the drain order occ[base, base + N); the drawn
-// samples are removed.  One block.
-__global__ __launch_bounds__(kAssignThreads) void drain_select_kernel(
-    uint64_t seed, uint64_t ticket, int64_t N, int64_t bb, int64_t occ_base,
-    int32_t* __restrict__ occ, int32_t* __restrict__ slots, int32_t* __restrict__ seen,
-    long long* __restrict__ sample_id, unsigned long long* __restrict__ hist,
+// Batch that takes its samples out of the list occ (ring of C positions from
+// occ_base, N entries): the Reservoir after reception ends and FIRO draw
+// bb distinct positions by partial Fisher-Yates (shuffle = 1: step j swaps
+// positions j and j + floor(w_j (N - j) / 2^64), w_j = Philox(seed; j,
+// ticket, 1), and takes position j); FIFO takes the first bb (shuffle = 0).
+// The shuffled positions that stay in the list are written back, the taken
+// slots are pushed on the free queue from position free_tail, and their
+// metadata cleared.  One block.
+__global__ __launch_bounds__(kAssignThreads) void list_take_kernel(
+    uint64_t seed, uint64_t ticket, int64_t N, int64_t bb, int shuffle, int64_t occ_base, int64_t C,
+    int32_t* __restrict__ occ, int32_t* __restrict__ free_q, int64_t free_tail, int32_t* __restrict__ slots,
+    int32_t* __restrict__ seen, long long* __restrict__ sample_id, unsigned long long* __restrict__ hist,
     ResCounters* __restrict__ ctr) {
   __shared__ int s_r[kMaxDrainBatch];
   __shared__ int s_par[kMaxDrainBatch];
@@ -360,20 +375,27 @@ __global__ __launch_bounds__(kAssignThreads) void drain_select_kernel(
   __shared__ int s_last[kMaxDrainBatch];
   __shared__ long long s_dU, s_dS;
   const int tid = threadIdx.x, nt = blockDim.x;
-  int32_t* base = occ + occ_base;
+  auto pos = [&](int64_t p) { return (occ_base + p) % C; };
   if (tid == 0) { s_dU = 0; s_dS = 0; }
-  for (long long j = tid; j < bb; j += nt) {
-    const uint64_t w = draw_word(seed, (uint64_t)j, ticket, kKindSample);
-    s_r[j] = (int)(j + (long long)range_map(w, (uint64_t)(N - j)));
+  if (shuffle) {
+    for (long long j = tid; j < bb; j += nt) {
+      const uint64_t w = draw_word(seed, (uint64_t)j, ticket, kKindSample);
+      s_r[j] = (int)(j + (long long)range_map(w, (uint64_t)(N - j)));
+    }
+    __syncthreads();
+    resolve_partial_shuffle((int)bb, s_r, [&](int p) { return (int)occ[pos(p)]; }, s_par, s_par2, s_lv, s_pre,
+                            s_taken, s_last);
+    // Persist the shuffle for positions that stay in the list.
+    for (long long j = tid; j < bb; j += nt)
+      if (s_r[j] >= bb && s_last[j]) occ[pos(s_r[j])] = s_pre[j];
+  } else {
+    for (long long j = tid; j < bb; j += nt) s_taken[j] = occ[pos(j)];
   }
   __syncthreads();
-  resolve_partial_shuffle((int)bb, s_r, base, s_par, s_par2, s_lv, s_pre, s_taken, s_last);
-  // Persist the shuffle for positions that stay in the buffer.
-  for (long long j = tid; j < bb; j += nt)
-    if (s_r[j] >= bb && s_last[j]) base[s_r[j]] = s_pre[j];
   for (long long j = tid; j < bb; j += nt) {
     const int slot = s_taken[j];
     slots[j] = slot;
+    free_q[(free_tail + j) % C] = slot;
     const int c = seen[slot] + 1;
     atomicAdd(&hist[min(c, kHistLen - 1)], 1ull);
     if (c == 1) atomicAdd((unsigned long long*)&s_dU, 1ull);
@@ -388,6 +410,33 @@ __global__ __launch_bounds__(kAssignThreads) void drain_select_kernel(
     ctr->N -= bb;
     ctr->total_deleted += bb;
     ctr->total_draws += bb;
+  }
+}
+
+// FIFO / FIRO put, metadata decisions: the a = min(k, C - N) accepted rows
+// take the slots at the head of the free queue and are appended to the list.
+// a and every ring position are known on the host.
+__global__ void list_put_kernel(int64_t a, int64_t N, int64_t occ_base, int64_t free_head, int64_t C,
+                                const int32_t* __restrict__ free_q, int32_t* __restrict__ occ,
+                                int32_t* __restrict__ put_slots, ResCounters* __restrict__ ctr,
+                                long long* __restrict__ accepted_out) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < a) {
+    const int32_t slot = free_q[(free_head + i) % C];
+    put_slots[i] = slot;
+    occ[(occ_base + N + i) % C] = slot;
+  }
+  if (i == 0) {
+    const long long base_id = ctr->next_sample_id;
+    ctr->U += a;
+    ctr->N += a;
+    ctr->total_put += a;
+    ctr->next_sample_id = base_id + a;
+    ctr->last_accepted = a;
+    ctr->last_free = a;     // no row replaces a stored sample
+    ctr->last_evicted = 0;
+    ctr->last_base_id = base_id;
+    if (accepted_out) *accepted_out = a;
   }
 }
 
@@ -421,6 +470,7 @@ using ot::ResCounters;
 
 struct ot_reservoir {
   int device = 0;
+  int policy = OT_POLICY_RESERVOIR;
   int64_t C = 0, T = 0, x_dim = 0, u_dim = 0, ldxs = 0, ldus = 0;
   uint64_t seed = 0;
   float* xslab = nullptr;
@@ -428,6 +478,7 @@ struct ot_reservoir {
   int32_t* seen = nullptr;
   long long* sample_id = nullptr;
   int32_t* occ = nullptr;
+  int32_t* free_q = nullptr;   // FIFO / FIRO: ring of free slots
   int32_t* put_slots = nullptr;
   int32_t* tile_cnt = nullptr;
   int32_t* tile_off = nullptr;
@@ -441,7 +492,8 @@ struct ot_reservoir {
   std::mutex mu;
   uint64_t next_ticket = 0;
   int64_t n_host = 0;      // N, known from the call sequence
-  int64_t occ_base = 0;    // drain order offset
+  int64_t occ_base = 0;    // ring position of the list's first entry (drain, FIFO, FIRO)
+  int64_t free_head = 0;   // ring position of the first free slot (FIFO, FIRO)
   bool reception_over = false;
   ot::PhaseTimer timer;
 };
@@ -457,6 +509,7 @@ void free_reservoir(ot_reservoir* r) {
   (void)hipFree(r->seen);
   (void)hipFree(r->sample_id);
   (void)hipFree(r->occ);
+  (void)hipFree(r->free_q);
   (void)hipFree(r->put_slots);
   (void)hipFree(r->tile_cnt);
   (void)hipFree(r->tile_off);
@@ -501,16 +554,20 @@ bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) ==
 }  // namespace
 
 extern "C" int reservoir_create(ot_reservoir** out, int64_t capacity, int64_t threshold,
-                                int64_t x_dim, int64_t u_dim, uint64_t seed, void* order_stream) {
+                                int64_t x_dim, int64_t u_dim, uint64_t seed, int32_t policy,
+                                void* order_stream) {
   ot::clear_error();
   OT_REQUIRE(out != nullptr, "reservoir_create: out is NULL");
   *out = nullptr;
+  OT_REQUIRE(policy == OT_POLICY_RESERVOIR || policy == OT_POLICY_FIFO || policy == OT_POLICY_FIRO,
+             "reservoir_create: unknown policy %d", (int)policy);
   OT_REQUIRE(capacity >= 1 && capacity <= 0x7fffffffLL, "reservoir_create: capacity %lld outside [1, 2^31-1]",
              (long long)capacity);
   OT_REQUIRE(threshold >= 0, "reservoir_create: threshold < 0");
   OT_REQUIRE(x_dim >= 1 && x_dim <= 4096, "reservoir_create: x_dim outside [1, 4096]");
   OT_REQUIRE(u_dim >= 1 && u_dim <= (1LL << 31), "reservoir_create: u_dim outside [1, 2^31]");
   ot_reservoir* r = new ot_reservoir();
+  r->policy = policy;
   r->C = capacity;
   r->T = threshold;
   r->x_dim = x_dim;
@@ -529,6 +586,7 @@ extern "C" int reservoir_create(ot_reservoir** out, int64_t capacity, int64_t th
   if ((rc = dev_alloc(&r->seen, (size_t)capacity))) return fail(rc);
   if ((rc = dev_alloc(&r->sample_id, (size_t)capacity))) return fail(rc);
   if ((rc = dev_alloc(&r->occ, (size_t)capacity))) return fail(rc);
+  if ((rc = dev_alloc(&r->free_q, (size_t)capacity))) return fail(rc);
   if ((rc = dev_alloc(&r->put_slots, (size_t)ot::kMaxPut))) return fail(rc);
   r->ntiles = ot::ceil_div(capacity, ot::kTile);
   if ((rc = dev_alloc(&r->tile_cnt, (size_t)r->ntiles))) return fail(rc);
@@ -550,6 +608,11 @@ extern "C" int reservoir_create(ot_reservoir** out, int64_t capacity, int64_t th
   hipLaunchKernelGGL(ot::init_meta_kernel, dim3((unsigned)ot::ceil_div(n_init, 256)), dim3(256), 0,
                      r->stream, r->seen, r->sample_id, capacity, r->hist, r->ctr);
   if (hipGetLastError() != hipSuccess) return fail(ot::set_error(OT_E_HIP, "init_meta_kernel launch failed"));
+  if (policy != OT_POLICY_RESERVOIR) {   // every slot free, in slot order
+    hipLaunchKernelGGL(ot::iota_kernel, dim3((unsigned)ot::ceil_div(capacity, 256)), dim3(256), 0, r->stream,
+                       r->free_q, capacity);
+    if (hipGetLastError() != hipSuccess) return fail(ot::set_error(OT_E_HIP, "iota_kernel launch failed"));
+  }
   if (hipStreamSynchronize(r->stream) != hipSuccess)
     return fail(ot::set_error(OT_E_HIP, "reservoir_create: stream synchronise failed"));
   *out = r;
@@ -576,6 +639,30 @@ extern "C" int reservoir_put(ot_reservoir* r, const float* x, int64_t ldx, const
   int rc = enter(r, cs);
   if (rc) return rc;
   ot::PhaseTimer& tm = r->timer;
+  if (r->policy != OT_POLICY_RESERVOIR) {
+    // FIFO / FIRO: the accepted prefix and every ring position are host-known
+    const int64_t a = std::min<int64_t>(k, r->C - r->n_host);
+    tm.mark(r->stream, OT_PH_PUT_ASSIGN, 0);
+    hipLaunchKernelGGL(ot::list_put_kernel, dim3((unsigned)std::max<int64_t>(1, ot::ceil_div(a, 256))), dim3(256),
+                       0, r->stream, a, r->n_host, r->occ_base, r->free_head, r->C, r->free_q, r->occ,
+                       r->put_slots, r->ctr, reinterpret_cast<long long*>(accepted_dev));
+    OT_LAUNCHED("list_put_kernel");
+    tm.mark(r->stream, OT_PH_PUT_ASSIGN, 1);
+    if (a > 0) {
+      tm.mark(r->stream, OT_PH_PUT_COPY, 0);
+      const int vec_ok = aligned16(u) && (ldu % 4 == 0);
+      const int64_t segs = ot::ceil_div(r->u_dim, ot::kCopySeg);
+      hipLaunchKernelGGL(ot::put_copy_kernel, dim3((unsigned)(segs * a)), dim3(ot::kCopyThreads), 0, r->stream,
+                         x, ldx, u, ldu, r->put_slots, r->ctr, r->xslab, r->ldxs, r->uslab, r->ldus, r->x_dim,
+                         r->u_dim, segs, vec_ok, r->seen, r->sample_id, r->hist, r->C);
+      OT_LAUNCHED("put_copy_kernel");
+      tm.mark(r->stream, OT_PH_PUT_COPY, 1);
+    }
+    tm.next_call();
+    r->n_host += a;
+    r->free_head = (r->free_head + a) % r->C;
+    return leave(r, cs);
+  }
   tm.mark(r->stream, OT_PH_PUT_ASSIGN, 0);
   // Replacement is possible only if N + k > C (host-known N); only then are
   // the seen slots indexed.
@@ -622,6 +709,10 @@ extern "C" int reservoir_sample_batch(ot_reservoir* r, int64_t b, void* stream, 
   OT_REQUIRE(u_out == nullptr || lduo >= r->u_dim, "reservoir_sample_batch: lduo < u_dim");
   OT_REQUIRE(x_out == nullptr || ldxo >= r->x_dim, "reservoir_sample_batch: ldxo < x_dim");
   hipStream_t cs = static_cast<hipStream_t>(stream);
+  const bool list_take = r->policy != OT_POLICY_RESERVOIR;   // FIFO / FIRO take samples out
+  if (list_take)
+    OT_REQUIRE(b <= ot::kMaxDrainBatch, "reservoir_sample_batch: b=%lld above %lld for a FIFO / FIRO buffer",
+               (long long)b, (long long)ot::kMaxDrainBatch);
   std::lock_guard<std::mutex> lock(r->mu);
   int64_t drawn = b;
   if (r->reception_over) {
@@ -629,6 +720,10 @@ extern "C" int reservoir_sample_batch(ot_reservoir* r, int64_t b, void* stream, 
     OT_REQUIRE(b <= ot::kMaxDrainBatch, "reservoir_sample_batch: b=%lld above %lld while draining",
                (long long)b, (long long)ot::kMaxDrainBatch);
     drawn = std::min<int64_t>(b, r->n_host);
+  } else if (r->policy == OT_POLICY_FIFO) {
+    if (r->n_host < b) return OT_NOT_READY;           // a batch as soon as the buffer holds one
+  } else if (r->policy == OT_POLICY_FIRO) {
+    if (r->n_host <= r->T || r->n_host < b) return OT_NOT_READY;
   } else if (r->n_host <= r->T) {
     return OT_NOT_READY;
   }
@@ -638,16 +733,18 @@ extern "C" int reservoir_sample_batch(ot_reservoir* r, int64_t b, void* stream, 
   if (rc) return rc;
   ot::PhaseTimer& tm = r->timer;
   tm.mark(r->stream, OT_PH_SELECT, 0);
-  if (!r->reception_over) {
+  if (!r->reception_over && !list_take) {
     hipLaunchKernelGGL(ot::select_kernel, dim3((unsigned)ot::ceil_div(b, 256)), dim3(256), 0, r->stream,
                        r->seed, ticket, r->n_host, b, slots, r->seen, r->ctr);
     OT_LAUNCHED("select_kernel");
   } else {
-    hipLaunchKernelGGL(ot::drain_select_kernel, dim3(1), dim3(ot::kAssignThreads), 0, r->stream, r->seed,
-                       ticket, r->n_host, drawn, r->occ_base, r->occ, slots, r->seen, r->sample_id,
-                       r->hist, r->ctr);
-    OT_LAUNCHED("drain_select_kernel");
-    r->occ_base += drawn;
+    // free queue tail: C - N entries follow its head
+    const int64_t free_tail = (r->free_head + r->C - r->n_host) % r->C;
+    hipLaunchKernelGGL(ot::list_take_kernel, dim3(1), dim3(ot::kAssignThreads), 0, r->stream, r->seed, ticket,
+                       r->n_host, drawn, r->policy == OT_POLICY_FIFO ? 0 : 1, r->occ_base, r->C, r->occ,
+                       r->free_q, free_tail, slots, r->seen, r->sample_id, r->hist, r->ctr);
+    OT_LAUNCHED("list_take_kernel");
+    r->occ_base = (r->occ_base + drawn) % r->C;
     r->n_host -= drawn;
   }
   tm.mark(r->stream, OT_PH_SELECT, 1);
@@ -673,6 +770,7 @@ extern "C" int reservoir_end_reception(ot_reservoir* r) {
   if (r->reception_over) return ot::set_error(OT_E_STATE, "reservoir_end_reception: already over");
   r->reception_over = true;
   r->T = 0;
+  if (r->policy != OT_POLICY_RESERVOIR) return OT_OK;   // the list is already maintained
   r->occ_base = 0;
   if (r->n_host > 0) {
     hipLaunchKernelGGL(ot::iota_kernel, dim3((unsigned)ot::ceil_div(r->n_host, 256)), dim3(256), 0, r->stream,
@@ -702,6 +800,8 @@ extern "C" int reservoir_stats(ot_reservoir* r, ot_reservoir_stats* out) {
   out->next_sample_id = c.next_sample_id;
   out->reception_over = r->reception_over ? 1 : 0;
   out->hist_len = ot::kHistLen;
+  out->policy = r->policy;
+  out->reserved = 0;
   return OT_OK;
 }
 

@@ -18,3 +18,4 @@ def compare_meta(gres, ores, hist_len):
     assert (st["n"], st["unseen"], st["seen"]) == (ores.N, ores.U, ores.S)
     assert st["total_put"] == ores.total_put and st["total_evicted"] == ores.total_evicted
     assert st["total_draws"] == ores.total_draws and st["next_ticket"] == ores.next_ticket
+    assert st["total_deleted"] == ores.total_deleted

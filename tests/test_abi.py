@@ -54,9 +54,11 @@ def test_version_and_error_string(lib):
 def test_validation_errors_before_device_work(lib):
     from paper_2309_16743_amd import _abi
     h = C.c_void_p()
-    assert lib.reservoir_create(C.byref(h), 0, 0, 6, 10, 0, None) == _abi.OT_E_INVAL
+    assert lib.reservoir_create(C.byref(h), 0, 0, 6, 10, 0, 0, None) == _abi.OT_E_INVAL
     assert b"capacity" in lib.ot_last_error()
-    assert lib.reservoir_create(C.byref(h), 10, -1, 6, 10, 0, None) == _abi.OT_E_INVAL
+    assert lib.reservoir_create(C.byref(h), 10, -1, 6, 10, 0, 0, None) == _abi.OT_E_INVAL
+    assert lib.reservoir_create(C.byref(h), 10, 1, 6, 10, 0, 3, None) == _abi.OT_E_INVAL
+    assert b"policy" in lib.ot_last_error()
     assert lib.reservoir_put(None, None, 0, None, 0, 1, None, None, None) == _abi.OT_E_INVAL
     assert lib.reservoir_sample_batch(None, 4, None, None, None, 0, None, 0, None, None) == _abi.OT_E_INVAL
     w = (C.c_int64 * 3)(6, 0, 4)

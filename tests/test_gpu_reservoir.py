@@ -178,3 +178,78 @@ def test_concurrent_producers_replay_in_ticket_order():
             assert np.array_equal(u, ou)
     compare_meta(g, o, 64)
     g.close()
+
+
+@pytest.mark.parametrize("policy,C,T,d,seed,ops", [
+    ("fifo", 64, 0, 256, 3, 150),
+    ("fifo", 97, 0, 1003, 4, 150),      # prime capacity, ragged rows: the slot ring wraps many times
+    ("firo", 64, 20, 256, 5, 150),
+    ("firo", 300, 50, 4099, 6, 120),    # rows longer than one copy segment
+])
+def test_list_policy_sequence_bit_exact(policy, C, T, d, seed, ops):
+    """FIFO / FIRO (evict on read) against the oracle's buffers: statuses,
+    tickets, accepted counts, taken slots, gathered rows, per-slot metadata
+    and counters bit-exact over puts and batches that cycle the slots, then
+    the drain after end_reception."""
+    from paper_2309_16743_amd import OT_NOT_READY, OT_OK, OT_POLICY_FIFO, OT_POLICY_FIRO, Reservoir
+    from oracle import buffers as obf
+    print(f"{policy} sequence C={C} T={T} d={d} seed={seed}", flush=True)
+    rng = np.random.default_rng(seed)
+    g = Reservoir(C, T, 6, d, seed, policy=OT_POLICY_FIFO if policy == "fifo" else OT_POLICY_FIRO)
+    o = (obf.FIFOBuffer if policy == "fifo" else obf.FIROBuffer)(C, T, 6, d, seed)
+    key = 0
+    acc = torch.zeros(1, dtype=torch.int64, device=DEV)
+    batches = 0
+    for step in range(ops):
+        if rng.random() < 0.5:
+            k = int(rng.integers(0, 50))
+            keys = np.arange(key, key + k)
+            u, x = hash_rows(keys, d), hash_inputs(keys)
+            ud, xd = padded(k, d), padded(k, 6)
+            if k:
+                ud.copy_(torch.from_numpy(u))
+                xd.copy_(torch.from_numpy(x))
+            t = g.put(xd if k else None, ud if k else None, accepted=acc)
+            _, a, ot_, _ = o.put(x, u, k=k)
+            assert t == ot_
+            torch.cuda.synchronize()
+            assert int(acc.item()) == a
+            key += a
+        else:
+            b = int(rng.integers(1, 40))
+            slots = torch.empty(b, dtype=torch.int32, device=DEV)
+            ub, xb = padded(b, d), padded(b, 6)
+            st, n, t = g.sample_batch(b, slots, x_out=xb, u_out=ub)
+            ost, oslots, ox, ou, ot_ = o.sample_batch(b)
+            assert st == ost
+            if st == OT_OK:
+                batches += 1
+                assert t == ot_ and n == b
+                torch.cuda.synchronize()
+                assert np.array_equal(slots.cpu().numpy(), np.array(oslots))
+                assert np.array_equal(ub.cpu().numpy(), ou)
+                assert np.array_equal(xb.cpu().numpy(), ox)
+            else:
+                assert st == OT_NOT_READY
+        if step % 10 == 9:
+            compare_meta(g, o, 64)
+    compare_meta(g, o, 64)
+    assert batches > 10 and o.total_put > 2 * C
+    g.end_reception()
+    o.end_reception()
+    while True:
+        b = int(rng.integers(1, 40))
+        slots = torch.empty(b, dtype=torch.int32, device=DEV)
+        ub = padded(b, d)
+        st, n, t = g.sample_batch(b, slots, u_out=ub)
+        ost, oslots, _, ou, _ = o.sample_batch(b)
+        assert st == ost
+        if st != OT_OK:
+            break
+        torch.cuda.synchronize()
+        assert n == len(oslots)
+        assert np.array_equal(slots[:n].cpu().numpy(), np.array(oslots))
+        assert np.array_equal(ub[:n].cpu().numpy(), ou)
+        compare_meta(g, o, 64)
+    assert o.N == 0 and g.stats()["policy"] == (1 if policy == "fifo" else 2)
+    g.close()
