@@ -63,6 +63,9 @@ def parse_args():
     p.add_argument("--steps", type=int, default=None, help="timed steps (default 2000 fp32, 100 bf16)")
     p.add_argument("--warmup", type=int, default=None, help="untimed steps before timing (default 50 / 5)")
     p.add_argument("--config", default="heat-100x100")
+    p.add_argument("--policy-comparison", action="store_true",
+                   help="instead of the throughput benchmark: stream the heat-100x100 ensemble once through the "
+                        "Reservoir, FIRO and FIFO buffers and report train steps and samples/s per buffer")
     p.add_argument("--one-stream", action="store_true",
                    help="run the reservoir and the train step on one stream (default: the reservoir's put, draw "
                         "and gather of the next batch overlap the current train step on a second stream)")
@@ -469,6 +472,60 @@ def run_heat(args, w):
     return line
 
 
+def run_policy_comparison(args, w):
+    """The paper's buffer comparison (Sec. 4.3, Fig. 2 / Table 1) on this
+    workload's production schedule: the whole ensemble is streamed once through
+    each buffer (one put of the wave's rows per iteration, then a train step
+    whenever the buffer yields a batch), then reception ends and the buffer is
+    drained.  Reports per policy the train steps, trained samples, GPU time and
+    trained samples/s; the Reservoir repeats samples, so it trains more batches
+    from the same production."""
+    import torch
+
+    from fixtures import heat
+    from paper_2309_16743_amd import OT_POLICY_FIFO, OT_POLICY_FIRO, OT_POLICY_RESERVOIR
+    from paper_2309_16743_amd.online import OnlineTrainer
+    X = heat.sample_parameters(w.n_sims, w.data_seed)
+    inputs = heat.inputs_for(X, w.tau)
+    fields = heat.heat_fields(X, w.grid, w.tau)
+    dev = torch.device("cuda:0")
+    inputs_d = torch.from_numpy(inputs).to(dev)
+    fields_d = torch.from_numpy(fields).to(dev)
+    stream = torch.cuda.Stream(device=dev)
+    out = {}
+    for name, policy in (("reservoir", OT_POLICY_RESERVOIR), ("firo", OT_POLICY_FIRO), ("fifo", OT_POLICY_FIFO)):
+        with torch.cuda.stream(stream):
+            tr = OnlineTrainer(w.widths, w.batch, w.capacity, w.threshold, w.wave, w.tau, inputs_d, fields_d,
+                               w.reservoir_seed, w.init_seed, lr=w.lr, stream=stream, policy=policy)
+            e0, e1, e2 = (torch.cuda.Event(enable_timing=True) for _ in range(3))
+            torch.cuda.synchronize()
+            e0.record(stream)
+            steps_stream = 0
+            for _ in range(w.n_chunks):
+                steps_stream += int(tr.iterate())
+            e1.record(stream)
+            tr.res.end_reception()
+            steps_drain = 0
+            while tr.sample_and_train():
+                steps_drain += 1
+            e2.record(stream)
+            torch.cuda.synchronize()
+            st = tr.res.stats()
+            steps = steps_stream + steps_drain
+            ms = e0.elapsed_time(e2)
+            out[name] = {"train_steps": steps, "steps_while_streaming": steps_stream, "steps_draining": steps_drain,
+                         "trained_samples": st["total_draws"], "produced_samples": st["total_put"],
+                         "batches_per_1000_produced": round(1000.0 * steps / max(st["total_put"], 1), 2),
+                         "gpu_ms": round(ms, 2), "streaming_ms": round(e0.elapsed_time(e1), 2),
+                         "samples_per_s": round(st["total_draws"] / (ms * 1e-3), 1),
+                         "last_loss": float(tr.loss.item())}
+            tr.close()
+    return {"metric": "buffer comparison: trained samples per produced sample and samples/s (Sec. 4.3)",
+            "workload": w.name, "production": f"{w.n_chunks} puts of {w.wave} rows (the ensemble once), "
+                                              f"then end of reception and drain",
+            "batch": w.batch, "capacity": w.capacity, "threshold": w.threshold, "policies": out}
+
+
 def run_field(args, w):
     import torch
 
@@ -714,7 +771,13 @@ def main():
                   file=sys.stderr)
             sys.exit(2)
         w = configs.ALL[args.config]
-        line = run_heat(args, w) if w.fields == "ftcs" else run_field(args, w)
+        if args.policy_comparison:
+            if w.fields != "ftcs":
+                print("--policy-comparison streams an FTCS ensemble (tiny-16x16 or heat-100x100)", file=sys.stderr)
+                sys.exit(2)
+            line = run_policy_comparison(args, w)
+        else:
+            line = run_heat(args, w) if w.fields == "ftcs" else run_field(args, w)
     text = json.dumps(line)
     print(text, flush=True)
     if args.out:

@@ -16,7 +16,7 @@ from typing import Callable, Optional
 
 import torch
 
-from . import OT_FP32, OT_BF16, OT_OK, Reservoir, Surrogate
+from . import OT_FP32, OT_BF16, OT_OK, OT_POLICY_RESERVOIR, Reservoir, Surrogate
 
 
 def _round_up(v: int, m: int) -> int:
@@ -38,7 +38,7 @@ class OnlineTrainer:
                  init_seed: int, precision: int = OT_FP32, lr: float = 1e-3,
                  stream: Optional[torch.cuda.Stream] = None, record_steps: int = 0,
                  chunk_fn: Optional[Callable] = None, n_chunks: int = 0, device=None, flags: int = 0,
-                 overlap: bool = False):
+                 overlap: bool = False, policy: int = OT_POLICY_RESERVOIR):
         self.stream = stream if stream is not None else torch.cuda.current_stream()
         self.widths = tuple(widths)
         self.batch, self.wave, self.tau = batch, wave, tau
@@ -55,7 +55,8 @@ class OnlineTrainer:
         self.overlap = overlap
         # default-priority stream of its own for the reservoir when overlapping
         self.res_stream = torch.cuda.Stream(device=dev) if overlap else self.stream
-        self.res = Reservoir(capacity, threshold, x_dim, d, reservoir_seed, order_stream=self.res_stream)
+        self.res = Reservoir(capacity, threshold, x_dim, d, reservoir_seed, order_stream=self.res_stream,
+                             policy=policy)
         self.sur = Surrogate(widths, precision=precision, lr=lr, seed=init_seed, max_batch=batch, flags=flags)
         nbuf = 2 if overlap else 1
         self.xbufs = [torch.empty(batch, _round_up(x_dim, 4), device=dev)[:, :x_dim] for _ in range(nbuf)]
