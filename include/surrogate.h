@@ -99,6 +99,18 @@ int surrogate_train_step(ot_surrogate* s, const float* x, int64_t ldx, const flo
 int surrogate_predict(ot_surrogate* s, const float* x, int64_t ldx, int64_t n, float* y,
                       int64_t ldy, void* stream);
 
+/* Validation loss (Sec. 4.4 validates on simulations never used for
+ * training): the mean over n x widths[L] of (f_theta(x) - u)^2 with the
+ * current parameters, by the train step's forward and fused-MSE kernels;
+ * parameters, gradients and Adam state are untouched.  Rows are processed in
+ * chunks of the workspace size and their squared residuals summed in fp64 in
+ * a fixed order.  x: n rows at stride ldx; u: n target rows at stride ldu
+ * (multiple of 4, 16-byte aligned); loss_dev: device fp32 scalar (required).
+ * Asynchronous on `stream`; calls on one surrogate must not overlap.
+ * Errors: OT_E_INVAL, OT_E_HIP. */
+int surrogate_eval_loss(ot_surrogate* s, const float* x, int64_t ldx, const float* u,
+                        int64_t ldu, int64_t n, void* stream, float* loss_dev);
+
 /* Kernel phases of one train step, for the timing hook below. */
 enum ot_surrogate_phase {
   OT_PH_FWD_HIDDEN = 0,    /* hidden-layer forward GEMMs (bias + ReLU epilogue) */

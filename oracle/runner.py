@@ -7,6 +7,16 @@ chunk i of the streamed ensemble (while chunks remain), then draws a batch of
 B and, if the buffer answered with a batch, runs one train step (forward, MSE,
 backward, Adam).  The GPU path is driven by the same loop, so both see the
 same ticket sequence.
+
+Training instrumentation of Sec. 4.4-4.5, optional:
+  * learning-rate schedule: the rate starts at lr0 and is halved every
+    `every_samples` trained samples down to a floor lr_min (the paper halves
+    1e-3 every 1000 batches of 10, i.e. every 10,000 samples, to 2.5e-4); the
+    rate of a step is set from the samples trained before it;
+  * validation: the mean squared error of the current surrogate on held-out
+    simulations, every `validate_every` train steps, taken after that step;
+  * repetition histogram: how many times each sample that entered the buffer
+    was drawn (residents and samples that left alike).
 """
 from __future__ import annotations
 
@@ -16,8 +26,24 @@ import numpy as np
 
 from fixtures.configs import Workload, chunk_for_iteration
 
-from .mlp import Adam, init_params, loss_and_grads
+from .mlp import Adam, init_params, loss_and_grads, mse, predict
 from .reservoir import NOT_READY, OK, Reservoir
+
+
+def halving_lr(lr0: float, samples_trained: int, every_samples: int, lr_min: float) -> float:
+    """lr0 halved once per completed block of every_samples trained samples, floored at lr_min."""
+    return max(lr0 * 0.5 ** (samples_trained // every_samples), lr_min)
+
+
+def repetition_histogram(res, length: int) -> np.ndarray:
+    """h[k] = number of samples that entered the buffer and were drawn k times
+    (k >= length - 1 counted in the last bin)."""
+    h = np.zeros(length, np.int64)
+    for k, c in res.evict_hist.items():
+        h[min(k, length - 1)] += c
+    for s in res.occ:
+        h[min(int(res.seen_count[s]), length - 1)] += 1
+    return h
 
 
 def chunk_arrays(w: Workload, inputs: np.ndarray, fields: np.ndarray, chunk: int):
@@ -30,16 +56,20 @@ def chunk_arrays(w: Workload, inputs: np.ndarray, fields: np.ndarray, chunk: int
 
 def run(w: Workload, inputs: np.ndarray, fields: np.ndarray, n_steps: int,
         params=None, bf16: Optional[bool] = None, keep_grads: Iterable[int] = (),
-        lr: Optional[float] = None) -> Dict:
-    """Run the schedule until n_steps train steps are done; return the trace."""
+        lr: Optional[float] = None, lr_halving: Optional[tuple] = None,
+        validation: Optional[tuple] = None) -> Dict:
+    """Run the schedule until n_steps train steps are done; return the trace.
+    lr_halving: (every_samples, lr_min); validation: (X_val, U_val, every)."""
     if bf16 is None:
         bf16 = w.precision == "bf16"
     res = Reservoir(w.capacity, w.threshold, inputs.shape[-1], fields.shape[-1], w.reservoir_seed)
     if params is None:
         params = init_params(w.widths, w.init_seed)
-    opt = Adam(lr=w.lr if lr is None else lr)
+    lr0 = w.lr if lr is None else lr
+    opt = Adam(lr=lr0)
     keep = set(keep_grads)
-    trace = dict(losses=[], slots=[], tickets=[], put_accepted=[], grads={}, params_at={})
+    trace = dict(losses=[], slots=[], tickets=[], put_accepted=[], grads={}, params_at={}, lrs=[],
+                 val_losses={})
     i = done = 0
     while done < n_steps:
         chunk = chunk_for_iteration(w, i)
@@ -49,9 +79,15 @@ def run(w: Workload, inputs: np.ndarray, fields: np.ndarray, n_steps: int,
             trace["put_accepted"].append(acc)
         st, slots, xb, ub, ticket = res.sample_batch(w.batch)
         if st == OK:
+            if lr_halving is not None:
+                opt.lr = halving_lr(lr0, done * w.batch, *lr_halving)
+            trace["lrs"].append(opt.lr)
             loss, grads = loss_and_grads(params, xb, ub, bf16=bf16)
             params = opt.step(params, grads)
             done += 1
+            if validation is not None and done % validation[2] == 0:
+                Xv, Uv = validation[0], validation[1]
+                trace["val_losses"][done] = mse(predict(params, Xv, bf16=bf16), Uv)
             trace["losses"].append(loss)
             trace["slots"].append(np.array(slots, dtype=np.int64))
             trace["tickets"].append(ticket)

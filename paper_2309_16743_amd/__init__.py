@@ -23,7 +23,7 @@ __all__ = [
     "reservoir_end_reception", "reservoir_stats", "reservoir_read_meta", "reservoir_read_rows",
     "reservoir_destroy", "surrogate_create", "surrogate_set_params", "surrogate_get_params",
     "surrogate_get_grads", "surrogate_get_adam_state", "surrogate_set_lr", "surrogate_train_step",
-    "surrogate_predict", "surrogate_destroy", "load", "last_error", "OTError",
+    "surrogate_predict", "surrogate_eval_loss", "surrogate_destroy", "load", "last_error", "OTError",
     "OT_OK", "OT_NOT_READY", "OT_EMPTY", "OT_E_INVAL", "OT_E_CLOSED", "OT_E_STATE", "OT_FP32", "OT_BF16",
     "OT_SURROGATE_KEEP_GRADS", "OT_POLICY_RESERVOIR", "OT_POLICY_FIFO", "OT_POLICY_FIRO",
 ]
@@ -213,6 +213,13 @@ class Surrogate:
         check("surrogate_predict", load().surrogate_predict(self._h, xp, ldx, x.shape[0], yp, ldy,
                                                             _stream_handle(stream)))
 
+    def eval_loss(self, x, u, loss, stream=None) -> None:
+        """Validation MSE of the current surrogate on rows x -> u into the device scalar `loss`."""
+        xp, ldx = _rows(x, "x")
+        up, ldu = _rows(u, "u")
+        check("surrogate_eval_loss", load().surrogate_eval_loss(self._h, xp, ldx, up, ldu, x.shape[0],
+                                                                _stream_handle(stream), _dev_ptr(loss)))
+
     def timing_begin(self, phases, max_steps: int) -> None:
         mask = sum(1 << _abi.SURROGATE_PHASES.index(p) for p in phases)
         check("surrogate_timing_begin", load().surrogate_timing_begin(self._h, mask, max_steps))
@@ -282,6 +289,10 @@ def surrogate_set_params(s: Surrogate, layer, W=None, b=None) -> None:
 
 def surrogate_get_params(s: Surrogate, layer):
     return s.get_params(layer)
+
+
+def surrogate_eval_loss(s: Surrogate, x, u, loss, stream=None):
+    return s.eval_loss(x, u, loss, stream)
 
 
 def surrogate_get_grads(s: Surrogate, layer):

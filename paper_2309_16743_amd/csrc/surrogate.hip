@@ -199,6 +199,27 @@ __global__ __launch_bounds__(256) void loss_finalize_kernel(const double* __rest
   }
 }
 
+// Evaluation loss over row chunks: acc = (first ? 0 : acc) + sum(partials),
+// partials added in a fixed order; the last chunk writes acc * inv_count.
+__global__ __launch_bounds__(256) void loss_accumulate_kernel(const double* __restrict__ partials, int64_t n,
+                                                              double* __restrict__ acc, int first, int last,
+                                                              double inv_count, float* __restrict__ loss) {
+  __shared__ double red[256];
+  double s = 0.0;
+  for (int64_t i = threadIdx.x; i < n; i += 256) s += partials[i];
+  red[threadIdx.x] = s;
+  __syncthreads();
+  for (int w = 128; w > 0; w >>= 1) {
+    if ((int)threadIdx.x < w) red[threadIdx.x] += red[threadIdx.x + w];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) {
+    const double t = (first ? 0.0 : *acc) + red[0];
+    *acc = t;
+    if (last && loss) *loss = (float)(t * inv_count);
+  }
+}
+
 // Adam over the flat parameter buffer (adam1 in adam.h), except the 16-byte
 // groups [hole, hole + hole_len) (the output-layer weights when their update
 // is fused into the weight-gradient GEMM).  Streaming kernel: two 16-byte
@@ -399,6 +420,7 @@ struct ot_surrogate {
   float* l1_part = nullptr;
   int64_t l1_part_elems = 0;
   float* loss_last = nullptr;
+  double* eval_acc = nullptr;   // running sum of squared residuals of surrogate_eval_loss
   ot::PhaseTimer timer;
   // OT_BF16 only
   uint16_t* pb = nullptr;                  // bf16 copy of the flat parameters
@@ -456,6 +478,7 @@ void free_surrogate(ot_surrogate* s) {
   (void)hipFree(s->m);
   (void)hipFree(s->v);
   (void)hipFree(s->loss_last);
+  (void)hipFree(s->eval_acc);
   (void)hipFree(s->pb);
   (void)hipFree(s->colsum);
   delete s;
@@ -837,8 +860,12 @@ int forward_hidden_bf16(ot_surrogate* s, const float* X, int64_t ldx, int64_t ro
   return OT_OK;
 }
 
-int train_step_bf16(ot_surrogate* s, const float* x, int64_t ldx, const float* u, int64_t ldu, int64_t b,
-                    hipStream_t st, float* loss_dev) {
+// bf16 forward of b rows and the output layer's fused MSE epilogue: dY (bf16)
+// into dz16[L], per-block loss partials; with bias_grad also the output bias
+// gradient (column sums of the rounded dY) into grads.  *n_partials receives
+// the number of loss partials.
+int forward_mse_bf16(ot_surrogate* s, const float* x, int64_t ldx, const float* u, int64_t ldu, int64_t b,
+                     hipStream_t st, bool bias_grad, int64_t* n_partials) {
   const int L = s->L;
   const int64_t D = s->widths[L];
   ot::PhaseTimer& tm = s->timer;
@@ -847,39 +874,51 @@ int train_step_bf16(ot_surrogate* s, const float* x, int64_t ldx, const float* u
   if ((rc = forward_hidden_bf16(s, x, ldx, b, st))) return rc;
   tm.mark(st, OT_PH_FWD_HIDDEN, 1);
   const Layer& lo = s->layers[L - 1];
-  int64_t n_partials = 0;
-  {
-    GemmBArgs g = bargs0();
-    g.A = s->act16[L - 1];
-    g.lda = s->ld[L - 1];
-    g.B = s->pb + lo.w_off;
-    g.ldb = lo.ldw;
-    g.C = s->dz16[L];
-    g.ldc = s->ld[L];
-    g.M = b;
-    g.N = D;
-    g.K = lo.in;
-    g.bias = s->params + lo.b_off;
-    g.target = u;
-    g.ldt = ldu;
-    g.scale = (float)(2.0 / ((double)b * (double)D));
-    g.loss_partials = s->loss_partials;
+  GemmBArgs g = bargs0();
+  g.A = s->act16[L - 1];
+  g.lda = s->ld[L - 1];
+  g.B = s->pb + lo.w_off;
+  g.ldb = lo.ldw;
+  g.C = s->dz16[L];
+  g.ldc = s->ld[L];
+  g.M = b;
+  g.N = D;
+  g.K = lo.in;
+  g.bias = s->params + lo.b_off;
+  g.target = u;
+  g.ldt = ldu;
+  g.scale = (float)(2.0 / ((double)b * (double)D));
+  g.loss_partials = s->loss_partials;
+  if (bias_grad) {
     // output bias gradient: per m-tile column sums of the rounded dY
     const int64_t mtiles = ot::ceil_div(b, 64);
     if ((rc = ensure_colsum(s, mtiles * s->ld[L]))) return rc;
     g.colsum = s->colsum;
     g.colsum_ld = s->ld[L];
-    n_partials = make_plan_b(g.M, g.N, g.K, false).blocks;
-    if (n_partials > s->n_partials_cap) return ot::set_error(OT_E_STATE, "loss partial buffer too small");
-    const Plan pf = make_plan_b(g.M, g.N, g.K, false);
-    if ((rc = run_gemm_b<LayB::KMajor, LayB::KMajor, EpiB::MseBf>(s, g, st, "bf16 output forward+MSE", false,
-                                                                  OT_PH_FWD_OUTPUT)))
-      return rc;
+  }
+  const Plan pf = make_plan_b(g.M, g.N, g.K, false);
+  *n_partials = pf.blocks;
+  if (pf.blocks > s->n_partials_cap) return ot::set_error(OT_E_STATE, "loss partial buffer too small");
+  if ((rc = run_gemm_b<LayB::KMajor, LayB::KMajor, EpiB::MseBf>(s, g, st, "bf16 output forward+MSE", false,
+                                                                OT_PH_FWD_OUTPUT)))
+    return rc;
+  if (bias_grad) {
     const int64_t used_mtiles = ot::ceil_div(b, pf.cfg == kBPipe ? 256 : (pf.cfg == kB128 ? 128 : 64));
     hipLaunchKernelGGL(ot::colsum_reduce_kernel, dim3((unsigned)ot::ceil_div(D, 256)), dim3(256), 0, st, s->colsum,
                        used_mtiles, D, s->ld[L], s->grads + lo.b_off);
     OT_LAUNCHED("colsum_reduce_kernel");
   }
+  return OT_OK;
+}
+
+int train_step_bf16(ot_surrogate* s, const float* x, int64_t ldx, const float* u, int64_t ldu, int64_t b,
+                    hipStream_t st, float* loss_dev) {
+  const int L = s->L;
+  const int64_t D = s->widths[L];
+  ot::PhaseTimer& tm = s->timer;
+  int rc;
+  int64_t n_partials = 0;
+  if ((rc = forward_mse_bf16(s, x, ldx, u, ldu, b, st, true, &n_partials))) return rc;
   tm.mark(st, OT_PH_LOSS, 0);
   hipLaunchKernelGGL(ot::loss_finalize_kernel, dim3(1), dim3(256), 0, st, s->loss_partials, n_partials,
                      1.0 / ((double)b * (double)D), loss_dev, s->loss_last);
@@ -1051,6 +1090,7 @@ extern "C" int surrogate_create(ot_surrogate** out, const int64_t* widths, int32
   if ((rc = salloc((void**)&s->m, bytes))) return fail(rc);
   if ((rc = salloc((void**)&s->v, bytes))) return fail(rc);
   if ((rc = salloc((void**)&s->loss_last, 16))) return fail(rc);
+  if ((rc = salloc((void**)&s->eval_acc, 16))) return fail(rc);
   const unsigned fb = (unsigned)ot::ceil_div(s->n_flat, 256);
   for (float* p : {s->params, s->grads, s->m, s->v}) {
     hipLaunchKernelGGL(ot::fill_kernel, dim3(fb), dim3(256), 0, 0, p, s->n_flat, 0.f);
@@ -1177,17 +1217,59 @@ static int adam_step(ot_surrogate* s, hipStream_t st) {
   return OT_OK;
 }
 
+// fp32 forward of b rows and the output layer's fused bias + MSE epilogue:
+// dY = 2 (Y - U) / (B D) into dz[L], per-block loss partials.
+static int forward_mse_f32(ot_surrogate* s, const float* x, int64_t ldx, const float* u, int64_t ldu, int64_t b,
+                           hipStream_t st, int64_t* n_partials) {
+  const int L = s->L;
+  const int64_t D = s->widths[L];
+  ot::PhaseTimer& tm = s->timer;
+  int rc;
+  tm.mark(st, OT_PH_FWD_HIDDEN, 0);
+  if ((rc = forward_hidden(s, x, ldx, b, st))) return rc;
+  tm.mark(st, OT_PH_FWD_HIDDEN, 1);
+  const Layer& lo = s->layers[L - 1];
+  GemmArgs g = args0();
+  g.A = (L == 1) ? x : s->act[L - 1];
+  g.lda = (L == 1) ? ldx : s->ld[L - 1];
+  g.B = s->params + lo.w_off;
+  g.ldb = lo.ldw;
+  g.C = s->dz[L];
+  g.ldc = s->ld[L];
+  g.M = b;
+  g.N = D;
+  g.K = lo.in;
+  g.bias = s->params + lo.b_off;
+  g.target = u;
+  g.ldt = ldu;
+  g.scale = (float)(2.0 / ((double)b * (double)D));
+  g.loss_partials = s->loss_partials;
+  *n_partials = make_plan(g.M, g.N, g.K, false).blocks;
+  if (*n_partials > s->n_partials_cap) return ot::set_error(OT_E_STATE, "loss partial buffer too small");
+  return run_gemm<Lay::KMajor, Lay::KMajor, 1>(s, g, Epi::Mse, st, "output forward+MSE", false, OT_PH_FWD_OUTPUT);
+}
+
+// Input checks shared by train_step and eval_loss (before any state changes).
+static int check_batch(ot_surrogate* s, const float* x, int64_t ldx, const float* u, int64_t ldu, const char* what) {
+  int rc = check_input(s, x, ldx);
+  if (rc) return rc;
+  const int L = s->L;
+  OT_REQUIRE(u != nullptr && ldu >= s->widths[L] && ldu % 4 == 0 && aligned16(u),
+             "%s: targets need 16-byte alignment and ldu >= D, ldu %% 4 == 0", what);
+  if (L == 1 && s->layers[0].in <= ot::kMaxSmallK)
+    OT_REQUIRE(aligned16(x) && ldx % 4 == 0, "single-layer nets need 16-byte aligned x, ldx %% 4 == 0");
+  return OT_OK;
+}
+
 extern "C" int surrogate_train_step(ot_surrogate* s, const float* x, int64_t ldx, const float* u, int64_t ldu,
                                     int64_t b, void* stream, float* loss_dev) {
   ot::clear_error();
   OT_REQUIRE(s != nullptr, "surrogate_train_step: NULL surrogate");
   OT_REQUIRE(b >= 1 && b <= (1LL << 20), "surrogate_train_step: b outside [1, 2^20]");
-  int rc = check_input(s, x, ldx);
+  int rc = check_batch(s, x, ldx, u, ldu, "surrogate_train_step");
   if (rc) return rc;
   const int L = s->L;
   const int64_t D = s->widths[L];
-  OT_REQUIRE(u != nullptr && ldu >= D && ldu % 4 == 0 && aligned16(u),
-             "surrogate_train_step: targets need 16-byte alignment and ldu >= D, ldu %% 4 == 0");
   if ((rc = ensure_workspace(s, b))) return rc;
   hipStream_t st = static_cast<hipStream_t>(stream);
   begin_step(s);
@@ -1197,37 +1279,8 @@ extern "C" int surrogate_train_step(ot_surrogate* s, const float* x, int64_t ldx
     return adam_step(s, st);
   }
   ot::PhaseTimer& tm = s->timer;
-  // ---- forward: hidden layers
-  tm.mark(st, OT_PH_FWD_HIDDEN, 0);
-  if ((rc = forward_hidden(s, x, ldx, b, st))) return rc;
-  tm.mark(st, OT_PH_FWD_HIDDEN, 1);
-  // ---- output layer with fused bias + MSE: dY = 2 (Y - U) / (B D), loss partials
-  const Layer& lo = s->layers[L - 1];
   int64_t n_partials = 0;
-  {
-    GemmArgs g = args0();
-    g.A = (L == 1) ? x : s->act[L - 1];
-    g.lda = (L == 1) ? ldx : s->ld[L - 1];
-    g.B = s->params + lo.w_off;
-    g.ldb = lo.ldw;
-    g.C = s->dz[L];
-    g.ldc = s->ld[L];
-    g.M = b;
-    g.N = D;
-    g.K = lo.in;
-    g.bias = s->params + lo.b_off;
-    g.target = u;
-    g.ldt = ldu;
-    g.scale = (float)(2.0 / ((double)b * (double)D));
-    g.loss_partials = s->loss_partials;
-    if (L == 1 && lo.in <= ot::kMaxSmallK)
-      OT_REQUIRE(aligned16(x) && ldx % 4 == 0, "single-layer nets need 16-byte aligned x, ldx %% 4 == 0");
-    n_partials = make_plan(g.M, g.N, g.K, false).blocks;
-    if (n_partials > s->n_partials_cap) return ot::set_error(OT_E_STATE, "loss partial buffer too small");
-    if ((rc = run_gemm<Lay::KMajor, Lay::KMajor, 1>(s, g, Epi::Mse, st, "output forward+MSE", false,
-                                                    OT_PH_FWD_OUTPUT)))
-      return rc;
-  }
+  if ((rc = forward_mse_f32(s, x, ldx, u, ldu, b, st, &n_partials))) return rc;
   tm.mark(st, OT_PH_LOSS, 0);
   hipLaunchKernelGGL(ot::loss_finalize_kernel, dim3(1), dim3(256), 0, st, s->loss_partials, n_partials,
                      1.0 / ((double)b * (double)D), loss_dev, s->loss_last);
@@ -1317,6 +1370,32 @@ extern "C" int surrogate_train_step(ot_surrogate* s, const float* x, int64_t ldx
   if (L >= 2) tm.mark(st, OT_PH_BWD_HIDDEN, 1);
 
   return adam_step(s, st);
+}
+
+extern "C" int surrogate_eval_loss(ot_surrogate* s, const float* x, int64_t ldx, const float* u, int64_t ldu,
+                                   int64_t n, void* stream, float* loss_dev) {
+  ot::clear_error();
+  OT_REQUIRE(s != nullptr, "surrogate_eval_loss: NULL surrogate");
+  OT_REQUIRE(n >= 1, "surrogate_eval_loss: n < 1");
+  OT_REQUIRE(loss_dev != nullptr, "surrogate_eval_loss: loss_dev is NULL");
+  int rc = check_batch(s, x, ldx, u, ldu, "surrogate_eval_loss");
+  if (rc) return rc;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  const int64_t chunk = std::max<int64_t>(s->ws_rows, 1);
+  const int64_t D = s->widths[s->L];
+  for (int64_t r0 = 0; r0 < n; r0 += chunk) {
+    const int64_t rows = std::min(chunk, n - r0);
+    int64_t n_partials = 0;
+    rc = (s->precision == OT_BF16)
+             ? forward_mse_bf16(s, x + r0 * ldx, ldx, u + r0 * ldu, ldu, rows, st, false, &n_partials)
+             : forward_mse_f32(s, x + r0 * ldx, ldx, u + r0 * ldu, ldu, rows, st, &n_partials);
+    if (rc) return rc;
+    hipLaunchKernelGGL(ot::loss_accumulate_kernel, dim3(1), dim3(256), 0, st, s->loss_partials, n_partials,
+                       s->eval_acc, r0 == 0 ? 1 : 0, r0 + rows >= n ? 1 : 0, 1.0 / ((double)n * (double)D),
+                       loss_dev);
+    OT_LAUNCHED("loss_accumulate_kernel");
+  }
+  return OT_OK;
 }
 
 extern "C" int surrogate_timing_begin(ot_surrogate* s, uint32_t phase_mask, int64_t max_steps) {

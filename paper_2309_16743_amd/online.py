@@ -12,8 +12,10 @@ so every drawn slot) is the same as on one stream.
 """
 from __future__ import annotations
 
+from dataclasses import dataclass
 from typing import Callable, Optional
 
+import numpy as np
 import torch
 
 from . import OT_FP32, OT_BF16, OT_OK, OT_POLICY_RESERVOIR, Reservoir, Surrogate
@@ -21,6 +23,20 @@ from . import OT_FP32, OT_BF16, OT_OK, OT_POLICY_RESERVOIR, Reservoir, Surrogate
 
 def _round_up(v: int, m: int) -> int:
     return (v + m - 1) // m * m
+
+
+@dataclass(frozen=True)
+class HalvingLR:
+    """Learning-rate schedule of Sec. 4.4-4.5: start at lr0, halve once per
+    every_samples trained samples, never below lr_min (the paper: 1e-3 halved
+    every 10,000 samples down to 2.5e-4).  Called with the number of samples
+    trained before a step, returns that step's rate."""
+    lr0: float = 1e-3
+    every_samples: int = 10_000
+    lr_min: float = 2.5e-4
+
+    def __call__(self, samples_trained: int) -> float:
+        return max(self.lr0 * 0.5 ** (samples_trained // self.every_samples), self.lr_min)
 
 
 class OnlineTrainer:
@@ -38,7 +54,8 @@ class OnlineTrainer:
                  init_seed: int, precision: int = OT_FP32, lr: float = 1e-3,
                  stream: Optional[torch.cuda.Stream] = None, record_steps: int = 0,
                  chunk_fn: Optional[Callable] = None, n_chunks: int = 0, device=None, flags: int = 0,
-                 overlap: bool = False, policy: int = OT_POLICY_RESERVOIR):
+                 overlap: bool = False, policy: int = OT_POLICY_RESERVOIR,
+                 lr_schedule: Optional[Callable[[int], float]] = None):
         self.stream = stream if stream is not None else torch.cuda.current_stream()
         self.widths = tuple(widths)
         self.batch, self.wave, self.tau = batch, wave, tau
@@ -79,6 +96,9 @@ class OnlineTrainer:
         self.iteration = 0
         self.steps_done = 0
         self.chunk_cursor = 0
+        self.lr_schedule = lr_schedule
+        self.lr = lr
+        self.val_loss = torch.zeros(1, device=dev)
 
     def chunk_views(self, c: int):
         if self.chunk_fn is not None:
@@ -118,6 +138,11 @@ class OnlineTrainer:
             self.ready[j].record(self.res_stream)
             self.stream.wait_event(self.ready[j])
         loss = self.loss_log[self.steps_done:self.steps_done + 1] if rec else self.loss
+        if self.lr_schedule is not None:
+            lr = self.lr_schedule(self.steps_done * self.batch)
+            if lr != self.lr:
+                self.sur.set_lr(lr)       # host-side rate, taken by the next enqueued step
+                self.lr = lr
         self.sur.train_step(xb, ub, stream=self.stream, loss=loss)
         if self.overlap:
             self.released[j].record(self.stream)
@@ -138,6 +163,24 @@ class OnlineTrainer:
             if self.chunk_cursor >= self.n_chunks and not wrap and self.res.stats()["n"] <= self.res.threshold:
                 raise RuntimeError("schedule ran out of data before the buffer became ready")
             self.iterate(wrap)
+
+    def validate(self, x: torch.Tensor, u: torch.Tensor, out: Optional[torch.Tensor] = None) -> torch.Tensor:
+        """Validation MSE of the current surrogate on held-out rows x -> u,
+        enqueued on the training stream after the steps so far (Sec. 4.4
+        validates on the training thread).  Returns the device scalar."""
+        out = self.val_loss if out is None else out
+        self.sur.eval_loss(x, u, out, stream=self.stream)
+        return out
+
+    def repetition_histogram(self) -> np.ndarray:
+        """h[k] = samples that entered the buffer and were drawn k times so far
+        (samples that left the buffer and residents; the last bin collects
+        the tail), as the paper's histogram of repetitions (Sec. 4.3)."""
+        seen, _, hist = self.res.read_meta()
+        h = hist.astype(np.int64).copy()
+        resident = seen[seen >= 0]
+        np.add.at(h, np.minimum(resident, len(h) - 1), 1)
+        return h
 
     def close(self):
         self.res.close()

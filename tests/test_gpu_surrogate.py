@@ -218,3 +218,63 @@ def test_tiny_workload_overlapped_streams():
         W, b = tr.sur.get_params(l)
         assert rel(W, ref["params"][l][0]) < 1e-3 and rel(b, ref["params"][l][1]) < 1e-3
     tr.close()
+
+
+def test_tiny_workload_schedule_validation_histogram():
+    """The 16x16 schedule with the learning rate halved every 640 trained
+    samples down to 2.5e-4 and validation every 25 steps on two held-out
+    simulations (surrogate_eval_loss): slots bit-exact, loss series, final
+    parameters and validation losses within 1e-3 relative of the oracle; the
+    repetition histogram bit-exact."""
+    from paper_2309_16743_amd.online import HalvingLR, OnlineTrainer
+    w = configs.TINY
+    X = heat.sample_parameters(w.n_sims, w.data_seed)
+    inputs = heat.inputs_for(X, w.tau)
+    fields = heat.heat_fields(X, w.grid, w.tau)
+    Xv = heat.sample_parameters(2, 99)
+    iv, fv = heat.inputs_for(Xv, w.tau).reshape(-1, 6), heat.heat_fields(Xv, w.grid, w.tau).reshape(-1, 256)
+    ref = runner.run(w, inputs, fields, n_steps=100, lr_halving=(640, 2.5e-4), validation=(iv, fv, 25))
+    tr = OnlineTrainer(w.widths, w.batch, w.capacity, w.threshold, w.wave, w.tau,
+                       torch.from_numpy(inputs).to(DEV), torch.from_numpy(fields).to(DEV),
+                       w.reservoir_seed, w.init_seed, lr=w.lr, record_steps=100,
+                       lr_schedule=HalvingLR(1e-3, 640, 2.5e-4))
+    ivd, fvd = padded_from(iv), padded_from(fv)
+    val = {}
+    while tr.steps_done < 100:
+        if tr.iterate() and tr.steps_done % 25 == 0:
+            val[tr.steps_done] = tr.validate(ivd, fvd, torch.zeros(1, device=DEV))
+    torch.cuda.synchronize()
+    assert tr.lr == 2.5e-4
+    slots = tr.slot_log.cpu().numpy()
+    for i in range(100):
+        assert np.array_equal(slots[i], ref["slots"][i]), i
+    assert rel(tr.loss_log.cpu().numpy(), ref["losses"]) < 1e-3
+    for k, v in ref["val_losses"].items():
+        assert abs(val[k].item() - v) / v < 1e-3, (k, val[k].item(), v)
+    for l in range(3):
+        W, b = tr.sur.get_params(l)
+        assert rel(W, ref["params"][l][0]) < 1e-3 and rel(b, ref["params"][l][1]) < 1e-3
+    h = tr.repetition_histogram()
+    assert np.array_equal(h, runner.repetition_histogram(ref["reservoir"], len(h)))
+    tr.close()
+
+
+@pytest.mark.parametrize("widths,n,bf16", [((6, 64, 64, 256), 200, False), ((6, 37, 50, 123), 77, False),
+                                           ((6, 100, 77, 1001), 150, True)])
+def test_eval_loss(widths, n, bf16):
+    """surrogate_eval_loss over more rows than the workspace (chunked) against
+    the oracle's MSE of its prediction; parameters untouched."""
+    from paper_2309_16743_amd import OT_BF16, OT_FP32, Surrogate
+    params, X, U = problem(widths, n, seed=21)
+    s = Surrogate(widths, precision=OT_BF16 if bf16 else OT_FP32, max_batch=64, seed=0)
+    for l, (W, b) in enumerate(params):
+        s.set_params(l, W.astype(np.float32), b.astype(np.float32))
+    loss = torch.zeros(1, device=DEV)
+    s.eval_loss(padded_from(X), padded_from(U), loss)
+    torch.cuda.synchronize()
+    ref = mlp.mse(mlp.predict(params, X.astype(np.float64), bf16=bf16), U.astype(np.float64))
+    assert abs(loss.item() - ref) / ref < (1e-3 if bf16 else 1e-5), (loss.item(), ref)
+    for l in range(len(widths) - 1):
+        W, b = s.get_params(l)
+        assert np.array_equal(W, params[l][0].astype(np.float32))
+    s.close()

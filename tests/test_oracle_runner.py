@@ -43,3 +43,28 @@ def test_oracle_never_imports_the_gpu_package():
             for n in names:
                 assert not n.startswith("paper_2309_16743_amd"), (fn, n)
                 assert not n.startswith("torch"), (fn, n)
+
+
+def test_halving_schedule_closed_form():
+    """Sec. 4.5: 1e-3 halved every 10,000 trained samples, floored at 2.5e-4."""
+    lr = lambda n: runner.halving_lr(1e-3, n, 10_000, 2.5e-4)
+    assert [lr(n) for n in (0, 9_999, 10_000, 19_999, 20_000, 30_000, 10**6)] == \
+        [1e-3, 1e-3, 5e-4, 5e-4, 2.5e-4, 2.5e-4, 2.5e-4]
+    from paper_2309_16743_amd.online import HalvingLR      # the trainer's schedule, same printed values
+    h = HalvingLR()
+    assert [h(n) for n in (0, 9_999, 10_000, 20_000, 10**6)] == [1e-3, 1e-3, 5e-4, 2.5e-4, 2.5e-4]
+
+
+def test_schedule_validation_and_repetition_histogram():
+    w, inputs, fields = tiny_data()
+    Xv = heat.sample_parameters(2, 99)
+    iv, fv = heat.inputs_for(Xv, w.tau).reshape(-1, 6), heat.heat_fields(Xv, w.grid, w.tau).reshape(-1, 256)
+    tr = runner.run(w, inputs, fields, n_steps=100, lr_halving=(640, 2.5e-4), validation=(iv, fv, 25))
+    # 32 samples per step: the rate halves after steps 20 and 40, then stays at the floor
+    assert tr["lrs"][:21] == [1e-3] * 20 + [5e-4] and tr["lrs"][40:] == [2.5e-4] * 60
+    assert sorted(tr["val_losses"]) == [25, 50, 75, 100]
+    assert all(np.isfinite(v) and v > 0 for v in tr["val_losses"].values())
+    res = tr["reservoir"]
+    h = runner.repetition_histogram(res, 256)
+    assert h.sum() == res.total_put                                  # every sample that entered, once
+    assert int((np.arange(256) * h).sum()) == res.total_draws       # every draw, once
