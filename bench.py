@@ -431,6 +431,38 @@ def result_line(w, args, K, warmup, r, config: dict) -> dict:
     }
 
 
+def instrumentation(tr, w, stream) -> dict:
+    """Training instrumentation of Sec. 3.1 and 4.3-4.4, measured after the
+    timed region: one validation pass (surrogate_eval_loss) over 10 held-out
+    simulations (the paper's validation set size), timed with events on the
+    training stream; the repetition histogram of the run so far; and one
+    synchronous checkpoint of reservoir and surrogate to host memory."""
+    import torch
+
+    from fixtures import heat
+    Xv = heat.sample_parameters(10, w.data_seed + 1000)
+    iv = torch.from_numpy(heat.inputs_for(Xv, w.tau).reshape(-1, w.widths[0])).to(tr.xb.device)
+    fv = torch.from_numpy(heat.heat_fields(Xv, w.grid, w.tau).reshape(-1, w.widths[-1])).to(tr.xb.device)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    tr.validate(iv, fv)                        # warm
+    e0.record(stream)
+    val = tr.validate(iv, fv)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    h = tr.repetition_histogram()
+    last = int(np.max(np.nonzero(h)[0])) if h.any() else 0
+    t0 = time.perf_counter()
+    ck = tr.checkpoint()                       # synchronous snapshot to host memory
+    t_ck = time.perf_counter() - t0
+    ck_bytes = sum(int(v.nbytes) for v in ck.values())
+    del ck
+    return {"validation": {"rows": int(iv.shape[0]), "ms": round(e0.elapsed_time(e1), 3),
+                           "loss": round(float(val.item()), 4)},
+            "checkpoint": {"bytes": ck_bytes, "s": round(t_ck, 3), "gb_per_s": round(ck_bytes / t_ck / 1e9, 2)},
+            "repetition_histogram": {"draws_per_sample": h[:last + 1].tolist(),
+                                     "last_bin_is_tail": last == len(h) - 1}}
+
+
 def run_heat(args, w):
     import torch
 
@@ -459,11 +491,13 @@ def run_heat(args, w):
         print(f"[bench] setup done: {tr.steps_done} train steps, reservoir {tr.res.stats()['n']} samples",
               file=sys.stderr, flush=True)
         r = timed_region(tr, w, K, args.profile_steps or 200, stream, lambda: tr.put_next(wrap=True))
+        instr = instrumentation(tr, w, stream)
     config = {"workload": w.name, "fields": f"FTCS heat {w.grid}x{w.grid}, {w.n_sims} sims x {w.tau} steps",
               "widths": list(w.widths), "batch": w.batch, "capacity": w.capacity, "threshold": w.threshold,
               "put_rows_per_step": w.wave, "precision": w.precision,
               "reservoir_stream": "one stream" if args.one_stream else "overlapped with the train step"}
     line = result_line(w, args, K, warmup, r, config)
+    line["instrumentation"] = instr
     tr.close()
     del inputs_d, fields_d
     torch.cuda.empty_cache()

@@ -159,6 +159,25 @@ int reservoir_read_meta(ot_reservoir* r, int32_t* seen_count, int64_t* sample_id
 int reservoir_read_rows(ot_reservoir* r, const int32_t* slots_host, int64_t n,
                         float* x_host, float* u_host);
 
+/* Checkpoint / restore (the paper's server is checkpointed regularly and a
+ * failed server restarts from its last checkpoint, Sec. 3.1).  Synchronous:
+ * both wait for the reservoir's queued work.  The checkpoint is a host blob
+ * holding the policy, shape, threshold, seed, ticket counter, counters,
+ * eviction histogram, per-slot metadata, list and free-slot rings, and the
+ * x and u rows of every stored sample; restoring it into a reservoir created
+ * with the same capacity, x_dim, u_dim and policy reproduces the state, so
+ * later calls with the same tickets give the same slots and rows as the
+ * reservoir that was checkpointed.
+ * reservoir_checkpoint_size: *bytes = blob size for the current state.
+ * reservoir_checkpoint: writes the blob into buf (caller-owned host memory
+ *   of at least that size).  Errors: OT_E_INVAL (buffer too small), OT_E_HIP.
+ * reservoir_restore: replaces the reservoir's state with the blob's.
+ *   Errors: OT_E_INVAL (not a reservoir checkpoint, other shape or policy,
+ *   truncated or inconsistent blob: nothing is changed), OT_E_HIP. */
+int reservoir_checkpoint_size(ot_reservoir* r, int64_t* bytes);
+int reservoir_checkpoint(ot_reservoir* r, void* buf, int64_t bytes);
+int reservoir_restore(ot_reservoir* r, const void* buf, int64_t bytes);
+
 /* Kernel phases of the reservoir calls, for the timing hook below. */
 enum ot_reservoir_phase {
   OT_PH_PUT_ASSIGN = 0,  /* put: slot assignment and eviction draws */

@@ -111,6 +111,21 @@ int surrogate_predict(ot_surrogate* s, const float* x, int64_t ldx, int64_t n, f
 int surrogate_eval_loss(ot_surrogate* s, const float* x, int64_t ldx, const float* u,
                         int64_t ldu, int64_t n, void* stream, float* loss_dev);
 
+/* Checkpoint / restore of the training state (Sec. 3.1: the server is
+ * checkpointed and restarts from its last checkpoint).  Synchronous.  The
+ * blob holds precision, widths, the Adam step counter and hyper-parameters,
+ * and the fp32 parameters and both Adam moments; gradients are recomputed by
+ * every step and the bf16 weight copy is rounded again from the master
+ * weights, so a restored surrogate continues bit for bit.
+ * surrogate_checkpoint_size: *bytes = blob size.
+ * surrogate_checkpoint: writes the blob into buf (host, >= that size).
+ * surrogate_restore: into a surrogate created with the same widths and
+ *   precision.  Errors: OT_E_INVAL (buffer too small, not a surrogate
+ *   checkpoint, other shape or precision: nothing is changed), OT_E_HIP. */
+int surrogate_checkpoint_size(ot_surrogate* s, int64_t* bytes);
+int surrogate_checkpoint(ot_surrogate* s, void* buf, int64_t bytes);
+int surrogate_restore(ot_surrogate* s, const void* buf, int64_t bytes);
+
 /* Kernel phases of one train step, for the timing hook below. */
 enum ot_surrogate_phase {
   OT_PH_FWD_HIDDEN = 0,    /* hidden-layer forward GEMMs (bias + ReLU epilogue) */

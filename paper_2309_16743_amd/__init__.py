@@ -23,7 +23,8 @@ __all__ = [
     "reservoir_end_reception", "reservoir_stats", "reservoir_read_meta", "reservoir_read_rows",
     "reservoir_destroy", "surrogate_create", "surrogate_set_params", "surrogate_get_params",
     "surrogate_get_grads", "surrogate_get_adam_state", "surrogate_set_lr", "surrogate_train_step",
-    "surrogate_predict", "surrogate_eval_loss", "surrogate_destroy", "load", "last_error", "OTError",
+    "surrogate_predict", "surrogate_eval_loss", "surrogate_checkpoint", "surrogate_restore",
+    "reservoir_checkpoint", "reservoir_restore", "surrogate_destroy", "load", "last_error", "OTError",
     "OT_OK", "OT_NOT_READY", "OT_EMPTY", "OT_E_INVAL", "OT_E_CLOSED", "OT_E_STATE", "OT_FP32", "OT_BF16",
     "OT_SURROGATE_KEEP_GRADS", "OT_POLICY_RESERVOIR", "OT_POLICY_FIFO", "OT_POLICY_FIRO",
 ]
@@ -54,6 +55,15 @@ def _rows(t, what: str):
     if t.dtype != torch.float32 or t.dim() != 2 or (t.shape[1] > 1 and t.stride(1) != 1):
         raise ValueError(f"{what}: expected a 2-D float32 tensor with unit column stride")
     return _dev_ptr(t), t.stride(0) if t.shape[0] > 1 else max(t.stride(0), t.shape[1])
+
+
+def _checkpoint(handle, kind: str) -> np.ndarray:
+    lib = load()
+    n = C.c_int64()
+    check(f"{kind}_checkpoint_size", getattr(lib, f"{kind}_checkpoint_size")(handle, C.byref(n)))
+    buf = np.empty(n.value, np.uint8)
+    check(f"{kind}_checkpoint", getattr(lib, f"{kind}_checkpoint")(handle, buf.ctypes.data, buf.nbytes))
+    return buf
 
 
 class Reservoir:
@@ -118,6 +128,14 @@ class Reservoir:
         check("reservoir_read_rows", load().reservoir_read_rows(self._h, slots.ctypes.data, len(slots),
                                                                  x.ctypes.data, u.ctypes.data))
         return x, u
+
+    def checkpoint(self) -> np.ndarray:
+        """Synchronous snapshot of the whole reservoir state as a host byte array."""
+        return _checkpoint(self._h, "reservoir")
+
+    def restore(self, blob: np.ndarray) -> None:
+        b = np.ascontiguousarray(blob, dtype=np.uint8)
+        check("reservoir_restore", load().reservoir_restore(self._h, b.ctypes.data, b.nbytes))
 
     def timing_begin(self, phases, max_calls: int) -> None:
         mask = sum(1 << _abi.RESERVOIR_PHASES.index(p) for p in phases)
@@ -213,6 +231,14 @@ class Surrogate:
         check("surrogate_predict", load().surrogate_predict(self._h, xp, ldx, x.shape[0], yp, ldy,
                                                             _stream_handle(stream)))
 
+    def checkpoint(self) -> np.ndarray:
+        """Synchronous snapshot of parameters, Adam moments and step counter."""
+        return _checkpoint(self._h, "surrogate")
+
+    def restore(self, blob: np.ndarray) -> None:
+        b = np.ascontiguousarray(blob, dtype=np.uint8)
+        check("surrogate_restore", load().surrogate_restore(self._h, b.ctypes.data, b.nbytes))
+
     def eval_loss(self, x, u, loss, stream=None) -> None:
         """Validation MSE of the current surrogate on rows x -> u into the device scalar `loss`."""
         xp, ldx = _rows(x, "x")
@@ -289,6 +315,22 @@ def surrogate_set_params(s: Surrogate, layer, W=None, b=None) -> None:
 
 def surrogate_get_params(s: Surrogate, layer):
     return s.get_params(layer)
+
+
+def reservoir_checkpoint(r: Reservoir) -> np.ndarray:
+    return r.checkpoint()
+
+
+def reservoir_restore(r: Reservoir, blob) -> None:
+    r.restore(blob)
+
+
+def surrogate_checkpoint(s: Surrogate) -> np.ndarray:
+    return s.checkpoint()
+
+
+def surrogate_restore(s: Surrogate, blob) -> None:
+    s.restore(blob)
 
 
 def surrogate_eval_loss(s: Surrogate, x, u, loss, stream=None):

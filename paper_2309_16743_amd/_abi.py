@@ -63,6 +63,12 @@ SIGNATURES = {
     "surrogate_get_params": (C.c_int, [vp, i32, vp, vp]),
     "surrogate_get_grads": (C.c_int, [vp, i32, vp, vp]),
     "surrogate_eval_loss": (C.c_int, [vp, vp, i64, vp, i64, i64, vp, vp]),
+    "surrogate_checkpoint_size": (C.c_int, [vp, C.POINTER(i64)]),
+    "surrogate_checkpoint": (C.c_int, [vp, vp, i64]),
+    "surrogate_restore": (C.c_int, [vp, vp, i64]),
+    "reservoir_checkpoint_size": (C.c_int, [vp, C.POINTER(i64)]),
+    "reservoir_checkpoint": (C.c_int, [vp, vp, i64]),
+    "reservoir_restore": (C.c_int, [vp, vp, i64]),
     "surrogate_get_adam_state": (C.c_int, [vp, i32, vp, vp, vp, vp, C.POINTER(i64)]),
     "surrogate_set_lr": (C.c_int, [vp, f32]),
     "surrogate_train_step": (C.c_int, [vp, vp, i64, vp, i64, i64, vp, vp]),

@@ -46,6 +46,42 @@ struct PhaseTimer {
 };
 inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
+// Sequential writer / reader of a checkpoint blob in caller-owned host memory.
+// Every access is bounds-checked; ok() turns false at the first overrun and
+// later accesses do nothing.
+struct BlobWriter {
+  unsigned char* p;
+  int64_t cap, off = 0;
+  bool good = true;
+  BlobWriter(void* buf, int64_t bytes) : p(static_cast<unsigned char*>(buf)), cap(bytes) {}
+  unsigned char* take(int64_t n) {
+    if (!good || n < 0 || off + n > cap) { good = false; return nullptr; }
+    unsigned char* q = p + off;
+    off += n;
+    return q;
+  }
+  template <class T> void put(const T& v) {
+    if (unsigned char* q = take(sizeof(T))) __builtin_memcpy(q, &v, sizeof(T));
+  }
+};
+struct BlobReader {
+  const unsigned char* p;
+  int64_t cap, off = 0;
+  bool good = true;
+  BlobReader(const void* buf, int64_t bytes) : p(static_cast<const unsigned char*>(buf)), cap(bytes) {}
+  const unsigned char* take(int64_t n) {
+    if (!good || n < 0 || off + n > cap) { good = false; return nullptr; }
+    const unsigned char* q = p + off;
+    off += n;
+    return q;
+  }
+  template <class T> T get() {
+    T v{};
+    if (const unsigned char* q = take(sizeof(T))) __builtin_memcpy(&v, q, sizeof(T));
+    return v;
+  }
+};
+
 }  // namespace ot
 
 // Evaluate a HIP call; on failure record the message and return OT_E_HIP.

@@ -26,6 +26,7 @@
 // min(b, N).  So readiness (N > T) never needs a device read-back.
 #include <algorithm>
 #include <mutex>
+#include <vector>
 
 #include "common.h"
 #include "philox.h"
@@ -836,6 +837,159 @@ extern "C" int reservoir_read_rows(ot_reservoir* r, const int32_t* slots_host, i
       OT_HIP(hipMemcpy(u_host + i * r->u_dim, r->uslab + s * r->ldus, r->u_dim * sizeof(float),
                        hipMemcpyDeviceToHost));
   }
+  return OT_OK;
+}
+
+// ------------------------------------------------------------------ checkpoint
+// Blob layout (host memory, native byte order): magic "OTRESV1", then int64
+// fields policy, C, T, x_dim, u_dim, seed, next_ticket, n_host, occ_base,
+// free_head, reception_over, n_rows, hist_len; the device counter block; the
+// eviction histogram (uint64[hist_len]); seen int32[C], sample_id int64[C],
+// occ int32[C], free_q int32[C]; then the x_dim + u_dim fp32 values of every
+// occupied slot in ascending slot order.
+namespace {
+
+constexpr char kResMagic[8] = {'O', 'T', 'R', 'E', 'S', 'V', '1', 0};
+constexpr int64_t kResHeaderWords = 13;
+
+int64_t res_blob_bytes(const ot_reservoir* r, int64_t n_rows) {
+  return 8 + kResHeaderWords * 8 + (int64_t)sizeof(ResCounters) + ot::kHistLen * 8 + r->C * (4 + 8 + 4 + 4) +
+         n_rows * (r->x_dim + r->u_dim) * 4;
+}
+
+// Runs [first, last] of consecutive slots with seen >= 0, in ascending order.
+template <class F>
+int for_each_occupied_run(const std::vector<int32_t>& seen, F f) {
+  const int64_t C = (int64_t)seen.size();
+  int64_t row = 0;
+  for (int64_t s0 = 0; s0 < C;) {
+    if (seen[s0] < 0) { ++s0; continue; }
+    int64_t s1 = s0;
+    while (s1 + 1 < C && seen[s1 + 1] >= 0) ++s1;
+    int rc = f(s0, s1 - s0 + 1, row);
+    if (rc) return rc;
+    row += s1 - s0 + 1;
+    s0 = s1 + 1;
+  }
+  return OT_OK;
+}
+
+}  // namespace
+
+extern "C" int reservoir_checkpoint_size(ot_reservoir* r, int64_t* bytes) {
+  ot::clear_error();
+  OT_REQUIRE(r != nullptr && bytes != nullptr, "reservoir_checkpoint_size: NULL argument");
+  std::lock_guard<std::mutex> lock(r->mu);
+  OT_HIP(hipStreamSynchronize(r->stream));
+  ResCounters c;
+  OT_HIP(hipMemcpy(&c, r->ctr, sizeof c, hipMemcpyDeviceToHost));
+  *bytes = res_blob_bytes(r, c.N);
+  return OT_OK;
+}
+
+extern "C" int reservoir_checkpoint(ot_reservoir* r, void* buf, int64_t bytes) {
+  ot::clear_error();
+  OT_REQUIRE(r != nullptr && buf != nullptr, "reservoir_checkpoint: NULL argument");
+  std::lock_guard<std::mutex> lock(r->mu);
+  OT_HIP(hipStreamSynchronize(r->stream));
+  const int64_t C = r->C;
+  ResCounters c;
+  std::vector<unsigned long long> hist(ot::kHistLen);
+  std::vector<int32_t> seen(C), occ(C), freeq(C);
+  std::vector<long long> ids(C);
+  OT_HIP(hipMemcpy(&c, r->ctr, sizeof c, hipMemcpyDeviceToHost));
+  OT_HIP(hipMemcpy(hist.data(), r->hist, ot::kHistLen * 8, hipMemcpyDeviceToHost));
+  OT_HIP(hipMemcpy(seen.data(), r->seen, C * 4, hipMemcpyDeviceToHost));
+  OT_HIP(hipMemcpy(ids.data(), r->sample_id, C * 8, hipMemcpyDeviceToHost));
+  OT_HIP(hipMemcpy(occ.data(), r->occ, C * 4, hipMemcpyDeviceToHost));
+  OT_HIP(hipMemcpy(freeq.data(), r->free_q, C * 4, hipMemcpyDeviceToHost));
+  int64_t n_rows = 0;
+  for (int32_t v : seen) n_rows += v >= 0;
+  if (n_rows != c.N || n_rows != r->n_host)
+    return ot::set_error(OT_E_STATE, "reservoir_checkpoint: %lld occupied slots but N = %lld (host %lld)",
+                         (long long)n_rows, (long long)c.N, (long long)r->n_host);
+  OT_REQUIRE(bytes >= res_blob_bytes(r, n_rows), "reservoir_checkpoint: buffer of %lld bytes, %lld needed",
+             (long long)bytes, (long long)res_blob_bytes(r, n_rows));
+  ot::BlobWriter w(buf, bytes);
+  __builtin_memcpy(w.take(8), kResMagic, 8);
+  for (int64_t v : {(int64_t)r->policy, C, r->T, r->x_dim, r->u_dim, (int64_t)r->seed, (int64_t)r->next_ticket,
+                    r->n_host, r->occ_base, r->free_head, (int64_t)r->reception_over, n_rows,
+                    (int64_t)ot::kHistLen})
+    w.put(v);
+  w.put(c);
+  __builtin_memcpy(w.take(ot::kHistLen * 8), hist.data(), ot::kHistLen * 8);
+  __builtin_memcpy(w.take(C * 4), seen.data(), C * 4);
+  __builtin_memcpy(w.take(C * 8), ids.data(), C * 8);
+  __builtin_memcpy(w.take(C * 4), occ.data(), C * 4);
+  __builtin_memcpy(w.take(C * 4), freeq.data(), C * 4);
+  const int64_t row_bytes = (r->x_dim + r->u_dim) * 4;
+  unsigned char* rows = w.take(n_rows * row_bytes);
+  if (!w.good) return ot::set_error(OT_E_STATE, "reservoir_checkpoint: blob overrun");
+  return for_each_occupied_run(seen, [&](int64_t s0, int64_t n, int64_t row) -> int {
+    unsigned char* dst = rows + row * row_bytes;
+    OT_HIP(hipMemcpy2D(dst, row_bytes, r->xslab + s0 * r->ldxs, r->ldxs * 4, r->x_dim * 4, n,
+                       hipMemcpyDeviceToHost));
+    OT_HIP(hipMemcpy2D(dst + r->x_dim * 4, row_bytes, r->uslab + s0 * r->ldus, r->ldus * 4, r->u_dim * 4, n,
+                       hipMemcpyDeviceToHost));
+    return OT_OK;
+  });
+}
+
+extern "C" int reservoir_restore(ot_reservoir* r, const void* buf, int64_t bytes) {
+  ot::clear_error();
+  OT_REQUIRE(r != nullptr && buf != nullptr, "reservoir_restore: NULL argument");
+  ot::BlobReader rd(buf, bytes);
+  const unsigned char* magic = rd.take(8);
+  OT_REQUIRE(magic != nullptr && __builtin_memcmp(magic, kResMagic, 8) == 0, "reservoir_restore: not a reservoir checkpoint");
+  int64_t h[kResHeaderWords];
+  for (int64_t& v : h) v = rd.get<int64_t>();
+  const int64_t policy = h[0], C = h[1], T = h[2], x_dim = h[3], u_dim = h[4], n_host = h[7], occ_base = h[8],
+                free_head = h[9], n_rows = h[11], hist_len = h[12];
+  OT_REQUIRE(rd.good, "reservoir_restore: truncated header");
+  OT_REQUIRE(policy == r->policy && C == r->C && x_dim == r->x_dim && u_dim == r->u_dim,
+             "reservoir_restore: checkpoint of a different buffer (policy %lld, C %lld, x_dim %lld, u_dim %lld)",
+             (long long)policy, (long long)C, (long long)x_dim, (long long)u_dim);
+  OT_REQUIRE(hist_len == ot::kHistLen && T >= 0 && n_host >= 0 && n_host <= C && n_rows == n_host &&
+                 occ_base >= 0 && occ_base < C && free_head >= 0 && free_head < C,
+             "reservoir_restore: inconsistent checkpoint header");
+  OT_REQUIRE(bytes >= res_blob_bytes(r, n_rows), "reservoir_restore: checkpoint truncated");
+  const ResCounters c = rd.get<ResCounters>();
+  const unsigned char* hist = rd.take(ot::kHistLen * 8);
+  std::vector<int32_t> seen(C);
+  __builtin_memcpy(seen.data(), rd.take(C * 4), C * 4);
+  const unsigned char* ids = rd.take(C * 8);
+  const unsigned char* occ = rd.take(C * 4);
+  const unsigned char* freeq = rd.take(C * 4);
+  const int64_t row_bytes = (x_dim + u_dim) * 4;
+  const unsigned char* rows = rd.take(n_rows * row_bytes);
+  OT_REQUIRE(rd.good, "reservoir_restore: checkpoint truncated");
+  int64_t occupied = 0;
+  for (int32_t v : seen) occupied += v >= 0;
+  OT_REQUIRE(occupied == n_rows && c.N == n_rows, "reservoir_restore: inconsistent slot metadata");
+  std::lock_guard<std::mutex> lock(r->mu);
+  OT_HIP(hipStreamSynchronize(r->stream));
+  OT_HIP(hipMemcpy(r->ctr, &c, sizeof c, hipMemcpyHostToDevice));
+  OT_HIP(hipMemcpy(r->hist, hist, ot::kHistLen * 8, hipMemcpyHostToDevice));
+  OT_HIP(hipMemcpy(r->seen, seen.data(), C * 4, hipMemcpyHostToDevice));
+  OT_HIP(hipMemcpy(r->sample_id, ids, C * 8, hipMemcpyHostToDevice));
+  OT_HIP(hipMemcpy(r->occ, occ, C * 4, hipMemcpyHostToDevice));
+  OT_HIP(hipMemcpy(r->free_q, freeq, C * 4, hipMemcpyHostToDevice));
+  int rc = for_each_occupied_run(seen, [&](int64_t s0, int64_t n, int64_t row) -> int {
+    const unsigned char* src = rows + row * row_bytes;
+    OT_HIP(hipMemcpy2D(r->xslab + s0 * r->ldxs, r->ldxs * 4, src, row_bytes, r->x_dim * 4, n,
+                       hipMemcpyHostToDevice));
+    OT_HIP(hipMemcpy2D(r->uslab + s0 * r->ldus, r->ldus * 4, src + r->x_dim * 4, row_bytes, r->u_dim * 4, n,
+                       hipMemcpyHostToDevice));
+    return OT_OK;
+  });
+  if (rc) return rc;
+  r->T = T;
+  r->seed = (uint64_t)h[5];
+  r->next_ticket = (uint64_t)h[6];
+  r->n_host = n_host;
+  r->occ_base = occ_base;
+  r->free_head = free_head;
+  r->reception_over = h[10] != 0;
   return OT_OK;
 }
 

@@ -1398,6 +1398,80 @@ extern "C" int surrogate_eval_loss(ot_surrogate* s, const float* x, int64_t ldx,
   return OT_OK;
 }
 
+// ------------------------------------------------------------------ checkpoint
+// Blob layout (host memory, native byte order): magic "OTSURV1", int64
+// precision, n_widths, widths[n_widths], t, n_flat; float lr, beta1, beta2,
+// eps; then the flat fp32 parameters, first and second Adam moments
+// (n_flat each, the device layout).  Gradients are not state (every step
+// recomputes them); the bf16 weight copy is rounded again from the restored
+// master weights.
+namespace {
+constexpr char kSurMagic[8] = {'O', 'T', 'S', 'U', 'R', 'V', '1', 0};
+
+int64_t sur_blob_bytes(const ot_surrogate* s) {
+  return 8 + 8 * (2 + (int64_t)s->widths.size() + 2) + 4 * 4 + 3 * s->n_flat * 4;
+}
+}  // namespace
+
+extern "C" int surrogate_checkpoint_size(ot_surrogate* s, int64_t* bytes) {
+  ot::clear_error();
+  OT_REQUIRE(s != nullptr && bytes != nullptr, "surrogate_checkpoint_size: NULL argument");
+  *bytes = sur_blob_bytes(s);
+  return OT_OK;
+}
+
+extern "C" int surrogate_checkpoint(ot_surrogate* s, void* buf, int64_t bytes) {
+  ot::clear_error();
+  OT_REQUIRE(s != nullptr && buf != nullptr, "surrogate_checkpoint: NULL argument");
+  OT_REQUIRE(bytes >= sur_blob_bytes(s), "surrogate_checkpoint: buffer of %lld bytes, %lld needed",
+             (long long)bytes, (long long)sur_blob_bytes(s));
+  OT_HIP(hipDeviceSynchronize());
+  ot::BlobWriter w(buf, bytes);
+  __builtin_memcpy(w.take(8), kSurMagic, 8);
+  w.put((int64_t)s->precision);
+  w.put((int64_t)s->widths.size());
+  for (int64_t v : s->widths) w.put(v);
+  w.put(s->t);
+  w.put(s->n_flat);
+  for (float v : {s->lr, s->beta1, s->beta2, s->eps}) w.put(v);
+  for (const float* src : {s->params, s->m, s->v})
+    OT_HIP(hipMemcpy(w.take(s->n_flat * 4), src, s->n_flat * 4, hipMemcpyDeviceToHost));
+  return w.good ? OT_OK : ot::set_error(OT_E_STATE, "surrogate_checkpoint: blob overrun");
+}
+
+extern "C" int surrogate_restore(ot_surrogate* s, const void* buf, int64_t bytes) {
+  ot::clear_error();
+  OT_REQUIRE(s != nullptr && buf != nullptr, "surrogate_restore: NULL argument");
+  ot::BlobReader rd(buf, bytes);
+  const unsigned char* magic = rd.take(8);
+  OT_REQUIRE(magic != nullptr && __builtin_memcmp(magic, kSurMagic, 8) == 0,
+             "surrogate_restore: not a surrogate checkpoint");
+  const int64_t precision = rd.get<int64_t>(), nw = rd.get<int64_t>();
+  OT_REQUIRE(rd.good && precision == s->precision && nw == (int64_t)s->widths.size(),
+             "surrogate_restore: checkpoint of a different surrogate (precision or depth)");
+  for (int64_t i = 0; i < nw; ++i)
+    OT_REQUIRE(rd.get<int64_t>() == s->widths[i], "surrogate_restore: width %lld differs", (long long)i);
+  const int64_t t = rd.get<int64_t>(), n_flat = rd.get<int64_t>();
+  float hp[4];
+  for (float& v : hp) v = rd.get<float>();
+  OT_REQUIRE(rd.good && n_flat == s->n_flat && t >= 0, "surrogate_restore: inconsistent checkpoint header");
+  OT_REQUIRE(bytes >= sur_blob_bytes(s), "surrogate_restore: checkpoint truncated");
+  OT_HIP(hipDeviceSynchronize());
+  for (float* dst : {s->params, s->m, s->v}) OT_HIP(hipMemcpy(dst, rd.take(n_flat * 4), n_flat * 4, hipMemcpyHostToDevice));
+  if (s->pb) {
+    hipLaunchKernelGGL(ot::to_bf16_kernel, dim3((unsigned)ot::ceil_div(n_flat, 256)), dim3(256), 0, 0, s->params, s->pb,
+                       n_flat);
+    OT_LAUNCHED("to_bf16_kernel");
+    OT_HIP(hipDeviceSynchronize());
+  }
+  s->t = t;
+  s->lr = hp[0];
+  s->beta1 = hp[1];
+  s->beta2 = hp[2];
+  s->eps = hp[3];
+  return OT_OK;
+}
+
 extern "C" int surrogate_timing_begin(ot_surrogate* s, uint32_t phase_mask, int64_t max_steps) {
   ot::clear_error();
   OT_REQUIRE(s != nullptr, "surrogate_timing_begin: NULL surrogate");

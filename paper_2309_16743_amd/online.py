@@ -25,6 +25,57 @@ def _round_up(v: int, m: int) -> int:
     return (v + m - 1) // m * m
 
 
+class ReceptionLog:
+    """Log of received messages per client (Sec. 3.1: the server keeps one, so
+    that after a client restart the messages it already received are
+    discarded).  A message is a (client, time step) key; it counts as received
+    once a put accepted its row.  Acceptance is known on the device (the
+    Reservoir accepts a prefix that depends on its unseen count), so each put
+    leaves its accepted count in a device word and the log resolves those
+    counts only when a key that was offered before arrives again: new keys
+    never wait for the device."""
+
+    def __init__(self, device):
+        self.received = set()
+        self.offered = set()
+        self.pending = []                  # (keys of one put in row order, index into the device counts)
+        self.counts = torch.zeros(4096, dtype=torch.int64, device=device)
+        self.next_count = 0
+
+    def count_slot(self) -> torch.Tensor:
+        """Device int64 word for the next put's accepted count."""
+        if self.next_count == len(self.counts):
+            self.resolve()
+        i = self.next_count
+        self.next_count += 1
+        return self.counts[i:i + 1]
+
+    def record(self, keys, count_slot_index: int) -> None:
+        self.offered.update(keys)
+        self.pending.append((list(keys), count_slot_index))
+
+    def resolve(self) -> None:
+        """Read the pending accepted counts (waits for the puts)."""
+        if self.pending:
+            a = self.counts[:self.next_count].cpu().tolist()
+            for keys, i in self.pending:
+                self.received.update(keys[:a[i]])
+                self.offered.difference_update(keys[a[i]:])     # refused rows may come again
+            self.pending = []
+        self.next_count = 0
+
+    def new_rows(self, keys) -> np.ndarray:
+        """Mask of the rows whose keys were not received yet."""
+        if not any(k in self.offered for k in keys):
+            return np.ones(len(keys), dtype=bool)
+        self.resolve()
+        return np.array([k not in self.received for k in keys], dtype=bool)
+
+    def keys(self) -> np.ndarray:
+        self.resolve()
+        return np.array(sorted(self.received), dtype=np.int64).reshape(-1, 2)
+
+
 @dataclass(frozen=True)
 class HalvingLR:
     """Learning-rate schedule of Sec. 4.4-4.5: start at lr0, halve once per
@@ -55,7 +106,7 @@ class OnlineTrainer:
                  stream: Optional[torch.cuda.Stream] = None, record_steps: int = 0,
                  chunk_fn: Optional[Callable] = None, n_chunks: int = 0, device=None, flags: int = 0,
                  overlap: bool = False, policy: int = OT_POLICY_RESERVOIR,
-                 lr_schedule: Optional[Callable[[int], float]] = None):
+                 lr_schedule: Optional[Callable[[int], float]] = None, reception_log: bool = False):
         self.stream = stream if stream is not None else torch.cuda.current_stream()
         self.widths = tuple(widths)
         self.batch, self.wave, self.tau = batch, wave, tau
@@ -99,6 +150,7 @@ class OnlineTrainer:
         self.lr_schedule = lr_schedule
         self.lr = lr
         self.val_loss = torch.zeros(1, device=dev)
+        self.log = ReceptionLog(dev) if reception_log else None
 
     def chunk_views(self, c: int):
         if self.chunk_fn is not None:
@@ -107,17 +159,44 @@ class OnlineTrainer:
         s0 = w * self.wave
         return self.inputs[s0:s0 + self.wave, k, :], self.fields[s0:s0 + self.wave, k, :]
 
+    def chunk_keys(self, c: int):
+        """(client, time step) message keys of the rows of chunk c."""
+        if self.chunk_fn is not None:
+            return [(c, i) for i in range(self.wave)]
+        w, k = divmod(c % self.n_chunks, self.tau)
+        return [(w * self.wave + s, k) for s in range(self.wave)]
+
     def put_next(self, wrap: bool = False) -> bool:
         """Put the next chunk; after the last chunk, wrap around only if asked."""
         if self.chunk_cursor >= self.n_chunks and not wrap:
             return False
-        x, u = self.chunk_views(self.chunk_cursor)
+        self.offer_chunk(self.chunk_cursor)
+        self.chunk_cursor += 1
+        return True
+
+    def offer_chunk(self, c: int) -> None:
+        """Put the rows of chunk c (with a reception log: only rows not received before)."""
+        x, u = self.chunk_views(c)
         if self.overlap and self.serialize:
             self._train_done.record(self.stream)
             self.res_stream.wait_event(self._train_done)
-        self.res.put(x, u, stream=self.res_stream, accepted=self.accepted)
-        self.chunk_cursor += 1
-        return True
+        if self.log is None:
+            self.res.put(x, u, stream=self.res_stream, accepted=self.accepted)
+            return
+        keys = self.chunk_keys(c)
+        keep = self.log.new_rows(keys)
+        i = 0
+        while i < len(keys):                      # one put per run of consecutive new rows
+            if not keep[i]:
+                i += 1
+                continue
+            j = i
+            while j < len(keys) and keep[j]:
+                j += 1
+            slot = self.log.count_slot()
+            self.res.put(x[i:j], u[i:j], stream=self.res_stream, accepted=slot)
+            self.log.record(keys[i:j], self.log.next_count - 1)
+            i = j
 
     def sample_only(self) -> bool:
         """Draw a batch without gathering or training (marks samples seen)."""
@@ -181,6 +260,31 @@ class OnlineTrainer:
         resident = seen[seen >= 0]
         np.add.at(h, np.minimum(resident, len(h) - 1), 1)
         return h
+
+    def checkpoint(self) -> dict:
+        """Synchronous snapshot of the whole online-training state: reservoir,
+        surrogate (parameters and Adam state), the loop's counters and
+        learning rate, and the reception log.  Arrays only (np.savez-able)."""
+        torch.cuda.synchronize()
+        state = np.array([self.chunk_cursor, self.steps_done, self.iteration], dtype=np.int64)
+        out = {"reservoir": self.res.checkpoint(), "surrogate": self.sur.checkpoint(), "loop": state,
+               "lr": np.array([self.lr], dtype=np.float64)}
+        if self.log is not None:
+            out["received"] = self.log.keys()
+        return out
+
+    def restore(self, ckpt: dict) -> None:
+        """Continue from a checkpoint() of a trainer built with the same arguments."""
+        torch.cuda.synchronize()
+        self.res.restore(ckpt["reservoir"])
+        self.sur.restore(ckpt["surrogate"])
+        self.chunk_cursor, self.steps_done, self.iteration = (int(v) for v in ckpt["loop"])
+        self.lr = float(ckpt["lr"][0])
+        self.released_recorded = [False] * len(self.released_recorded)
+        if self.log is not None:
+            self.log = ReceptionLog(self.xb.device)
+            self.log.received = {tuple(int(v) for v in k) for k in ckpt.get("received", np.zeros((0, 2)))}
+            self.log.offered = set(self.log.received)
 
     def close(self):
         self.res.close()
