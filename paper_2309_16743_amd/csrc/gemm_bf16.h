@@ -569,7 +569,9 @@ __global__ __launch_bounds__(256, OCC) void gemm_bf16_pipe_kernel(GemmBArgs g) {
   constexpr int STAGE_BYTES = (A_CH + B_CH) * 16;
   // epilogue chunk: CH_F fragments (32 CH_F rows) of each wave staged at once
   constexpr int EP = WN + 4;
-  constexpr int CH_F = (4 * FM * 32 * EP * 4 <= S * STAGE_BYTES) ? FM : FM / 2;
+  constexpr int CH_F = (4 * FM * 32 * EP * 4 <= S * STAGE_BYTES)         ? FM
+                       : (4 * (FM / 2) * 32 * EP * 4 <= S * STAGE_BYTES) ? FM / 2
+                                                                        : FM / 4;
   static_assert(CH_F >= 1 && 4 * CH_F * 32 * EP * 4 <= S * STAGE_BYTES, "epilogue staging");
   __shared__ __attribute__((aligned(16))) unsigned char smem[S * STAGE_BYTES];
   __shared__ double s_red[8 + 2 * WN];

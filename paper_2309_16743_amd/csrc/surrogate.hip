@@ -767,6 +767,10 @@ Plan make_plan_b(int64_t M, int64_t N, int64_t K, bool allow_split, bool pipe_ok
 template <LayB LA, LayB LB, EpiB E>
 hipError_t launch_cfg_b(int cfg, const GemmBArgs& g, int64_t splits, hipStream_t st) {
   // 256 x 128 tile, k tile 32, 3 stages, 2 blocks per CU
+  if constexpr (E == EpiB::AdamF32) {
+    // fused Adam: 128 x 256 tiles, so each tile row of the updated parameters is 1 KB contiguous
+    if (cfg == kBPipe) return ot::launch_gemm_bf16_pipe<128, 256, kPipeBK, 3, 2, LA, LB, E>(g, splits, st);
+  }
   if (cfg == kBPipe) return ot::launch_gemm_bf16_pipe<256, 128, kPipeBK, 3, 2, LA, LB, E>(g, splits, st);
   if (cfg == kB128) return ot::launch_gemm_bf16<4, 4, LA, LB, E, kBK>(g, splits, st);
   return ot::launch_gemm_bf16<2, 2, LA, LB, E, kBK>(g, splits, st);
