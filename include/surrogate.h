@@ -130,13 +130,16 @@ int surrogate_restore(ot_surrogate* s, const void* buf, int64_t bytes);
 enum ot_surrogate_phase {
   OT_PH_FWD_HIDDEN = 0,    /* hidden-layer forward GEMMs (bias + ReLU epilogue) */
   OT_PH_FWD_OUTPUT = 1,    /* output-layer forward GEMM with the fused MSE epilogue */
-  OT_PH_LOSS = 2,          /* loss reduction */
+  OT_PH_LOSS = 2,          /* not recorded: the loss is reduced in the step's last pass */
   OT_PH_WGRAD_OUTPUT = 3,  /* output-layer weight-gradient GEMM (with bias gradient) */
   OT_PH_IGRAD_OUTPUT = 4,  /* output-layer input-gradient GEMM */
   OT_PH_IGRAD_REDUCE = 5,  /* split-K reduction + ReLU mask of that gradient */
   OT_PH_BWD_HIDDEN = 6,    /* hidden-layer backward */
-  OT_PH_ADAM = 7,          /* Adam over all parameters */
-  OT_PH_WGRAD_REDUCE = 8,  /* split-K reduction of the output-layer weight gradient */
+  OT_PH_ADAM = 7,          /* the step's last pass (Adam over the parameters not updated in a fused
+                              epilogue, and the loss); not recorded when that pass runs inside the
+                              output layer's split-K Adam reduction (fp32, fused) */
+  OT_PH_WGRAD_REDUCE = 8,  /* split-K reduction of the output-layer weight gradient (fused: with
+                              Adam on W_L and b_L and the step's last pass) */
   OT_SURROGATE_PHASES = 9
 };
 

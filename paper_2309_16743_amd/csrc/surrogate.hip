@@ -179,26 +179,6 @@ __global__ void splitk_epilogue_kernel(const float* __restrict__ ws, int64_t spl
   }
 }
 
-// loss = sum(partials) / count, partials added in a fixed order.
-__global__ __launch_bounds__(256) void loss_finalize_kernel(const double* __restrict__ partials, int64_t n,
-                                                            double inv_count, float* __restrict__ loss_a,
-                                                            float* __restrict__ loss_b) {
-  __shared__ double red[256];
-  double s = 0.0;
-  for (int64_t i = threadIdx.x; i < n; i += 256) s += partials[i];
-  red[threadIdx.x] = s;
-  __syncthreads();
-  for (int w = 128; w > 0; w >>= 1) {
-    if ((int)threadIdx.x < w) red[threadIdx.x] += red[threadIdx.x + w];
-    __syncthreads();
-  }
-  if (threadIdx.x == 0) {
-    const float l = (float)(red[0] * inv_count);
-    if (loss_a) *loss_a = l;
-    if (loss_b) *loss_b = l;
-  }
-}
-
 // Evaluation loss over row chunks: acc = (first ? 0 : acc) + sum(partials),
 // partials added in a fixed order; the last chunk writes acc * inv_count.
 __global__ __launch_bounds__(256) void loss_accumulate_kernel(const double* __restrict__ partials, int64_t n,
@@ -220,24 +200,53 @@ __global__ __launch_bounds__(256) void loss_accumulate_kernel(const double* __re
   }
 }
 
-// Adam over the flat parameter buffer (adam1 in adam.h), except the 16-byte
-// groups [hole, hole + hole_len) (the output-layer weights when their update
-// is fused into the weight-gradient GEMM).  Streaming kernel: two 16-byte
-// groups per thread and pass (eight loads in flight), non-temporal accesses
-// (the state is touched once per step).
-__global__ __launch_bounds__(256) void adam_kernel(float* __restrict__ p, const float* __restrict__ g,
-                                                   float* __restrict__ m, float* __restrict__ v, int64_t n4,
-                                                   int64_t hole, int64_t hole_len, AdamArgs a,
-                                                   uint16_t* __restrict__ pb) {
-  f32x4* P = reinterpret_cast<f32x4*>(p);
-  const f32x4* G = reinterpret_cast<const f32x4*>(g);
-  f32x4* Mv = reinterpret_cast<f32x4*>(m);
-  f32x4* V = reinterpret_cast<f32x4*>(v);
-  u16x4* PB = reinterpret_cast<u16x4*>(pb);
-  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-  const int64_t n = n4 - hole_len;   // groups to update
-  auto at = [&](int64_t i) { return i < hole ? i : i + hole_len; };
-  int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+// The last pass of a train step: Adam over every parameter except the
+// output-layer weights when their update is fused (the 16-byte groups
+// [hole, hole + hole_len)), and the batch loss from the forward's partial sums.
+struct AdamRest {
+  float* p;
+  const float* g;
+  float* m;
+  float* v;
+  uint16_t* pb;            // bf16 copy of the weights (nullable)
+  int64_t n4, hole, hole_len;
+  const double* partials;  // loss partials of the output forward (nullable: no loss)
+  int64_t n_partials;
+  double inv_count;        // 1 / (B D)
+  float* loss_a;           // receive the loss (each nullable)
+  float* loss_b;
+};
+
+// loss = sum(partials) / count with the partials added in a fixed order
+// (strided per thread, then a tree over the 256 threads).  One block of 256.
+__device__ void reduce_loss_256(const AdamRest& r) {
+  __shared__ double red[256];
+  double s = 0.0;
+  for (int64_t i = threadIdx.x; i < r.n_partials; i += 256) s += r.partials[i];
+  red[threadIdx.x] = s;
+  __syncthreads();
+  for (int w = 128; w > 0; w >>= 1) {
+    if ((int)threadIdx.x < w) red[threadIdx.x] += red[threadIdx.x + w];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) {
+    const float l = (float)(red[0] * r.inv_count);
+    if (r.loss_a) *r.loss_a = l;
+    if (r.loss_b) *r.loss_b = l;
+  }
+}
+
+// Adam (adam1 in adam.h) over groups i = start, start + stride, ... of the
+// non-hole 16-byte groups.  Two groups per thread and pass (eight loads in
+// flight), non-temporal accesses (the state is touched once per step).
+__device__ __forceinline__ void adam_groups(const AdamRest& r, const AdamArgs& a, int64_t i, int64_t stride) {
+  f32x4* P = reinterpret_cast<f32x4*>(r.p);
+  const f32x4* G = reinterpret_cast<const f32x4*>(r.g);
+  f32x4* Mv = reinterpret_cast<f32x4*>(r.m);
+  f32x4* V = reinterpret_cast<f32x4*>(r.v);
+  u16x4* PB = reinterpret_cast<u16x4*>(r.pb);
+  const int64_t n = r.n4 - r.hole_len;   // groups to update
+  auto at = [&](int64_t k) { return k < r.hole ? k : k + r.hole_len; };
   for (; i + stride < n; i += 2 * stride) {
     f32x4 pp[2], gg[2], mm[2], vv[2];
 #pragma unroll
@@ -255,7 +264,7 @@ __global__ __launch_bounds__(256) void adam_kernel(float* __restrict__ p, const 
       __builtin_nontemporal_store(pp[u], P + j);
       __builtin_nontemporal_store(mm[u], Mv + j);
       __builtin_nontemporal_store(vv[u], V + j);
-      if (pb)   // bf16 copy of the updated master weights
+      if (PB)   // bf16 copy of the updated master weights
         __builtin_nontemporal_store(u16x4{f2bf(pp[u][0]), f2bf(pp[u][1]), f2bf(pp[u][2]), f2bf(pp[u][3])}, PB + j);
     }
   }
@@ -266,28 +275,49 @@ __global__ __launch_bounds__(256) void adam_kernel(float* __restrict__ p, const 
     P[j] = pp;
     Mv[j] = mm;
     V[j] = vv;
-    if (pb) PB[j] = u16x4{f2bf(pp[0]), f2bf(pp[1]), f2bf(pp[2]), f2bf(pp[3])};
+    if (PB) PB[j] = u16x4{f2bf(pp[0]), f2bf(pp[1]), f2bf(pp[2]), f2bf(pp[3])};
   }
 }
 
-// Split-K reduction fused with Adam (fp32 output layer): the weight gradient
+// Standalone last pass: block 0 also forms the loss.
+__global__ __launch_bounds__(256) void adam_kernel(AdamRest r, AdamArgs a) {
+  if (blockIdx.x == 0 && r.partials) reduce_loss_256(r);
+  adam_groups(r, a, (int64_t)blockIdx.x * 256 + threadIdx.x, (int64_t)gridDim.x * 256);
+}
+
+// Split-K reduction fused with Adam (fp32 output layer), blocks of 256: the
+// first main_blocks blocks take one 4-column group each: the weight gradient
 // of element (m, n) is sum_s ws[s][m][n] in split order, exactly as the
-// split-K epilogue would store it; Adam then updates p, mo, vo at
-// m * ldp + n.  Threads of column group 0 also reduce the split row sums
-// rs[s][m] into rowsum_out[m] (the bias gradient; its Adam update is part of
-// the standalone pass).
-__global__ void splitk_adam_kernel(const float* __restrict__ ws, int64_t splits, int64_t split_stride, int64_t M,
-                                   int64_t N, int64_t ldws, float* __restrict__ p, float* __restrict__ mo,
-                                   float* __restrict__ vo, int64_t ldp, AdamArgs a, const float* __restrict__ rs,
-                                   int64_t rs_stride, float* __restrict__ rowsum_out) {
+// split-K epilogue would store it; Adam then updates p, mo, vo at m * ldp + n;
+// threads of column group 0 also reduce the split row sums rs[s][m] into
+// rowsum_out[m] (the bias gradient) and, when bias_p is given, apply Adam to
+// the bias element m (bias_p, bias_m, bias_v).  The remaining blocks run the
+// rest of the step's last pass (AdamRest: the parameters outside the output
+// layer, then the loss in the first of them), so the step needs no separate
+// Adam launch.
+__global__ __launch_bounds__(256) void splitk_adam_kernel(const float* __restrict__ ws, int64_t splits,
+                                                          int64_t split_stride, int64_t M, int64_t N, int64_t ldws,
+                                                          float* __restrict__ p, float* __restrict__ mo,
+                                                          float* __restrict__ vo, int64_t ldp, AdamArgs a,
+                                                          const float* __restrict__ rs, int64_t rs_stride,
+                                                          float* __restrict__ rowsum_out, float* __restrict__ bias_p,
+                                                          float* __restrict__ bias_m, float* __restrict__ bias_v,
+                                                          int64_t main_blocks, AdamRest rest) {
+  if ((int64_t)blockIdx.x >= main_blocks) {
+    const int64_t rb = blockIdx.x - main_blocks;
+    if (rb == 0 && rest.partials) reduce_loss_256(rest);
+    adam_groups(rest, a, rb * 256 + threadIdx.x, ((int64_t)gridDim.x - main_blocks) * 256);
+    return;
+  }
   const int64_t groups = (N + 3) / 4;
-  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
   if (t >= M * groups) return;
   const int64_t m = t / groups, n = (t % groups) * 4;
   if (rowsum_out && n == 0) {
     float r = rs[m];
     for (int64_t q = 1; q < splits; ++q) r += rs[q * rs_stride + m];
     rowsum_out[m] = r;
+    if (bias_p) adam1(bias_p[m], r, bias_m[m], bias_v[m], a);
   }
   const int cnt = (int)min((int64_t)4, N - n);
   const int64_t o = m * ldp + n;
@@ -621,9 +651,13 @@ int ensure_split_ws(ot_surrogate* s, int64_t elems, int64_t rs_elems) {
 // C = epi(A B) with the plan's tile shape; split-K runs write partial sums to
 // the workspace and a second kernel applies the epilogue (fixed split order).
 // ph_gemm / ph_reduce: timing phases of the two halves (-1: not timed).
+// rest (Adam epilogue only, nullable): the step's last pass (other parameters
+// and loss); when the product is split it runs in extra blocks of the split-K
+// Adam reduction and *rest_done is set.
 template <Lay LA, Lay LB, int ROLE = 0>
 int run_gemm(ot_surrogate* s, GemmArgs g, Epi epi, hipStream_t st, const char* what, bool allow_split,
-             int ph_gemm = -1, int ph_reduce = -1, int64_t* blocks_out = nullptr) {
+             int ph_gemm = -1, int ph_reduce = -1, int64_t* blocks_out = nullptr,
+             const ot::AdamRest* rest = nullptr, bool* rest_done = nullptr) {
   const Plan p = make_plan(g.M, g.N, g.K, allow_split && epi != Epi::Mse);
   if (blocks_out) *blocks_out = p.blocks;
   ot::PhaseTimer& tm = s->timer;
@@ -652,9 +686,26 @@ int run_gemm(ot_surrogate* s, GemmArgs g, Epi epi, hipStream_t st, const char* w
   if (ph_reduce >= 0) tm.mark(st, ph_reduce, 0);
   const int64_t work = g.M * ot::ceil_div(g.N, 4);
   if (epi == Epi::Adam) {
-    hipLaunchKernelGGL(ot::splitk_adam_kernel, dim3((unsigned)ot::ceil_div(work, 128)), dim3(128), 0, st, s->splitws,
-                       p.splits, h.split_stride, g.M, g.N, ldws, g.C, g.adam_m, g.adam_v, g.ldc, g.adam, h.rowsum,
-                       h.rowsum_stride, g.rowsum);
+    const int64_t main_blocks = ot::ceil_div(work, 256);
+    int64_t rest_blocks = 0;
+    ot::AdamRest r{};
+    float *bp = nullptr, *bm = nullptr, *bv = nullptr;
+    if (rest && g.rowsum) {
+      // the output layer is the last segment of the flat buffer: its bias gets
+      // its update from the thread that reduces its gradient, the rest pass
+      // covers the layers before it
+      r = *rest;
+      r.hole_len = r.n4 - r.hole;
+      const int64_t boff = g.rowsum - s->grads;
+      bp = s->params + boff;
+      bm = s->m + boff;
+      bv = s->v + boff;
+      rest_blocks = std::max<int64_t>(1, std::min<int64_t>(ot::ceil_div(r.n4 - r.hole_len, 512), 4096));
+      if (rest_done) *rest_done = true;
+    }
+    hipLaunchKernelGGL(ot::splitk_adam_kernel, dim3((unsigned)(main_blocks + rest_blocks)), dim3(256), 0, st,
+                       s->splitws, p.splits, h.split_stride, g.M, g.N, ldws, g.C, g.adam_m, g.adam_v, g.ldc, g.adam,
+                       h.rowsum, h.rowsum_stride, g.rowsum, bp, bm, bv, main_blocks, r);
     OT_LAUNCHED("splitk_adam_kernel");
     if (ph_reduce >= 0) tm.mark(st, ph_reduce, 1);
     return OT_OK;
@@ -915,19 +966,14 @@ int forward_mse_bf16(ot_surrogate* s, const float* x, int64_t ldx, const float* 
   return OT_OK;
 }
 
+// Forward, fused MSE and backward of the bf16 path (the loss is reduced and
+// Adam applied by the step's last pass); *n_partials: loss partials written.
 int train_step_bf16(ot_surrogate* s, const float* x, int64_t ldx, const float* u, int64_t ldu, int64_t b,
-                    hipStream_t st, float* loss_dev) {
+                    hipStream_t st, int64_t* n_partials) {
   const int L = s->L;
-  const int64_t D = s->widths[L];
   ot::PhaseTimer& tm = s->timer;
   int rc;
-  int64_t n_partials = 0;
-  if ((rc = forward_mse_bf16(s, x, ldx, u, ldu, b, st, true, &n_partials))) return rc;
-  tm.mark(st, OT_PH_LOSS, 0);
-  hipLaunchKernelGGL(ot::loss_finalize_kernel, dim3(1), dim3(256), 0, st, s->loss_partials, n_partials,
-                     1.0 / ((double)b * (double)D), loss_dev, s->loss_last);
-  OT_LAUNCHED("loss_finalize_kernel");
-  tm.mark(st, OT_PH_LOSS, 1);
+  if ((rc = forward_mse_bf16(s, x, ldx, u, ldu, b, st, true, n_partials))) return rc;
 
   for (int l = L; l >= 1; --l) {
     if (l == L - 1) tm.mark(st, OT_PH_BWD_HIDDEN, 0);
@@ -1202,22 +1248,36 @@ static void begin_step(ot_surrogate* s) {
   s->fused_step = s->fuse_out && !(s->L == 1 && lo.in <= ot::kMaxSmallK);
 }
 
-// Adam over every parameter (and the bf16 weight copy in OT_BF16 mode)
-// except the output-layer weights when the step updated them in the fused
-// epilogue.
-static int adam_step(ot_surrogate* s, hipStream_t st) {
-  ot::PhaseTimer& tm = s->timer;
-  const int64_t n4 = s->n_flat / 4;
+// The step's last pass: Adam over every parameter (and the bf16 weight copy
+// in OT_BF16 mode) except the output-layer weights when the step updated them
+// in the fused epilogue, with the loss from the forward's partial sums
+// reduced in its first block.
+static ot::AdamRest make_rest(ot_surrogate* s, int64_t n_partials, int64_t rows, float* loss_dev) {
   const Layer& lo = s->layers[s->L - 1];
-  const int64_t hole = s->fused_step ? lo.w_off / 4 : 0;
-  const int64_t hole_len = s->fused_step ? (lo.b_off - lo.w_off) / 4 : 0;
-  const int64_t blocks = std::max<int64_t>(1, std::min<int64_t>(ot::ceil_div(n4 - hole_len, 256), 32768));
+  ot::AdamRest r{};
+  r.p = s->params;
+  r.g = s->grads;
+  r.m = s->m;
+  r.v = s->v;
+  r.pb = s->pb;
+  r.n4 = s->n_flat / 4;
+  r.hole = s->fused_step ? lo.w_off / 4 : 0;
+  r.hole_len = s->fused_step ? (lo.b_off - lo.w_off) / 4 : 0;
+  r.partials = s->loss_partials;
+  r.n_partials = n_partials;
+  r.inv_count = 1.0 / ((double)rows * (double)s->widths[s->L]);
+  r.loss_a = loss_dev;
+  r.loss_b = s->loss_last;
+  return r;
+}
+
+static int adam_step(ot_surrogate* s, hipStream_t st, const ot::AdamRest& r) {
+  ot::PhaseTimer& tm = s->timer;
+  const int64_t blocks = std::max<int64_t>(1, std::min<int64_t>(ot::ceil_div(r.n4 - r.hole_len, 256), 32768));
   tm.mark(st, OT_PH_ADAM, 0);
-  hipLaunchKernelGGL(ot::adam_kernel, dim3((unsigned)blocks), dim3(256), 0, st, s->params, s->grads, s->m, s->v, n4,
-                     hole, hole_len, s->step_adam, s->pb);
+  hipLaunchKernelGGL(ot::adam_kernel, dim3((unsigned)blocks), dim3(256), 0, st, r, s->step_adam);
   OT_LAUNCHED("adam_kernel");
   tm.mark(st, OT_PH_ADAM, 1);
-  tm.next_call();
   return OT_OK;
 }
 
@@ -1278,102 +1338,108 @@ extern "C" int surrogate_train_step(ot_surrogate* s, const float* x, int64_t ldx
   hipStream_t st = static_cast<hipStream_t>(stream);
   begin_step(s);
 
-  if (s->precision == OT_BF16) {
-    if ((rc = train_step_bf16(s, x, ldx, u, ldu, b, st, loss_dev))) return rc;
-    return adam_step(s, st);
-  }
   ot::PhaseTimer& tm = s->timer;
   int64_t n_partials = 0;
+  if (s->precision == OT_BF16) {
+    if ((rc = train_step_bf16(s, x, ldx, u, ldu, b, st, &n_partials))) return rc;
+    rc = adam_step(s, st, make_rest(s, n_partials, b, loss_dev));
+    tm.next_call();
+    return rc;
+  }
   if ((rc = forward_mse_f32(s, x, ldx, u, ldu, b, st, &n_partials))) return rc;
-  tm.mark(st, OT_PH_LOSS, 0);
-  hipLaunchKernelGGL(ot::loss_finalize_kernel, dim3(1), dim3(256), 0, st, s->loss_partials, n_partials,
-                     1.0 / ((double)b * (double)D), loss_dev, s->loss_last);
-  OT_LAUNCHED("loss_finalize_kernel");
-  tm.mark(st, OT_PH_LOSS, 1);
+  const ot::AdamRest rest = make_rest(s, n_partials, b, loss_dev);
+  bool rest_done = false;
 
-  // ---- backward, layer by layer from the output
-  for (int l = L; l >= 1; --l) {
-    if (l == L - 1) tm.mark(st, OT_PH_BWD_HIDDEN, 0);
+  // weight and bias gradient of layer l: dW = dZ^T A_in, db = column sums of
+  // dZ; for the output layer of a fused step, Adam on W_L in the epilogue (or
+  // the split-K reduction, which then also runs the step's last pass)
+  auto wgrad = [&](int l) -> int {
     const int ph_w = (l == L) ? OT_PH_WGRAD_OUTPUT : -1;
     const Layer& ly = s->layers[l - 1];
     const float* A_in = (l == 1) ? x : s->act[l - 1];
     const int64_t ld_in = (l == 1) ? ldx : s->ld[l - 1];
     float* dW = s->grads + ly.w_off;
     float* db = s->grads + ly.b_off;
-    const bool fused = (l == L) && s->fused_step;
-    // weight and bias gradient: dW = dZ^T A_in, db = column sums of dZ;
-    // fused: Adam on W_L in the epilogue (or split-K reduction) instead of a store
-    auto wgrad = [&]() -> int {
-      if (l == 1 && ly.in <= ot::kMaxSmallK) {
-        if (ph_w >= 0) tm.mark(st, ph_w, 0);
-        const int64_t rows_per = ot::ceil_div(b, kL1Parts);
-        const int64_t P = ot::ceil_div(b, rows_per);
-        hipLaunchKernelGGL(ot::small_k_wgrad_partial_kernel, dim3((unsigned)ot::ceil_div(ly.out, 64), (unsigned)P),
-                           dim3(256), 0, st, s->dz[1], s->ld[1], x, ldx, s->l1_part, b, ly.out, ly.in, rows_per,
-                           (const uint16_t*)nullptr);
-        OT_LAUNCHED("small_k_wgrad_partial_kernel");
-        const int64_t n = ly.out * (ly.in + 1);
-        hipLaunchKernelGGL(ot::small_k_wgrad_reduce_kernel, dim3((unsigned)ot::ceil_div(n, 256)), dim3(256), 0, st,
-                           s->l1_part, P, ly.out, ly.in, dW, ly.ldw, db);
-        OT_LAUNCHED("small_k_wgrad_reduce_kernel");
-        if (ph_w >= 0) tm.mark(st, ph_w, 1);
-        return OT_OK;
-      }
-      GemmArgs g = args0();
-      g.A = s->dz[l];
-      g.lda = s->ld[l];
-      g.B = A_in;
-      g.ldb = ld_in;
-      g.C = dW;
-      g.ldc = ly.ldw;
-      g.M = ly.out;
-      g.N = ly.in;
-      g.K = b;
-      g.rowsum = db;
-      Epi epi = Epi::Store;
-      if (fused) {
-        g.C = s->params + ly.w_off;
-        g.adam_m = s->m + ly.w_off;
-        g.adam_v = s->v + ly.w_off;
-        g.adam = s->step_adam;
-        epi = Epi::Adam;
-      }
-      return (l == L) ? run_gemm<Lay::MNMajor, Lay::MNMajor, 1>(s, g, epi, st, "weight gradient", true, ph_w,
-                                                                OT_PH_WGRAD_REDUCE)
-                      : run_gemm<Lay::MNMajor, Lay::MNMajor, 0>(s, g, epi, st, "weight gradient", true);
-    };
-    // input gradient dA_{l-1} = dZ_l W_l, then the ReLU mask of layer l-1
-    auto igrad = [&]() -> int {
-      GemmArgs g = args0();
-      g.A = s->dz[l];
-      g.lda = s->ld[l];
-      g.B = s->params + ly.w_off;
-      g.ldb = ly.ldw;
-      g.M = b;
-      g.N = ly.in;
-      g.K = ly.out;
-      g.C = s->dz[l - 1];
-      g.ldc = s->ld[l - 1];
-      g.mask = s->act[l - 1];
-      g.ldmask = s->ld[l - 1];
-      return (l == L) ? run_gemm<Lay::KMajor, Lay::MNMajor, 1>(s, g, Epi::Mask, st, "input gradient", true,
-                                                               OT_PH_IGRAD_OUTPUT, OT_PH_IGRAD_REDUCE)
-                      : run_gemm<Lay::KMajor, Lay::MNMajor, 0>(s, g, Epi::Mask, st, "input gradient", true);
-    };
+    if (l == 1 && ly.in <= ot::kMaxSmallK) {
+      if (ph_w >= 0) tm.mark(st, ph_w, 0);
+      const int64_t rows_per = ot::ceil_div(b, kL1Parts);
+      const int64_t P = ot::ceil_div(b, rows_per);
+      hipLaunchKernelGGL(ot::small_k_wgrad_partial_kernel, dim3((unsigned)ot::ceil_div(ly.out, 64), (unsigned)P),
+                         dim3(256), 0, st, s->dz[1], s->ld[1], x, ldx, s->l1_part, b, ly.out, ly.in, rows_per,
+                         (const uint16_t*)nullptr);
+      OT_LAUNCHED("small_k_wgrad_partial_kernel");
+      const int64_t n = ly.out * (ly.in + 1);
+      hipLaunchKernelGGL(ot::small_k_wgrad_reduce_kernel, dim3((unsigned)ot::ceil_div(n, 256)), dim3(256), 0, st,
+                         s->l1_part, P, ly.out, ly.in, dW, ly.ldw, db);
+      OT_LAUNCHED("small_k_wgrad_reduce_kernel");
+      if (ph_w >= 0) tm.mark(st, ph_w, 1);
+      return OT_OK;
+    }
+    GemmArgs g = args0();
+    g.A = s->dz[l];
+    g.lda = s->ld[l];
+    g.B = A_in;
+    g.ldb = ld_in;
+    g.C = dW;
+    g.ldc = ly.ldw;
+    g.M = ly.out;
+    g.N = ly.in;
+    g.K = b;
+    g.rowsum = db;
+    if (l == L && s->fused_step) {
+      g.C = s->params + ly.w_off;
+      g.adam_m = s->m + ly.w_off;
+      g.adam_v = s->v + ly.w_off;
+      g.adam = s->step_adam;
+      return run_gemm<Lay::MNMajor, Lay::MNMajor, 1>(s, g, Epi::Adam, st, "weight gradient + Adam", true, ph_w,
+                                                     OT_PH_WGRAD_REDUCE, nullptr, &rest, &rest_done);
+    }
+    return (l == L) ? run_gemm<Lay::MNMajor, Lay::MNMajor, 1>(s, g, Epi::Store, st, "weight gradient", true, ph_w,
+                                                              OT_PH_WGRAD_REDUCE)
+                    : run_gemm<Lay::MNMajor, Lay::MNMajor, 0>(s, g, Epi::Store, st, "weight gradient", true);
+  };
+  // input gradient dA_{l-1} = dZ_l W_l, then the ReLU mask of layer l-1
+  auto igrad = [&](int l) -> int {
+    const Layer& ly = s->layers[l - 1];
+    GemmArgs g = args0();
+    g.A = s->dz[l];
+    g.lda = s->ld[l];
+    g.B = s->params + ly.w_off;
+    g.ldb = ly.ldw;
+    g.M = b;
+    g.N = ly.in;
+    g.K = ly.out;
+    g.C = s->dz[l - 1];
+    g.ldc = s->ld[l - 1];
+    g.mask = s->act[l - 1];
+    g.ldmask = s->ld[l - 1];
+    return (l == L) ? run_gemm<Lay::KMajor, Lay::MNMajor, 1>(s, g, Epi::Mask, st, "input gradient", true,
+                                                             OT_PH_IGRAD_OUTPUT, OT_PH_IGRAD_REDUCE)
+                    : run_gemm<Lay::KMajor, Lay::MNMajor, 0>(s, g, Epi::Mask, st, "input gradient", true);
+  };
+
+  // ---- backward, layer by layer from the output.  A fused step computes the
+  // output layer's input gradient first (it reads W_L), runs the hidden
+  // layers, and updates W_L last, so that its split-K reduction can carry the
+  // step's last pass.
+  const bool defer_out = s->fused_step && L >= 2;
+  for (int l = L; l >= 1; --l) {
+    if (l == L - 1) tm.mark(st, OT_PH_BWD_HIDDEN, 0);
     if (l == 1) {
-      if ((rc = wgrad())) return rc;
+      if ((rc = wgrad(1))) return rc;
       break;
     }
-    // the fused update rewrites W_L, which the input gradient reads first
-    if (fused) {
-      if ((rc = igrad()) || (rc = wgrad())) return rc;
-    } else {
-      if ((rc = wgrad()) || (rc = igrad())) return rc;
+    if (l == L && defer_out) {
+      if ((rc = igrad(l))) return rc;
+      continue;
     }
+    if ((rc = wgrad(l)) || (rc = igrad(l))) return rc;
   }
   if (L >= 2) tm.mark(st, OT_PH_BWD_HIDDEN, 1);
-
-  return adam_step(s, st);
+  if (defer_out && (rc = wgrad(L))) return rc;
+  if (!rest_done) rc = adam_step(s, st, rest);
+  tm.next_call();
+  return rc;
 }
 
 extern "C" int surrogate_eval_loss(ot_surrogate* s, const float* x, int64_t ldx, const float* u, int64_t ldu,
