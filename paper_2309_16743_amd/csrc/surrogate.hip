@@ -17,6 +17,7 @@
 #include "common.h"
 #include "gemm_bf16.h"
 #include "gemm_f32.h"
+#include "hidden_small.h"
 #include "philox.h"
 #include "surrogate.h"
 
@@ -449,6 +450,10 @@ struct ot_surrogate {
   int64_t n_partials_cap = 0;
   float* l1_part = nullptr;
   int64_t l1_part_elems = 0;
+  bool small_hidden = false;    // fp32 6 -> H1 -> H2 -> D net with H1, H2 <= 256: fused narrow-layer kernels
+  float* hs_part1 = nullptr;    // their partial sums (layer-1 gradient per row tile, layer-2 per k split)
+  float* hs_part2 = nullptr;
+  float* hs_part2b = nullptr;
   float* loss_last = nullptr;
   double* eval_acc = nullptr;   // running sum of squared residuals of surrogate_eval_loss
   ot::PhaseTimer timer;
@@ -489,6 +494,10 @@ void free_workspace(ot_surrogate* s) {
   (void)hipFree(s->rsws);
   (void)hipFree(s->loss_partials);
   (void)hipFree(s->l1_part);
+  (void)hipFree(s->hs_part1);
+  (void)hipFree(s->hs_part2);
+  (void)hipFree(s->hs_part2b);
+  s->hs_part1 = s->hs_part2 = s->hs_part2b = nullptr;
   s->splitws = nullptr;
   s->splitws_elems = 0;
   s->rsws = nullptr;
@@ -538,6 +547,13 @@ int ensure_workspace(ot_surrogate* s, int64_t rows) {
   if ((rc = salloc((void**)&s->loss_partials, (size_t)s->n_partials_cap * sizeof(double)))) return rc;
   s->l1_part_elems = kL1Parts * s->widths[1] * (s->widths[0] + 1);
   if ((rc = salloc((void**)&s->l1_part, (size_t)s->l1_part_elems * sizeof(float)))) return rc;
+  if (s->small_hidden) {
+    const int64_t h1 = s->widths[1], h2 = s->widths[2], in0 = s->widths[0];
+    const int64_t n_rt = ot::ceil_div(rows, ot::kHfRows), n_kc = ot::ceil_div(rows, ot::kHbRows);
+    if ((rc = salloc((void**)&s->hs_part1, (size_t)(n_rt * h1 * (in0 + 1)) * sizeof(float)))) return rc;
+    if ((rc = salloc((void**)&s->hs_part2, (size_t)(n_kc * h2 * h1) * sizeof(float)))) return rc;
+    if ((rc = salloc((void**)&s->hs_part2b, (size_t)(n_kc * h2) * sizeof(float)))) return rc;
+  }
   s->ws_rows = rows;
   return OT_OK;
 }
@@ -730,6 +746,15 @@ bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) ==
 // Forward pass of layers 1..L-1 into act[]; rows x widths[0] input at X.
 int forward_hidden(ot_surrogate* s, const float* X, int64_t ldx, int64_t rows, hipStream_t st) {
   const int L = s->L;
+  if (s->small_hidden) {
+    const Layer &l1 = s->layers[0], &l2 = s->layers[1];
+    const dim3 grid((unsigned)ot::ceil_div(rows, ot::kHfRows), (unsigned)ot::ceil_div(l2.out, ot::kHfCols));
+    hipLaunchKernelGGL(ot::hidden_fwd_small_kernel, grid, dim3(256), 0, st, X, ldx, (int)l1.in,
+                       s->params + l1.w_off, l1.ldw, s->params + l1.b_off, (int)l1.out, s->params + l2.w_off, l2.ldw,
+                       s->params + l2.b_off, (int)l2.out, s->act[1], s->ld[1], s->act[2], s->ld[2], rows);
+    OT_LAUNCHED("hidden_fwd_small_kernel");
+    return OT_OK;
+  }
   for (int l = 1; l < L; ++l) {
     const Layer& ly = s->layers[l - 1];
     const float* W = s->params + ly.w_off;
@@ -1109,6 +1134,8 @@ extern "C" int surrogate_create(ot_surrogate** out, const int64_t* widths, int32
   s->beta2 = beta2;
   s->eps = eps;
   s->fuse_out = (flags & OT_SURROGATE_KEEP_GRADS) == 0;
+  s->small_hidden = precision == OT_FP32 && n_widths == 4 && widths[0] <= ot::kSmallIn &&
+                    widths[1] <= ot::kSmallH && widths[2] <= ot::kSmallH;
   s->ld.resize(n_widths);
   for (int i = 0; i < n_widths; ++i) s->ld[i] = ot::round_up(widths[i], 8);
   int64_t off = 0;
@@ -1424,7 +1451,27 @@ extern "C" int surrogate_train_step(ot_surrogate* s, const float* x, int64_t ldx
   // step's last pass.
   const bool defer_out = s->fused_step && L >= 2;
   for (int l = L; l >= 1; --l) {
-    if (l == L - 1) tm.mark(st, OT_PH_BWD_HIDDEN, 0);
+    if (l == L - 1) {
+      tm.mark(st, OT_PH_BWD_HIDDEN, 0);
+      if (s->small_hidden) {   // layers 2 and 1 in two launches
+        const Layer &l1 = s->layers[0], &l2 = s->layers[1];
+        const int64_t n_rt = ot::ceil_div(b, ot::kHfRows), n_kc = ot::ceil_div(b, ot::kHbRows);
+        const int64_t nA = n_rt * ot::ceil_div(l1.out, ot::kHfCols);
+        const int64_t nB = n_kc * ot::ceil_div(l2.out, ot::kHbTile) * ot::ceil_div(l1.out, ot::kHbTile);
+        hipLaunchKernelGGL(ot::hidden_bwd_small_kernel, dim3((unsigned)(nA + nB)), dim3(256), 0, st, s->dz[2],
+                           s->ld[2], s->act[1], s->ld[1], x, ldx, (int)l1.in, s->params + l2.w_off, l2.ldw,
+                           (int)l1.out, (int)l2.out, b, s->dz[1], s->ld[1], s->hs_part1, s->hs_part2, s->hs_part2b,
+                           nA);
+        OT_LAUNCHED("hidden_bwd_small_kernel");
+        const int64_t n_out = l2.out * l1.out + l2.out + l1.out * (l1.in + 1);
+        hipLaunchKernelGGL(ot::hidden_bwd_reduce_kernel, dim3((unsigned)ot::ceil_div(n_out, 256)), dim3(256), 0, st,
+                           s->hs_part1, n_rt, s->hs_part2, s->hs_part2b, n_kc, (int)l1.in, (int)l1.out, (int)l2.out,
+                           s->grads + l1.w_off, l1.ldw, s->grads + l1.b_off, s->grads + l2.w_off, l2.ldw,
+                           s->grads + l2.b_off);
+        OT_LAUNCHED("hidden_bwd_reduce_kernel");
+        break;
+      }
+    }
     if (l == 1) {
       if ((rc = wgrad(1))) return rc;
       break;
