@@ -70,6 +70,29 @@ __device__ __forceinline__ void stage_tile(float* dst, int ls, const float* __re
   }
 }
 
+// One 16 x 16 MFMA output block over kp (a multiple of 4) k values: lane l
+// reads its A operand at pa[k * sa] and its B operand at pb[k * sb] for
+// k = k0 (k0 = 0, 4, 8, ...; the lane's own k offset is folded into pa, pb).
+// Four accumulator chains take the k steps in turn (four MFMAs in flight
+// instead of one dependent chain), each step's operands are read while the
+// previous steps run, and the chains are added in a fixed order at the end.
+__device__ __forceinline__ f32x4v mfma_row_dot(const float* pa, int sa, const float* pb, int sb, int kp) {
+  f32x4v acc[4] = {};
+  int k0 = 0;
+  for (; k0 + 16 <= kp; k0 += 16) {
+    float a[4], b[4];
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      a[c] = pa[(k0 + 4 * c) * sa];
+      b[c] = pb[(k0 + 4 * c) * sb];
+    }
+#pragma unroll
+    for (int c = 0; c < 4; ++c) acc[c] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[c], b[c], acc[c], 0, 0, 0);
+  }
+  for (int c = 0; k0 < kp; k0 += 4, ++c) acc[c] = __builtin_amdgcn_mfma_f32_16x16x4f32(pa[k0 * sa], pb[k0 * sb], acc[c], 0, 0, 0);
+  return (acc[0] + acc[1]) + (acc[2] + acc[3]);
+}
+
 // Forward of layers 1 and 2 for rows r0 .. r0 + 15 and layer-2 units
 // c0 .. c0 + 63.  Wave w computes the 16 x 16 output block of units
 // c0 + 16 w .. c0 + 16 w + 15.  Blocks of column tile 0 also store A1.
@@ -79,67 +102,39 @@ __global__ __launch_bounds__(256) void hidden_fwd_small_kernel(
     int h2, float* __restrict__ A1, int64_t lda1, float* __restrict__ A2, int64_t lda2, int64_t rows) {
   __shared__ __attribute__((aligned(16))) float sA1[kHfRows * kStrideA];
   __shared__ __attribute__((aligned(16))) float sW2[kHfCols * kStrideA];
-  __shared__ float sW1[kSmallH][kSmallIn + 1];
-  __shared__ float sB1[kSmallH];
   __shared__ float sX[kHfRows][kSmallIn];
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int64_t r0 = (int64_t)blockIdx.x * kHfRows;
   const int c0 = blockIdx.y * kHfCols;
-  // W2 rows c0 .. c0 + 63 (all h1 columns), W1 (h1 x in0), X rows
+  // W2 rows c0 .. c0 + 63 (all h1 columns) and X rows into LDS; thread j
+  // keeps W1 row j and b1[j] in registers (layer 1 is one unit per thread)
+  const int j = tid;
+  float wj[kSmallIn], bj = 0.f;
+#pragma unroll
+  for (int k = 0; k < kSmallIn; ++k) wj[k] = (j < h1 && k < in0) ? W1[(int64_t)j * ldw1 + k] : 0.f;
+  if (j < h1) bj = b1[j];
   stage_tile<kHfCols, kSmallH>(sW2, kStrideA, W2, ldw2, c0, h2, 0, h1);
   {
-    float wv[kSmallH * kSmallIn / 256];
-#pragma unroll
-    for (int q = 0; q < kSmallH * kSmallIn / 256; ++q) {
-      const int e = tid + 256 * q, j = e / kSmallIn, k = e % kSmallIn;
-      wv[q] = (j < h1 && k < in0) ? W1[(int64_t)j * ldw1 + k] : 0.f;
-    }
-#pragma unroll
-    for (int q = 0; q < kSmallH * kSmallIn / 256; ++q) {
-      const int e = tid + 256 * q;
-      sW1[e / kSmallIn][e % kSmallIn] = wv[q];
-    }
     const int r = tid / kSmallIn, k = tid % kSmallIn;
     sX[r][k] = (r0 + r < rows && k < in0) ? X[(r0 + r) * ldx + k] : 0.f;
-    sB1[tid] = tid < h1 ? b1[tid] : 0.f;
   }
   __syncthreads();
-  // layer 1 (K = in0 on the vector units); thread = (row r, 16 units)
+  // layer 1 (K = in0 on the vector units; X and W1 are zero beyond in0, so the
+  // padded terms add exact zeros); sX reads are broadcasts
   const int h1p = (h1 + 3) & ~3;
-  {
-    const int r = tid / 16, j0 = (tid % 16) * 16;
-    float xr[kSmallIn];
+#pragma unroll 4
+  for (int r = 0; r < kHfRows; ++r) {
+    float z = bj;
 #pragma unroll
-    for (int k = 0; k < kSmallIn; ++k) xr[k] = sX[r][k];
-#pragma unroll
-    for (int jj = 0; jj < 16; ++jj) {
-      const int j = j0 + jj;
-      float a = 0.f;
-      if (j < h1) {
-        float z = sB1[j];
-        for (int k = 0; k < in0; ++k) z += xr[k] * sW1[j][k];
-        a = z > 0.f ? z : 0.f;
-        if (blockIdx.y == 0 && r0 + r < rows) A1[(r0 + r) * lda1 + j] = a;
-      }
-      sA1[r * kStrideA + j] = a;
-    }
+    for (int k = 0; k < kSmallIn; ++k) z += sX[r][k] * wj[k];
+    const float a = (j < h1 && z > 0.f) ? z : 0.f;
+    if (j < h1 && blockIdx.y == 0 && r0 + r < rows) A1[(r0 + r) * lda1 + j] = a;
+    sA1[r * kStrideA + j] = a;
   }
   __syncthreads();
   // layer 2: D[16 x 16] = A1 tile (16 x h1) * W2 block^T, k steps of 4
   const int ci = 16 * w + (lane & 15);
-  f32x4v acc = {0.f, 0.f, 0.f, 0.f};
-  {
-    // operands of step k0 + 4 are read while step k0's MFMA runs
-    const float* pa = sA1 + (lane & 15) * kStrideA + (lane >> 4);
-    const float* pb = sW2 + ci * kStrideA + (lane >> 4);
-    float a = pa[0], b = pb[0];
-    for (int k0 = 0; k0 < h1p; k0 += 4) {
-      const float an = (k0 + 4 < h1p) ? pa[k0 + 4] : 0.f, bn = (k0 + 4 < h1p) ? pb[k0 + 4] : 0.f;
-      acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, acc, 0, 0, 0);
-      a = an;
-      b = bn;
-    }
-  }
+  f32x4v acc = mfma_row_dot(sA1 + (lane & 15) * kStrideA + (lane >> 4), 1, sW2 + ci * kStrideA + (lane >> 4), 1, h1p);
   const int c = c0 + ci;
   if (c < h2) {
     const float bias = b2[c];
@@ -192,18 +187,8 @@ __global__ __launch_bounds__(256) void hidden_bwd_small_kernel(
     __syncthreads();
     const int h2p = (h2 + 3) & ~3;
     const int ci = 16 * w + (lane & 15);
-    f32x4v acc = {0.f, 0.f, 0.f, 0.f};
-    {
-      const float* pa = sD2 + (lane & 15) * kStrideA + (lane >> 4);
-      const float* pb = sW + (lane >> 4) * kStrideB + ci;
-      float a = pa[0], b = pb[0];
-      for (int k0 = 0; k0 < h2p; k0 += 4) {
-        const float an = (k0 + 4 < h2p) ? pa[k0 + 4] : 0.f, bn = (k0 + 4 < h2p) ? pb[(k0 + 4) * kStrideB] : 0.f;
-        acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, acc, 0, 0, 0);
-        a = an;
-        b = bn;
-      }
-    }
+    const f32x4v acc =
+        mfma_row_dot(sD2 + (lane & 15) * kStrideA + (lane >> 4), 1, sW + (lane >> 4) * kStrideB + ci, kStrideB, h2p);
     const int i = c0 + ci;
     for (int q = 0; q < 4; ++q) {
       const int r = 4 * (lane >> 4) + q;

@@ -175,13 +175,12 @@ __global__ __launch_bounds__(kAssignThreads) void put_assign_kernel(
     int64_t k, uint64_t ticket, uint64_t seed, int64_t C, int may_evict, const int32_t* __restrict__ tile_cnt,
     int64_t ntiles, int32_t* __restrict__ tile_off, int32_t* __restrict__ victim_pos,
     int32_t* __restrict__ put_slots, ResCounters* __restrict__ ctr, long long* __restrict__ accepted_out) {
-  __shared__ int s_r[kMaxPut];
-  __shared__ int s_par[kMaxPut];
-  __shared__ int s_par2[kMaxPut];
-  __shared__ int s_lv[kMaxPut];
-  __shared__ int s_pre[kMaxPut];
-  __shared__ int s_taken[kMaxPut];
-  __shared__ int s_last[kMaxPut];
+  // seven arrays of max(k, 1) ints in dynamic LDS (sized by the launch, so a
+  // small put does not hold a CU's LDS)
+  extern __shared__ int s_dyn[];
+  const int64_t cap = k > 0 ? k : 1;
+  int *s_r = s_dyn, *s_par = s_r + cap, *s_par2 = s_par + cap, *s_lv = s_par2 + cap, *s_pre = s_lv + cap,
+      *s_taken = s_pre + cap, *s_last = s_taken + cap;
   __shared__ int s_wave[kAssignThreads / 64];
   __shared__ int s_total;
 
@@ -367,13 +366,11 @@ __global__ __launch_bounds__(kAssignThreads) void list_take_kernel(
     int32_t* __restrict__ occ, int32_t* __restrict__ free_q, int64_t free_tail, int32_t* __restrict__ slots,
     int32_t* __restrict__ seen, long long* __restrict__ sample_id, unsigned long long* __restrict__ hist,
     ResCounters* __restrict__ ctr) {
-  __shared__ int s_r[kMaxDrainBatch];
-  __shared__ int s_par[kMaxDrainBatch];
-  __shared__ int s_par2[kMaxDrainBatch];
-  __shared__ int s_lv[kMaxDrainBatch];
-  __shared__ int s_pre[kMaxDrainBatch];
-  __shared__ int s_taken[kMaxDrainBatch];
-  __shared__ int s_last[kMaxDrainBatch];
+  // seven arrays of max(bb, 1) ints in dynamic LDS, sized by the launch
+  extern __shared__ int s_dyn[];
+  const int64_t cap = bb > 0 ? bb : 1;
+  int *s_r = s_dyn, *s_par = s_r + cap, *s_par2 = s_par + cap, *s_lv = s_par2 + cap, *s_pre = s_lv + cap,
+      *s_taken = s_pre + cap, *s_last = s_taken + cap;
   __shared__ long long s_dU, s_dS;
   const int tid = threadIdx.x, nt = blockDim.x;
   auto pos = [&](int64_t p) { return (occ_base + p) % C; };
@@ -602,6 +599,15 @@ extern "C" int reservoir_create(ot_reservoir** out, int64_t capacity, int64_t th
       return fail(ot::set_error(OT_E_HIP, "hipStreamCreate failed"));
     r->own_stream = true;
   }
+  {
+    // the assignment and take kernels size their LDS per call, up to 7 ints per row of the largest call
+    const int max_dyn = (int)(7 * std::max(ot::kMaxPut, ot::kMaxDrainBatch) * sizeof(int));
+    if (hipFuncSetAttribute(reinterpret_cast<const void*>(&ot::put_assign_kernel),
+                            hipFuncAttributeMaxDynamicSharedMemorySize, max_dyn) != hipSuccess ||
+        hipFuncSetAttribute(reinterpret_cast<const void*>(&ot::list_take_kernel),
+                            hipFuncAttributeMaxDynamicSharedMemorySize, max_dyn) != hipSuccess)
+      return fail(ot::set_error(OT_E_HIP, "hipFuncSetAttribute (dynamic LDS) failed"));
+  }
   if (hipEventCreateWithFlags(&r->ev_in, hipEventDisableTiming) != hipSuccess ||
       hipEventCreateWithFlags(&r->ev_out, hipEventDisableTiming) != hipSuccess)
     return fail(ot::set_error(OT_E_HIP, "hipEventCreate failed"));
@@ -673,7 +679,8 @@ extern "C" int reservoir_put(ot_reservoir* r, const float* x, int64_t ldx, const
                        r->C, r->tile_cnt);
     OT_LAUNCHED("seen_tile_count_kernel");
   }
-  hipLaunchKernelGGL(ot::put_assign_kernel, dim3(1), dim3(ot::kAssignThreads), 0, r->stream, k, ticket, r->seed,
+  hipLaunchKernelGGL(ot::put_assign_kernel, dim3(1), dim3(ot::kAssignThreads),
+                     (unsigned)(7 * std::max<int64_t>(k, 1) * sizeof(int)), r->stream, k, ticket, r->seed,
                      r->C, may_evict, r->tile_cnt, r->ntiles, r->tile_off, r->victim_pos, r->put_slots, r->ctr,
                      reinterpret_cast<long long*>(accepted_dev));
   OT_LAUNCHED("put_assign_kernel");
@@ -741,7 +748,8 @@ extern "C" int reservoir_sample_batch(ot_reservoir* r, int64_t b, void* stream, 
   } else {
     // free queue tail: C - N entries follow its head
     const int64_t free_tail = (r->free_head + r->C - r->n_host) % r->C;
-    hipLaunchKernelGGL(ot::list_take_kernel, dim3(1), dim3(ot::kAssignThreads), 0, r->stream, r->seed, ticket,
+    hipLaunchKernelGGL(ot::list_take_kernel, dim3(1), dim3(ot::kAssignThreads),
+                       (unsigned)(7 * std::max<int64_t>(drawn, 1) * sizeof(int)), r->stream, r->seed, ticket,
                        r->n_host, drawn, r->policy == OT_POLICY_FIFO ? 0 : 1, r->occ_base, r->C, r->occ,
                        r->free_q, free_tail, slots, r->seen, r->sample_id, r->hist, r->ctr);
     OT_LAUNCHED("list_take_kernel");

@@ -253,3 +253,44 @@ def test_list_policy_sequence_bit_exact(policy, C, T, d, seed, ops):
         compare_meta(g, o, 64)
     assert o.N == 0 and g.stats()["policy"] == (1 if policy == "fifo" else 2)
     g.close()
+
+
+@pytest.mark.parametrize("policy", [0, 2])
+def test_largest_put_and_take(policy):
+    """A put of the largest chunk (4096 rows) into a full buffer whose every
+    sample is seen (4096 evictions for the Reservoir), and a 4096-row batch
+    (drain for the Reservoir, random take for FIRO): bit-exact against the
+    oracle (these calls use the most LDS of the assignment and take kernels)."""
+    from paper_2309_16743_amd import OT_OK, Reservoir
+    from oracle import buffers as obf
+    C, d, k = 8192, 64, 4096
+    g = Reservoir(C, 0, 6, d, 21, policy=policy)
+    o = (orv.Reservoir if policy == 0 else obf.FIROBuffer)(C, 0, 6, d, 21)
+    key = 0
+    for _ in range(3):
+        keys = np.arange(key, key + k)
+        ud, xd = padded(k, d), padded(k, 6)
+        ud.copy_(torch.from_numpy(hash_rows(keys, d)))
+        xd.copy_(torch.from_numpy(hash_inputs(keys)))
+        g.put(xd, ud)
+        _, a, _, _ = o.put(hash_inputs(keys), hash_rows(keys, d), k=k)
+        key += a
+        if policy == 0:          # draw every sample at least once before the next put
+            for _ in range(8):
+                slots = torch.empty(k, dtype=torch.int32, device=DEV)
+                assert g.sample_batch(k, slots)[0] == OT_OK
+                st, oslots, _, _, _ = o.sample_batch(k)
+                torch.cuda.synchronize()
+                assert np.array_equal(slots.cpu().numpy(), np.array(oslots))
+    compare_meta(g, o, 64)
+    g.end_reception()
+    o.end_reception()
+    slots = torch.empty(k, dtype=torch.int32, device=DEV)
+    ub = padded(k, d)
+    st, n, _ = g.sample_batch(k, slots, u_out=ub)
+    ost, oslots, _, ou, _ = o.sample_batch(k)
+    torch.cuda.synchronize()
+    assert st == ost == OT_OK and n == k
+    assert np.array_equal(slots.cpu().numpy(), np.array(oslots)) and np.array_equal(ub.cpu().numpy(), ou)
+    compare_meta(g, o, 64)
+    g.close()
