@@ -108,11 +108,11 @@ def kernel_sources(label: str):
     csrc = os.path.join(ROOT, "paper_2309_16743_amd", "csrc")
     files = ["common.h"]
     if label.startswith("gemm_fp32"):
-        files += ["gemm_f32.h", "surrogate.hip"]
+        files += ["adam.h", "gemm_f32.h", "surrogate.hip"]
     elif label.startswith("gemm_bf16"):
-        files += ["gemm_bf16.h", "surrogate.hip"]
+        files += ["adam.h", "gemm_bf16.h", "surrogate.hip"]
     elif label == "adam_kernel":
-        files += ["surrogate.hip"]
+        files += ["adam.h", "surrogate.hip"]
     else:
         files += ["reservoir.hip", "philox.h"]
     return [os.path.join(csrc, f) for f in files]
@@ -132,6 +132,8 @@ def kernel_matches(label: str, name: str) -> bool:
     if label in ("adam_kernel", "gather_kernel", "put_copy_kernel"):
         return f"ot::{label}(" in name
     phase = label.split("(")[1].rstrip(")")
+    if phase == "wgrad_output + fused Adam":       # bf16 weight gradient with the Adam epilogue
+        return "gemm_bf16_pipe_kernel<" in name and "(ot::LayB)1, (ot::LayB)1, (ot::EpiB)6" in name
     if label.startswith("gemm_fp32"):
         lay = {"fwd_output": "(ot::Lay)0, (ot::Lay)0", "wgrad_output": "(ot::Lay)1, (ot::Lay)1",
                "igrad_output": "(ot::Lay)0, (ot::Lay)1"}[phase]
