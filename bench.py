@@ -33,8 +33,9 @@ iterations (one put and one draw each).
 Prints one JSON line.  `value` is samples processed per second by the train
 step (batch size x steps / time), from HIP events on the work stream over the
 timed steps.  `roofline` reports the dominant kernel's algorithmic rate
-against MI355X's datasheet peak, from HIP events around that kernel inside the
-same timed region.  `cpu_baseline` times the plain fp64 CPU oracle on a
+against MI355X's datasheet peak, from HIP events that the library hands to
+that kernel's launch (hipExtLaunchKernel stamps them with the kernel's own
+start and end) on the stream it runs on, inside the same timed region.  `cpu_baseline` times the plain fp64 CPU oracle on a
 bounded sample of the same workload on this host.
 """
 from __future__ import annotations
@@ -366,7 +367,7 @@ def cpu_baseline_scaled(w, seconds: float) -> dict:
 
 
 def timed_region(tr, w, K, profile_steps, stream, wrap_put):
-    """Breakdown pass (all phases), then K timed steps with events around the
+    """Breakdown pass (all phases), then K timed steps with events on the
     dominant kernel and the gather."""
     import torch
 

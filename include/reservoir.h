@@ -187,9 +187,12 @@ enum ot_reservoir_phase {
   OT_RESERVOIR_PHASES = 4
 };
 
-/* Profiling hook: record HIP events on the ordering stream around the
- * kernels of every phase in phase_mask for the next max_calls put or sample
- * calls.  Allocates 2 events per phase and call. */
+/* Profiling hook: time the kernels of every phase in phase_mask for the next
+ * max_calls put or sample calls with HIP events on the ordering stream.  The
+ * single-kernel phases PUT_COPY and GATHER hand their events to the launch
+ * (hipExtLaunchKernel), which stamps them with the kernel's own start and
+ * end; the others record events before and after their kernels.  Allocates 2
+ * events per phase and call. */
 int reservoir_timing_begin(ot_reservoir* r, uint32_t phase_mask, int64_t max_calls);
 
 /* Wait for the recorded events and return summed milliseconds and counts per

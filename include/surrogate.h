@@ -143,9 +143,13 @@ enum ot_surrogate_phase {
   OT_SURROGATE_PHASES = 9
 };
 
-/* Profiling hook: record HIP events around the kernels of every phase in
- * phase_mask (bit p = phase p) for the next max_steps train steps, on the
- * stream each step runs on.  Allocates 2 events per phase and step. */
+/* Profiling hook: time every phase in phase_mask (bit p = phase p) for the
+ * next max_steps train steps with HIP events on the stream each step runs on.
+ * A phase that is one kernel launch (the output-layer GEMMs) passes its
+ * events to that launch (hipExtLaunchKernel), so they take the kernel's own
+ * start and end; other phases record events before and after their kernels,
+ * which also counts the dispatch gaps.  Allocates 2 events per phase and
+ * step. */
 int surrogate_timing_begin(ot_surrogate* s, uint32_t phase_mask, int64_t max_steps);
 
 /* Wait for the recorded events; ms_total[p] receives the summed duration of

@@ -2,6 +2,7 @@
 // small device utilities.  Not part of the public C ABI.
 #pragma once
 
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -36,6 +37,18 @@ struct PhaseTimer {
     if (!on(phase)) return;
     const size_t i = (size_t)((call * nph + phase) * 2 + which);
     if (hipEventRecord(ev[i], st) == hipSuccess) rec[i] = 1;
+  }
+  // Start and stop events of a phase that is a single kernel, for
+  // hipExtLaunchKernelGGL: the runtime then stamps them with that kernel's own
+  // start and end (mark() around a launch also counts the dispatch gap before
+  // the kernel).  Both stay null while the phase is not timed.
+  void kernel_events(int phase, hipEvent_t* start, hipEvent_t* stop) {
+    *start = *stop = nullptr;
+    if (!on(phase)) return;
+    const size_t i = (size_t)((call * nph + phase) * 2);
+    *start = ev[i];
+    *stop = ev[i + 1];
+    rec[i] = rec[i + 1] = 1;
   }
   void next_call() {
     if (mask) ++call;

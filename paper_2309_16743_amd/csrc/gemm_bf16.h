@@ -500,12 +500,14 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmBArgs g) {
   e.finish(g, tm, s_red);
 }
 
+// t0 / t1 (nullable): events that take the kernel's own start and end times.
 template <int FM, int FN, LayB LA, LayB LB, EpiB EPI, int BK>
-hipError_t launch_gemm_bf16(const GemmBArgs& g, int64_t splits, hipStream_t stream) {
+hipError_t launch_gemm_bf16(const GemmBArgs& g, int64_t splits, hipStream_t stream, hipEvent_t t0 = nullptr,
+                            hipEvent_t t1 = nullptr) {
   constexpr int BM = 32 * FM, BN = 32 * FN;
   const int64_t tiles = ((g.M + BM - 1) / BM) * ((g.N + BN - 1) / BN);
-  hipLaunchKernelGGL((gemm_bf16_kernel<FM, FN, LA, LB, EPI, BK>), dim3((unsigned)tiles, (unsigned)splits), dim3(256), 0,
-                     stream, g);
+  hipExtLaunchKernelGGL((gemm_bf16_kernel<FM, FN, LA, LB, EPI, BK>), dim3((unsigned)tiles, (unsigned)splits),
+                        dim3(256), 0, stream, t0, t1, 0, g);
   return hipGetLastError();
 }
 
@@ -723,10 +725,11 @@ __global__ __launch_bounds__(256, OCC) void gemm_bf16_pipe_kernel(GemmBArgs g) {
 }
 
 template <int BM, int BN, int BK, int S, int OCC, LayB LA, LayB LB, EpiB EPI>
-hipError_t launch_gemm_bf16_pipe(const GemmBArgs& g, int64_t splits, hipStream_t stream) {
+hipError_t launch_gemm_bf16_pipe(const GemmBArgs& g, int64_t splits, hipStream_t stream, hipEvent_t t0 = nullptr,
+                                 hipEvent_t t1 = nullptr) {
   const int64_t tiles = ((g.M + BM - 1) / BM) * ((g.N + BN - 1) / BN);
-  hipLaunchKernelGGL((gemm_bf16_pipe_kernel<BM, BN, BK, S, OCC, LA, LB, EPI>), dim3((unsigned)tiles, (unsigned)splits),
-                     dim3(256), 0, stream, g);
+  hipExtLaunchKernelGGL((gemm_bf16_pipe_kernel<BM, BN, BK, S, OCC, LA, LB, EPI>),
+                        dim3((unsigned)tiles, (unsigned)splits), dim3(256), 0, stream, t0, t1, 0, g);
   return hipGetLastError();
 }
 

@@ -411,14 +411,16 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_f32_kernel(GemmArgs g) {
   }
 }
 
-// Host launcher.  Returns the hipError_t of the launch.
+// Host launcher.  Returns the hipError_t of the launch.  t0 / t1 (nullable):
+// events that take the kernel's own start and end times.
 template <int WGM, int WGN, int FM, int FN, Lay LA, Lay LB, Epi EPI, int BK = 16, int ROLE = 0>
-hipError_t launch_gemm_f32(const GemmArgs& g, int64_t splits, hipStream_t stream) {
+hipError_t launch_gemm_f32(const GemmArgs& g, int64_t splits, hipStream_t stream, hipEvent_t t0 = nullptr,
+                           hipEvent_t t1 = nullptr) {
   constexpr int BM = 16 * FM * WGM, BN = 16 * FN * WGN;
   const int64_t tiles = ((g.M + BM - 1) / BM) * ((g.N + BN - 1) / BN);
   dim3 grid((unsigned)tiles, (unsigned)splits);
-  hipLaunchKernelGGL((gemm_f32_kernel<WGM, WGN, FM, FN, LA, LB, EPI, BK, ROLE>), grid, dim3(64 * WGM * WGN), 0, stream,
-                     g);
+  hipExtLaunchKernelGGL((gemm_f32_kernel<WGM, WGN, FM, FN, LA, LB, EPI, BK, ROLE>), grid, dim3(64 * WGM * WGN), 0,
+                        stream, t0, t1, 0, g);
   return hipGetLastError();
 }
 

@@ -656,14 +656,15 @@ extern "C" int reservoir_put(ot_reservoir* r, const float* x, int64_t ldx, const
     OT_LAUNCHED("list_put_kernel");
     tm.mark(r->stream, OT_PH_PUT_ASSIGN, 1);
     if (a > 0) {
-      tm.mark(r->stream, OT_PH_PUT_COPY, 0);
+      hipEvent_t t0, t1;
+      tm.kernel_events(OT_PH_PUT_COPY, &t0, &t1);
       const int vec_ok = aligned16(u) && (ldu % 4 == 0);
       const int64_t segs = ot::ceil_div(r->u_dim, ot::kCopySeg);
-      hipLaunchKernelGGL(ot::put_copy_kernel, dim3((unsigned)(segs * a)), dim3(ot::kCopyThreads), 0, r->stream,
-                         x, ldx, u, ldu, r->put_slots, r->ctr, r->xslab, r->ldxs, r->uslab, r->ldus, r->x_dim,
-                         r->u_dim, segs, vec_ok, r->seen, r->sample_id, r->hist, r->C);
+      hipExtLaunchKernelGGL(ot::put_copy_kernel, dim3((unsigned)(segs * a)), dim3(ot::kCopyThreads), 0, r->stream,
+                            t0, t1, 0, x, ldx, u, ldu, r->put_slots, (const ot::ResCounters*)r->ctr, r->xslab,
+                            r->ldxs, r->uslab, r->ldus, r->x_dim, r->u_dim, segs, vec_ok, r->seen, r->sample_id,
+                            r->hist, r->C);
       OT_LAUNCHED("put_copy_kernel");
-      tm.mark(r->stream, OT_PH_PUT_COPY, 1);
     }
     tm.next_call();
     r->n_host += a;
@@ -691,14 +692,14 @@ extern "C" int reservoir_put(ot_reservoir* r, const float* x, int64_t ldx, const
   }
   tm.mark(r->stream, OT_PH_PUT_ASSIGN, 1);
   if (k > 0) {
-    tm.mark(r->stream, OT_PH_PUT_COPY, 0);
+    hipEvent_t t0, t1;
+    tm.kernel_events(OT_PH_PUT_COPY, &t0, &t1);
     const int vec_ok = aligned16(u) && (ldu % 4 == 0);
     const int64_t segs = ot::ceil_div(r->u_dim, ot::kCopySeg);
-    hipLaunchKernelGGL(ot::put_copy_kernel, dim3((unsigned)(segs * k)), dim3(ot::kCopyThreads), 0, r->stream,
-                       x, ldx, u, ldu, r->put_slots, r->ctr, r->xslab, r->ldxs, r->uslab, r->ldus, r->x_dim,
-                       r->u_dim, segs, vec_ok, r->seen, r->sample_id, r->hist, r->C);
+    hipExtLaunchKernelGGL(ot::put_copy_kernel, dim3((unsigned)(segs * k)), dim3(ot::kCopyThreads), 0, r->stream, t0,
+                          t1, 0, x, ldx, u, ldu, r->put_slots, (const ot::ResCounters*)r->ctr, r->xslab, r->ldxs,
+                          r->uslab, r->ldus, r->x_dim, r->u_dim, segs, vec_ok, r->seen, r->sample_id, r->hist, r->C);
     OT_LAUNCHED("put_copy_kernel");
-    tm.mark(r->stream, OT_PH_PUT_COPY, 1);
   }
   tm.next_call();
   r->n_host = std::min<int64_t>(r->C, r->n_host + k);
@@ -758,14 +759,15 @@ extern "C" int reservoir_sample_batch(ot_reservoir* r, int64_t b, void* stream, 
   }
   tm.mark(r->stream, OT_PH_SELECT, 1);
   if (u_out || x_out) {
-    tm.mark(r->stream, OT_PH_GATHER, 0);
+    hipEvent_t t0, t1;
+    tm.kernel_events(OT_PH_GATHER, &t0, &t1);
     const int vec_ok = (u_out == nullptr) || (aligned16(u_out) && (lduo % 4 == 0));
     const int64_t segs = ot::ceil_div(r->u_dim, ot::kCopySeg);
-    hipLaunchKernelGGL(ot::gather_kernel, dim3((unsigned)(segs * drawn)), dim3(ot::kCopyThreads), 0, r->stream,
-                       slots, r->xslab, r->ldxs, r->uslab, r->ldus, x_out, ldxo, u_out, lduo, r->x_dim,
-                       r->u_dim, segs, vec_ok);
+    hipExtLaunchKernelGGL(ot::gather_kernel, dim3((unsigned)(segs * drawn)), dim3(ot::kCopyThreads), 0, r->stream,
+                          t0, t1, 0, (const int32_t*)slots, (const float*)r->xslab, r->ldxs,
+                          (const float*)r->uslab, r->ldus, x_out, ldxo, u_out, lduo, r->x_dim, r->u_dim, segs,
+                          vec_ok);
     OT_LAUNCHED("gather_kernel");
-    tm.mark(r->stream, OT_PH_GATHER, 1);
   }
   tm.next_call();
   if (count_out) *count_out = drawn;

@@ -609,24 +609,25 @@ Plan make_plan(int64_t M, int64_t N, int64_t K, bool allow_split) {
 }
 
 template <Lay LA, Lay LB, Epi EPI, int ROLE>
-hipError_t launch_cfg(int cfg, const GemmArgs& g, int64_t splits, hipStream_t st) {
+hipError_t launch_cfg(int cfg, const GemmArgs& g, int64_t splits, hipStream_t st, hipEvent_t t0, hipEvent_t t1) {
   switch (cfg) {
-    case kC128x128: return ot::launch_gemm_f32<2, 2, 4, 4, LA, LB, EPI, 16, ROLE>(g, splits, st);
-    case kC64x128: return ot::launch_gemm_f32<2, 2, 2, 4, LA, LB, EPI, 16, ROLE>(g, splits, st);
-    default: return ot::launch_gemm_f32<2, 2, 2, 2, LA, LB, EPI, 16, ROLE>(g, splits, st);
+    case kC128x128: return ot::launch_gemm_f32<2, 2, 4, 4, LA, LB, EPI, 16, ROLE>(g, splits, st, t0, t1);
+    case kC64x128: return ot::launch_gemm_f32<2, 2, 2, 4, LA, LB, EPI, 16, ROLE>(g, splits, st, t0, t1);
+    default: return ot::launch_gemm_f32<2, 2, 2, 2, LA, LB, EPI, 16, ROLE>(g, splits, st, t0, t1);
   }
 }
 
 template <Lay LA, Lay LB, int ROLE>
-hipError_t launch_epi(Epi epi, int cfg, const GemmArgs& g, int64_t splits, hipStream_t st) {
+hipError_t launch_epi(Epi epi, int cfg, const GemmArgs& g, int64_t splits, hipStream_t st, hipEvent_t t0 = nullptr,
+                      hipEvent_t t1 = nullptr) {
   switch (epi) {
-    case Epi::Store: return launch_cfg<LA, LB, Epi::Store, ROLE>(cfg, g, splits, st);
-    case Epi::Bias: return launch_cfg<LA, LB, Epi::Bias, ROLE>(cfg, g, splits, st);
-    case Epi::BiasRelu: return launch_cfg<LA, LB, Epi::BiasRelu, ROLE>(cfg, g, splits, st);
-    case Epi::Mse: return launch_cfg<LA, LB, Epi::Mse, ROLE>(cfg, g, splits, st);
-    case Epi::SplitK: return launch_cfg<LA, LB, Epi::SplitK, ROLE>(cfg, g, splits, st);
-    case Epi::Adam: return launch_cfg<LA, LB, Epi::Adam, ROLE>(cfg, g, splits, st);
-    default: return launch_cfg<LA, LB, Epi::Mask, ROLE>(cfg, g, splits, st);
+    case Epi::Store: return launch_cfg<LA, LB, Epi::Store, ROLE>(cfg, g, splits, st, t0, t1);
+    case Epi::Bias: return launch_cfg<LA, LB, Epi::Bias, ROLE>(cfg, g, splits, st, t0, t1);
+    case Epi::BiasRelu: return launch_cfg<LA, LB, Epi::BiasRelu, ROLE>(cfg, g, splits, st, t0, t1);
+    case Epi::Mse: return launch_cfg<LA, LB, Epi::Mse, ROLE>(cfg, g, splits, st, t0, t1);
+    case Epi::SplitK: return launch_cfg<LA, LB, Epi::SplitK, ROLE>(cfg, g, splits, st, t0, t1);
+    case Epi::Adam: return launch_cfg<LA, LB, Epi::Adam, ROLE>(cfg, g, splits, st, t0, t1);
+    default: return launch_cfg<LA, LB, Epi::Mask, ROLE>(cfg, g, splits, st, t0, t1);
   }
 }
 
@@ -679,10 +680,10 @@ int run_gemm(ot_surrogate* s, GemmArgs g, Epi epi, hipStream_t st, const char* w
   ot::PhaseTimer& tm = s->timer;
   if (p.splits == 1) {
     g.k_chunk = g.K;
-    if (ph_gemm >= 0) tm.mark(st, ph_gemm, 0);
-    hipError_t e = launch_epi<LA, LB, ROLE>(epi, p.cfg, g, 1, st);
+    hipEvent_t t0 = nullptr, t1 = nullptr;
+    if (ph_gemm >= 0) tm.kernel_events(ph_gemm, &t0, &t1);
+    hipError_t e = launch_epi<LA, LB, ROLE>(epi, p.cfg, g, 1, st, t0, t1);
     if (e != hipSuccess) return ot::set_error(OT_E_HIP, "launch of %s GEMM failed: %s", what, hipGetErrorString(e));
-    if (ph_gemm >= 0) tm.mark(st, ph_gemm, 1);
     return OT_OK;
   }
   const int64_t ldws = ot::round_up(g.N, 4);
@@ -695,10 +696,10 @@ int run_gemm(ot_surrogate* s, GemmArgs g, Epi epi, hipStream_t st, const char* w
   h.k_chunk = p.k_chunk;
   h.rowsum = g.rowsum ? s->rsws : nullptr;
   h.rowsum_stride = g.M;
-  if (ph_gemm >= 0) tm.mark(st, ph_gemm, 0);
-  hipError_t e = launch_epi<LA, LB, ROLE>(Epi::SplitK, p.cfg, h, p.splits, st);
+  hipEvent_t t0 = nullptr, t1 = nullptr;
+  if (ph_gemm >= 0) tm.kernel_events(ph_gemm, &t0, &t1);
+  hipError_t e = launch_epi<LA, LB, ROLE>(Epi::SplitK, p.cfg, h, p.splits, st, t0, t1);
   if (e != hipSuccess) return ot::set_error(OT_E_HIP, "launch of %s GEMM failed: %s", what, hipGetErrorString(e));
-  if (ph_gemm >= 0) tm.mark(st, ph_gemm, 1);
   if (ph_reduce >= 0) tm.mark(st, ph_reduce, 0);
   const int64_t work = g.M * ot::ceil_div(g.N, 4);
   if (epi == Epi::Adam) {
@@ -841,15 +842,16 @@ Plan make_plan_b(int64_t M, int64_t N, int64_t K, bool allow_split, bool pipe_ok
 }
 
 template <LayB LA, LayB LB, EpiB E>
-hipError_t launch_cfg_b(int cfg, const GemmBArgs& g, int64_t splits, hipStream_t st) {
+hipError_t launch_cfg_b(int cfg, const GemmBArgs& g, int64_t splits, hipStream_t st, hipEvent_t t0 = nullptr,
+                        hipEvent_t t1 = nullptr) {
   // 256 x 128 tile, k tile 32, 3 stages, 2 blocks per CU
   if constexpr (E == EpiB::AdamF32) {
     // fused Adam: 128 x 256 tiles, so each tile row of the updated parameters is 1 KB contiguous
-    if (cfg == kBPipe) return ot::launch_gemm_bf16_pipe<128, 256, kPipeBK, 3, 2, LA, LB, E>(g, splits, st);
+    if (cfg == kBPipe) return ot::launch_gemm_bf16_pipe<128, 256, kPipeBK, 3, 2, LA, LB, E>(g, splits, st, t0, t1);
   }
-  if (cfg == kBPipe) return ot::launch_gemm_bf16_pipe<256, 128, kPipeBK, 3, 2, LA, LB, E>(g, splits, st);
-  if (cfg == kB128) return ot::launch_gemm_bf16<4, 4, LA, LB, E, kBK>(g, splits, st);
-  return ot::launch_gemm_bf16<2, 2, LA, LB, E, kBK>(g, splits, st);
+  if (cfg == kBPipe) return ot::launch_gemm_bf16_pipe<256, 128, kPipeBK, 3, 2, LA, LB, E>(g, splits, st, t0, t1);
+  if (cfg == kB128) return ot::launch_gemm_bf16<4, 4, LA, LB, E, kBK>(g, splits, st, t0, t1);
+  return ot::launch_gemm_bf16<2, 2, LA, LB, E, kBK>(g, splits, st, t0, t1);
 }
 
 // C = epi(A B) on bf16 operands; split-K runs write fp32 partials and a
@@ -862,10 +864,10 @@ int run_gemm_b(ot_surrogate* s, GemmBArgs g, hipStream_t st, const char* what, b
   ot::PhaseTimer& tm = s->timer;
   if (p.splits == 1) {
     g.k_chunk = p.k_chunk;
-    if (ph_gemm >= 0) tm.mark(st, ph_gemm, 0);
-    hipError_t e = launch_cfg_b<LA, LB, E>(p.cfg, g, 1, st);
+    hipEvent_t t0 = nullptr, t1 = nullptr;
+    if (ph_gemm >= 0) tm.kernel_events(ph_gemm, &t0, &t1);
+    hipError_t e = launch_cfg_b<LA, LB, E>(p.cfg, g, 1, st, t0, t1);
     if (e != hipSuccess) return ot::set_error(OT_E_HIP, "launch of %s GEMM failed: %s", what, hipGetErrorString(e));
-    if (ph_gemm >= 0) tm.mark(st, ph_gemm, 1);
     return OT_OK;
   }
   if constexpr (E == EpiB::MseBf || E == EpiB::AdamF32) {
@@ -881,10 +883,10 @@ int run_gemm_b(ot_surrogate* s, GemmBArgs g, hipStream_t st, const char* what, b
     h.k_chunk = p.k_chunk;
     h.rowsum = g.rowsum ? s->rsws : nullptr;
     h.rowsum_stride = g.M;
-    if (ph_gemm >= 0) tm.mark(st, ph_gemm, 0);
-    hipError_t e = launch_cfg_b<LA, LB, EpiB::SplitK>(p.cfg, h, p.splits, st);
+    hipEvent_t t0 = nullptr, t1 = nullptr;
+    if (ph_gemm >= 0) tm.kernel_events(ph_gemm, &t0, &t1);
+    hipError_t e = launch_cfg_b<LA, LB, EpiB::SplitK>(p.cfg, h, p.splits, st, t0, t1);
     if (e != hipSuccess) return ot::set_error(OT_E_HIP, "launch of %s GEMM failed: %s", what, hipGetErrorString(e));
-    if (ph_gemm >= 0) tm.mark(st, ph_gemm, 1);
     if (ph_reduce >= 0) tm.mark(st, ph_reduce, 0);
     const int64_t work = g.M * ot::ceil_div(g.N, 4);
     if constexpr (E == EpiB::StoreF32 || E == EpiB::BiasF32) {
