@@ -82,6 +82,9 @@ def parse_args():
                    help="no GPU work: turn the counter CSVs of two rocprofv3 --pmc runs (FETCH_SIZE, WRITE_SIZE) of "
                         "this workload with --pmc-calibration into per-launch HBM bytes of its dominant kernel "
                         "(--kernel) and record them in profiles/hbm_traffic.json")
+    p.add_argument("--library-reference", action="store_true",
+                   help="instead of the benchmark: time torch's own GEMMs (hipBLASLt / rocBLAS) on this workload's "
+                        "three output-layer products, without epilogues, for comparison with the library's kernels")
     p.add_argument("--kernel", default=None, help="roofline kernel label for --summarize-pmc")
     p.add_argument("--pmc-command", default="", help="command line recorded with --summarize-pmc")
     return p.parse_args()
@@ -784,6 +787,53 @@ def run_stress(args):
     return line
 
 
+def run_library_reference(w) -> dict:
+    """torch.matmul on the output layer's forward (A W^T), weight-gradient
+    (dY^T A) and input-gradient (dY W) shapes of workload w, in its GEMM
+    precision, plus a square 8192 product; plain products without the fused
+    epilogues of the library's kernels.  Comparison only."""
+    import torch
+    dev = torch.device("cuda:0")
+    dt = torch.float32 if w.precision == "fp32" else torch.bfloat16
+    torch.backends.cuda.matmul.allow_tf32 = False
+    B, H, D = w.batch, w.widths[-2], w.widths[-1]
+    g = torch.Generator(device=dev)
+    g.manual_seed(0)
+    A = torch.randn(B, H, device=dev, generator=g).to(dt)
+    W = torch.randn(D, H, device=dev, generator=g).to(dt)
+    dY = torch.randn(B, D, device=dev, generator=g).to(dt)
+
+    def avg_us(fn, it):
+        for _ in range(3):
+            fn()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record()
+        for _ in range(it):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) * 1e3 / it
+
+    it = 50 if w.precision == "fp32" else 10
+    flop = 2.0 * B * H * D
+    peak = PEAK_FP32_MFMA if w.precision == "fp32" else PEAK_BF16_MFMA
+    out = {}
+    for name, fn in (("fwd_output", lambda: torch.matmul(A, W.t())), ("wgrad_output", lambda: torch.matmul(dY.t(), A)),
+                     ("igrad_output", lambda: torch.matmul(dY, W))):
+        us = avg_us(fn, it)
+        out[name] = {"avg_us": round(us, 2), "tflops": round(flop / us / 1e6, 1), "frac": round(flop / us * 1e6 / peak, 4)}
+    del A, W, dY
+    torch.cuda.empty_cache()
+    X = torch.randn(8192, 8192, device=dev, generator=g).to(dt)
+    us = avg_us(lambda: torch.matmul(X, X), 10)
+    out["square_8192"] = {"avg_us": round(us, 1), "tflops": round(2 * 8192 ** 3 / us / 1e6, 1),
+                          "frac": round(2 * 8192 ** 3 / us * 1e6 / peak, 4)}
+    return {"metric": "torch GEMM reference on the output-layer shapes (no epilogues)", "workload": w.name,
+            "dtype": "f32" if w.precision == "fp32" else "bf16", "shapes": {"B": B, "H": H, "D": D},
+            "torch": torch.__version__, "gemms": out}
+
+
 def main():
     args = parse_args()
     if args.summarize_pmc:
@@ -808,7 +858,9 @@ def main():
                   file=sys.stderr)
             sys.exit(2)
         w = configs.ALL[args.config]
-        if args.policy_comparison:
+        if args.library_reference:
+            line = run_library_reference(w)
+        elif args.policy_comparison:
             if w.fields != "ftcs":
                 print("--policy-comparison streams an FTCS ensemble (tiny-16x16 or heat-100x100)", file=sys.stderr)
                 sys.exit(2)

@@ -5,7 +5,7 @@ import os
 import numpy as np
 
 from fixtures import configs, heat
-from oracle import runner
+from oracle import mlp, runner
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 
@@ -64,6 +64,8 @@ def test_schedule_validation_and_repetition_histogram():
     assert tr["lrs"][:21] == [1e-3] * 20 + [5e-4] and tr["lrs"][40:] == [2.5e-4] * 60
     assert sorted(tr["val_losses"]) == [25, 50, 75, 100]
     assert all(np.isfinite(v) and v > 0 for v in tr["val_losses"].values())
+    # validation follows the step it is taken at: the last one sees the final parameters
+    assert tr["val_losses"][100] == mlp.mse(mlp.predict(tr["params"], iv), fv)
     res = tr["reservoir"]
     h = runner.repetition_histogram(res, 256)
     assert h.sum() == res.total_put                                  # every sample that entered, once
