@@ -103,7 +103,7 @@ __device__ __forceinline__ int64_t xcd_remap_b(int64_t p, int64_t g) {
 // is staged, so their latency overlaps the staging.  MseBf also accumulates the
 // loss partial of the block and, per m-tile, the column sums of the rounded dY
 // (the output bias gradient) when g.colsum is set (finish()).
-template <int WN, EpiB EPI>
+template <int WN, EpiB EPI, int NW = 4>
 struct BEpi {
   static constexpr int EP = WN + 4;
   static constexpr int CG = WN / 4;               // column groups of 4
@@ -282,9 +282,9 @@ struct BEpi {
     }
   }
 
-  // Block-level reductions of MseBf (loss partial, per-m-tile column sums).
-  // Waves with the same wn share a column half; wave w's column half is w / 2.
-  // s_red: >= 8 doubles + 4 * WN floats of LDS.
+  // Block-level reductions of MseBf (loss partial, per-m-tile column sums)
+  // over the block's NW wavefronts.  Waves 2 j and 2 j + 1 share column group
+  // j.  s_red: >= 8 doubles + NW * WN floats of LDS.
   __device__ __forceinline__ void finish(const GemmBArgs& g, int64_t tm, double* s_red) {
     if constexpr (EPI == EpiB::MseBf) {
       const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
@@ -294,12 +294,15 @@ struct BEpi {
       // lanes, then the two wavefronts of each column half
       for (int c = 0; c < 4; ++c)
         for (int off = CG; off < 64; off <<= 1) csum[c] += __shfl_xor(csum[c], off, 64);
-      float* xs = reinterpret_cast<float*>(s_red + 8);   // 4 waves x WN floats
+      float* xs = reinterpret_cast<float*>(s_red + 8);   // NW waves x WN floats
       if (rl == 0)
         for (int c = 0; c < 4; ++c) xs[wid * WN + 4 * cg + c] = csum[c];
       lds_barrier();
-      if (tid == 0)
-        g.loss_partials[blockIdx.y * gridDim.x + blockIdx.x] = ((s_red[0] + s_red[1]) + s_red[2]) + s_red[3];
+      if (tid == 0) {
+        double t = s_red[0];
+        for (int w = 1; w < NW; ++w) t += s_red[w];
+        g.loss_partials[blockIdx.y * gridDim.x + blockIdx.x] = t;
+      }
       if (g.colsum && (wid & 1) == 0 && rl == 0) {
         for (int c = 0; c < 4; ++c) {
           const int64_t n = col + c;
@@ -558,10 +561,11 @@ __device__ __forceinline__ int kswz(int row) {
 }
 __device__ __forceinline__ int mswz(int row) { return 4 * (row & 3); }
 
-template <int BM, int BN, int BK, int S, int OCC, LayB LA, LayB LB, EpiB EPI>
-__global__ __launch_bounds__(256, OCC) void gemm_bf16_pipe_kernel(GemmBArgs g) {
-  constexpr int NT = 256;
-  constexpr int WM = BM / 2, WN = BN / 2, FM = WM / 32, FN = WN / 32;
+template <int BM, int BN, int BK, int S, int OCC, LayB LA, LayB LB, EpiB EPI, int NWN = 2>
+__global__ __launch_bounds__(128 * NWN, OCC) void gemm_bf16_pipe_kernel(GemmBArgs g) {
+  constexpr int NW = 2 * NWN, NT = 64 * NW;                       // 2 x NWN wavefronts
+  constexpr int WM = BM / 2, WN = BN / NWN, FM = WM / 32, FN = WN / 32;
+  static_assert(NW <= 8, "loss partial slots");
   constexpr int KC = BK / 8;                                      // chunks per KMajor row
   constexpr int A_CH = BM * BK / 8, B_CH = BN * BK / 8;          // 16-byte chunks per stage
   constexpr int LA_N = A_CH / NT, LB_N = B_CH / NT;               // loads per thread per k tile
@@ -571,12 +575,12 @@ __global__ __launch_bounds__(256, OCC) void gemm_bf16_pipe_kernel(GemmBArgs g) {
   constexpr int STAGE_BYTES = (A_CH + B_CH) * 16;
   // epilogue chunk: CH_F fragments (32 CH_F rows) of each wave staged at once
   constexpr int EP = WN + 4;
-  constexpr int CH_F = (4 * FM * 32 * EP * 4 <= S * STAGE_BYTES)         ? FM
-                       : (4 * (FM / 2) * 32 * EP * 4 <= S * STAGE_BYTES) ? FM / 2
-                                                                        : FM / 4;
-  static_assert(CH_F >= 1 && 4 * CH_F * 32 * EP * 4 <= S * STAGE_BYTES, "epilogue staging");
+  constexpr int CH_F = (NW * FM * 32 * EP * 4 <= S * STAGE_BYTES)         ? FM
+                       : (NW * (FM / 2) * 32 * EP * 4 <= S * STAGE_BYTES) ? FM / 2
+                                                                         : FM / 4;
+  static_assert(CH_F >= 1 && NW * CH_F * 32 * EP * 4 <= S * STAGE_BYTES, "epilogue staging");
   __shared__ __attribute__((aligned(16))) unsigned char smem[S * STAGE_BYTES];
-  __shared__ double s_red[8 + 2 * WN];
+  __shared__ double s_red[8 + NW * WN / 2];
 
   const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
   const int wm = wid % 2, wn = wid / 2;
@@ -595,11 +599,11 @@ __global__ __launch_bounds__(256, OCC) void gemm_bf16_pipe_kernel(GemmBArgs g) {
   const int nk = (int)((kend - kbeg) / BK);
 
   // Per-thread global offsets (elements) of its chunks, relative to the k tile start.
-  // Chunk ci = (i * 4 + wid) * 64 + lane of operand X sits in LDS slot ci.
+  // Chunk ci = (i * NW + wid) * 64 + lane of operand X sits in LDS slot ci.
   int64_t a_off[LA_N], b_off[LB_N];
 #pragma unroll
   for (int i = 0; i < LA_N; ++i) {
-    const int ci = (i * 4 + wid) * 64 + lane;
+    const int ci = (i * NW + wid) * 64 + lane;
     if constexpr (LA == LayB::KMajor) {
       const int row = ci / KC, pc = ci % KC, lc = pc ^ kswz<BK>(row);
       const int64_t m = min(m0 + row, g.M - 1);
@@ -613,7 +617,7 @@ __global__ __launch_bounds__(256, OCC) void gemm_bf16_pipe_kernel(GemmBArgs g) {
   }
 #pragma unroll
   for (int i = 0; i < LB_N; ++i) {
-    const int ci = (i * 4 + wid) * 64 + lane;
+    const int ci = (i * NW + wid) * 64 + lane;
     if constexpr (LB == LayB::KMajor) {
       const int row = ci / KC, pc = ci % KC, lc = pc ^ kswz<BK>(row);
       const int64_t n = min(n0 + row, g.N - 1);
@@ -634,12 +638,12 @@ __global__ __launch_bounds__(256, OCC) void gemm_bf16_pipe_kernel(GemmBArgs g) {
 #pragma unroll
     for (int i = 0; i < LA_N; ++i) {
       const uint16_t* src = (LA == LayB::KMajor) ? g.A + a_off[i] + k0 : g.A + a_off[i] + k0 * g.lda;
-      __builtin_amdgcn_global_load_lds(src, (lds_void*)(sa + (i * 4 + wid) * 1024), 16, 0, 0);
+      __builtin_amdgcn_global_load_lds(src, (lds_void*)(sa + (i * NW + wid) * 1024), 16, 0, 0);
     }
 #pragma unroll
     for (int i = 0; i < LB_N; ++i) {
       const uint16_t* src = (LB == LayB::KMajor) ? g.B + b_off[i] + k0 : g.B + b_off[i] + k0 * g.ldb;
-      __builtin_amdgcn_global_load_lds(src, (lds_void*)(sb + (i * 4 + wid) * 1024), 16, 0, 0);
+      __builtin_amdgcn_global_load_lds(src, (lds_void*)(sb + (i * NW + wid) * 1024), 16, 0, 0);
     }
   };
 
@@ -649,19 +653,50 @@ __global__ __launch_bounds__(256, OCC) void gemm_bf16_pipe_kernel(GemmBArgs g) {
   // KMajor: lane l reads row base + l%32, 8 k-values at 16 kk + 8 (l/32).
   // MNMajor: 16-lane group q covers columns base + 16 (q%2) .. +15 and k rows
   // 16 kk + 8 (q/2) .. +7, read as two transposed 4-row blocks.
+  //
+  // The reads are inline assembly: the compiler cannot tell a read of one
+  // stage from the direct global -> LDS loads still in flight into the
+  // others, and before the first read of every k tile it would wait for all
+  // of them (vmcnt(0)), which removes the prefetch.  A stage is known to be
+  // complete from tile_ready(); frag_wait() waits for the reads themselves.
+  typedef int i32x4 __attribute__((ext_vector_type(4)));
+  typedef int i32x2 __attribute__((ext_vector_type(2)));
+  typedef __attribute__((address_space(3))) const unsigned char lds_u8;
+  auto lds_addr = [](const unsigned char* p) -> uint32_t { return (uint32_t)(size_t)(lds_u8*)p; };
   auto frag = [&](const unsigned char* st, int cpr, bool kmajor, int base, int kk) -> bf16x8 {
     if (kmajor) {
       const int row = base + lane % 32;
       const int lc = 2 * kk + lane / 32;
-      return *reinterpret_cast<const bf16x8*>(st + (row * KC + (lc ^ kswz<BK>(row))) * 16);
+      i32x4 v;
+      asm volatile("ds_read_b128 %0, %1" : "=v"(v) : "v"(lds_addr(st + (row * KC + (lc ^ kswz<BK>(row))) * 16)));
+      return __builtin_bit_cast(bf16x8, v);
     }
     const int c = lane % 16, q = lane / 16;
     const int col = base + 16 * (q & 1) + 4 * (c % 4);
     const int r0 = 16 * kk + 8 * (q >> 1) + c / 4, r1 = r0 + 4;
     const int ch = col / 8, half = (col / 4) & 1;
-    bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(st + (r0 * cpr + (ch ^ mswz(r0))) * 16 + half * 8));
-    bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(st + (r1 * cpr + (ch ^ mswz(r1))) * 16 + half * 8));
-    return bf16x8{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+    i32x2 lo, hi;
+    asm volatile("ds_read_b64_tr_b16 %0, %1" : "=v"(lo) : "v"(lds_addr(st + (r0 * cpr + (ch ^ mswz(r0))) * 16 + half * 8)));
+    asm volatile("ds_read_b64_tr_b16 %0, %1" : "=v"(hi) : "v"(lds_addr(st + (r1 * cpr + (ch ^ mswz(r1))) * 16 + half * 8)));
+    const bf16x4 l = __builtin_bit_cast(bf16x4, lo), h = __builtin_bit_cast(bf16x4, hi);
+    return bf16x8{l[0], l[1], l[2], l[3], h[0], h[1], h[2], h[3]};
+  };
+  // Wait for the outstanding fragment reads; each fragment passes through an
+  // empty statement after the wait, so no use of it can move above the wait.
+  auto frag_wait = [](bf16x8 (&af)[FM], bf16x8 (&bf)[FN]) {
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+#pragma unroll
+    for (int f = 0; f < FM; ++f) {
+      i32x4 v = __builtin_bit_cast(i32x4, af[f]);
+      asm volatile("" : "+v"(v));
+      af[f] = __builtin_bit_cast(bf16x8, v);
+    }
+#pragma unroll
+    for (int h = 0; h < FN; ++h) {
+      i32x4 v = __builtin_bit_cast(i32x4, bf[h]);
+      asm volatile("" : "+v"(v));
+      bf[h] = __builtin_bit_cast(bf16x8, v);
+    }
   };
 
   f32x16 acc[FM][FN];
@@ -673,31 +708,66 @@ __global__ __launch_bounds__(256, OCC) void gemm_bf16_pipe_kernel(GemmBArgs g) {
   // vmcnt wait with lgkm / exp counters left unconstrained (gfx9 encoding)
 #define OT_WAIT_VM(n) __builtin_amdgcn_s_waitcnt(((n) & 0xF) | (0x7 << 4) | (0xF << 8) | (((n) >> 4) << 14))
   constexpr int PER_TILE = LA_N + LB_N;
+  constexpr int KK = BK / 16;
   static_assert((S - 2) * PER_TILE <= 63, "vmcnt range");
-  for (int s = 0; s < S - 1; ++s)
-    if (s < nk) issue(s, s);
-  for (int kt = 0; kt < nk; ++kt) {
-    // tile kt's loads are the oldest outstanding ones; up to S - 2 later tiles may stay in flight
-    const int ahead = min(S - 2, nk - 1 - kt);
+  // Wait until tile t's loads (the oldest of tiles t .. min(t + S - 2, nk - 1)
+  // still outstanding) have landed, then make every wave's loads visible.
+  auto tile_ready = [&](int t) {
+    const int ahead = min(S - 2, nk - 1 - t);
     if (ahead >= 2) OT_WAIT_VM(2 * PER_TILE);
     else if (ahead == 1) OT_WAIT_VM(PER_TILE);
     else OT_WAIT_VM(0);
     lds_barrier();
-    if (kt + S - 1 < nk) issue(kt + S - 1, (kt + S - 1) % S);
-    const unsigned char* sa = smem + (kt % S) * STAGE_BYTES;
+  };
+  auto load_frags = [&](int t, int kk, bf16x8 (&af)[FM], bf16x8 (&bf)[FN]) {
+    const unsigned char* sa = smem + (t % S) * STAGE_BYTES;
     const unsigned char* sb = sa + A_CH * 16;
 #pragma unroll
-    for (int kk = 0; kk < BK / 16; ++kk) {
-      bf16x8 af[FM], bfr[FN];
+    for (int f = 0; f < FM; ++f) af[f] = frag(sa, BM / 8, LA == LayB::KMajor, WM * wm + 32 * f, kk);
 #pragma unroll
-      for (int f = 0; f < FM; ++f) af[f] = frag(sa, BM / 8, LA == LayB::KMajor, WM * wm + 32 * f, kk);
+    for (int h = 0; h < FN; ++h) bf[h] = frag(sb, BN / 8, LB == LayB::KMajor, WN * wn + 32 * h, kk);
+  };
+
+  // Software pipeline: the fragments of the next 16-deep step are read while
+  // the MFMAs of the current one run, across k tiles too.  The barrier that
+  // publishes tile t + 1 comes before the MFMAs of tile t's last step, whose
+  // fragments are already in registers, so stage t % S is free after it and
+  // receives tile t + S.
+  for (int s = 0; s < S - 1; ++s)
+    if (s < nk) issue(s, s);
+  bf16x8 af[FM], bfr[FN];
+  if (nk > 0) {
+    tile_ready(0);
+    if (S - 1 < nk) issue(S - 1, S - 1);
+    load_frags(0, 0, af, bfr);
+    frag_wait(af, bfr);
+  }
+  for (int kt = 0; kt < nk; ++kt) {
 #pragma unroll
-      for (int h = 0; h < FN; ++h) bfr[h] = frag(sb, BN / 8, LB == LayB::KMajor, WN * wn + 32 * h, kk);
+    for (int kk = 0; kk < KK; ++kk) {
+      bf16x8 an[FM], bn[FN];
+      const bool more = (kk + 1 < KK) || (kt + 1 < nk);
+      if (kk + 1 < KK) {
+        load_frags(kt, kk + 1, an, bn);
+      } else if (kt + 1 < nk) {
+        tile_ready(kt + 1);
+        if (kt + S < nk) issue(kt + S, kt % S);
+        load_frags(kt + 1, 0, an, bn);
+      }
+      __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
       for (int f = 0; f < FM; ++f)
 #pragma unroll
         for (int h = 0; h < FN; ++h)
           acc[f][h] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[f], bfr[h], acc[f][h], 0, 0, 0);
+      __builtin_amdgcn_sched_barrier(0);
+      if (more) {
+        frag_wait(an, bn);
+#pragma unroll
+        for (int f = 0; f < FM; ++f) af[f] = an[f];
+#pragma unroll
+        for (int h = 0; h < FN; ++h) bfr[h] = bn[h];
+      }
     }
   }
 #undef OT_WAIT_VM
@@ -706,7 +776,7 @@ __global__ __launch_bounds__(256, OCC) void gemm_bf16_pipe_kernel(GemmBArgs g) {
   // Epilogue in FM / CH_F chunks of 32 CH_F rows per wave, staged through the
   // (now free) stage buffers.
   float* ep = reinterpret_cast<float*>(smem) + wid * (CH_F * 32 * EP);
-  BEpi<WN, EPI> e(g, n0 + WN * wn);
+  BEpi<WN, EPI, NW> e(g, n0 + WN * wn);
 #pragma unroll
   for (int c0 = 0; c0 < FM; c0 += CH_F) {
     e.template rows<CH_F * 32>(g, ep, m0 + WM * wm + 32 * c0, split, [&] {
@@ -724,12 +794,12 @@ __global__ __launch_bounds__(256, OCC) void gemm_bf16_pipe_kernel(GemmBArgs g) {
   e.finish(g, tm, s_red);
 }
 
-template <int BM, int BN, int BK, int S, int OCC, LayB LA, LayB LB, EpiB EPI>
+template <int BM, int BN, int BK, int S, int OCC, LayB LA, LayB LB, EpiB EPI, int NWN = 2>
 hipError_t launch_gemm_bf16_pipe(const GemmBArgs& g, int64_t splits, hipStream_t stream, hipEvent_t t0 = nullptr,
                                  hipEvent_t t1 = nullptr) {
   const int64_t tiles = ((g.M + BM - 1) / BM) * ((g.N + BN - 1) / BN);
-  hipExtLaunchKernelGGL((gemm_bf16_pipe_kernel<BM, BN, BK, S, OCC, LA, LB, EPI>),
-                        dim3((unsigned)tiles, (unsigned)splits), dim3(256), 0, stream, t0, t1, 0, g);
+  hipExtLaunchKernelGGL((gemm_bf16_pipe_kernel<BM, BN, BK, S, OCC, LA, LB, EPI, NWN>),
+                        dim3((unsigned)tiles, (unsigned)splits), dim3(128 * NWN), 0, stream, t0, t1, 0, g);
   return hipGetLastError();
 }
 

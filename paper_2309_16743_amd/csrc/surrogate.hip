@@ -792,24 +792,39 @@ using ot::LayB;
 // bf16 tiles: the pipelined 256 x 128 kernel (k tile 32, direct-to-LDS loads,
 // two blocks per CU) for large products; 128 x 128 (4 x 4 fragments per wave)
 // and 64 x 64 (2 x 2) with a k tile of 32 otherwise.
-enum CfgB : int { kB128 = 0, kB64 = 1, kBPipe = 2 };
+enum CfgB : int { kB128 = 0, kB64 = 1, kBPipe = 2, kBPipeW = 3 };
 constexpr int kBK = 32;
 constexpr int kPipeBK = 32;
 
 int64_t tiles_b(int cfg, int64_t M, int64_t N) {
   if (cfg == kBPipe) return ot::gemm_bf16_pipe_tiles<256, 128>(M, N);
+  if (cfg == kBPipeW) return ot::gemm_bf16_pipe_tiles<256, 256>(M, N);
   return cfg == kB128 ? ot::gemm_bf16_tiles<4, 4>(M, N) : ot::gemm_bf16_tiles<2, 2>(M, N);
 }
 
 // The pipelined kernel when k is a multiple of its 32-deep k tile and its
-// tiles give about one block per CU or more (long k ranges split until about
-// four blocks per CU, keeping at least 32 k tiles per split); else 128 x 128
-// tiles when they give about two blocks per CU; long k ranges are split over
-// 128 x 128 tiles, shorter ones over 64 x 64.
+// tiles give about one block per CU or more: products split over long k
+// ranges take 256 x 256 tiles of eight wavefronts (one block per CU; splits
+// until about two blocks per CU, keeping at least 32 k tiles per split),
+// the others 256 x 128 tiles of four wavefronts (two blocks per CU).  Else
+// 128 x 128 tiles when they give about two blocks per CU; long k ranges are
+// split over 128 x 128 tiles, shorter ones over 64 x 64.
 // pipe_ok: the pipelined kernel may be used (it has no row-sum output).
 Plan make_plan_b(int64_t M, int64_t N, int64_t K, bool allow_split, bool pipe_ok = true) {
   constexpr int64_t kCUs = 256;
   Plan p;
+  if (pipe_ok && allow_split && K % kPipeBK == 0 && M >= 256 && N >= 256) {
+    const int64_t t = tiles_b(kBPipeW, M, N);
+    int64_t sp = 1;
+    while (t * sp < 2 * kCUs - 32 && K / (2 * sp) >= 32 * kPipeBK) sp *= 2;
+    if (sp > 1 && t * sp >= kCUs - 16) {
+      p.cfg = kBPipeW;
+      p.k_chunk = ot::round_up(ot::ceil_div(K, sp), kPipeBK);
+      p.splits = std::max<int64_t>(1, ot::ceil_div(K, p.k_chunk));
+      p.blocks = t * p.splits;
+      return p;
+    }
+  }
   if (pipe_ok && K % kPipeBK == 0 && M >= 256 && N >= 128) {
     const int64_t t = tiles_b(kBPipe, M, N);
     int64_t sp = 1;
@@ -850,6 +865,10 @@ hipError_t launch_cfg_b(int cfg, const GemmBArgs& g, int64_t splits, hipStream_t
     if (cfg == kBPipe) return ot::launch_gemm_bf16_pipe<128, 256, kPipeBK, 3, 2, LA, LB, E>(g, splits, st, t0, t1);
   }
   if (cfg == kBPipe) return ot::launch_gemm_bf16_pipe<256, 128, kPipeBK, 3, 2, LA, LB, E>(g, splits, st, t0, t1);
+  if constexpr (E != EpiB::AdamF32 && E != EpiB::MseBf) {
+    // split products: 256 x 256 tile, eight wavefronts, 4 stages (128 KB of LDS), one block per CU
+    if (cfg == kBPipeW) return ot::launch_gemm_bf16_pipe<256, 256, kPipeBK, 4, 1, LA, LB, E, 4>(g, splits, st, t0, t1);
+  }
   if (cfg == kB128) return ot::launch_gemm_bf16<4, 4, LA, LB, E, kBK>(g, splits, st, t0, t1);
   return ot::launch_gemm_bf16<2, 2, LA, LB, E, kBK>(g, splits, st, t0, t1);
 }
