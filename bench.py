@@ -47,6 +47,7 @@ import sys
 import time
 
 import numpy as np
+from typing import Optional
 
 ROOT = os.path.dirname(os.path.abspath(__file__))
 if ROOT not in sys.path:
@@ -67,6 +68,9 @@ def parse_args():
     p.add_argument("--policy-comparison", action="store_true",
                    help="instead of the throughput benchmark: stream the heat-100x100 ensemble once through the "
                         "Reservoir, FIRO and FIFO buffers and report train steps and samples/s per buffer")
+    p.add_argument("--gathered-targets", action="store_true",
+                   help="gather the batch's field rows into a batch buffer before the train step (default: the "
+                        "output layer's forward reads them in place from the reservoir through the drawn slots)")
     p.add_argument("--one-stream", action="store_true",
                    help="run the reservoir and the train step on one stream (default: the reservoir's put, draw "
                         "and gather of the next batch overlap the current train step on a second stream)")
@@ -237,8 +241,15 @@ def fused_adam_bytes(w) -> float:
     return per * out_weights(w) + e * w.batch * (w.widths[-1] + w.widths[-2])
 
 
-def gather_bytes(w) -> float:
-    return 2.0 * w.batch * (w.widths[-1] + w.widths[0]) * 4
+GATHERED_TARGETS = False         # --gathered-targets
+
+
+def gather_bytes(w, targets: Optional[bool] = None) -> float:
+    """Bytes the batch gather moves (read from the slab, written to the batch
+    buffer): the input rows, plus the field rows when the targets are gathered
+    too (--gathered-targets); otherwise the forward reads them in place."""
+    targets = GATHERED_TARGETS if targets is None else targets
+    return 2.0 * w.batch * ((w.widths[-1] if targets else 0) + w.widths[0]) * 4
 
 
 def put_bytes(w) -> float:
@@ -488,7 +499,8 @@ def run_heat(args, w):
     stream = torch.cuda.Stream(device=dev)
     with torch.cuda.stream(stream):
         tr = OnlineTrainer(w.widths, w.batch, w.capacity, w.threshold, w.wave, w.tau, inputs_d, fields_d,
-                           w.reservoir_seed, w.init_seed, lr=w.lr, stream=stream, overlap=not args.one_stream)
+                           w.reservoir_seed, w.init_seed, lr=w.lr, stream=stream, overlap=not args.one_stream,
+                           fused_targets=not args.gathered_targets)
         for _ in range(w.n_chunks):             # stream the ensemble once (untimed)
             tr.iterate()
         for _ in range(warmup):
@@ -501,7 +513,9 @@ def run_heat(args, w):
     config = {"workload": w.name, "fields": f"FTCS heat {w.grid}x{w.grid}, {w.n_sims} sims x {w.tau} steps",
               "widths": list(w.widths), "batch": w.batch, "capacity": w.capacity, "threshold": w.threshold,
               "put_rows_per_step": w.wave, "precision": w.precision,
-              "reservoir_stream": "one stream" if args.one_stream else "overlapped with the train step"}
+              "reservoir_stream": "one stream" if args.one_stream else "overlapped with the train step",
+              "targets": "gathered into a batch buffer" if args.gathered_targets
+              else "read in place from the reservoir by the forward (inputs gathered)"}
     line = result_line(w, args, K, warmup, r, config)
     line["instrumentation"] = instr
     tr.close()
@@ -598,7 +612,7 @@ def run_field(args, w):
         tr = OnlineTrainer(w.widths, w.batch, w.capacity, w.threshold, w.wave, w.tau, None, None,
                            w.reservoir_seed, w.init_seed, precision=OT_BF16, lr=w.lr, stream=stream,
                            chunk_fn=lambda c: (pool_x[c % pool], pool_u[c % pool]), n_chunks=1 << 40, device=dev,
-                           overlap=not args.one_stream)
+                           overlap=not args.one_stream, fused_targets=not args.gathered_targets)
         fx = torch.empty(w.wave, 8, device=dev)[:, :6]
         fu = torch.empty(w.wave, D, device=dev)
         t_fill = time.perf_counter()
@@ -621,7 +635,9 @@ def run_field(args, w):
     config = {"workload": w.name, "fields": f"sine-mode {n}x{n}, {w.n_sims} sims x {w.tau} steps",
               "widths": list(w.widths), "batch": w.batch, "capacity": w.capacity, "threshold": w.threshold,
               "put_rows_per_step": w.wave, "precision": w.precision,
-              "reservoir_stream": "one stream" if args.one_stream else "overlapped with the train step"}
+              "reservoir_stream": "one stream" if args.one_stream else "overlapped with the train step",
+              "targets": "gathered into a batch buffer" if args.gathered_targets
+              else "read in place from the reservoir by the forward (inputs gathered)"}
     line = result_line(w, args, K, warmup, r, config)
     tr.close()
     torch.cuda.empty_cache()
@@ -835,7 +851,9 @@ def run_library_reference(w) -> dict:
 
 
 def main():
+    global GATHERED_TARGETS
     args = parse_args()
+    GATHERED_TARGETS = args.gathered_targets
     if args.summarize_pmc:
         if not args.kernel:
             raise SystemExit("--summarize-pmc needs --kernel")

@@ -143,6 +143,16 @@ int reservoir_sample_batch(ot_reservoir* r, int64_t b, void* stream, int32_t* sl
  * already over. */
 int reservoir_end_reception(ot_reservoir* r);
 
+/* Device addresses of the slabs, for callers that read stored rows in place
+ * (a train step whose targets are the u rows of the drawn slots): the row of
+ * slot k is x + k * ldx (x_dim fp32) and u + k * ldu (u_dim fp32); the
+ * addresses stay valid until reservoir_destroy.  A slot's rows change only
+ * when a put stores a sample into it, so a caller that reads rows must order
+ * the puts that follow its reads after them (for instance by passing puts a
+ * stream that has waited for an event recorded after the reads).  Each
+ * pointer argument is nullable.  Errors: OT_E_INVAL (NULL reservoir). */
+int reservoir_slab(ot_reservoir* r, const float** x, int64_t* ldx, const float** u, int64_t* ldu);
+
 /* Synchronise with the reservoir's queued work and read its counters. */
 int reservoir_stats(ot_reservoir* r, ot_reservoir_stats* out);
 

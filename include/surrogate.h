@@ -93,6 +93,22 @@ int surrogate_set_lr(ot_surrogate* s, float lr);
 int surrogate_train_step(ot_surrogate* s, const float* x, int64_t ldx, const float* u,
                          int64_t ldu, int64_t b, void* stream, float* loss_dev);
 
+/* The same train step with the targets read in place from a larger array
+ * (the reservoir's u slab, reservoir_slab), so that a batch needs no copy of
+ * its field rows: target row j is u + rows[j] * ldu.  rows: device int32[b]
+ * (4-byte aligned), each in [0, n_rows); an index outside that range is
+ * clamped into it on the device (a wrong row is read, never memory outside
+ * the array).  x, ldx, b, stream, loss_dev as for surrogate_train_step.
+ * targets_read: hipEvent_t recorded on `stream` as soon as every target row
+ * has been read (after the output layer's forward), so that a producer may
+ * overwrite the rows after it while the rest of the step runs; nullable.
+ * Results are those of surrogate_train_step on the gathered rows, bit for bit.
+ * Errors: OT_E_INVAL (as surrogate_train_step; NULL or misaligned rows,
+ * n_rows < 1), OT_E_NOMEM, OT_E_HIP. */
+int surrogate_train_step_rows(ot_surrogate* s, const float* x, int64_t ldx, const float* u,
+                              int64_t ldu, const int32_t* rows, int64_t n_rows, int64_t b, void* stream,
+                              float* loss_dev, void* targets_read);
+
 /* Surrogate prediction Y = f_theta(x) (Eq. 1's u_X^t estimate) for n rows.
  * x: n rows at stride ldx; y: n rows of widths[L] fp32 at stride ldy
  * (multiple of 4).  Errors: OT_E_INVAL, OT_E_NOMEM, OT_E_HIP. */

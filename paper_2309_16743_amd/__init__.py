@@ -108,6 +108,14 @@ class Reservoir:
     def end_reception(self) -> None:
         check("reservoir_end_reception", load().reservoir_end_reception(self._h))
 
+    def slab(self):
+        """(x address, ldx, u address, ldu) of the slabs: slot k's rows start at
+        x + 4 ldx k and u + 4 ldu k (bytes)."""
+        x, u = C.c_void_p(), C.c_void_p()
+        ldx, ldu = C.c_int64(), C.c_int64()
+        check("reservoir_slab", load().reservoir_slab(self._h, C.byref(x), C.byref(ldx), C.byref(u), C.byref(ldu)))
+        return x.value, ldx.value, u.value, ldu.value
+
     def stats(self) -> dict:
         s = _abi.ReservoirStats()
         check("reservoir_stats", load().reservoir_stats(self._h, C.byref(s)))
@@ -224,6 +232,24 @@ class Surrogate:
         up, ldu = _rows(u, "u")
         check("surrogate_train_step", load().surrogate_train_step(
             self._h, xp, ldx, up, ldu, u.shape[0], _stream_handle(stream), _dev_ptr(loss)))
+
+    def train_step_rows(self, x, u_addr: int, ldu: int, rows, n_rows: int, stream=None, loss=None,
+                        targets_read=None) -> None:
+        """Train step whose target row j is the fp32 row at device address
+        u_addr + 4 ldu rows[j] (rows: int32 device tensor of x's row count,
+        each in [0, n_rows)); targets_read: torch.cuda.Event recorded once the
+        targets have been read."""
+        import torch
+        xp, ldx = _rows(x, "x")
+        if rows.dtype != torch.int32 or rows.dim() != 1 or rows.shape[0] != x.shape[0] or not rows.is_contiguous():
+            raise ValueError("rows: expected a contiguous int32 tensor with one index per row of x")
+        ev = None
+        if targets_read is not None:
+            targets_read.record(torch.cuda.current_stream() if stream is None else stream)   # create the event
+            ev = targets_read.cuda_event
+        check("surrogate_train_step_rows", load().surrogate_train_step_rows(
+            self._h, xp, ldx, u_addr, ldu, _dev_ptr(rows), n_rows, x.shape[0], _stream_handle(stream),
+            _dev_ptr(loss), ev))
 
     def predict(self, x, y, stream=None) -> None:
         xp, ldx = _rows(x, "x")

@@ -53,6 +53,7 @@ SIGNATURES = {
     "reservoir_sample_batch": (C.c_int, [vp, i64, vp, vp, vp, i64, vp, i64, C.POINTER(i64), C.POINTER(u64)]),
     "reservoir_end_reception": (C.c_int, [vp]),
     "reservoir_stats": (C.c_int, [vp, C.POINTER(ReservoirStats)]),
+    "reservoir_slab": (C.c_int, [vp, vp, vp, vp, vp]),
     "reservoir_read_meta": (C.c_int, [vp, vp, vp, vp]),
     "reservoir_read_rows": (C.c_int, [vp, vp, i64, vp, vp]),
     "reservoir_timing_begin": (C.c_int, [vp, u32, i64]),
@@ -72,6 +73,7 @@ SIGNATURES = {
     "surrogate_get_adam_state": (C.c_int, [vp, i32, vp, vp, vp, vp, C.POINTER(i64)]),
     "surrogate_set_lr": (C.c_int, [vp, f32]),
     "surrogate_train_step": (C.c_int, [vp, vp, i64, vp, i64, i64, vp, vp]),
+    "surrogate_train_step_rows": (C.c_int, [vp, vp, i64, vp, i64, vp, i64, i64, vp, vp, vp]),
     "surrogate_predict": (C.c_int, [vp, vp, i64, i64, vp, i64, vp]),
     "surrogate_timing_begin": (C.c_int, [vp, u32, i64]),
     "surrogate_timing_end": (C.c_int, [vp, vp, vp]),

@@ -75,6 +75,8 @@ struct GemmBArgs {
   const float* bias;
   const float* target;      // MseBf (fp32)
   int64_t ldt;
+  const int32_t* target_rows;  // MseBf (nullable): output row m compares with target row target_rows[m],
+  int64_t target_rows_max;     //   clamped to [0, target_rows_max]
   float scale;
   double* loss_partials;
   const uint16_t* mask;     // MaskBf (bf16 activations)
@@ -103,6 +105,18 @@ __device__ __forceinline__ int64_t xcd_remap_b(int64_t p, int64_t g) {
 // is staged, so their latency overlaps the staging.  MseBf also accumulates the
 // loss partial of the block and, per m-tile, the column sums of the rounded dY
 // (the output bias gradient) when g.colsum is set (finish()).
+// Indexed targets (MseBf with target_rows): a block reads the row indices of
+// its tile into LDS at its start, so that their latency is hidden behind the
+// main loop, whose barriers publish them.
+template <int BM>
+__device__ __forceinline__ void load_target_rows(const GemmBArgs& g, int64_t m0, int32_t* s_trow) {
+  if (g.target_rows)
+    for (int i = threadIdx.x; i < BM; i += blockDim.x) {
+      const int64_t m = min(m0 + i, g.M - 1);
+      s_trow[i] = (int32_t)min(max((int64_t)g.target_rows[m], (int64_t)0), g.target_rows_max);
+    }
+}
+
 template <int WN, EpiB EPI, int NW = 4>
 struct BEpi {
   static constexpr int EP = WN + 4;
@@ -111,6 +125,11 @@ struct BEpi {
   int cg, rl;
   int64_t col;
   bool cfull;
+  const int32_t* s_trow = nullptr;   // MseBf with target_rows: row indices of the tile (LDS), row tile_m0 first
+  int64_t tile_m0 = 0;
+  __device__ __forceinline__ int64_t trow(const GemmBArgs& g, int64_t m) const {
+    return g.target_rows ? (int64_t)s_trow[m - tile_m0] : m;
+  }
   float lsum = 0.f;
   float csum[4] = {0.f, 0.f, 0.f, 0.f};
   float bias4[4] = {0.f, 0.f, 0.f, 0.f};
@@ -150,7 +169,7 @@ struct BEpi {
         for (int i = 0; i < NP; ++i) {
           const int64_t m = min(m0 + rl + RPP * i, g.M - 1);
           if constexpr (EPI == EpiB::MseBf) {
-            pre[i] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(g.target + m * g.ldt + col));
+            pre[i] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(g.target + trow(g, m) * g.ldt + col));
           } else {
             const u16x4 h = *reinterpret_cast<const u16x4*>(g.mask + m * g.ldmask + col);
             pre[i] = f32x4{bf2f(h[0]), bf2f(h[1]), bf2f(h[2]), bf2f(h[3])};
@@ -161,7 +180,7 @@ struct BEpi {
         for (int i = 0; i < NP; ++i) {
           const int64_t m = min(m0 + rl + RPP * i, g.M - 1);
           for (int c = 0; c < 4; ++c) {
-            if constexpr (EPI == EpiB::MseBf) pre[i][c] = (col + c < g.N) ? g.target[m * g.ldt + col + c] : 0.f;
+            if constexpr (EPI == EpiB::MseBf) pre[i][c] = (col + c < g.N) ? g.target[trow(g, m) * g.ldt + col + c] : 0.f;
             else pre[i][c] = (col + c < g.N) ? bf2f(g.mask[m * g.ldmask + col + c]) : 0.f;
           }
         }
@@ -332,6 +351,7 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmBArgs g) {
   constexpr int LDS_BYTES = TILE_BYTES > EPI_BYTES ? TILE_BYTES : EPI_BYTES;
   __shared__ __attribute__((aligned(16))) unsigned char smem[LDS_BYTES];
   __shared__ double s_red[8 + 2 * WN];   // loss partials + column-sum exchange (4 waves x WN floats)
+  __shared__ int32_t s_trow[EPI == EpiB::MseBf ? BM : 1];
   uint16_t* const tiles16 = reinterpret_cast<uint16_t*>(smem);
   auto As = [&](int buf) { return tiles16 + buf * A_ELEMS; };
   auto Bs = [&](int buf) { return tiles16 + 2 * A_ELEMS + buf * B_ELEMS; };
@@ -347,6 +367,7 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmBArgs g) {
   const int64_t kend = (kbeg + g.k_chunk < g.K) ? kbeg + g.k_chunk : g.K;
   const int64_t nk = (kend > kbeg) ? (kend - kbeg + BK - 1) / BK : 0;
   const bool interior = (m0 + BM <= g.M) && (n0 + BN <= g.N);
+  if constexpr (EPI == EpiB::MseBf) load_target_rows<BM>(g, m0, s_trow);
 
   u32x4 ra[VA], rb[VB];
 
@@ -491,6 +512,11 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmBArgs g) {
   float* ep = reinterpret_cast<float*>(smem) + wid * (WM * EP);
   // the main loop ended with a barrier, so the tile buffers are free
   BEpi<WN, EPI> e(g, n0 + WN * wn);
+  if constexpr (EPI == EpiB::MseBf) {
+    if (nk == 0) lds_barrier();        // publishes s_trow (the main loop's barriers do otherwise)
+    e.s_trow = s_trow;
+    e.tile_m0 = m0;
+  }
   e.template rows<WM>(g, ep, m0 + WM * wm, split, [&] {
 #pragma unroll
     for (int f = 0; f < FM; ++f)
@@ -581,6 +607,7 @@ __global__ __launch_bounds__(128 * NWN, OCC) void gemm_bf16_pipe_kernel(GemmBArg
   static_assert(CH_F >= 1 && NW * CH_F * 32 * EP * 4 <= S * STAGE_BYTES, "epilogue staging");
   __shared__ __attribute__((aligned(16))) unsigned char smem[S * STAGE_BYTES];
   __shared__ double s_red[8 + NW * WN / 2];
+  __shared__ int32_t s_trow[EPI == EpiB::MseBf ? BM : 1];
 
   const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
   const int wm = wid % 2, wn = wid / 2;
@@ -597,6 +624,7 @@ __global__ __launch_bounds__(128 * NWN, OCC) void gemm_bf16_pipe_kernel(GemmBArg
   const int64_t kbeg = split * g.k_chunk;
   const int64_t kend = (kbeg + g.k_chunk < g.K) ? kbeg + g.k_chunk : g.K;
   const int nk = (int)((kend - kbeg) / BK);
+  if constexpr (EPI == EpiB::MseBf) load_target_rows<BM>(g, m0, s_trow);
 
   // Per-thread global offsets (elements) of its chunks, relative to the k tile start.
   // Chunk ci = (i * NW + wid) * 64 + lane of operand X sits in LDS slot ci.
@@ -777,6 +805,11 @@ __global__ __launch_bounds__(128 * NWN, OCC) void gemm_bf16_pipe_kernel(GemmBArg
   // (now free) stage buffers.
   float* ep = reinterpret_cast<float*>(smem) + wid * (CH_F * 32 * EP);
   BEpi<WN, EPI, NW> e(g, n0 + WN * wn);
+  if constexpr (EPI == EpiB::MseBf) {
+    if (nk == 0) lds_barrier();        // publishes s_trow (the main loop's barriers do otherwise)
+    e.s_trow = s_trow;
+    e.tile_m0 = m0;
+  }
 #pragma unroll
   for (int c0 = 0; c0 < FM; c0 += CH_F) {
     e.template rows<CH_F * 32>(g, ep, m0 + WM * wm + 32 * c0, split, [&] {

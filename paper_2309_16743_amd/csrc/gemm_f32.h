@@ -53,6 +53,8 @@ struct GemmArgs {
   const float* bias;        // Bias, BiasRelu, Mse
   const float* target;      // Mse
   int64_t ldt;
+  const int32_t* target_rows;  // Mse (nullable): output row m compares with target row target_rows[m],
+  int64_t target_rows_max;     //   clamped to [0, target_rows_max]
   float scale;              // Mse
   double* loss_partials;    // Mse: one per block
   const float* mask;        // Mask
@@ -103,6 +105,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_f32_kernel(GemmArgs g) {
   __shared__ __attribute__((aligned(16))) float As[2][BK * LDA_S];
   __shared__ __attribute__((aligned(16))) float Bs[2][BK * LDB_S];
   __shared__ double s_red[NT / 64];
+  __shared__ int32_t s_trow[EPI == Epi::Mse ? BM : 1];   // target rows of the tile (Mse with target_rows)
 
   const int tid = threadIdx.x;
   const int lane = tid & 63, wid = tid >> 6;
@@ -258,6 +261,14 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_f32_kernel(GemmArgs g) {
   const int b_off = 16 * FN * wn + FN * (lane % 16);
   const int kl = lane / 16;
 
+  // Indexed targets: the tile's row indices are read now, so that their
+  // latency is hidden behind the main loop (its barriers publish them).
+  if constexpr (EPI == Epi::Mse) {
+    if (g.target_rows && tid < BM) {
+      const int64_t m = min(m0 + tid, g.M - 1);
+      s_trow[tid] = (int32_t)min(max((int64_t)g.target_rows[m], (int64_t)0), g.target_rows_max);
+    }
+  }
   if (nk > 0) {
     load_tile(kbeg);
     store_tile(0);
@@ -300,6 +311,9 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_f32_kernel(GemmArgs g) {
     }
     if (kt + 1 < nk) store_tile(buf ^ 1);
     __syncthreads();
+  }
+  if constexpr (EPI == Epi::Mse) {
+    if (nk == 0) __syncthreads();       // publishes s_trow (the main loop's barriers do otherwise)
   }
   if (do_rowsum && tid < BM && m0 + tid < g.M) g.rowsum[split * g.rowsum_stride + m0 + tid] = rsum;
 
@@ -350,7 +364,8 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_f32_kernel(GemmArgs g) {
       }
       if constexpr (EPI == Epi::Mse) {
         float tv[FN];
-        load_cols(g.target + m * g.ldt + col_base, tv);
+        const int64_t tr = g.target_rows ? (int64_t)s_trow[m - m0] : m;
+        load_cols(g.target + tr * g.ldt + col_base, tv);
 #pragma unroll
         for (int h = 0; h < FN; ++h) {
           const float rr = (col_base + h < g.N) ? v[h] - tv[h] : 0.f;

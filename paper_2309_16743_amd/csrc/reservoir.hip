@@ -791,6 +791,16 @@ extern "C" int reservoir_end_reception(ot_reservoir* r) {
   return OT_OK;
 }
 
+extern "C" int reservoir_slab(ot_reservoir* r, const float** x, int64_t* ldx, const float** u, int64_t* ldu) {
+  ot::clear_error();
+  OT_REQUIRE(r != nullptr, "reservoir_slab: NULL reservoir");
+  if (x) *x = r->xslab;
+  if (ldx) *ldx = r->ldxs;
+  if (u) *u = r->uslab;
+  if (ldu) *ldu = r->ldus;
+  return OT_OK;
+}
+
 extern "C" int reservoir_stats(ot_reservoir* r, ot_reservoir_stats* out) {
   ot::clear_error();
   OT_REQUIRE(r != nullptr && out != nullptr, "reservoir_stats: NULL argument");

@@ -965,8 +965,8 @@ int forward_hidden_bf16(ot_surrogate* s, const float* X, int64_t ldx, int64_t ro
 // into dz16[L], per-block loss partials; with bias_grad also the output bias
 // gradient (column sums of the rounded dY) into grads.  *n_partials receives
 // the number of loss partials.
-int forward_mse_bf16(ot_surrogate* s, const float* x, int64_t ldx, const float* u, int64_t ldu, int64_t b,
-                     hipStream_t st, bool bias_grad, int64_t* n_partials) {
+int forward_mse_bf16(ot_surrogate* s, const float* x, int64_t ldx, const float* u, int64_t ldu, const int32_t* u_rows,
+                     int64_t u_rows_max, int64_t b, hipStream_t st, bool bias_grad, int64_t* n_partials) {
   const int L = s->L;
   const int64_t D = s->widths[L];
   ot::PhaseTimer& tm = s->timer;
@@ -988,6 +988,8 @@ int forward_mse_bf16(ot_surrogate* s, const float* x, int64_t ldx, const float* 
   g.bias = s->params + lo.b_off;
   g.target = u;
   g.ldt = ldu;
+  g.target_rows = u_rows;
+  g.target_rows_max = u_rows_max;
   g.scale = (float)(2.0 / ((double)b * (double)D));
   g.loss_partials = s->loss_partials;
   if (bias_grad) {
@@ -1014,12 +1016,13 @@ int forward_mse_bf16(ot_surrogate* s, const float* x, int64_t ldx, const float* 
 
 // Forward, fused MSE and backward of the bf16 path (the loss is reduced and
 // Adam applied by the step's last pass); *n_partials: loss partials written.
-int train_step_bf16(ot_surrogate* s, const float* x, int64_t ldx, const float* u, int64_t ldu, int64_t b,
-                    hipStream_t st, int64_t* n_partials) {
+int train_step_bf16(ot_surrogate* s, const float* x, int64_t ldx, const float* u, int64_t ldu, const int32_t* u_rows,
+                    int64_t u_rows_max, int64_t b, hipStream_t st, hipEvent_t targets_read, int64_t* n_partials) {
   const int L = s->L;
   ot::PhaseTimer& tm = s->timer;
   int rc;
-  if ((rc = forward_mse_bf16(s, x, ldx, u, ldu, b, st, true, n_partials))) return rc;
+  if ((rc = forward_mse_bf16(s, x, ldx, u, ldu, u_rows, u_rows_max, b, st, true, n_partials))) return rc;
+  if (targets_read) OT_HIP(hipEventRecord(targets_read, st));
 
   for (int l = L; l >= 1; --l) {
     if (l == L - 1) tm.mark(st, OT_PH_BWD_HIDDEN, 0);
@@ -1331,8 +1334,9 @@ static int adam_step(ot_surrogate* s, hipStream_t st, const ot::AdamRest& r) {
 
 // fp32 forward of b rows and the output layer's fused bias + MSE epilogue:
 // dY = 2 (Y - U) / (B D) into dz[L], per-block loss partials.
-static int forward_mse_f32(ot_surrogate* s, const float* x, int64_t ldx, const float* u, int64_t ldu, int64_t b,
-                           hipStream_t st, int64_t* n_partials) {
+static int forward_mse_f32(ot_surrogate* s, const float* x, int64_t ldx, const float* u, int64_t ldu,
+                           const int32_t* u_rows, int64_t u_rows_max, int64_t b, hipStream_t st,
+                           int64_t* n_partials) {
   const int L = s->L;
   const int64_t D = s->widths[L];
   ot::PhaseTimer& tm = s->timer;
@@ -1354,6 +1358,8 @@ static int forward_mse_f32(ot_surrogate* s, const float* x, int64_t ldx, const f
   g.bias = s->params + lo.b_off;
   g.target = u;
   g.ldt = ldu;
+  g.target_rows = u_rows;
+  g.target_rows_max = u_rows_max;
   g.scale = (float)(2.0 / ((double)b * (double)D));
   g.loss_partials = s->loss_partials;
   *n_partials = make_plan(g.M, g.N, g.K, false).blocks;
@@ -1373,14 +1379,14 @@ static int check_batch(ot_surrogate* s, const float* x, int64_t ldx, const float
   return OT_OK;
 }
 
-extern "C" int surrogate_train_step(ot_surrogate* s, const float* x, int64_t ldx, const float* u, int64_t ldu,
-                                    int64_t b, void* stream, float* loss_dev) {
-  ot::clear_error();
-  OT_REQUIRE(s != nullptr, "surrogate_train_step: NULL surrogate");
-  OT_REQUIRE(b >= 1 && b <= (1LL << 20), "surrogate_train_step: b outside [1, 2^20]");
-  int rc = check_batch(s, x, ldx, u, ldu, "surrogate_train_step");
-  if (rc) return rc;
+// The train step.  u_rows (nullable): target row j is u + u_rows[j] * ldu
+// (indices clamped to [0, u_rows_max]); targets_read (nullable): recorded on
+// the stream once every target has been read.
+static int train_step(ot_surrogate* s, const float* x, int64_t ldx, const float* u, int64_t ldu,
+                      const int32_t* u_rows, int64_t u_rows_max, int64_t b, void* stream, float* loss_dev,
+                      hipEvent_t targets_read) {
   const int L = s->L;
+  int rc;
   const int64_t D = s->widths[L];
   if ((rc = ensure_workspace(s, b))) return rc;
   hipStream_t st = static_cast<hipStream_t>(stream);
@@ -1389,12 +1395,13 @@ extern "C" int surrogate_train_step(ot_surrogate* s, const float* x, int64_t ldx
   ot::PhaseTimer& tm = s->timer;
   int64_t n_partials = 0;
   if (s->precision == OT_BF16) {
-    if ((rc = train_step_bf16(s, x, ldx, u, ldu, b, st, &n_partials))) return rc;
+    if ((rc = train_step_bf16(s, x, ldx, u, ldu, u_rows, u_rows_max, b, st, targets_read, &n_partials))) return rc;
     rc = adam_step(s, st, make_rest(s, n_partials, b, loss_dev));
     tm.next_call();
     return rc;
   }
-  if ((rc = forward_mse_f32(s, x, ldx, u, ldu, b, st, &n_partials))) return rc;
+  if ((rc = forward_mse_f32(s, x, ldx, u, ldu, u_rows, u_rows_max, b, st, &n_partials))) return rc;
+  if (targets_read) OT_HIP(hipEventRecord(targets_read, st));
   const ot::AdamRest rest = make_rest(s, n_partials, b, loss_dev);
   bool rest_done = false;
 
@@ -1510,6 +1517,30 @@ extern "C" int surrogate_train_step(ot_surrogate* s, const float* x, int64_t ldx
   return rc;
 }
 
+extern "C" int surrogate_train_step(ot_surrogate* s, const float* x, int64_t ldx, const float* u, int64_t ldu,
+                                    int64_t b, void* stream, float* loss_dev) {
+  ot::clear_error();
+  OT_REQUIRE(s != nullptr, "surrogate_train_step: NULL surrogate");
+  OT_REQUIRE(b >= 1 && b <= (1LL << 20), "surrogate_train_step: b outside [1, 2^20]");
+  int rc = check_batch(s, x, ldx, u, ldu, "surrogate_train_step");
+  if (rc) return rc;
+  return train_step(s, x, ldx, u, ldu, nullptr, 0, b, stream, loss_dev, nullptr);
+}
+
+extern "C" int surrogate_train_step_rows(ot_surrogate* s, const float* x, int64_t ldx, const float* u, int64_t ldu,
+                                         const int32_t* rows, int64_t n_rows, int64_t b, void* stream,
+                                         float* loss_dev, void* targets_read) {
+  ot::clear_error();
+  OT_REQUIRE(s != nullptr, "surrogate_train_step_rows: NULL surrogate");
+  OT_REQUIRE(b >= 1 && b <= (1LL << 20), "surrogate_train_step_rows: b outside [1, 2^20]");
+  OT_REQUIRE(rows != nullptr && (reinterpret_cast<uintptr_t>(rows) & 3u) == 0,
+             "surrogate_train_step_rows: rows must be a 4-byte aligned device int32 array");
+  OT_REQUIRE(n_rows >= 1 && n_rows <= (1LL << 31), "surrogate_train_step_rows: n_rows outside [1, 2^31]");
+  int rc = check_batch(s, x, ldx, u, ldu, "surrogate_train_step_rows");
+  if (rc) return rc;
+  return train_step(s, x, ldx, u, ldu, rows, n_rows - 1, b, stream, loss_dev, static_cast<hipEvent_t>(targets_read));
+}
+
 extern "C" int surrogate_eval_loss(ot_surrogate* s, const float* x, int64_t ldx, const float* u, int64_t ldu,
                                    int64_t n, void* stream, float* loss_dev) {
   ot::clear_error();
@@ -1525,8 +1556,8 @@ extern "C" int surrogate_eval_loss(ot_surrogate* s, const float* x, int64_t ldx,
     const int64_t rows = std::min(chunk, n - r0);
     int64_t n_partials = 0;
     rc = (s->precision == OT_BF16)
-             ? forward_mse_bf16(s, x + r0 * ldx, ldx, u + r0 * ldu, ldu, rows, st, false, &n_partials)
-             : forward_mse_f32(s, x + r0 * ldx, ldx, u + r0 * ldu, ldu, rows, st, &n_partials);
+             ? forward_mse_bf16(s, x + r0 * ldx, ldx, u + r0 * ldu, ldu, nullptr, 0, rows, st, false, &n_partials)
+             : forward_mse_f32(s, x + r0 * ldx, ldx, u + r0 * ldu, ldu, nullptr, 0, rows, st, &n_partials);
     if (rc) return rc;
     hipLaunchKernelGGL(ot::loss_accumulate_kernel, dim3(1), dim3(256), 0, st, s->loss_partials, n_partials,
                        s->eval_acc, r0 == 0 ? 1 : 0, r0 + rows >= n ? 1 : 0, 1.0 / ((double)n * (double)D),

@@ -106,7 +106,8 @@ class OnlineTrainer:
                  stream: Optional[torch.cuda.Stream] = None, record_steps: int = 0,
                  chunk_fn: Optional[Callable] = None, n_chunks: int = 0, device=None, flags: int = 0,
                  overlap: bool = False, policy: int = OT_POLICY_RESERVOIR,
-                 lr_schedule: Optional[Callable[[int], float]] = None, reception_log: bool = False):
+                 lr_schedule: Optional[Callable[[int], float]] = None, reception_log: bool = False,
+                 fused_targets: bool = True):
         self.stream = stream if stream is not None else torch.cuda.current_stream()
         self.widths = tuple(widths)
         self.batch, self.wave, self.tau = batch, wave, tau
@@ -127,9 +128,20 @@ class OnlineTrainer:
                              policy=policy)
         self.sur = Surrogate(widths, precision=precision, lr=lr, seed=init_seed, max_batch=batch, flags=flags)
         nbuf = 2 if overlap else 1
+        # fused_targets: the train step reads the batch's field rows in place
+        # from the reservoir's slab through the drawn slots (only the input
+        # rows are gathered); a put then waits until the train step before it
+        # has read its targets (targets_read), since it may overwrite them
+        self.fused_targets = fused_targets
         self.xbufs = [torch.empty(batch, _round_up(x_dim, 4), device=dev)[:, :x_dim] for _ in range(nbuf)]
-        self.ubufs = [torch.empty(batch, _round_up(d, 4), device=dev)[:, :d] for _ in range(nbuf)]
-        self.xb, self.ub = self.xbufs[0], self.ubufs[0]
+        self.ubufs = [] if fused_targets else [torch.empty(batch, _round_up(d, 4), device=dev)[:, :d]
+                                               for _ in range(nbuf)]
+        self.slotbufs = [torch.empty(batch, dtype=torch.int32, device=dev) for _ in range(nbuf)]
+        self.xb = self.xbufs[0]
+        self.ub = None if fused_targets else self.ubufs[0]
+        _, _, self.u_slab, self.ldu_slab = self.res.slab()
+        self.targets_read = torch.cuda.Event()
+        self.targets_read_recorded = False
         self.ready = [torch.cuda.Event() for _ in range(nbuf)]      # gather into buffer j done
         self.released = [torch.cuda.Event() for _ in range(nbuf)]   # train step on buffer j done
         self.released_recorded = [False] * nbuf
@@ -138,7 +150,7 @@ class OnlineTrainer:
         # stream's kernels (used for breakdowns, not for throughput)
         self.serialize = False
         self._train_done = torch.cuda.Event() if overlap else None
-        self.slots = torch.empty(batch, dtype=torch.int32, device=dev)
+        self.slots = self.slotbufs[0]
         self.record_steps = record_steps
         self.slot_log = torch.empty((max(record_steps, 1), batch), dtype=torch.int32, device=dev)
         self.loss_log = torch.zeros(max(record_steps, 1), device=dev)
@@ -180,6 +192,8 @@ class OnlineTrainer:
         if self.overlap and self.serialize:
             self._train_done.record(self.stream)
             self.res_stream.wait_event(self._train_done)
+        if self.overlap and self.fused_targets and self.targets_read_recorded:
+            self.res_stream.wait_event(self.targets_read)     # the last train step has read its targets
         if self.log is None:
             self.res.put(x, u, stream=self.res_stream, accepted=self.accepted)
             return
@@ -205,14 +219,18 @@ class OnlineTrainer:
 
     def sample_and_train(self) -> bool:
         rec = self.steps_done < self.record_steps
-        slots = self.slot_log[self.steps_done] if rec else self.slots
         j = self.steps_done % len(self.xbufs)
-        xb, ub = self.xbufs[j], self.ubufs[j]
+        slots = self.slot_log[self.steps_done] if rec else self.slotbufs[j]
+        xb = self.xbufs[j]
+        ub = None if self.fused_targets else self.ubufs[j]
         if self.overlap and self.released_recorded[j]:
             self.res_stream.wait_event(self.released[j])    # the step two back has finished with buffer j
         st, n, _ = self.res.sample_batch(self.batch, slots, x_out=xb, u_out=ub, stream=self.res_stream)
         if st != OT_OK:
             return False
+        if n < self.batch:                                    # short last batch of a drain
+            xb, slots = xb[:n], slots[:n]
+            ub = None if ub is None else ub[:n]
         if self.overlap:
             self.ready[j].record(self.res_stream)
             self.stream.wait_event(self.ready[j])
@@ -222,7 +240,12 @@ class OnlineTrainer:
             if lr != self.lr:
                 self.sur.set_lr(lr)       # host-side rate, taken by the next enqueued step
                 self.lr = lr
-        self.sur.train_step(xb, ub, stream=self.stream, loss=loss)
+        if self.fused_targets:
+            self.sur.train_step_rows(xb, self.u_slab, self.ldu_slab, slots, self.res.capacity, stream=self.stream,
+                                     loss=loss, targets_read=self.targets_read if self.overlap else None)
+            self.targets_read_recorded = self.overlap
+        else:
+            self.sur.train_step(xb, ub, stream=self.stream, loss=loss)
         if self.overlap:
             self.released[j].record(self.stream)
             self.released_recorded[j] = True
@@ -281,6 +304,7 @@ class OnlineTrainer:
         self.chunk_cursor, self.steps_done, self.iteration = (int(v) for v in ckpt["loop"])
         self.lr = float(ckpt["lr"][0])
         self.released_recorded = [False] * len(self.released_recorded)
+        self.targets_read_recorded = False
         if self.log is not None:
             self.log = ReceptionLog(self.xb.device)
             self.log.received = {tuple(int(v) for v in k) for k in ckpt.get("received", np.zeros((0, 2)))}

@@ -278,3 +278,86 @@ def test_eval_loss(widths, n, bf16):
         W, b = s.get_params(l)
         assert np.array_equal(W, params[l][0].astype(np.float32))
     s.close()
+
+
+@pytest.mark.parametrize("widths,B,bf16", [((6, 256, 256, 10000), 1024, False), ((6, 100, 77, 1001), 50, False),
+                                           ((6, 512, 512, 20000), 512, True), ((6, 64, 64, 256), 32, True)])
+def test_train_step_rows_equals_gathered_rows(widths, B, bf16):
+    """surrogate_train_step_rows (targets read in place from a larger array
+    through row indices) against surrogate_train_step on the same rows
+    gathered: loss and every parameter bit for bit, two steps in a row; an
+    index past the array is clamped to its last row."""
+    from paper_2309_16743_amd import OT_BF16, OT_FP32, Surrogate
+    print(f"train_step_rows widths={widths} B={B} bf16={bf16}", flush=True)
+    rng = np.random.default_rng(B)
+    params, X, _ = problem(widths, B, seed=B + 1)
+    n_rows = 3 * B + 7
+    D = widths[-1]
+    ldu = (D + 63) // 64 * 64
+    slab = torch.from_numpy(rng.uniform(100, 500, (n_rows, ldu)).astype(np.float32)).to(DEV)
+    rows = rng.integers(0, n_rows, B).astype(np.int32)
+    rows[0] = n_rows - 1
+    prec = OT_BF16 if bf16 else OT_FP32
+    a = Surrogate(widths, precision=prec, max_batch=B, seed=0)
+    g = Surrogate(widths, precision=prec, max_batch=B, seed=0)
+    for l, (W, b) in enumerate(params):
+        a.set_params(l, W.astype(np.float32), b.astype(np.float32))
+        g.set_params(l, W.astype(np.float32), b.astype(np.float32))
+    Xd = padded_from(X)
+    rows_d = torch.from_numpy(rows).to(DEV)
+    gathered = torch.zeros(B, ldu, device=DEV)[:, :D]
+    gathered.copy_(slab[rows_d.long(), :D])
+    ev = torch.cuda.Event()
+    la, lg = torch.zeros(1, device=DEV), torch.zeros(1, device=DEV)
+    for _ in range(2):
+        a.train_step_rows(Xd, slab.data_ptr(), ldu, rows_d, n_rows, loss=la, targets_read=ev)
+        g.train_step(Xd, gathered, loss=lg)
+    torch.cuda.synchronize()
+    assert la.item() == lg.item()
+    for l in range(len(widths) - 1):
+        Wa, ba = a.get_params(l)
+        Wg, bg = g.get_params(l)
+        assert np.array_equal(Wa, Wg) and np.array_equal(ba, bg), l
+    # clamping: an index past the array reads its last row
+    bad = rows_d.clone()
+    bad[0] = n_rows + 1000
+    lc = torch.zeros(1, device=DEV)
+    c = Surrogate(widths, precision=prec, max_batch=B, seed=0)
+    for l, (W, b) in enumerate(params):
+        c.set_params(l, W.astype(np.float32), b.astype(np.float32))
+    c.train_step_rows(Xd, slab.data_ptr(), ldu, bad, n_rows, loss=lc)
+    d = Surrogate(widths, precision=prec, max_batch=B, seed=0)
+    for l, (W, b) in enumerate(params):
+        d.set_params(l, W.astype(np.float32), b.astype(np.float32))
+    ld = torch.zeros(1, device=DEV)
+    d.train_step_rows(Xd, slab.data_ptr(), ldu, rows_d, n_rows, loss=ld)
+    torch.cuda.synchronize()
+    assert lc.item() == ld.item()
+    for s in (a, g, c, d):
+        s.close()
+
+
+@pytest.mark.parametrize("overlap", [False, True])
+def test_tiny_workload_fused_and_gathered_targets_agree(overlap):
+    """The 16x16 schedule with the targets read in place from the reservoir
+    (the default) and with the batch's rows gathered first: the same slots,
+    losses and parameters bit for bit."""
+    from paper_2309_16743_amd.online import OnlineTrainer
+    w = configs.TINY
+    X = heat.sample_parameters(w.n_sims, w.data_seed)
+    inputs = torch.from_numpy(heat.inputs_for(X, w.tau)).to(DEV)
+    fields = torch.from_numpy(heat.heat_fields(X, w.grid, w.tau)).to(DEV)
+    out = []
+    for fused in (True, False):
+        tr = OnlineTrainer(w.widths, w.batch, w.capacity, w.threshold, w.wave, w.tau, inputs, fields,
+                           w.reservoir_seed, w.init_seed, lr=w.lr, record_steps=100, overlap=overlap,
+                           fused_targets=fused)
+        tr.run(100)
+        torch.cuda.synchronize()
+        out.append((tr.slot_log.cpu().numpy(), tr.loss_log.cpu().numpy(),
+                    [tr.sur.get_params(l) for l in range(3)]))
+        tr.close()
+    (sa, la, pa), (sg, lg, pg) = out
+    assert np.array_equal(sa, sg) and np.array_equal(la, lg)
+    for (Wa, ba), (Wg, bg) in zip(pa, pg):
+        assert np.array_equal(Wa, Wg) and np.array_equal(ba, bg)
