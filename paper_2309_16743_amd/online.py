@@ -142,6 +142,7 @@ class OnlineTrainer:
         _, _, self.u_slab, self.ldu_slab = self.res.slab()
         self.targets_read = torch.cuda.Event()
         self.targets_read_recorded = False
+        self._targets_waited = False
         self.ready = [torch.cuda.Event() for _ in range(nbuf)]      # gather into buffer j done
         self.released = [torch.cuda.Event() for _ in range(nbuf)]   # train step on buffer j done
         self.released_recorded = [False] * nbuf
@@ -192,8 +193,7 @@ class OnlineTrainer:
         if self.overlap and self.serialize:
             self._train_done.record(self.stream)
             self.res_stream.wait_event(self._train_done)
-        if self.overlap and self.fused_targets and self.targets_read_recorded:
-            self.res_stream.wait_event(self.targets_read)     # the last train step has read its targets
+        self._wait_targets_read()                 # a put may overwrite rows the last train step reads
         if self.log is None:
             self.res.put(x, u, stream=self.res_stream, accepted=self.accepted)
             return
@@ -217,14 +217,25 @@ class OnlineTrainer:
         st, _, _ = self.res.sample_batch(self.batch, self.slots, stream=self.res_stream)
         return st == OT_OK
 
+    def _wait_targets_read(self) -> None:
+        """Overlapped fused mode: order the reservoir stream after the last
+        train step's targets_read event (once per recording).  That event
+        follows, on the training stream, every earlier train step, so the
+        buffers of the step two back are free after it too."""
+        if self.overlap and self.fused_targets and self.targets_read_recorded and not self._targets_waited:
+            self.res_stream.wait_event(self.targets_read)
+            self._targets_waited = True
+
     def sample_and_train(self) -> bool:
         rec = self.steps_done < self.record_steps
         j = self.steps_done % len(self.xbufs)
         slots = self.slot_log[self.steps_done] if rec else self.slotbufs[j]
         xb = self.xbufs[j]
         ub = None if self.fused_targets else self.ubufs[j]
-        if self.overlap and self.released_recorded[j]:
-            self.res_stream.wait_event(self.released[j])    # the step two back has finished with buffer j
+        # the step two back has finished with buffer j
+        if self.overlap and not self.fused_targets and self.released_recorded[j]:
+            self.res_stream.wait_event(self.released[j])
+        self._wait_targets_read()
         st, n, _ = self.res.sample_batch(self.batch, slots, x_out=xb, u_out=ub, stream=self.res_stream)
         if st != OT_OK:
             return False
@@ -244,9 +255,10 @@ class OnlineTrainer:
             self.sur.train_step_rows(xb, self.u_slab, self.ldu_slab, slots, self.res.capacity, stream=self.stream,
                                      loss=loss, targets_read=self.targets_read if self.overlap else None)
             self.targets_read_recorded = self.overlap
+            self._targets_waited = False
         else:
             self.sur.train_step(xb, ub, stream=self.stream, loss=loss)
-        if self.overlap:
+        if self.overlap and not self.fused_targets:
             self.released[j].record(self.stream)
             self.released_recorded[j] = True
         self.steps_done += 1
