@@ -58,6 +58,7 @@ SHAPES = [
     ((6, 512, 512, 20000), 512),       # pipelined 256 x 128 kernel, the bf16 workloads' batch
     ((6, 512, 512, 30001), 320),       # pipelined kernel with ragged M and N (clamped edges)
     ((6, 1024, 1024, 69984), 512),     # split-K pipelined input gradient (63 splits, ragged last split)
+    ((6, 2048, 2048, 2048, 4096), 1024),   # the deep 1000x1000 net's hidden widths and batch
 ]
 
 
@@ -170,3 +171,32 @@ def test_full_width_output_rows_bf16():
     assert np.array_equal(Wf, W) and np.array_equal(bf, b)
     s.close()
     f.close()
+
+
+def test_full_width_targets_in_place_bf16():
+    """6-1024-1024-1,000,000 at batch 512 with the targets read in place from
+    a 600-row array through row indices (the benchmark's path): the same loss
+    and the same parameters, bit for bit, as the step on the gathered rows."""
+    from paper_2309_16743_amd import OT_BF16, Surrogate
+    widths, B, seed, n_rows = (6, 1024, 1024, 1_000_000), 512, 5, 600
+    rng = np.random.default_rng(12)
+    X = np.concatenate([rng.uniform(100, 500, (B, 5)), rng.uniform(0.01, 1.0, (B, 1))], axis=1).astype(np.float32)
+    slab = torch.empty(n_rows, widths[-1], device=DEV)
+    slab.uniform_(100, 500, generator=torch.Generator(device=DEV).manual_seed(3))
+    rows = torch.from_numpy(rng.integers(0, n_rows, B).astype(np.int32)).to(DEV)
+    a = Surrogate(widths, precision=OT_BF16, max_batch=B, seed=seed)
+    g = Surrogate(widths, precision=OT_BF16, max_batch=B, seed=seed)
+    Xd = padded_from(X)
+    la, lg = torch.zeros(1, device=DEV), torch.zeros(1, device=DEV)
+    a.train_step_rows(Xd, slab.data_ptr(), widths[-1], rows, n_rows, loss=la)
+    gathered = slab[rows.long()]
+    g.train_step(Xd, gathered, loss=lg)
+    torch.cuda.synchronize()
+    del gathered
+    assert la.item() == lg.item()
+    for l in range(3):
+        Wa, ba = a.get_params(l)
+        Wg, bg = g.get_params(l)
+        assert np.array_equal(Wa, Wg) and np.array_equal(ba, bg), l
+    a.close()
+    g.close()
