@@ -68,6 +68,9 @@ def parse_args():
     p.add_argument("--policy-comparison", action="store_true",
                    help="instead of the throughput benchmark: stream the heat-100x100 ensemble once through the "
                         "Reservoir, FIRO and FIFO buffers and report train steps and samples/s per buffer")
+    p.add_argument("--prefilled", action="store_true",
+                   help="no puts in the timed steps: draws and train steps on the reservoir as the setup left it "
+                        "(the paper's throughput with production suspended); default: one put per step")
     p.add_argument("--gathered-targets", action="store_true",
                    help="gather the batch's field rows into a batch buffer before the train step (default: the "
                         "output layer's forward reads them in place from the reservoir through the drawn slots)")
@@ -313,6 +316,47 @@ def roofline_entry(w, phase: str, avg_s: float) -> dict:
             "per_launch_bytes": work, "avg_us": round(avg_s * 1e6, 2)}
 
 
+def achievable_rates(precision: str) -> dict:
+    """Rates this GPU reaches outside the library, measured live for context:
+    a device-to-device copy of 1 GiB (read + write) and torch's GEMM on
+    8192 x 8192 x 8192 in the workload's precision."""
+    import torch
+    dev = torch.device("cuda:0")
+
+    def avg_ms(fn, it):
+        fn()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record()
+        for _ in range(it):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / it
+
+    a = torch.empty(CAL_FLOATS, device=dev)
+    b = torch.empty_like(a)
+    a.fill_(1.0)
+    copy_gbs = 2 * CAL_FLOATS * 4 / (avg_ms(lambda: b.copy_(a), 5) * 1e-3) / 1e9
+    del a, b
+    dt = torch.float32 if precision == "fp32" else torch.bfloat16
+    torch.backends.cuda.matmul.allow_tf32 = False
+    x = torch.ones(8192, 8192, device=dev, dtype=dt)
+    ms = avg_ms(lambda: torch.matmul(x, x), 3 if precision == "fp32" else 10)
+    del x
+    torch.cuda.empty_cache()
+    return {"hbm_copy_gbs": round(copy_gbs, 1), "gemm_tflops": round(2 * 8192 ** 3 / (ms * 1e-3) / 1e12, 1),
+            "gemm": f"torch.matmul 8192^3 {'fp32' if precision == 'fp32' else 'bf16'}"}
+
+
+def with_achievable(roof: dict, ach: dict) -> dict:
+    """Adds the fraction of the live-measured achievable rate of the same unit."""
+    ref = ach["hbm_copy_gbs"] if roof["unit"] == "GB/s" else ach["gemm_tflops"]
+    out = dict(roof)
+    out["frac_achievable"] = round(roof["achieved"] / ref, 4)
+    return out
+
+
 def cpu_baseline(w, inputs, fields, seconds: float) -> dict:
     """The fp64 oracle (put + draw + train step) on this host, bounded in time."""
     from oracle import mlp
@@ -425,8 +469,10 @@ def timed_region(tr, w, K, profile_steps, stream, wrap_put):
     else:
         dom_ms, dom_n = tr.sur.timing_end()[dom_phase]
         dom_avg_s = dom_ms / dom_n * 1e-3
+    achievable = achievable_rates(w.precision)      # after the timed region, which it does not disturb
     return dict(gpu_ms=gpu_ms, wall=wall, windows=windows, breakdown=breakdown, dom_phase=dom_phase,
-                dom_avg_s=dom_avg_s, gather_avg_s=g_ms / g_n * 1e-3, loss=float(tr.loss.item()))
+                achievable=achievable, dom_avg_s=dom_avg_s, gather_avg_s=g_ms / g_n * 1e-3,
+                loss=float(tr.loss.item()))
 
 
 def result_line(w, args, K, warmup, r, config: dict) -> dict:
@@ -438,7 +484,8 @@ def result_line(w, args, K, warmup, r, config: dict) -> dict:
         "warmup": warmup, "ms_per_step": round(r["gpu_ms"] / K, 4), "higher_is_better": True,
         "scaling": "weak", "vs_baseline": None, "dtype": "f32" if w.precision == "fp32" else "bf16",
         "data": "synthetic", "config": config,
-        "roofline": roofline_entry(w, r["dom_phase"], r["dom_avg_s"]),
+        "roofline": with_achievable(roofline_entry(w, r["dom_phase"], r["dom_avg_s"]), r["achievable"]),
+        "achievable": r["achievable"],
         "reservoir_gather": {"achieved": round(gather_rate / 1e9, 1), "unit": "GB/s",
                              "frac_hbm": round(gather_rate / PEAK_HBM, 4),
                              "avg_us": round(r["gather_avg_s"] * 1e6, 2)},
@@ -508,14 +555,15 @@ def run_heat(args, w):
         torch.cuda.synchronize()
         print(f"[bench] setup done: {tr.steps_done} train steps, reservoir {tr.res.stats()['n']} samples",
               file=sys.stderr, flush=True)
-        r = timed_region(tr, w, K, args.profile_steps or 200, stream, lambda: tr.put_next(wrap=True))
+        r = timed_region(tr, w, K, args.profile_steps or 200, stream, (lambda: None) if args.prefilled else (lambda: tr.put_next(wrap=True)))
         instr = instrumentation(tr, w, stream)
     config = {"workload": w.name, "fields": f"FTCS heat {w.grid}x{w.grid}, {w.n_sims} sims x {w.tau} steps",
               "widths": list(w.widths), "batch": w.batch, "capacity": w.capacity, "threshold": w.threshold,
               "put_rows_per_step": w.wave, "precision": w.precision,
               "reservoir_stream": "one stream" if args.one_stream else "overlapped with the train step",
               "targets": "gathered into a batch buffer" if args.gathered_targets
-              else "read in place from the reservoir by the forward (inputs gathered)"}
+              else "read in place from the reservoir by the forward (inputs gathered)",
+              "timed_puts": "none (pre-filled reservoir)" if args.prefilled else "one per step"}
     line = result_line(w, args, K, warmup, r, config)
     line["instrumentation"] = instr
     tr.close()
@@ -631,13 +679,14 @@ def run_field(args, w):
         print(f"[bench] filled {n_stored} samples ({n_stored * D * 4 / 1e9:.0f} GB) in "
               f"{time.perf_counter() - t_fill:.1f} s; {tr.steps_done} warm-up steps",
               file=sys.stderr, flush=True)
-        r = timed_region(tr, w, K, args.profile_steps or 20, stream, lambda: tr.put_next(wrap=True))
+        r = timed_region(tr, w, K, args.profile_steps or 20, stream, (lambda: None) if args.prefilled else (lambda: tr.put_next(wrap=True)))
     config = {"workload": w.name, "fields": f"sine-mode {n}x{n}, {w.n_sims} sims x {w.tau} steps",
               "widths": list(w.widths), "batch": w.batch, "capacity": w.capacity, "threshold": w.threshold,
               "put_rows_per_step": w.wave, "precision": w.precision,
               "reservoir_stream": "one stream" if args.one_stream else "overlapped with the train step",
               "targets": "gathered into a batch buffer" if args.gathered_targets
-              else "read in place from the reservoir by the forward (inputs gathered)"}
+              else "read in place from the reservoir by the forward (inputs gathered)",
+              "timed_puts": "none (pre-filled reservoir)" if args.prefilled else "one per step"}
     line = result_line(w, args, K, warmup, r, config)
     tr.close()
     torch.cuda.empty_cache()
@@ -765,6 +814,7 @@ def run_stress(args):
     g_rate = B * row_bytes / g_avg
     put_rate = rows_in * row_bytes / (c_ms * 1e-3)
     dom = "gather" if g_ms >= c_ms else "put_copy"
+    ach = achievable_rates("fp32")
     if dom == "gather":
         roof = {"bound": "hbm", "kernel": "gather_kernel", "achieved": round(g_rate / 1e9, 1), "peak": PEAK_HBM / 1e9,
                 "unit": "GB/s", "frac": round(g_rate / PEAK_HBM, 4), "traffic": traffic_for(w.name, "gather_kernel"),
@@ -782,7 +832,8 @@ def run_stress(args):
         "config": {"workload": w.name, "row_floats": D, "capacity": w.capacity, "threshold": w.threshold,
                    "producer_streams": P, "chunk": k, "batch": B,
                    "rows": "hash rows (value = hash of the row key, exact in fp32)"},
-        "roofline": roof,
+        "roofline": with_achievable(roof, ach),
+        "achievable": ach,
         "put": {"achieved": round(put_rate / 1e9, 1), "unit": "GB/s", "frac_hbm": round(put_rate / PEAK_HBM, 4),
                 "rows_accepted": rows_in, "rows_offered": k * K, "copy_ms": round(c_ms, 3)},
         "gather": {"achieved": round(g_rate / 1e9, 1), "unit": "GB/s", "frac_hbm": round(g_rate / PEAK_HBM, 4),
