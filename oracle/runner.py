@@ -8,6 +8,9 @@ B and, if the buffer answered with a batch, runs one train step (forward, MSE,
 backward, Adam).  The GPU path is driven by the same loop, so both see the
 same ticket sequence.
 
+run_to_drain() streams the whole schedule through any of the three buffers
+and then drains it after the end of reception.
+
 Training instrumentation of Sec. 4.4-4.5, optional:
   * learning-rate schedule: the rate starts at lr0 and is halved every
     `every_samples` trained samples down to a floor lr_min (the paper halves
@@ -44,6 +47,41 @@ def repetition_histogram(res, length: int) -> np.ndarray:
     for s in res.occ:
         h[min(int(res.seen_count[s]), length - 1)] += 1
     return h
+
+
+def run_to_drain(w: Workload, inputs: np.ndarray, fields: np.ndarray, buffer) -> Dict:
+    """The whole production schedule through `buffer` (a Reservoir, FIFOBuffer
+    or FIROBuffer built by the caller), then the end of reception and the
+    drain (Sec. 3.2.3): iteration i puts chunk i and trains on a batch when the
+    buffer yields one; after the last chunk, end_reception and train on every
+    batch the buffer yields until it answers EMPTY (the last one may be short).
+    Returns the trace (losses, slots, batch sizes, final parameters)."""
+    params = init_params(w.widths, w.init_seed)
+    opt = Adam(lr=w.lr)
+    trace = dict(losses=[], slots=[], sizes=[])
+
+    def train(xb, ub, slots):
+        nonlocal params
+        loss, grads = loss_and_grads(params, xb, ub)
+        params = opt.step(params, grads)
+        trace["losses"].append(loss)
+        trace["slots"].append(np.array(slots, dtype=np.int64))
+        trace["sizes"].append(len(slots))
+
+    for chunk in range(w.n_chunks):
+        xs, us = chunk_arrays(w, inputs, fields, chunk)
+        buffer.put(xs, us)
+        st, slots, xb, ub, _ = buffer.sample_batch(w.batch)
+        if st == OK:
+            train(xb, ub, slots)
+    buffer.end_reception()
+    while True:
+        st, slots, xb, ub, _ = buffer.sample_batch(w.batch)
+        if st != OK:
+            break
+        train(xb, ub, slots)
+    trace["params"] = params
+    return trace
 
 
 def chunk_arrays(w: Workload, inputs: np.ndarray, fields: np.ndarray, chunk: int):

@@ -361,3 +361,46 @@ def test_tiny_workload_fused_and_gathered_targets_agree(overlap):
     assert np.array_equal(sa, sg) and np.array_equal(la, lg)
     for (Wa, ba), (Wg, bg) in zip(pa, pg):
         assert np.array_equal(Wa, Wg) and np.array_equal(ba, bg)
+
+
+@pytest.mark.parametrize("policy_name", ["reservoir", "fifo", "firo"])
+@pytest.mark.parametrize("overlap", [False, True])
+def test_tiny_schedule_to_drain_per_policy(policy_name, overlap):
+    """The whole 16x16 schedule through each buffer policy, then the end of
+    reception and the drain with training on every batch (the last one may be
+    short): slots of every batch bit-exact, batch sizes equal, loss series and
+    final parameters within 1e-3 relative of the oracle's run_to_drain."""
+    from oracle.buffers import FIFOBuffer, FIROBuffer
+    from oracle.reservoir import Reservoir
+    from paper_2309_16743_amd import OT_POLICY_FIFO, OT_POLICY_FIRO, OT_POLICY_RESERVOIR
+    from paper_2309_16743_amd.online import OnlineTrainer
+    cls, policy = {"reservoir": (Reservoir, OT_POLICY_RESERVOIR), "fifo": (FIFOBuffer, OT_POLICY_FIFO),
+                   "firo": (FIROBuffer, OT_POLICY_FIRO)}[policy_name]
+    print(f"schedule to drain policy={policy_name} overlap={overlap}", flush=True)
+    w = configs.TINY
+    X = heat.sample_parameters(w.n_sims, w.data_seed)
+    inputs = heat.inputs_for(X, w.tau)
+    fields = heat.heat_fields(X, w.grid, w.tau)
+    ref = runner.run_to_drain(w, inputs, fields,
+                              cls(w.capacity, w.threshold, inputs.shape[-1], fields.shape[-1], w.reservoir_seed))
+    n = len(ref["losses"])
+    tr = OnlineTrainer(w.widths, w.batch, w.capacity, w.threshold, w.wave, w.tau,
+                       torch.from_numpy(inputs).to(DEV), torch.from_numpy(fields).to(DEV),
+                       w.reservoir_seed, w.init_seed, lr=w.lr, record_steps=n, overlap=overlap, policy=policy)
+    for _ in range(w.n_chunks):
+        tr.iterate()
+    torch.cuda.synchronize()
+    tr.res.end_reception()
+    while tr.sample_and_train():
+        pass
+    torch.cuda.synchronize()
+    assert tr.steps_done == n
+    slots = tr.slot_log.cpu().numpy()
+    for i in range(n):
+        k = ref["sizes"][i]
+        assert np.array_equal(slots[i][:k], ref["slots"][i]), i
+    assert rel(tr.loss_log.cpu().numpy(), ref["losses"]) < 1e-3
+    for l in range(3):
+        W, b = tr.sur.get_params(l)
+        assert rel(W, ref["params"][l][0]) < 1e-3 and rel(b, ref["params"][l][1]) < 1e-3
+    tr.close()

@@ -70,3 +70,25 @@ def test_schedule_validation_and_repetition_histogram():
     h = runner.repetition_histogram(res, 256)
     assert h.sum() == res.total_put                                  # every sample that entered, once
     assert int((np.arange(256) * h).sum()) == res.total_draws       # every draw, once
+
+
+def test_run_to_drain_uses_every_sample_once_with_fifo_and_firo():
+    """FIFO and FIRO through the whole 16x16 schedule and the drain: every
+    produced sample is trained on exactly once (the slots of each sample id
+    are never repeated), batches are full except possibly the last, and the
+    Reservoir trains on more batches from the same production."""
+    from oracle.buffers import FIFOBuffer, FIROBuffer
+    from oracle.reservoir import Reservoir
+    w, inputs, fields = tiny_data()
+    n = w.n_chunks * w.wave
+    res = {}
+    for name, cls in (("fifo", FIFOBuffer), ("firo", FIROBuffer), ("reservoir", Reservoir)):
+        buf = cls(w.capacity, w.threshold, inputs.shape[-1], fields.shape[-1], w.reservoir_seed)
+        tr = runner.run_to_drain(w, inputs, fields, buf)
+        res[name] = tr
+        assert all(np.isfinite(tr["losses"]))
+        if name != "reservoir":
+            assert sum(tr["sizes"]) == n
+            assert all(s == w.batch for s in tr["sizes"][:-1])
+            assert buf.total_draws == n and buf.N == 0
+    assert len(res["reservoir"]["losses"]) > len(res["fifo"]["losses"])
