@@ -7,7 +7,10 @@ batch draw with replacement and its gather, and one train step of the MLP
 surrogate (forward, fused MSE, backward, Adam).  The reservoir's put, draw and
 gather for the next batch run on a second stream while the current batch
 trains (two batch buffers, ordered by events), as the paper's aggregator and
-training threads run concurrently; --one-stream runs everything on one stream.
+training threads run concurrently; --one-stream runs everything on one stream,
+as does a workload whose batch targets are under 1 MiB (tiny-16x16), where the
+step is launch-latency-bound and two cross-stream waits cost more than the
+overlap gains.
 
 Default workload (--config heat-100x100): 100x100 heat fields from an FTCS
 solver, 1000 simulations x 100 steps, MLP 6-256-256-10000 fp32, batch 1024,
@@ -76,7 +79,9 @@ def parse_args():
                         "output layer's forward reads them in place from the reservoir through the drawn slots)")
     p.add_argument("--one-stream", action="store_true",
                    help="run the reservoir and the train step on one stream (default: the reservoir's put, draw "
-                        "and gather of the next batch overlap the current train step on a second stream)")
+                        "and gather of the next batch overlap the current train step on a second stream, unless "
+                        "a batch's targets are under 1 MiB: then the step is launch-latency-bound and the two "
+                        "cross-stream waits per step cost more than the overlap gains, so one stream is used)")
     p.add_argument("--profile-steps", type=int, default=None,
                    help="steps of the per-kernel breakdown pass (all phases timed)")
     p.add_argument("--cpu-seconds", type=float, default=15.0,
@@ -113,6 +118,22 @@ def pmc_calibration():
     torch.cuda.synchronize()
     del a, b
     torch.cuda.empty_cache()
+
+
+SMALL_STEP_BYTES = 1 << 20
+
+
+def one_stream(args, w) -> bool:
+    """Whether the reservoir work runs on the train step's stream."""
+    return args.one_stream or w.batch * w.widths[-1] * 4 < SMALL_STEP_BYTES
+
+
+def stream_mode(args, w) -> str:
+    if args.one_stream:
+        return "one stream"
+    if one_stream(args, w):
+        return "one stream (a batch's targets are under 1 MiB: latency-bound step)"
+    return "overlapped with the train step"
 
 
 def kernel_sources(label: str):
@@ -546,7 +567,7 @@ def run_heat(args, w):
     stream = torch.cuda.Stream(device=dev)
     with torch.cuda.stream(stream):
         tr = OnlineTrainer(w.widths, w.batch, w.capacity, w.threshold, w.wave, w.tau, inputs_d, fields_d,
-                           w.reservoir_seed, w.init_seed, lr=w.lr, stream=stream, overlap=not args.one_stream,
+                           w.reservoir_seed, w.init_seed, lr=w.lr, stream=stream, overlap=not one_stream(args, w),
                            fused_targets=not args.gathered_targets)
         for _ in range(w.n_chunks):             # stream the ensemble once (untimed)
             tr.iterate()
@@ -560,7 +581,7 @@ def run_heat(args, w):
     config = {"workload": w.name, "fields": f"FTCS heat {w.grid}x{w.grid}, {w.n_sims} sims x {w.tau} steps",
               "widths": list(w.widths), "batch": w.batch, "capacity": w.capacity, "threshold": w.threshold,
               "put_rows_per_step": w.wave, "precision": w.precision,
-              "reservoir_stream": "one stream" if args.one_stream else "overlapped with the train step",
+              "reservoir_stream": stream_mode(args, w),
               "targets": "gathered into a batch buffer" if args.gathered_targets
               else "read in place from the reservoir by the forward (inputs gathered)",
               "timed_puts": "none (pre-filled reservoir)" if args.prefilled else "one per step"}
@@ -660,7 +681,7 @@ def run_field(args, w):
         tr = OnlineTrainer(w.widths, w.batch, w.capacity, w.threshold, w.wave, w.tau, None, None,
                            w.reservoir_seed, w.init_seed, precision=OT_BF16, lr=w.lr, stream=stream,
                            chunk_fn=lambda c: (pool_x[c % pool], pool_u[c % pool]), n_chunks=1 << 40, device=dev,
-                           overlap=not args.one_stream, fused_targets=not args.gathered_targets)
+                           overlap=not one_stream(args, w), fused_targets=not args.gathered_targets)
         fx = torch.empty(w.wave, 8, device=dev)[:, :6]
         fu = torch.empty(w.wave, D, device=dev)
         t_fill = time.perf_counter()
@@ -683,7 +704,7 @@ def run_field(args, w):
     config = {"workload": w.name, "fields": f"sine-mode {n}x{n}, {w.n_sims} sims x {w.tau} steps",
               "widths": list(w.widths), "batch": w.batch, "capacity": w.capacity, "threshold": w.threshold,
               "put_rows_per_step": w.wave, "precision": w.precision,
-              "reservoir_stream": "one stream" if args.one_stream else "overlapped with the train step",
+              "reservoir_stream": stream_mode(args, w),
               "targets": "gathered into a batch buffer" if args.gathered_targets
               else "read in place from the reservoir by the forward (inputs gathered)",
               "timed_puts": "none (pre-filled reservoir)" if args.prefilled else "one per step"}
