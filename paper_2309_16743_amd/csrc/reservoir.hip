@@ -461,6 +461,18 @@ __global__ __launch_bounds__(kCopyThreads) void gather_kernel(
       x_out[row * ldxo + c] = xslab[slot * ldxs + c];
 }
 
+// Gather of the input rows alone (the field rows are read in place by the
+// train step): one thread per copied value.  grid = ceil(b x_dim / 256).
+__global__ __launch_bounds__(256) void gather_x_kernel(const int32_t* __restrict__ slots,
+                                                       const float* __restrict__ xslab, int64_t ldxs,
+                                                       float* __restrict__ x_out, int64_t ldxo, int64_t x_dim,
+                                                       int64_t b) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= b * x_dim) return;
+  const int64_t row = i / x_dim, c = i % x_dim;
+  x_out[row * ldxo + c] = xslab[(int64_t)slots[row] * ldxs + c];
+}
+
 }  // namespace ot
 
 // ===================================================================== host side
@@ -758,7 +770,14 @@ extern "C" int reservoir_sample_batch(ot_reservoir* r, int64_t b, void* stream, 
     r->n_host -= drawn;
   }
   tm.mark(r->stream, OT_PH_SELECT, 1);
-  if (u_out || x_out) {
+  if (x_out && !u_out) {
+    hipEvent_t t0, t1;
+    tm.kernel_events(OT_PH_GATHER, &t0, &t1);
+    hipExtLaunchKernelGGL(ot::gather_x_kernel, dim3((unsigned)ot::ceil_div(drawn * r->x_dim, 256)), dim3(256), 0,
+                          r->stream, t0, t1, 0, (const int32_t*)slots, (const float*)r->xslab, r->ldxs, x_out,
+                          ldxo, r->x_dim, drawn);
+    OT_LAUNCHED("gather_x_kernel");
+  } else if (u_out) {
     hipEvent_t t0, t1;
     tm.kernel_events(OT_PH_GATHER, &t0, &t1);
     const int vec_ok = (u_out == nullptr) || (aligned16(u_out) && (lduo % 4 == 0));
