@@ -27,6 +27,8 @@ def padded(rows, d):
     (64, 32, 256, 0, 60),        # the 16x16 workload's reservoir
     (97, 10, 1003, 5, 80),       # ragged row length, prime capacity
     (300, 50, 4099, 9, 60),      # rows longer than one copy segment
+    (1, 0, 1, 3, 40),            # one slot, no watermark, one-float rows
+    (2, 1, 5, 4, 50),            # two slots: every put past the first evicts
 ])
 def test_sequence_bit_exact(C, T, d, seed, ops):
     from paper_2309_16743_amd import OT_NOT_READY, OT_OK, Reservoir

@@ -62,6 +62,8 @@ SHAPES = [
     ((20, 48, 30), 17),              # first layer through the GEMM path
     ((6, 10), 9),                    # single layer
     ((6, 256, 256, 10000), 1024),    # the 100x100 workload's net at its batch
+    ((6, 8, 1), 1),                  # one sample, one output
+    ((6, 300, 300, 7), 2),           # two samples, hidden widths past one tile
 ]
 
 
