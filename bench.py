@@ -161,7 +161,7 @@ def sources_hash(label: str) -> str:
 
 def kernel_matches(label: str, name: str) -> bool:
     """Whether a rocprofv3 kernel name is the kernel behind a roofline label."""
-    if label in ("adam_kernel", "gather_kernel", "put_copy_kernel"):
+    if label in ("adam_kernel", "gather_kernel", "gather_x_kernel", "put_copy_kernel"):
         return f"ot::{label}(" in name
     phase = label.split("(")[1].rstrip(")")
     if phase == "wgrad_output + fused Adam":       # bf16 weight gradient with the Adam epilogue
@@ -330,7 +330,7 @@ def roofline_entry(w, phase: str, avg_s: float) -> dict:
                 "frac": round(work / avg_s / peak, 4), "traffic": traffic_for(w.name, label),
                 "per_launch_flops": work, "avg_us": round(avg_s * 1e6, 2)}
     work = {"adam": adam_bytes(w), "gather": gather_bytes(w)}[phase]
-    label = "adam_kernel" if phase == "adam" else "gather_kernel"
+    label = "adam_kernel" if phase == "adam" else ("gather_kernel" if GATHERED_TARGETS else "gather_x_kernel")
     return {"bound": "hbm", "kernel": label,
             "achieved": round(work / avg_s / 1e9, 1), "peak": PEAK_HBM / 1e9, "unit": "GB/s",
             "frac": round(work / avg_s / PEAK_HBM, 4), "traffic": traffic_for(w.name, label),
