@@ -66,4 +66,10 @@ def test_validation_errors_before_device_work(lib):
     w = (C.c_int64 * 3)(6, 8, 4)
     assert lib.surrogate_create(C.byref(h), w, 3, 0, 1e-3, 0.9, 0.999, 1e-8, 0, 16, 7) == _abi.OT_E_INVAL
     assert lib.surrogate_train_step(None, None, 0, None, 0, 1, None, None) == _abi.OT_E_INVAL
+    assert lib.surrogate_train_step_rows(None, None, 0, None, 0, None, 1, 1, None, None, None) == _abi.OT_E_INVAL
+    assert b"NULL surrogate" in lib.ot_last_error()
+    assert lib.surrogate_eval_loss(None, None, 0, None, 0, 1, None, None) == _abi.OT_E_INVAL
+    assert lib.surrogate_set_lr(None, C.c_float(1e-3)) == _abi.OT_E_INVAL
+    assert lib.reservoir_slab(None, None, None, None, None) == _abi.OT_E_INVAL
+    assert b"NULL reservoir" in lib.ot_last_error()
     assert lib.reservoir_destroy(None) == _abi.OT_OK
