@@ -89,7 +89,8 @@ struct FragVec<1> { typedef float T; };
 // ROLE only separates instantiations (0: hidden layers, 1: output layer) so
 // that profiles attribute the output-layer products to their own kernels.
 template <int WGM, int WGN, int FM, int FN, Lay LA, Lay LB, Epi EPI, int BK = 16, int ROLE = 0>
-__global__ __launch_bounds__(64 * WGM * WGN) void gemm_f32_kernel(GemmArgs g) {
+__global__ __launch_bounds__(64 * WGM * WGN)
+__attribute__((amdgpu_waves_per_eu((EPI == Epi::Mse && FM * FN == 8) ? 5 : 1))) void gemm_f32_kernel(GemmArgs g) {
   constexpr int NT = 64 * WGM * WGN;
   static_assert(BK % 16 == 0, "k tile must be a multiple of 16");
   constexpr int BM = 16 * FM * WGM;
@@ -357,8 +358,42 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_f32_kernel(GemmArgs g) {
   };
   float bv[FN];
   if constexpr (EPI == Epi::Bias || EPI == Epi::BiasRelu || EPI == Epi::Mse) load_cols(g.bias + col_base, bv);
+  // Mse: the block's targets pass through LDS (the B staging buffer, free
+  // after the main loop) in TP passes, each filled by direct global -> LDS
+  // loads and waited for once: read row by row from global memory, every
+  // row's wait would also wait for the previous row's dY stores (stores
+  // count in vmcnt).  A lane's rows r of pass p are p RP .. p RP + RP - 1;
+  // local row lr = ((wm 4 + lane / 16) RP + r - p RP) FM + f.  Tiles that
+  // cross N, or unaligned targets, read row by row.
+  constexpr int TB = 2 * BK * LDB_S;                              // floats of Bs
+  constexpr int TP = (BM * BN <= TB) ? 1 : (BM * BN / 2 <= TB) ? 2 : 4;
+  constexpr int RP = 4 / TP;
+  static_assert(EPI != Epi::Mse || (BM * BN / TP <= TB && 256 % BN == 0), "target staging");
+  const bool stage_t = (EPI == Epi::Mse) && (n0 + BN <= g.N) && (g.ldt % 4 == 0) &&
+                       ((reinterpret_cast<uintptr_t>(g.target) & 15) == 0);
+  float* Tl = &Bs[0][0];
+  auto fill_targets = [&](int p) {
+    typedef __attribute__((address_space(3))) void lds_void;
+    constexpr int ROWS_KB = 256 / BN;                             // target rows per 1 KB chunk
+    constexpr int CHUNKS = BM / TP * BN / 256;
+    __syncthreads();                                              // Bs no longer read
+    for (int c = wid; c < CHUNKS; c += NT / 64) {
+      const int lr = c * ROWS_KB + lane / (BN / 4);
+      const int ff = lr % FM, t = lr / FM, rr = t % RP, u = t / RP;
+      const int R = 16 * FM * (u / 4) + 4 * FM * (u % 4) + FM * (p * RP + rr) + ff;
+      const int64_t m = min(m0 + R, g.M - 1);
+      const int64_t tr = g.target_rows ? (int64_t)s_trow[m - m0] : m;
+      const float* src = g.target + tr * g.ldt + n0 + 4 * (lane % (BN / 4));
+      __builtin_amdgcn_global_load_lds(src, (lds_void*)(Tl + c * 256), 16, 0, 0);
+    }
+    __builtin_amdgcn_s_waitcnt((0x7 << 4) | (0xF << 8));        // vmcnt(0)
+    __syncthreads();
+  };
 #pragma unroll
   for (int r = 0; r < 4; ++r) {
+    if constexpr (EPI == Epi::Mse) {
+      if (r % RP == 0 && stage_t) fill_targets(r / RP);
+    }
 #pragma unroll
     for (int f = 0; f < FM; ++f) {
       const int64_t m = row_base + FM * r + f;
@@ -376,8 +411,15 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_f32_kernel(GemmArgs g) {
       }
       if constexpr (EPI == Epi::Mse) {
         float tv[FN];
-        const int64_t tr = g.target_rows ? (int64_t)s_trow[m - m0] : m;
-        load_cols(g.target + tr * g.ldt + col_base, tv);
+        if (stage_t) {
+          const int lr = ((wm * 4 + lane / 16) * RP + r % RP) * FM + f;
+          const float* tp = Tl + lr * BN + 16 * FN * wn + FN * (lane % 16);
+#pragma unroll
+          for (int h = 0; h < FN; ++h) tv[h] = tp[h];
+        } else {
+          const int64_t tr = g.target_rows ? (int64_t)s_trow[m - m0] : m;
+          load_cols(g.target + tr * g.ldt + col_base, tv);
+        }
 #pragma unroll
         for (int h = 0; h < FN; ++h) {
           const float rr = (col_base + h < g.N) ? v[h] - tv[h] : 0.f;
