@@ -406,3 +406,39 @@ def test_tiny_schedule_to_drain_per_policy(policy_name, overlap):
         W, b = tr.sur.get_params(l)
         assert rel(W, ref["params"][l][0]) < 1e-3 and rel(b, ref["params"][l][1]) < 1e-3
     tr.close()
+
+
+def test_timing_hooks_cover_the_timed_calls():
+    """The profiling hooks behind the benchmark's per-kernel table: every
+    output-layer GEMM phase is timed once per step and the reservoir's phases
+    once per call, with positive durations; calls past max_steps are not
+    counted and results are unchanged by timing."""
+    from paper_2309_16743_amd import Reservoir, Surrogate, _abi
+    widths, B = (6, 64, 64, 256), 32
+    params, X, U = problem(widths, B, seed=3)
+    s, ref = make_gpu(widths, params, B), make_gpu(widths, params, B)
+    Xd, Ud = padded_from(X), padded_from(U)
+    s.timing_begin(list(_abi.SURROGATE_PHASES), 3)
+    for _ in range(5):
+        s.train_step(Xd, Ud)
+        ref.train_step(Xd, Ud)
+    r = s.timing_end()
+    for p in ("fwd_output", "wgrad_output", "igrad_output"):
+        assert r[p][1] == 3 and r[p][0] > 0, (p, r.get(p))
+    for l in range(3):
+        W, b = s.get_params(l)
+        Wr, br = ref.get_params(l)
+        assert np.array_equal(W, Wr) and np.array_equal(b, br)
+    s.close()
+    ref.close()
+    res = Reservoir(64, 8, 6, 256, 1)
+    res.timing_begin(list(_abi.RESERVOIR_PHASES), 10)
+    res.put(padded_from(X), padded_from(U))
+    slots = torch.empty(16, dtype=torch.int32, device=DEV)
+    xb, ub = padded_from(np.zeros((16, 6), np.float32)), padded_from(np.zeros((16, 256), np.float32))
+    res.sample_batch(16, slots, x_out=xb, u_out=ub)
+    torch.cuda.synchronize()
+    rr = res.timing_end()
+    for p in _abi.RESERVOIR_PHASES:
+        assert rr[p][1] == 1 and rr[p][0] > 0, (p, rr.get(p))
+    res.close()
