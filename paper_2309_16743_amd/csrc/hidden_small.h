@@ -76,8 +76,8 @@ __device__ __forceinline__ void stage_tile(float* dst, int ls, const float* __re
 // Four accumulator chains take the k steps in turn (four MFMAs in flight
 // instead of one dependent chain), each step's operands are read while the
 // previous steps run, and the chains are added in a fixed order at the end.
-__device__ __forceinline__ f32x4v mfma_row_dot(const float* pa, int sa, const float* pb, int sb, int kp) {
-  f32x4v acc[4] = {};
+__device__ __forceinline__ void mfma_row_dot_chains(const float* pa, int sa, const float* pb, int sb, int kp,
+                                                    f32x4v (&acc)[4]) {
   int k0 = 0;
   for (; k0 + 16 <= kp; k0 += 16) {
     float a[4], b[4];
@@ -90,6 +90,12 @@ __device__ __forceinline__ f32x4v mfma_row_dot(const float* pa, int sa, const fl
     for (int c = 0; c < 4; ++c) acc[c] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[c], b[c], acc[c], 0, 0, 0);
   }
   for (int c = 0; k0 < kp; k0 += 4, ++c) acc[c] = __builtin_amdgcn_mfma_f32_16x16x4f32(pa[k0 * sa], pb[k0 * sb], acc[c], 0, 0, 0);
+}
+// The k range may be taken in pieces whose lengths before the last are
+// multiples of 16: every k step then lands on the same chain as in one call.
+__device__ __forceinline__ f32x4v mfma_row_dot(const float* pa, int sa, const float* pb, int sb, int kp) {
+  f32x4v acc[4] = {};
+  mfma_row_dot_chains(pa, sa, pb, sb, kp, acc);
   return (acc[0] + acc[1]) + (acc[2] + acc[3]);
 }
 
@@ -149,9 +155,13 @@ __global__ __launch_bounds__(256) void hidden_fwd_small_kernel(
 }
 
 constexpr int kMaskStride = kHfCols + 4;
-constexpr int kBwdSmem = kHfRows * kStrideA + kSmallH * kStrideB + kHfRows * (kHfCols + 1) + kHfRows * kSmallIn +
+// W2 is staged in two halves of its k range and role B's rows in two halves
+// of the split, so that a block needs 67 KB of LDS and two fit on a CU.
+constexpr int kWHalf = kSmallH / 2;
+constexpr int kHbHalf = kHbRows / 2;
+constexpr int kBwdSmem = kHfRows * kStrideA + kWHalf * kStrideB + kHfRows * (kHfCols + 1) + kHfRows * kSmallIn +
                          kHfRows * kMaskStride;
-static_assert(2 * kHbRows * kStrideB <= kBwdSmem, "role B staging");
+static_assert(2 * kHbHalf * kStrideB <= kBwdSmem, "role B staging");
 
 // Backward, part 1.  Blocks [0, nA) (role A): rows r0 .. r0 + 15, layer-1
 // units c0 .. c0 + 63: dA1 = dZ2 W2 (K = h2), dZ1 = dA1 * [A1 > 0] stored, and
@@ -169,8 +179,8 @@ __global__ __launch_bounds__(256) void hidden_bwd_small_kernel(
   if ((int64_t)blockIdx.x < nA) {
     // ---------------- role A
     float* sD2 = smem;                                   // [16][kStrideA]
-    float* sW = sD2 + kHfRows * kStrideA;                // [256][kStrideB]
-    float* sZ = sW + kSmallH * kStrideB;                 // [16][65]
+    float* sW = sD2 + kHfRows * kStrideA;                // [128][kStrideB]: one half of W2's k range
+    float* sZ = sW + kWHalf * kStrideB;                  // [16][65]
     float* sX = sZ + kHfRows * (kHfCols + 1);            // [16][kSmallIn]
     float* sM = sX + kHfRows * kSmallIn;                 // [16][kMaskStride]: A1 tile (ReLU mask)
     const int tiles_c = (h1 + kHfCols - 1) / kHfCols;
@@ -178,7 +188,7 @@ __global__ __launch_bounds__(256) void hidden_bwd_small_kernel(
     const int c0 = (int)(blockIdx.x % tiles_c) * kHfCols;
     const int64_t r0 = rt * kHfRows;
     stage_tile<kHfRows, kSmallH>(sD2, kStrideA, dZ2, ldd2, r0, rows, 0, h2);
-    stage_tile<kSmallH, kHfCols>(sW, kStrideB, W2, ldw2, 0, h2, c0, h1);
+    stage_tile<kWHalf, kHfCols>(sW, kStrideB, W2, ldw2, 0, h2, c0, h1);
     stage_tile<kHfRows, kHfCols>(sM, kMaskStride, A1, lda1, r0, rows, c0, h1);
     {
       const int r = tid / kSmallIn, k = tid % kSmallIn;
@@ -186,9 +196,19 @@ __global__ __launch_bounds__(256) void hidden_bwd_small_kernel(
     }
     __syncthreads();
     const int h2p = (h2 + 3) & ~3;
+    const int kh = h2p < kWHalf ? h2p : kWHalf;
     const int ci = 16 * w + (lane & 15);
-    const f32x4v acc =
-        mfma_row_dot(sD2 + (lane & 15) * kStrideA + (lane >> 4), 1, sW + (lane >> 4) * kStrideB + ci, kStrideB, h2p);
+    f32x4v ch[4] = {};
+    mfma_row_dot_chains(sD2 + (lane & 15) * kStrideA + (lane >> 4), 1, sW + (lane >> 4) * kStrideB + ci, kStrideB, kh,
+                        ch);
+    if (h2p > kWHalf) {                                   // second half of W2's k range
+      __syncthreads();
+      stage_tile<kWHalf, kHfCols>(sW, kStrideB, W2, ldw2, kWHalf, h2, c0, h1);
+      __syncthreads();
+      mfma_row_dot_chains(sD2 + (lane & 15) * kStrideA + kWHalf + (lane >> 4), 1, sW + (lane >> 4) * kStrideB + ci,
+                          kStrideB, h2p - kWHalf, ch);
+    }
+    const f32x4v acc = (ch[0] + ch[1]) + (ch[2] + ch[3]);
     const int i = c0 + ci;
     for (int q = 0; q < 4; ++q) {
       const int r = 4 * (lane >> 4) + q;
@@ -212,27 +232,30 @@ __global__ __launch_bounds__(256) void hidden_bwd_small_kernel(
     return;
   }
   // ---------------- role B: dW2[j][i] = sum_b dZ2[b][j] A1[b][i] over the split's rows
-  float* sD = smem;                          // [128][kStrideB]
-  float* sA = smem + kHbRows * kStrideB;     // [128][kStrideB]
+  float* sD = smem;                          // [64][kStrideB]: one half of the split's rows
+  float* sA = smem + kHbHalf * kStrideB;     // [64][kStrideB]
   const int64_t bid = blockIdx.x - nA;
   const int tj = (h2 + kHbTile - 1) / kHbTile, ti = (h1 + kHbTile - 1) / kHbTile;
   const int64_t kc = bid / (tj * ti);
   const int j0 = (int)((bid / ti) % tj) * kHbTile, i0 = (int)(bid % ti) * kHbTile;
-  const int64_t b0 = kc * kHbRows;
-  stage_tile<kHbRows, kHbTile>(sD, kStrideB, dZ2, ldd2, b0, rows, j0, h2);
-  stage_tile<kHbRows, kHbTile>(sA, kStrideB, A1, lda1, b0, rows, i0, h1);
-  __syncthreads();
-  // wave w: rows j0 + 16 w .. +15 of the tile, all 64 columns (4 accumulators)
+  // wave w: rows j0 + 16 w .. +15 of the tile, all 64 columns (4 accumulators);
+  // the split's rows are taken in two halves, in order
   f32x4v acc[4] = {};
-  {
+  float csum = 0.f;
+  for (int half = 0; half < 2; ++half) {
+    const int64_t b0 = kc * kHbRows + half * kHbHalf;
+    if (half) __syncthreads();
+    stage_tile<kHbHalf, kHbTile>(sD, kStrideB, dZ2, ldd2, b0, rows, j0, h2);
+    stage_tile<kHbHalf, kHbTile>(sA, kStrideB, A1, lda1, b0, rows, i0, h1);
+    __syncthreads();
     const float* pa = sD + (lane >> 4) * kStrideB + 16 * w + (lane & 15);
     const float* pb = sA + (lane >> 4) * kStrideB + (lane & 15);
     float a = pa[0], b[4];
 #pragma unroll
     for (int h = 0; h < 4; ++h) b[h] = pb[16 * h];
 #pragma unroll 4
-    for (int k0 = 0; k0 < kHbRows; k0 += 4) {
-      const int kn = (k0 + 4 < kHbRows ? k0 + 4 : k0) * kStrideB;
+    for (int k0 = 0; k0 < kHbHalf; k0 += 4) {
+      const int kn = (k0 + 4 < kHbHalf ? k0 + 4 : k0) * kStrideB;
       const float an = pa[kn];
       float bn[4];
 #pragma unroll
@@ -243,17 +266,15 @@ __global__ __launch_bounds__(256) void hidden_bwd_small_kernel(
 #pragma unroll
       for (int h = 0; h < 4; ++h) b[h] = bn[h];
     }
+    if (i0 == 0 && tid < kHbTile)
+      for (int r = 0; r < kHbHalf; ++r) csum += sD[r * kStrideB + tid];
   }
   for (int h = 0; h < 4; ++h)
     for (int q = 0; q < 4; ++q) {
       const int j = j0 + 16 * w + 4 * (lane >> 4) + q, i = i0 + 16 * h + (lane & 15);
       if (j < h2 && i < h1) part2[(kc * h2 + j) * h1 + i] = acc[h][q];
     }
-  if (i0 == 0 && tid < kHbTile && j0 + tid < h2) {
-    float s = 0.f;
-    for (int r = 0; r < kHbRows; ++r) s += sD[r * kStrideB + tid];
-    part2b[kc * h2 + j0 + tid] = s;
-  }
+  if (i0 == 0 && tid < kHbTile && j0 + tid < h2) part2b[kc * h2 + j0 + tid] = csum;
 }
 
 // Backward, part 2: dW2[j][i] = sum_kc part2[kc][j][i], db2[j] = sum_kc
