@@ -98,19 +98,35 @@ template <class Base>
 __device__ void resolve_partial_shuffle(int E, const int* r, Base base, int* par, int* par2,
                                         int* lv, int* pre, int* taken, int* last_writer) {
   const int nt = blockDim.x;
+  // The scans read 8 entries per step (independent LDS reads in flight) and
+  // examine them in index order, so they find the same indices as an
+  // entry-by-entry scan.
+  constexpr int U = 8;
   for (int j = threadIdx.x; j < E; j += nt) {
     const int rj = r[j];
     int lp = -1, lvj = -1;
-    for (int i = j - 1; i >= 0 && (lp < 0 || lvj < 0); --i) {
-      const int ri = r[i];
-      if (lp < 0 && ri == j) lp = i;
-      if (lvj < 0 && ri == rj) lvj = i;
+    for (int i0 = j - 1; i0 >= 0 && (lp < 0 || lvj < 0); i0 -= U) {
+      int v[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u) v[u] = (i0 - u >= 0) ? r[i0 - u] : -1;
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        if (i0 - u < 0) break;
+        if (lp < 0 && v[u] == j) lp = i0 - u;
+        if (lvj < 0 && v[u] == rj) lvj = i0 - u;
+      }
     }
     par[j] = lp >= 0 ? lp : j;
     lv[j] = lvj;
     int later = 1;
-    for (int i = j + 1; i < E; ++i)
-      if (r[i] == rj) { later = 0; break; }
+    for (int i0 = j + 1; i0 < E && later; i0 += U) {
+      int v[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u) v[u] = (i0 + u < E) ? r[i0 + u] : -1;
+#pragma unroll
+      for (int u = 0; u < U; ++u)
+        if (i0 + u < E && v[u] == rj) later = 0;
+    }
     last_writer[j] = later;
   }
   __syncthreads();
