@@ -935,7 +935,7 @@ def main():
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print(f"bench.py measures one GPU only; --gpus {args.gpus} (WORLD_SIZE {world}) is not supported: "
-              "this build has no multi-GPU path.", file=sys.stderr)
+              "the library has no multi-GPU path (one reservoir and one surrogate per GPU).", file=sys.stderr)
         sys.exit(2)
     from fixtures import configs
     if args.pmc_calibration:
