@@ -442,3 +442,34 @@ def test_timing_hooks_cover_the_timed_calls():
     for p in _abi.RESERVOIR_PHASES:
         assert rr[p][1] == 1 and rr[p][0] > 0, (p, rr.get(p))
     res.close()
+
+
+def test_full_net_online_schedule_with_evictions():
+    """The 100x100 workload's net (6-256-256-10,000 fp32) and batch (1024)
+    through the online loop as the benchmark runs it (two streams, targets
+    read in place from the reservoir), with a reservoir reduced to 1200 slots
+    so that evictions start within the run: 20 train steps, slots bit-exact,
+    loss series and final parameters within 1e-3 relative L2 of the oracle."""
+    import dataclasses
+    from paper_2309_16743_amd.online import OnlineTrainer
+    w = dataclasses.replace(configs.HEAT100, n_sims=40, wave=40, capacity=1200, threshold=1024)
+    print(f"full-net online schedule C={w.capacity} T={w.threshold} B={w.batch}", flush=True)
+    X = heat.sample_parameters(w.n_sims, w.data_seed)
+    inputs = heat.inputs_for(X, w.tau)
+    fields = heat.heat_fields(X, w.grid, w.tau)
+    n = 20
+    ref = runner.run(w, inputs, fields, n_steps=n)
+    tr = OnlineTrainer(w.widths, w.batch, w.capacity, w.threshold, w.wave, w.tau,
+                       torch.from_numpy(inputs).to(DEV), torch.from_numpy(fields).to(DEV),
+                       w.reservoir_seed, w.init_seed, lr=w.lr, record_steps=n, overlap=True)
+    tr.run(n)
+    torch.cuda.synchronize()
+    assert tr.res.stats()["total_evicted"] > 0
+    slots = tr.slot_log.cpu().numpy()
+    for i in range(n):
+        assert np.array_equal(slots[i], ref["slots"][i]), i
+    assert rel(tr.loss_log.cpu().numpy(), ref["losses"]) < 1e-3
+    for l in range(3):
+        W, b = tr.sur.get_params(l)
+        assert rel(W, ref["params"][l][0]) < 1e-3 and rel(b, ref["params"][l][1]) < 1e-3
+    tr.close()
