@@ -202,3 +202,37 @@ def test_full_width_targets_in_place_bf16():
         assert np.array_equal(Wa, Wg) and np.array_equal(ba, bg), l
     a.close()
     g.close()
+
+
+def test_mid_size_online_schedule_bf16():
+    """A 6-512-512-19,600 bf16 net (140x140 heat fields) at batch 512 through
+    the online loop as the benchmark runs it (two streams, targets read in
+    place, pipelined GEMM kernels, output-layer Adam fused into its weight
+    gradient), with a 700-slot reservoir so that puts evict during the run:
+    10 steps, slots bit-exact, loss series and final parameters within 2e-2
+    relative L2 of the oracle's bf16 mode."""
+    import dataclasses
+    from paper_2309_16743_amd import OT_BF16
+    from paper_2309_16743_amd.online import OnlineTrainer
+    w = dataclasses.replace(configs.HEAT100, grid=140, n_sims=24, wave=24, widths=(6, 512, 512, 19600),
+                            precision="bf16", batch=512, capacity=700, threshold=512)
+    print(f"bf16 mid-size online schedule widths={w.widths} B={w.batch} C={w.capacity}", flush=True)
+    X = heat.sample_parameters(w.n_sims, w.data_seed)
+    inputs = heat.inputs_for(X, w.tau)
+    fields = heat.heat_fields(X, w.grid, w.tau)
+    n = 10
+    ref = runner.run(w, inputs, fields, n_steps=n)
+    tr = OnlineTrainer(w.widths, w.batch, w.capacity, w.threshold, w.wave, w.tau,
+                       torch.from_numpy(inputs).to(DEV), torch.from_numpy(fields).to(DEV),
+                       w.reservoir_seed, w.init_seed, precision=OT_BF16, lr=w.lr, record_steps=n, overlap=True)
+    tr.run(n)
+    torch.cuda.synchronize()
+    assert tr.res.stats()["total_evicted"] > 0
+    slots = tr.slot_log.cpu().numpy()
+    for i in range(n):
+        assert np.array_equal(slots[i], ref["slots"][i]), i
+    assert rel(tr.loss_log.cpu().numpy(), ref["losses"]) < TOL
+    for l in range(3):
+        W, b = tr.sur.get_params(l)
+        assert rel(W, ref["params"][l][0]) < TOL and rel(b, ref["params"][l][1]) < TOL
+    tr.close()
