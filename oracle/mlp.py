@@ -23,11 +23,15 @@ forward GEMM (activations A_{l-1}, the bf16 copy of W_l) are rounded to bf16
 (round to nearest even from fp32); the output-layer gradient dY is rounded to
 bf16 before the backward GEMMs, as is every back-propagated dZ_l; bias
 gradients are sums of those rounded values; Adam works on fp32 master weights
-and fp32 gradients.  All accumulation here is fp64.
+and fp32 gradients.  All accumulation here is fp64.  The rounding points are
+named (BF16_ROUNDED below) so that a test can switch one of them, which is how
+the tests plant a misplaced rounding point in this module.
 
 Pins: central finite differences of the loss on tiny nets, torch fp64
 autograd of the same net, Adam's step-1 closed form (-lr * sign(g) up to eps),
-hand-computed MSE values.
+hand-computed MSE values; bf16 mode: a hand-worked one-hidden-layer example
+in which every rounding point changes the result, equality with fp64 mode on
+nets whose values are all bf16-representable, and closeness to fp64 mode.
 """
 from __future__ import annotations
 
@@ -79,16 +83,43 @@ def init_rows(widths, seed: int, layer: int, rows) -> Tuple[np.ndarray, np.ndarr
     return w.reshape(len(rows), fan_in), b
 
 
-def forward(params: Params, X: np.ndarray, bf16: bool = False):
-    """Return (Zs, As, Y): pre-activations, activations (As[0] = X), output."""
+# Rounding points of bf16 mode (the mixed-precision reading of Sec. 4.1's
+# "bf16 GEMMs with fp32 master weights"):
+#   "act"    - activations A_l (l >= 1) where a GEMM reads them (the forward of
+#              layer l + 1 and the weight gradient of layer l + 1);
+#   "weight" - the bf16 copy of W_l (l >= 2) read by the forward and by the
+#              input gradient;
+#   "dY"     - the output gradient 2 (Y - U) / (B D);
+#   "dZ"     - every back-propagated dZ_l (after the ReLU mask).
+# Bias gradients are column sums of the rounded dY / dZ.  Points that bf16 mode
+# leaves unrounded, named only so that a test can plant them as mistakes:
+#   "input"  - layer 1's input X and W_1 (layer 1 runs in fp32);
+#   "target" - the targets U;
+#   "db_raw" - bias gradients summed from dY / dZ before rounding.
+BF16_ROUNDED = frozenset({"act", "weight", "dY", "dZ"})
+
+
+def _rounder(bf16: bool, rounded):
+    points = (BF16_ROUNDED if rounded is None else frozenset(rounded)) if bf16 else frozenset()
+
+    def rnd(point: str, v: np.ndarray) -> np.ndarray:
+        return bf16_round(v) if point in points else v
+    return rnd, points
+
+
+def forward(params: Params, X: np.ndarray, bf16: bool = False, rounded=None):
+    """Return (Zs, As, Y): pre-activations, activations (As[0] = X), output.
+
+    rounded: the bf16 rounding points (default BF16_ROUNDED; tests only)."""
+    rnd, _ = _rounder(bf16, rounded)
     A = np.asarray(X, dtype=np.float64)
     As, Zs = [A], []
     L = len(params)
     for l, (W, b) in enumerate(params):
-        if bf16 and l > 0:
-            Z = bf16_round(A) @ bf16_round(W).T + b
+        if l > 0:
+            Z = rnd("act", A) @ rnd("weight", W).T + b
         else:
-            Z = A @ W.T + b
+            Z = rnd("input", A) @ rnd("input", W).T + b
         Zs.append(Z)
         if l < L - 1:
             A = np.maximum(Z, 0.0)
@@ -102,31 +133,29 @@ def mse(Y: np.ndarray, U: np.ndarray) -> float:
     return float(np.sum(R * R) / R.size)
 
 
-def loss_and_grads(params: Params, X: np.ndarray, U: np.ndarray, bf16: bool = False):
-    """MSE loss and its gradients with respect to every W_l and b_l."""
-    Zs, As, Y = forward(params, X, bf16=bf16)
-    U = np.asarray(U, dtype=np.float64)
+def loss_and_grads(params: Params, X: np.ndarray, U: np.ndarray, bf16: bool = False, rounded=None):
+    """MSE loss and its gradients with respect to every W_l and b_l.
+
+    rounded: the bf16 rounding points (default BF16_ROUNDED; tests only)."""
+    rnd, points = _rounder(bf16, rounded)
+    Zs, As, Y = forward(params, X, bf16=bf16, rounded=rounded)
+    U = rnd("target", np.asarray(U, dtype=np.float64))
     R = Y - U
     loss = float(np.sum(R * R) / R.size)
-    dZ = 2.0 * R / R.size                     # dLoss/dY
-    if bf16:
-        dZ = bf16_round(dZ)
+    dZ_raw = 2.0 * R / R.size                 # dLoss/dY
+    dZ = rnd("dY", dZ_raw)
     L = len(params)
     grads: Params = [None] * L                # type: ignore[list-item]
     for l in range(L - 1, -1, -1):
         W = params[l][0]
-        A_in = As[l]
-        if bf16 and l > 0:
-            dW = dZ.T @ bf16_round(A_in)
-        else:
-            dW = dZ.T @ A_in
-        db = dZ.sum(axis=0)
+        A_in = rnd("act", As[l]) if l > 0 else rnd("input", As[l])
+        dW = dZ.T @ A_in
+        db = (dZ_raw if "db_raw" in points else dZ).sum(axis=0)
         grads[l] = (dW, db)
         if l > 0:
-            dA = dZ @ (bf16_round(W) if bf16 else W)
-            dZ = dA * (Zs[l - 1] > 0.0)
-            if bf16:
-                dZ = bf16_round(dZ)
+            dA = dZ @ rnd("weight", W)
+            dZ_raw = dA * (Zs[l - 1] > 0.0)
+            dZ = rnd("dZ", dZ_raw)
     return loss, grads
 
 
@@ -165,6 +194,6 @@ class Adam:
         self.m[l], self.v[l] = tuple(ms), tuple(vs)
 
 
-def predict(params: Params, X: np.ndarray, bf16: bool = False) -> np.ndarray:
+def predict(params: Params, X: np.ndarray, bf16: bool = False, rounded=None) -> np.ndarray:
     """Surrogate output f_theta(X, t) for each input row."""
-    return forward(params, X, bf16=bf16)[2]
+    return forward(params, X, bf16=bf16, rounded=rounded)[2]

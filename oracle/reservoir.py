@@ -25,7 +25,8 @@ Readings taken where the paper is silent or loose:
 
 Every call that changes state takes the next ticket; refused calls do not.
 
-Pins: exact outcome distributions against a literal list model of Algorithm 1
+Pins: exact outcome distributions against a model of the buffer built from the
+behaviour Sec. 3.2.3 states
 (enumeration with exact fractions), deterministic invariants after every op,
 and statistical checks (uniformity, expected number of newly seen items,
 Appendix A residency).  The exact index path is this reading's own; it has no

@@ -12,6 +12,7 @@ so every drawn slot) is the same as on one stream.
 """
 from __future__ import annotations
 
+import contextlib
 from dataclasses import dataclass
 from typing import Callable, Optional
 
@@ -33,14 +34,24 @@ class ReceptionLog:
     Reservoir accepts a prefix that depends on its unseen count), so each put
     leaves its accepted count in a device word and the log resolves those
     counts only when a key that was offered before arrives again: new keys
-    never wait for the device."""
+    never wait for the device.
 
-    def __init__(self, device):
+    put_stream: the stream the puts run on (the reservoir's ordering stream).
+    The counts are cleared and read back on that stream, so a read waits for
+    every put enqueued before it, whichever stream is current (None: counts
+    in host memory, for host-only use)."""
+
+    def __init__(self, device, put_stream: Optional[torch.cuda.Stream] = None):
         self.received = set()
         self.offered = set()
         self.pending = []                  # (keys of one put in row order, index into the device counts)
-        self.counts = torch.zeros(4096, dtype=torch.int64, device=device)
+        self.put_stream = put_stream
+        with self._on_put_stream():
+            self.counts = torch.zeros(4096, dtype=torch.int64, device=device)
         self.next_count = 0
+
+    def _on_put_stream(self):
+        return torch.cuda.stream(self.put_stream) if self.put_stream is not None else contextlib.nullcontext()
 
     def count_slot(self) -> torch.Tensor:
         """Device int64 word for the next put's accepted count."""
@@ -57,7 +68,8 @@ class ReceptionLog:
     def resolve(self) -> None:
         """Read the pending accepted counts (waits for the puts)."""
         if self.pending:
-            a = self.counts[:self.next_count].cpu().tolist()
+            with self._on_put_stream():                   # ordered after the puts that write the counts
+                a = self.counts[:self.next_count].cpu().tolist()
             for keys, i in self.pending:
                 self.received.update(keys[:a[i]])
                 self.offered.difference_update(keys[a[i]:])     # refused rows may come again
@@ -163,7 +175,7 @@ class OnlineTrainer:
         self.lr_schedule = lr_schedule
         self.lr = lr
         self.val_loss = torch.zeros(1, device=dev)
-        self.log = ReceptionLog(dev) if reception_log else None
+        self.log = ReceptionLog(dev, self.res_stream) if reception_log else None
 
     def chunk_views(self, c: int):
         if self.chunk_fn is not None:
@@ -318,7 +330,7 @@ class OnlineTrainer:
         self.released_recorded = [False] * len(self.released_recorded)
         self.targets_read_recorded = False
         if self.log is not None:
-            self.log = ReceptionLog(self.xb.device)
+            self.log = ReceptionLog(self.xb.device, self.res_stream)
             self.log.received = {tuple(int(v) for v in k) for k in ckpt.get("received", np.zeros((0, 2)))}
             self.log.offered = set(self.log.received)
 

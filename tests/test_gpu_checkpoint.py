@@ -31,30 +31,35 @@ def make_trainer(w, inputs, fields, **kw):
                          w.reservoir_seed, w.init_seed, lr=w.lr, record_steps=200, reception_log=True, **kw)
 
 
-@pytest.mark.parametrize("precision", ["fp32", "bf16"])
-def test_restart_from_checkpoint_with_resent_messages(precision):
+@pytest.mark.parametrize("precision,overlap,ckpt_iter", [
+    ("fp32", False, 7), ("bf16", False, 7), ("fp32", True, 7), ("bf16", True, 7),
+    ("fp32", True, 3), ("fp32", False, 3)])
+def test_restart_from_checkpoint_with_resent_messages(precision, overlap, ckpt_iter):
+    """ckpt_iter 7: the checkpoint is taken after training started (iteration 4);
+    3: before the buffer reached its threshold.  overlap: puts and draws on the
+    reservoir's own stream, so the log reads accepted counts across streams."""
     from paper_2309_16743_amd import OT_BF16, OT_FP32
     w = configs.TINY
     X = heat.sample_parameters(w.n_sims, w.data_seed)
     inputs, fields = heat.inputs_for(X, w.tau), heat.heat_fields(X, w.grid, w.tau)
     prec = OT_BF16 if precision == "bf16" else OT_FP32
-    a = make_trainer(w, inputs, fields, precision=prec)
-    for _ in range(7):                                   # chunks 0..6 put, training from iteration 4
+    a = make_trainer(w, inputs, fields, precision=prec, overlap=overlap)
+    for _ in range(ckpt_iter):                           # chunks 0..ckpt_iter-1 put, training from iteration 4
         a.iterate()
     ckpt = a.checkpoint()
     steps_at_ckpt = a.steps_done
     for _ in range(3):
         a.iterate()
-    a.offer_chunk(5)                                     # a restarted client resends: discarded, no ticket
-    assert a.res.stats()["next_ticket"] == 10 + a.steps_done
+    a.offer_chunk(ckpt_iter + 1)                         # a restarted client resends: discarded, no ticket
+    assert a.res.stats()["next_ticket"] == ckpt_iter + 3 + a.steps_done
     while a.steps_done < 60:
         a.iterate()
     torch.cuda.synchronize()
 
-    b = make_trainer(w, inputs, fields, precision=prec)
+    b = make_trainer(w, inputs, fields, precision=prec, overlap=overlap)
     b.restore(ckpt)
     tickets0 = b.res.stats()["next_ticket"]
-    for c in range(7):                                   # every client starts again from its first step
+    for c in range(ckpt_iter):                           # every client starts again from its first step
         b.offer_chunk(c)
     assert b.res.stats()["next_ticket"] == tickets0     # all of them were received before the checkpoint
     while b.steps_done < 60:

@@ -5,7 +5,11 @@
 * Adam: the step-1 closed form (m_hat = g, v_hat = g^2, so the update is
   -lr * g / (|g| + eps)), and 100 steps against torch.optim.Adam in fp64;
 * MSE: hand-computed values;
-* bf16 rounding: hand cases at ties and against torch's bfloat16 conversion.
+* bf16 rounding: hand cases at ties and against torch's bfloat16 conversion;
+* bf16 mode: a hand-worked example in which each rounding point of the
+  mixed-precision reading changes the result (planted misplacements of those
+  points must fail it), equality with fp64 mode where every value is
+  bf16-representable, and closeness to fp64 mode on a workload-shaped net.
 """
 import numpy as np
 import pytest
@@ -146,3 +150,142 @@ def test_init_params_bounds_and_rows():
     rows = np.array([0, 5, 39])
     Wr, br = mlp.init_rows(widths, 3, 2, rows)
     assert np.array_equal(Wr, params[2][0][rows]) and np.array_equal(br, params[2][1][rows])
+
+
+# ---- bf16 mode (the mixed-precision reading of Sec. 4.1's bf16 workloads) ---------------
+#
+# A one-hidden-layer net, batch 1, input width 1, two hidden units (the second
+# dead), one output, worked by hand.  bf16 has 8 significant bits; in [1, 2)
+# its spacing is u = 2^-7 = 0.0078125, in [0.5, 1) it is 2^-8.
+#   x = 1.005859375 = 1 + 0.75u            (bf16: 1.0078125; layer 1 is fp32, so unrounded)
+#   W1 = [[1], [-1]], b1 = [0.25, 0]       -> Z1 = [1.255859375, -1.005859375]
+#   A1 = [1.255859375, 0]                  -> bf16(A1) = [1.2578125, 0]   (32.75u -> 33u)
+#   W2 = [[1.005859375, 5]], b2 = [0]      -> bf16(W2) = [[1.0078125, 5]]
+#   Y = 1.2578125 * 1.0078125 = 1.26763916015625
+#   U = 0.5166015625 (bf16 would give 0.515625; targets stay fp32)
+#   R = Y - U = 0.75103759765625; loss = R^2 (B D = 1) = 151413025 / 2^28
+#   dY = 2R = 1.5020751953125              -> bf16 1.5    (64.27u -> 64u)
+#   db2 = 1.5 (sum of the rounded dY)
+#   dW2 = dY * bf16(A1) = [1.5 * 1.2578125, 0] = [1.88671875, 0]
+#   dA1 = dY * bf16(W2) = [1.51171875, 7.5]; mask [1, 0] -> [1.51171875, 0]
+#   dZ1 = bf16 -> 1.515625                 (65.5u: a tie, to even 66u)
+#   dW1 = dZ1 * x = 1.515625 * 1.005859375 = 1.524505615234375; db1 = [1.515625, 0]
+HAND_PARAMS = [(np.array([[1.0], [-1.0]]), np.array([0.25, 0.0])),
+               (np.array([[1.005859375, 5.0]]), np.array([0.0]))]
+HAND_X = np.array([[1.005859375]])
+HAND_U = np.array([[0.5166015625]])
+HAND_LOSS = 151413025 / 2 ** 28
+HAND_GRADS = [(np.array([[1.524505615234375], [0.0]]), np.array([1.515625, 0.0])),
+              (np.array([[1.88671875, 0.0]]), np.array([1.5]))]
+
+
+def _hand_result(rounded=None):
+    loss, grads = mlp.loss_and_grads(HAND_PARAMS, HAND_X, HAND_U, bf16=True, rounded=rounded)
+    return loss, grads
+
+
+def _equals_hand(loss, grads):
+    return loss == HAND_LOSS and all(np.array_equal(g[i], h[i]) for g, h in zip(grads, HAND_GRADS)
+                                     for i in range(2))
+
+
+def test_bf16_hand_worked_one_hidden_layer():
+    loss, grads = _hand_result()
+    assert loss == HAND_LOSS
+    for (dW, db), (hW, hb) in zip(grads, HAND_GRADS):
+        assert np.array_equal(dW, hW) and np.array_equal(db, hb)
+    Y = mlp.predict(HAND_PARAMS, HAND_X, bf16=True)
+    assert Y[0, 0] == 1.26763916015625
+    # fp64 mode on the same net gives other values: every rounding is visible here
+    loss64, grads64 = mlp.loss_and_grads(HAND_PARAMS, HAND_X, HAND_U)
+    assert loss64 != HAND_LOSS and not np.array_equal(grads64[0][0], HAND_GRADS[0][0])
+
+
+# Each plant moves one rounding point of the bf16 reading; the quantities the
+# hand example says it changes must change.
+PLANTED = {
+    "no dZ rounding": (mlp.BF16_ROUNDED - {"dZ"}, "dW1 from 1.51171875 instead of 1.515625"),
+    "no dY rounding": (mlp.BF16_ROUNDED - {"dY"}, "db2 = 1.5020751953125"),
+    "no activation rounding": (mlp.BF16_ROUNDED - {"act"}, "Y from A1 = 1.255859375"),
+    "no weight rounding": (mlp.BF16_ROUNDED - {"weight"}, "Y from W2 = 1.005859375"),
+    "rounded layer-1 input": (mlp.BF16_ROUNDED | {"input"}, "dW1 = 1.515625 * 1.0078125"),
+    "rounded targets": (mlp.BF16_ROUNDED | {"target"}, "R from U = 0.515625"),
+    "db from unrounded dY": (mlp.BF16_ROUNDED | {"db_raw"}, "db2 = 1.5020751953125"),
+}
+
+
+@pytest.mark.parametrize("name", sorted(PLANTED))
+def test_bf16_planted_rounding_mistakes_fail_the_hand_example(name):
+    rounded, what = PLANTED[name]
+    loss, grads = _hand_result(rounded)
+    assert not _equals_hand(loss, grads), f"{name} ({what}) not detected"
+
+
+def test_bf16_planted_mistakes_hit_the_predicted_quantity():
+    _, g = _hand_result(PLANTED["no dZ rounding"][0])
+    assert g[0][0][0, 0] == 1.51171875 * 1.005859375
+    assert np.array_equal(g[1][0], HAND_GRADS[1][0]) and np.array_equal(g[1][1], HAND_GRADS[1][1])
+    _, g = _hand_result(PLANTED["rounded layer-1 input"][0])
+    assert g[0][0][0, 0] == 1.515625 * 1.0078125
+    _, g = _hand_result(PLANTED["db from unrounded dY"][0])
+    assert g[1][1][0] == 1.5020751953125 and np.array_equal(g[1][0], HAND_GRADS[1][0])
+    loss, _ = _hand_result(PLANTED["rounded targets"][0])
+    assert loss == (1.26763916015625 - 0.515625) ** 2
+    loss, _ = _hand_result(PLANTED["no activation rounding"][0])
+    assert loss == (1.255859375 * 1.0078125 - 0.5166015625) ** 2
+
+
+def _bf16_exact(v):
+    return np.array_equal(mlp.bf16_round(v), v)
+
+
+def test_bf16_mode_equals_fp64_when_every_value_is_representable():
+    """Small-integer nets with B*D a power of two: every operand, product sum
+    and gradient is exact in bf16 and in fp64, so the two modes agree bit for
+    bit (a dropped term, a wrong scale or an extra rounding would differ)."""
+    rng = np.random.default_rng(11)
+    checked = 0
+    for trial in range(400):
+        widths = (3, 4, 4, 2)
+        b = 4                                   # B * D = 8
+        params = [(rng.integers(-1, 2, size=(widths[l + 1], widths[l])).astype(np.float64),
+                   rng.integers(-2, 3, size=widths[l + 1]).astype(np.float64)) for l in range(3)]
+        X = rng.integers(0, 4, size=(b, widths[0])).astype(np.float64)
+        U = rng.integers(-8, 9, size=(b, widths[-1])).astype(np.float64)
+        Zs, As, Y = mlp.forward(params, X)
+        loss64, g64 = mlp.loss_and_grads(params, X, U)
+        R = Y - U
+        dY = 2.0 * R / R.size
+        dA = dY @ params[2][0]
+        dZ2 = dA * (Zs[1] > 0)
+        dZ1 = (dZ2 @ params[1][0]) * (Zs[0] > 0)
+        values = list(Zs) + list(As) + [dY, dA, dZ2, dZ1] + [a for pair in g64 for a in pair]
+        if not all(_bf16_exact(v) for v in values) or np.count_nonzero(R) == 0 or np.count_nonzero(dZ1) == 0:
+            continue
+        loss, g = mlp.loss_and_grads(params, X, U, bf16=True)
+        assert loss == loss64
+        for (a, c), (d, e) in zip(g, g64):
+            assert np.array_equal(a, d) and np.array_equal(c, e)
+        checked += 1
+        if checked == 20:
+            break
+    assert checked == 20
+
+
+def test_bf16_mode_close_to_fp64():
+    """bf16 against pure fp64 on a net shaped like the 16x16 workload (values
+    ~1e2 like the paper's temperatures): one bf16 rounding is <= 2^-9
+    relative, so per-tensor relative L2 differences of a few 2^-8 at most."""
+    widths = (6, 64, 64, 256)
+    params = mlp.init_params(widths, seed=1)
+    rng = np.random.default_rng(3)
+    X = np.concatenate([rng.uniform(100, 500, (32, 5)), rng.uniform(0.01, 0.1, (32, 1))], axis=1)
+    U = rng.uniform(100, 500, (32, 256))
+    loss, g = mlp.loss_and_grads(params, X, U, bf16=True)
+    loss64, g64 = mlp.loss_and_grads(params, X, U)
+    rels = [abs(loss - loss64) / loss64]
+    for (a, c), (d, e) in zip(g, g64):
+        rels += [np.linalg.norm(a - d) / np.linalg.norm(d), np.linalg.norm(c - e) / np.linalg.norm(e)]
+    print("bf16 vs fp64 relative L2 (loss, dW1, db1, dW2, db2, dW3, db3):", ["%.2e" % r for r in rels])
+    assert max(rels) < 2e-2
+    assert rels[0] > 0                         # the modes do differ

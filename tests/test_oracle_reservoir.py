@@ -2,7 +2,8 @@
 
 1. Exact distributions: for short operation sequences on tiny buffers, every
    draw outcome is enumerated with exact fractions, for the oracle and for a
-   literal two-list model of Algorithm 1; the distributions of everything
+   model of the buffer built from the behaviour Sec. 3.2.3 states
+   (tests/reservoir_model.py); the distributions of everything
    observable (accepted counts, batch contents in draw order, resident items
    with their draw counts) must be identical.
 2. Deterministic invariants after every operation on longer seeded runs.
@@ -17,7 +18,7 @@ import pytest
 
 from oracle import reservoir as rv
 from oracle.philox import KIND_EVICT, KIND_SAMPLE, draw_index
-from tests.alg1_lists import ListReservoir
+from tests.reservoir_model import BehaviourReservoir
 
 
 # --------------------------------------------------------------------------- enumeration
@@ -72,22 +73,20 @@ def run_slots_ids(C, T, ops, draw):
     return tuple(res), resident
 
 
-def run_lists(C, T, ops, draw):
-    m = ListReservoir(C, T, draw)
+def run_model(C, T, ops, draw):
+    m = BehaviourReservoir(C, T, draw)
     res = []
     for op in ops:
         if op[0] == "put":
             acc = 0
-            for _ in range(op[1]):
-                if not m.put():
-                    break
+            while acc < op[1] and m.store():
                 acc += 1
             res.append(("put", acc))
         elif op[0] == "batch":
             items = []
             status = None
             for _ in range(op[1]):
-                it = m.get()
+                it = m.draw_one()
                 if it in (m.NOT_READY, m.EMPTY):
                     if not items:
                         status = it
@@ -95,10 +94,9 @@ def run_lists(C, T, ops, draw):
                 items.append(it)
             res.append(("batch", status if status is not None else tuple(items)))
         else:
-            m.end_reception()
+            m.close()
             res.append(("end",))
-    resident = tuple(sorted((it, m.draw_count[it]) for it in m.seen + m.not_seen))
-    return tuple(res), resident
+    return tuple(res), m.resident()
 
 
 SEQUENCES = [
@@ -113,10 +111,10 @@ SEQUENCES = [
 
 
 @pytest.mark.parametrize("C,T,ops", SEQUENCES)
-def test_distribution_equals_literal_algorithm(C, T, ops):
+def test_distribution_equals_behavioural_model(C, T, ops):
     d_slots = enumerate_outcomes(lambda draw: run_slots_ids(C, T, ops, draw))
-    d_lists = enumerate_outcomes(lambda draw: run_lists(C, T, ops, draw))
-    assert d_slots == d_lists
+    d_model = enumerate_outcomes(lambda draw: run_model(C, T, ops, draw))
+    assert d_slots == d_model
 
 
 def test_enumeration_detects_a_biased_eviction():
@@ -138,7 +136,7 @@ def test_enumeration_detects_a_biased_eviction():
                 out.append(("batch", tuple(int(ids[s]) for s in slots)))
         return tuple(out), tuple(sorted((int(r.sample_id[s]), int(r.seen_count[s])) for s in r.occ))
 
-    assert enumerate_outcomes(biased) != enumerate_outcomes(lambda draw: run_lists(C, T, ops, draw))
+    assert enumerate_outcomes(biased) != enumerate_outcomes(lambda draw: run_model(C, T, ops, draw))
 
 
 # --------------------------------------------------------------------------- deterministic rules
