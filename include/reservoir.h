@@ -17,7 +17,8 @@
  * SC'11) with key (seed, 0) and counter (j, ticket, kind, 0), mapped onto
  * [0, n) as floor(w * n / 2^64); kind 1 = batch draw, 2 = eviction draw.
  * Tickets number the state-changing calls of one reservoir 0, 1, 2, ... in the
- * order the calls acquire the reservoir's lock; refused calls take no ticket.
+ * order the calls acquire the reservoir's lock; refused calls, and calls that
+ * fail before enqueueing any work, take no ticket.
  * Results depend only on (seed, the sequence of calls in ticket order).
  *
  * Memory and streams: the reservoir owns its device memory (slabs, per-slot
@@ -110,6 +111,9 @@ int reservoir_create(ot_reservoir** out, int64_t capacity, int64_t threshold,
  * j = replacement index); row F + j replaces victim j.  Each stored row gets
  * the next sample id and a seen count of 0.
  * accepted_dev: device int64 that receives a when the work runs (nullable).
+ * A buffer full of unseen samples (U = C) accepts a = 0: that "full" answer
+ * arrives only through accepted_dev; the status is still OT_OK, because U
+ * changes on the device and the host does not know it when the call returns.
  * ticket_out: host uint64 that receives the call's ticket (nullable).
  * FIFO / FIRO accept a = min(k, C - N) into the free slots (see above).
  * k may be 0 (takes a ticket, stores nothing).  1 <= k <= 4096 otherwise.

@@ -669,10 +669,12 @@ extern "C" int reservoir_put(ot_reservoir* r, const float* x, int64_t ldx, const
   hipStream_t cs = static_cast<hipStream_t>(stream);
   std::lock_guard<std::mutex> lock(r->mu);
   if (r->reception_over) return ot::set_error(OT_E_CLOSED, "reservoir_put: reception is over");
-  const uint64_t ticket = r->next_ticket++;
-  if (ticket_out) *ticket_out = ticket;
+  // the ticket is taken only once the ordering stream waits for the caller:
+  // a call that fails before enqueueing anything leaves the ticket sequence unchanged
   int rc = enter(r, cs);
   if (rc) return rc;
+  const uint64_t ticket = r->next_ticket++;
+  if (ticket_out) *ticket_out = ticket;
   ot::PhaseTimer& tm = r->timer;
   if (r->policy != OT_POLICY_RESERVOIR) {
     // FIFO / FIRO: the accepted prefix and every ring position are host-known
@@ -764,10 +766,10 @@ extern "C" int reservoir_sample_batch(ot_reservoir* r, int64_t b, void* stream, 
   } else if (r->n_host <= r->T) {
     return OT_NOT_READY;
   }
-  const uint64_t ticket = r->next_ticket++;
-  if (ticket_out) *ticket_out = ticket;
   int rc = enter(r, cs);
   if (rc) return rc;
+  const uint64_t ticket = r->next_ticket++;
+  if (ticket_out) *ticket_out = ticket;
   ot::PhaseTimer& tm = r->timer;
   tm.mark(r->stream, OT_PH_SELECT, 0);
   if (!r->reception_over && !list_take) {
