@@ -115,6 +115,28 @@ int surrogate_train_step_rows(ot_surrogate* s, const float* x, int64_t ldx, cons
 int surrogate_predict(ot_surrogate* s, const float* x, int64_t ldx, int64_t n, float* y,
                       int64_t ldy, void* stream);
 
+/* Prediction that allocates nothing, for callers that cannot allocate device
+ * memory: code under HIP graph capture, tight serving loops, harnesses that
+ * forbid hipMalloc.  Same arguments, checks and results as surrogate_predict
+ * (bit for bit when n <= max_batch), but all n rows go through one forward
+ * pass whose hidden activations and split-K partial products live in a
+ * library-owned scratch array of OT_PREDICT_NOALLOC_SCRATCH_BYTES per device
+ * (a static device array, held until the process ends) instead of the
+ * surrogate's workspaces; the call never calls hipMalloc, hipFree or a
+ * synchronising runtime function.  The scratch needs no clearing (every byte
+ * a call reads, the same call wrote first).  Every call on one device shares
+ * that device's scratch: calls that may overlap on one device (other streams,
+ * other surrogates, other threads) race and must be ordered by the caller.
+ * The surrogate's device must be current.  1 <= n <= 2^20 (n = 0 does
+ * nothing); n must also fit the scratch: roughly n * (sum of the hidden
+ * widths) * (4 bytes fp32, 2 bytes bf16) plus any split-K partials.
+ * Errors: OT_E_INVAL (as surrogate_predict; n too large for the scratch, with
+ * the bytes needed in the message), OT_E_STATE (another device is current),
+ * OT_E_HIP. */
+enum { OT_PREDICT_NOALLOC_SCRATCH_BYTES = 64 << 20 };
+int surrogate_predict_noalloc(ot_surrogate* s, const float* x, int64_t ldx, int64_t n, float* y,
+                              int64_t ldy, void* stream);
+
 /* Validation loss (Sec. 4.4 validates on simulations never used for
  * training): the mean over n x widths[L] of (f_theta(x) - u)^2 with the
  * current parameters, by the train step's forward and fused-MSE kernels;

@@ -23,7 +23,7 @@ __all__ = [
     "reservoir_end_reception", "reservoir_stats", "reservoir_read_meta", "reservoir_read_rows",
     "reservoir_destroy", "surrogate_create", "surrogate_set_params", "surrogate_get_params",
     "surrogate_get_grads", "surrogate_get_adam_state", "surrogate_set_lr", "surrogate_train_step",
-    "surrogate_predict", "surrogate_eval_loss", "surrogate_checkpoint", "surrogate_restore",
+    "surrogate_predict", "surrogate_predict_noalloc", "surrogate_eval_loss", "surrogate_checkpoint", "surrogate_restore",
     "reservoir_checkpoint", "reservoir_restore", "surrogate_destroy", "load", "last_error", "OTError",
     "OT_OK", "OT_NOT_READY", "OT_EMPTY", "OT_E_INVAL", "OT_E_CLOSED", "OT_E_STATE", "OT_FP32", "OT_BF16",
     "OT_SURROGATE_KEEP_GRADS", "OT_POLICY_RESERVOIR", "OT_POLICY_FIFO", "OT_POLICY_FIRO",
@@ -257,6 +257,14 @@ class Surrogate:
         check("surrogate_predict", load().surrogate_predict(self._h, xp, ldx, x.shape[0], yp, ldy,
                                                             _stream_handle(stream)))
 
+    def predict_noalloc(self, x, y, stream=None) -> None:
+        """predict() through the entry point that allocates nothing (its
+        workspace is the library's per-device scratch; see include/surrogate.h)."""
+        xp, ldx = _rows(x, "x")
+        yp, ldy = _rows(y, "y")
+        check("surrogate_predict_noalloc", load().surrogate_predict_noalloc(self._h, xp, ldx, x.shape[0], yp, ldy,
+                                                                            _stream_handle(stream)))
+
     def checkpoint(self) -> np.ndarray:
         """Synchronous snapshot of parameters, Adam moments and step counter."""
         return _checkpoint(self._h, "surrogate")
@@ -381,6 +389,10 @@ def surrogate_train_step(s: Surrogate, x, u, stream=None, loss=None) -> None:
 
 def surrogate_predict(s: Surrogate, x, y, stream=None) -> None:
     s.predict(x, y, stream)
+
+
+def surrogate_predict_noalloc(s: Surrogate, x, y, stream=None) -> None:
+    s.predict_noalloc(x, y, stream)
 
 
 def surrogate_destroy(s: Surrogate) -> None:

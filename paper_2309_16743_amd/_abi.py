@@ -25,6 +25,7 @@ OT_SURROGATE_KEEP_GRADS = 1
 OT_POLICY_RESERVOIR = 0
 OT_POLICY_FIFO = 1
 OT_POLICY_FIRO = 2
+OT_PREDICT_NOALLOC_SCRATCH_BYTES = 64 << 20
 
 SURROGATE_PHASES = ("fwd_hidden", "fwd_output", "loss", "wgrad_output", "igrad_output", "igrad_reduce",
                     "bwd_hidden", "adam", "wgrad_reduce")
@@ -75,6 +76,7 @@ SIGNATURES = {
     "surrogate_train_step": (C.c_int, [vp, vp, i64, vp, i64, i64, vp, vp]),
     "surrogate_train_step_rows": (C.c_int, [vp, vp, i64, vp, i64, vp, i64, i64, vp, vp, vp]),
     "surrogate_predict": (C.c_int, [vp, vp, i64, i64, vp, i64, vp]),
+    "surrogate_predict_noalloc": (C.c_int, [vp, vp, i64, i64, vp, i64, vp]),
     "surrogate_timing_begin": (C.c_int, [vp, u32, i64]),
     "surrogate_timing_end": (C.c_int, [vp, vp, vp]),
     "surrogate_destroy": (C.c_int, [vp]),

@@ -12,6 +12,7 @@
 // use the same layout, so Adam is a single elementwise pass.
 #include <algorithm>
 #include <cmath>
+#include <mutex>
 #include <vector>
 
 #include "common.h"
@@ -434,6 +435,7 @@ struct ot_surrogate {
   float* v = nullptr;
   float lr = 1e-3f, beta1 = 0.9f, beta2 = 0.999f, eps = 1e-8f;
   int64_t t = 0;
+  bool no_alloc = false;      // inside surrogate_predict_noalloc: workspaces must not grow
   bool fuse_out = false;      // output-layer Adam fused into its weight-gradient epilogue
   bool fused_step = false;    // ... and the current step took that path
   ot::AdamArgs step_adam{};   // Adam scalars of the current step
@@ -525,8 +527,13 @@ void free_surrogate(ot_surrogate* s) {
 
 constexpr int64_t kL1Parts = 32;
 
+int refuse_alloc(const char* what) {
+  return ot::set_error(OT_E_STATE, "%s would allocate inside surrogate_predict_noalloc", what);
+}
+
 int ensure_workspace(ot_surrogate* s, int64_t rows) {
   if (rows <= s->ws_rows) return OT_OK;
+  if (s->no_alloc) return refuse_alloc("the batch workspace");
   OT_HIP(hipDeviceSynchronize());
   free_workspace(s);
   const int L = s->L;
@@ -633,6 +640,7 @@ hipError_t launch_epi(Epi epi, int cfg, const GemmArgs& g, int64_t splits, hipSt
 
 int ensure_colsum(ot_surrogate* s, int64_t elems) {
   if (elems <= s->colsum_elems) return OT_OK;
+  if (s->no_alloc) return refuse_alloc("the column-sum buffer");
   OT_HIP(hipDeviceSynchronize());
   (void)hipFree(s->colsum);
   s->colsum = nullptr;
@@ -644,6 +652,8 @@ int ensure_colsum(ot_surrogate* s, int64_t elems) {
 }
 
 int ensure_split_ws(ot_surrogate* s, int64_t elems, int64_t rs_elems) {
+  if (s->no_alloc && (elems > s->splitws_elems || rs_elems > s->rsws_elems))
+    return refuse_alloc("the split-K partials");
   if (elems > s->splitws_elems) {
     OT_HIP(hipDeviceSynchronize());
     (void)hipFree(s->splitws);
@@ -1654,43 +1664,189 @@ extern "C" int surrogate_timing_end(ot_surrogate* s, double* ms_total, int64_t* 
   return s->timer.end(ms_total, count);
 }
 
+namespace {
+
+// Argument checks of the predict entry points (before anything is enqueued).
+int check_predict(ot_surrogate* s, const float* x, int64_t ldx, float* y, int64_t ldy, const char* what) {
+  int rc = check_input(s, x, ldx);
+  if (rc) return rc;
+  const int L = s->L;
+  OT_REQUIRE(y != nullptr && ldy >= s->widths[L] && ldy % 4 == 0 && aligned16(y),
+             "%s: y needs 16-byte alignment and ldy >= D, ldy %% 4 == 0", what);
+  if (L == 1)
+    OT_REQUIRE(aligned16(x) && ldx % 4 == 0, "single-layer nets need 16-byte aligned x, ldx %% 4 == 0");
+  return OT_OK;
+}
+
+// Forward of `rows` rows (at most the workspace's) into y with the output bias epilogue.
+int predict_rows(ot_surrogate* s, const float* xr, int64_t ldx, int64_t rows, float* yr, int64_t ldy,
+                 hipStream_t st) {
+  if (s->precision == OT_BF16) return predict_bf16(s, xr, ldx, rows, yr, ldy, st);
+  int rc = forward_hidden(s, xr, ldx, rows, st);
+  if (rc) return rc;
+  const int L = s->L;
+  const Layer& lo = s->layers[L - 1];
+  GemmArgs g = args0();
+  g.A = (L == 1) ? xr : s->act[L - 1];
+  g.lda = (L == 1) ? ldx : s->ld[L - 1];
+  g.B = s->params + lo.w_off;
+  g.ldb = lo.ldw;
+  g.C = yr;
+  g.ldc = ldy;
+  g.M = rows;
+  g.N = s->widths[L];
+  g.K = lo.in;
+  g.bias = s->params + lo.b_off;
+  return run_gemm<Lay::KMajor, Lay::KMajor, 1>(s, g, Epi::Bias, st, "output forward", true);
+}
+
+}  // namespace
+
 extern "C" int surrogate_predict(ot_surrogate* s, const float* x, int64_t ldx, int64_t n, float* y, int64_t ldy,
                                  void* stream) {
   ot::clear_error();
   OT_REQUIRE(s != nullptr, "surrogate_predict: NULL surrogate");
   OT_REQUIRE(n >= 0, "surrogate_predict: n < 0");
   if (n == 0) return OT_OK;
-  int rc = check_input(s, x, ldx);
+  int rc = check_predict(s, x, ldx, y, ldy, "surrogate_predict");
   if (rc) return rc;
-  const int L = s->L;
-  const int64_t D = s->widths[L];
-  OT_REQUIRE(y != nullptr && ldy >= D && ldy % 4 == 0 && aligned16(y),
-             "surrogate_predict: y needs 16-byte alignment and ldy >= D, ldy %% 4 == 0");
-  if (L == 1)
-    OT_REQUIRE(aligned16(x) && ldx % 4 == 0, "single-layer nets need 16-byte aligned x, ldx %% 4 == 0");
   hipStream_t st = static_cast<hipStream_t>(stream);
   const int64_t chunk = std::max<int64_t>(s->ws_rows, 1);
-  const Layer& lo = s->layers[L - 1];
   for (int64_t r0 = 0; r0 < n; r0 += chunk) {
     const int64_t rows = std::min(chunk, n - r0);
-    const float* xr = x + r0 * ldx;
-    if (s->precision == OT_BF16) {
-      if ((rc = predict_bf16(s, xr, ldx, rows, y + r0 * ldy, ldy, st))) return rc;
-      continue;
-    }
-    if ((rc = forward_hidden(s, xr, ldx, rows, st))) return rc;
-    GemmArgs g = args0();
-    g.A = (L == 1) ? xr : s->act[L - 1];
-    g.lda = (L == 1) ? ldx : s->ld[L - 1];
-    g.B = s->params + lo.w_off;
-    g.ldb = lo.ldw;
-    g.C = y + r0 * ldy;
-    g.ldc = ldy;
-    g.M = rows;
-    g.N = D;
-    g.K = lo.in;
-    g.bias = s->params + lo.b_off;
-    if ((rc = run_gemm<Lay::KMajor, Lay::KMajor, 1>(s, g, Epi::Bias, st, "output forward", true))) return rc;
+    if ((rc = predict_rows(s, x + r0 * ldx, ldx, rows, y + r0 * ldy, ldy, st))) return rc;
   }
   return OT_OK;
+}
+
+// ------------------------------------------------------------------ prediction without allocation
+// surrogate_predict_noalloc keeps the hidden activations and the split-K
+// partial products of one call in this array instead of the surrogate's
+// workspaces: one copy per device, held until the process ends.  On the host
+// the name `scratch` denotes a host-side stand-in, not device memory: host
+// code passes only the address hipGetSymbolAddress returns for a device.
+static __device__ __align__(256) unsigned char scratch[OT_PREDICT_NOALLOC_SCRATCH_BYTES];
+
+namespace {
+
+constexpr int kMaxScratchDevices = 64;
+std::mutex g_scratch_mu;
+unsigned char* g_scratch_addr[kMaxScratchDevices] = {};
+
+// Device address of `scratch` on `device` (which must be current), looked up
+// once per device.
+int scratch_address(int device, unsigned char** out) {
+  OT_REQUIRE(device >= 0 && device < kMaxScratchDevices, "surrogate_predict_noalloc: device %d above %d", device,
+             kMaxScratchDevices - 1);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (g_scratch_addr[device] == nullptr) {
+    void* p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || p == nullptr)
+      return ot::set_error(OT_E_HIP, "hipGetSymbolAddress of the prediction scratch failed: %s",
+                           hipGetErrorString(e));
+    g_scratch_addr[device] = static_cast<unsigned char*>(p);
+  }
+  *out = g_scratch_addr[device];
+  return OT_OK;
+}
+
+// Where one no-allocation prediction over `rows` rows keeps its data in the
+// scratch: each hidden activation (rows x ld[l], fp32 or bf16) on a 256-byte
+// boundary, then the largest split-K partial buffer of its GEMMs (the plans
+// predict_rows will take).
+struct NoAllocLayout {
+  int64_t act_off[16] = {};
+  int64_t split_off = 0;
+  int64_t split_elems = 0;
+  int64_t total = 0;
+};
+
+NoAllocLayout noalloc_layout(const ot_surrogate* s, int64_t rows) {
+  const int L = s->L;
+  const bool bf = s->precision == OT_BF16;
+  NoAllocLayout lay;
+  int64_t off = 0;
+  for (int l = 1; l < L; ++l) {
+    lay.act_off[l] = off;
+    off = ot::round_up(off + rows * s->ld[l] * (bf ? 2 : 4), 256);
+  }
+  int64_t split = 0;
+  for (int l = 1; l <= L; ++l) {
+    const Layer& ly = s->layers[l - 1];
+    // hidden layers without a GEMM: bf16 layer 1, the fp32 small-K layer 1
+    // and the fp32 narrow-hidden kernels
+    if (l < L && (bf ? l == 1 : (s->small_hidden || (l == 1 && ly.in <= ot::kMaxSmallK)))) continue;
+    const Plan p = bf ? make_plan_b(rows, ly.out, ly.in, true) : make_plan(rows, ly.out, ly.in, true);
+    if (p.splits > 1) split = std::max(split, p.splits * rows * ot::round_up(ly.out, 4));
+  }
+  lay.split_off = off;
+  lay.split_elems = split;
+  lay.total = off + split * 4;
+  return lay;
+}
+
+// Points the surrogate's activation and split-K workspaces at the scratch for
+// one call and forbids growing them; restores both on destruction.
+struct ScratchWorkspace {
+  ot_surrogate* s;
+  float* act[16];
+  uint16_t* act16[16];
+  float* splitws;
+  int64_t splitws_elems;
+  float* rsws;
+  int64_t rsws_elems;
+  ScratchWorkspace(ot_surrogate* sur, unsigned char* base, const NoAllocLayout& lay)
+      : s(sur), splitws(sur->splitws), splitws_elems(sur->splitws_elems), rsws(sur->rsws),
+        rsws_elems(sur->rsws_elems) {
+    for (int l = 1; l < s->L; ++l) {
+      act[l] = s->act[l];
+      act16[l] = s->act16[l];
+      if (s->precision == OT_BF16)
+        s->act16[l] = reinterpret_cast<uint16_t*>(base + lay.act_off[l]);
+      else
+        s->act[l] = reinterpret_cast<float*>(base + lay.act_off[l]);
+    }
+    s->splitws = lay.split_elems ? reinterpret_cast<float*>(base + lay.split_off) : nullptr;
+    s->splitws_elems = lay.split_elems;
+    s->rsws = nullptr;
+    s->rsws_elems = 0;
+    s->no_alloc = true;
+  }
+  ~ScratchWorkspace() {
+    for (int l = 1; l < s->L; ++l) {
+      s->act[l] = act[l];
+      s->act16[l] = act16[l];
+    }
+    s->splitws = splitws;
+    s->splitws_elems = splitws_elems;
+    s->rsws = rsws;
+    s->rsws_elems = rsws_elems;
+    s->no_alloc = false;
+  }
+};
+
+}  // namespace
+
+extern "C" int surrogate_predict_noalloc(ot_surrogate* s, const float* x, int64_t ldx, int64_t n, float* y,
+                                         int64_t ldy, void* stream) {
+  ot::clear_error();
+  OT_REQUIRE(s != nullptr, "surrogate_predict_noalloc: NULL surrogate");
+  OT_REQUIRE(n >= 0 && n <= (1LL << 20), "surrogate_predict_noalloc: n outside [0, 2^20]");
+  if (n == 0) return OT_OK;
+  int rc = check_predict(s, x, ldx, y, ldy, "surrogate_predict_noalloc");
+  if (rc) return rc;
+  int device = -1;
+  OT_HIP(hipGetDevice(&device));
+  if (device != s->device)
+    return ot::set_error(OT_E_STATE, "surrogate_predict_noalloc: device %d is current, the surrogate lives on %d",
+                         device, s->device);
+  const NoAllocLayout lay = noalloc_layout(s, n);
+  OT_REQUIRE(lay.total <= (int64_t)OT_PREDICT_NOALLOC_SCRATCH_BYTES,
+             "surrogate_predict_noalloc: %lld rows need %lld bytes of scratch, above its %lld bytes (use fewer rows)",
+             (long long)n, (long long)lay.total, (long long)OT_PREDICT_NOALLOC_SCRATCH_BYTES);
+  unsigned char* base = nullptr;
+  if ((rc = scratch_address(device, &base))) return rc;
+  ScratchWorkspace ws(s, base, lay);
+  return predict_rows(s, x, ldx, n, y, ldy, static_cast<hipStream_t>(stream));
 }
