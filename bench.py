@@ -12,19 +12,23 @@ as does a workload whose batch targets are under 1 MiB (tiny-16x16), where the
 step is launch-latency-bound and two cross-stream waits cost more than the
 overlap gains.
 
-Default workload (--config heat-100x100): 100x100 heat fields from an FTCS
-solver, 1000 simulations x 100 steps, MLP 6-256-256-10000 fp32, batch 1024,
-reservoir of 100,000 samples (threshold 16,667), chunks of the 100 concurrent
-simulations' current time step.  The whole ensemble is first streamed through
-the schedule (untimed), then the stream wraps around so every timed put
-replaces seen samples.
+Default workload (--config deep-sine-1000x1000): 1000x1000 fields (smooth
+sine-mode stand-ins for heat solutions, generated on the GPU), MLP
+6-2048-2048-2048-1,000,000 with bf16 GEMMs, fp32 master weights and Adam,
+batch 1024, a reservoir of 30,000 samples (120 GB) with threshold 5,000.  The
+reservoir is filled with generated chunks (untimed); during the timed steps
+8 producer streams (the paper's clients) each put chunks of 64 samples, one
+put per step in turn, concurrently with training ("mode B"); the same steps
+are then timed again with production suspended ("mode A", --prefilled makes
+it the headline).  --config sine-1000x1000: 6-1024-1024-1,000,000, batch
+512, 20,000 samples (80 GB), the same schedule.
 
---config sine-1000x1000 / deep-sine-1000x1000: 1000x1000 fields (smooth
-sine-mode stand-ins for heat solutions, generated on the GPU), bf16 GEMMs with
-fp32 master weights and Adam, batch 512 / 1024, reservoirs of 20,000 / 30,000
-samples (80 / 120 GB).  The reservoir is filled with generated chunks
-(untimed); timed puts cycle through a pool of pre-generated chunks of 64
-samples.
+--config heat-100x100: 100x100 heat fields from an FTCS solver, 1000
+simulations x 100 steps, MLP 6-256-256-10000 fp32, batch 1024, reservoir of
+100,000 samples (threshold 16,667), chunks of the 100 concurrent simulations'
+current time step.  The whole ensemble is first streamed through the
+schedule (untimed), then the stream wraps around so every timed put replaces
+seen samples.  --config tiny-16x16: the same at 16x16 (latency-bound).
 
 --config stress-100k-rows: the reservoir alone with rows of 100,000 floats,
 capacity 50,000 (20 GB slab), threshold 10,000, 64 producer streams putting
@@ -38,8 +42,10 @@ step (batch size x steps / time), from HIP events on the work stream over the
 timed steps.  `roofline` reports the dominant kernel's algorithmic rate
 against MI355X's datasheet peak, from HIP events that the library hands to
 that kernel's launch (hipExtLaunchKernel stamps them with the kernel's own
-start and end) on the stream it runs on, inside the same timed region.  `cpu_baseline` times the plain fp64 CPU oracle on a
-bounded sample of the same workload on this host.
+start and end) on the stream it runs on, inside the same timed region;
+`output_layer` does the same for the three output-layer GEMMs and
+`reservoir` for the put copies and the gather.  `cpu_baseline` times the
+plain fp64 CPU oracle on a bounded sample of the same workload on this host.
 """
 from __future__ import annotations
 
@@ -67,7 +73,9 @@ def parse_args():
     p.add_argument("--gpus", type=int, default=1)
     p.add_argument("--steps", type=int, default=None, help="timed steps (default 2000 fp32, 100 bf16)")
     p.add_argument("--warmup", type=int, default=None, help="untimed steps before timing (default 50 / 5)")
-    p.add_argument("--config", default="heat-100x100")
+    p.add_argument("--config", default="deep-sine-1000x1000")
+    p.add_argument("--producers", type=int, default=8,
+                   help="1000x1000 workloads: producer streams the timed puts come from, one put per step in turn")
     p.add_argument("--policy-comparison", action="store_true",
                    help="instead of the throughput benchmark: stream the heat-100x100 ensemble once through the "
                         "Reservoir, FIRO and FIFO buffers and report train steps and samples/s per buffer")
@@ -415,34 +423,90 @@ def cpu_baseline(w, inputs, fields, seconds: float) -> dict:
             "ms_per_step": round(dt / steps * 1e3, 1)}
 
 
-def cpu_baseline_scaled(w, seconds: float) -> dict:
-    """The fp64 oracle's train step at the bf16 workload's hidden widths but a
-    1/f slice of the output layer (the full 1M-wide output layer does not fit
-    a CPU time budget), timed and scaled by f; reservoir ops excluded."""
-    from oracle import mlp
+def _blas_threads() -> int:
     try:
         import threadpoolctl
-        blas_threads = max((b.get("num_threads", 1) for b in threadpoolctl.threadpool_info()), default=1)
+        return max((b.get("num_threads", 1) for b in threadpoolctl.threadpool_info()), default=1)
     except Exception:  # pragma: no cover
-        blas_threads = 1
-    f = 200
-    widths = list(w.widths[:-1]) + [w.widths[-1] // f]
+        return 1
+
+
+def linear_extrapolation(d1: float, t1: float, d2: float, t2: float, d: float):
+    """(a, b, t(d)) of the line t = a + b d through (d1, t1) and (d2, t2)."""
+    b = (t2 - t1) / (d2 - d1)
+    a = t1 - b * d1
+    return a, b, a + b * d
+
+
+def cpu_baseline_field(w, seconds: float) -> dict:
+    """The fp64 oracle's whole step at a 1000x1000 workload on this host.
+
+    Train step (bf16-rounding fp64 oracle): the hidden layers at full width,
+    the output layer at two slices of D (D/400 and D/200 outputs); a step's
+    time is a + b d in the output width d (every output-layer cost -- its
+    GEMMs, roundings and Adam -- is linear in d, the hidden layers are the
+    constant a), so the two timings give the full-width step without scaling
+    the hidden layers.  Reservoir (oracle put of one chunk + draw of a batch
+    with its gather) at the full row length on a host reservoir of B + 2 x
+    chunk rows (the per-step work does not depend on the capacity)."""
+    from fixtures import synthetic
+    from oracle import mlp
+    from oracle.reservoir import OK, Reservoir
+    blas_threads = _blas_threads()
     rng = np.random.default_rng(0)
-    params = mlp.init_params(widths, w.init_seed)
     X = np.concatenate([rng.uniform(100, 500, (w.batch, 5)), rng.uniform(0.01, 1.0, (w.batch, 1))], axis=1)
-    U = rng.uniform(100, 500, (w.batch, widths[-1]))
-    opt = mlp.Adam(lr=w.lr)
+    D = w.widths[-1]
+    timings = []
+    budget = seconds / 3
+    for f in (400, 200):
+        d = D // f
+        widths = list(w.widths[:-1]) + [d]
+        params = mlp.init_params(widths, w.init_seed)
+        U = rng.uniform(100, 500, (w.batch, d))
+        opt = mlp.Adam(lr=w.lr)
+        loss, grads = mlp.loss_and_grads(params, X, U, bf16=True)        # untimed first step
+        params = opt.step(params, grads)
+        steps = 0
+        t0 = time.perf_counter()
+        while steps < 1 or time.perf_counter() - t0 < budget:
+            loss, grads = mlp.loss_and_grads(params, X, U, bf16=True)
+            params = opt.step(params, grads)
+            steps += 1
+        timings.append((d, (time.perf_counter() - t0) / steps, steps))
+        del params, grads, opt, U
+    (d1, t1, n1), (d2, t2, n2) = timings
+    a, b, t_train = linear_extrapolation(d1, t1, d2, t2, D)
+    # reservoir ops at the full row length: a draw (with its gather) on a
+    # reservoir filled with unseen samples, then a put that replaces seen ones
+    C = w.batch + 2 * w.wave
+    res = Reservoir(C, w.batch, w.widths[0], D, w.reservoir_seed)
+    keys = np.arange(w.wave)
+    px = np.concatenate([rng.uniform(100, 500, (w.wave, 5)), np.full((w.wave, 1), 0.5)], axis=1).astype(np.float32)
+    pu = synthetic.hash_rows(keys, D).astype(np.float32)
+    while res.N < C:                                   # fill (untimed)
+        res.put(px, pu)
     steps = 0
     t0 = time.perf_counter()
-    while steps < 1 or time.perf_counter() - t0 < seconds:
-        loss, grads = mlp.loss_and_grads(params, X, U, bf16=True)
-        params = opt.step(params, grads)
+    while steps < 1 or time.perf_counter() - t0 < budget:
+        st, slots, xb, ub, _ = res.sample_batch(w.batch)
+        assert st == OK
+        del xb, ub
+        _, acc, _, _ = res.put(px, pu)
+        assert acc == w.wave
         steps += 1
-    dt = (time.perf_counter() - t0) / steps * f
-    return {"value": round(w.batch / dt, 3), "unit": "samples/s", "cores": blas_threads, "kind": "oracle",
-            "sample": f"{steps} fp64 bf16-rounding train steps of {'-'.join(map(str, widths))} "
-                      f"(output layer 1/{f} of {w.widths[-1]}), step time scaled by {f}; reservoir ops excluded",
-            "ms_per_step": round(dt * 1e3, 1)}
+    t_res = (time.perf_counter() - t0) / steps
+    del res
+    t_step = t_train + t_res
+    return {"value": round(w.batch / t_step, 3), "unit": "samples/s", "cores": blas_threads, "kind": "oracle",
+            "sample": f"fp64 oracle (bf16 rounding points) train steps of {'-'.join(map(str, w.widths[:-1]))} with "
+                      f"output slices of {d1} ({n1} steps, {t1:.3f} s each) and {d2} ({n2} steps, {t2:.3f} s) "
+                      f"outputs, the step time extrapolated linearly in the output width to {D} "
+                      f"(hidden layers {a:.3f} s + {b * 1e6:.3f} us per output unit); plus {steps} oracle "
+                      f"iterations of draw {w.batch} with gather + put {w.wave} rows of {D} floats on a host "
+                      f"reservoir of {C} rows ({t_res:.3f} s each); numpy BLAS threads {blas_threads}, "
+                      f"{len(os.sched_getaffinity(0))} host cores visible; reservoir copies one thread",
+            "ms_per_step": round(t_step * 1e3, 1), "train_ms": round(t_train * 1e3, 1),
+            "reservoir_ms": round(t_res * 1e3, 1)}
 
 
 def timed_region(tr, w, K, profile_steps, stream, wrap_put):
@@ -464,9 +528,11 @@ def timed_region(tr, w, K, profile_steps, stream, wrap_put):
     dominant = max((c for c in candidates if c in breakdown), key=lambda p: breakdown[p]["avg_us"])
     dom_phase = "gather" if dominant == "reservoir_gather" else dominant
 
-    if dom_phase != "gather":
-        tr.sur.timing_begin([dom_phase], K)
-    tr.res.timing_begin(["gather"], 2 * K)
+    # timed region: the dominant kernel, the three output-layer GEMMs, the put copies and the gather
+    out_phases = [p for p in ("fwd_output", "wgrad_output", "igrad_output") if p in breakdown]
+    sur_phases = [p for p in SURROGATE_PHASES if p in out_phases or p == dom_phase]
+    tr.sur.timing_begin(sur_phases, K)
+    tr.res.timing_begin(["put_copy", "gather"], 2 * K)
     n_win = K // 10
     ev = [torch.cuda.Event(enable_timing=True) for _ in range(n_win + 2)]
     torch.cuda.synchronize()
@@ -484,22 +550,76 @@ def timed_region(tr, w, K, profile_steps, stream, wrap_put):
     wall = time.perf_counter() - t0
     gpu_ms = ev[0].elapsed_time(ev[-1])
     windows = [ev[j].elapsed_time(ev[j + 1]) for j in range(n_win)]
-    g_ms, g_n = tr.res.timing_end()["gather"]
-    if dom_phase == "gather":
-        dom_avg_s = g_ms / g_n * 1e-3
-    else:
-        dom_ms, dom_n = tr.sur.timing_end()[dom_phase]
-        dom_avg_s = dom_ms / dom_n * 1e-3
+    res_t = tr.res.timing_end()
+    sur_t = tr.sur.timing_end()
+    g_ms, g_n = res_t["gather"]
+    phase_avg_s = {p: sur_t[p][0] / sur_t[p][1] * 1e-3 for p in sur_phases if p in sur_t}
+    put_avg_s = res_t["put_copy"][0] / res_t["put_copy"][1] * 1e-3 if "put_copy" in res_t else None
+    dom_avg_s = g_ms / g_n * 1e-3 if dom_phase == "gather" else phase_avg_s[dom_phase]
     achievable = achievable_rates(w.precision)      # after the timed region, which it does not disturb
     return dict(gpu_ms=gpu_ms, wall=wall, windows=windows, breakdown=breakdown, dom_phase=dom_phase,
                 achievable=achievable, dom_avg_s=dom_avg_s, gather_avg_s=g_ms / g_n * 1e-3,
-                loss=float(tr.loss.item()))
+                phase_avg_s=phase_avg_s, put_avg_s=put_avg_s, loss=float(tr.loss.item()))
+
+
+def steps_rate(tr, w, K, stream, wrap_put) -> dict:
+    """Samples/s of K more steps, HIP events on the work stream."""
+    import torch
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record(stream)
+    if tr.overlap:
+        tr.res_stream.wait_event(e0)
+    for _ in range(K):
+        wrap_put()
+        assert tr.sample_and_train()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1)
+    return {"value": round(w.batch * K / (ms * 1e-3), 1), "unit": "samples/s", "steps": K,
+            "ms_per_step": round(ms / K, 4)}
+
+
+def output_layer_entry(w, phase_avg_s: dict) -> dict:
+    """Rates of the output layer's three GEMMs measured in the timed region:
+    forward (+ fused MSE) and input gradient against the MFMA peak of their
+    precision; the weight gradient too, and in bf16, where it applies Adam to
+    the output weights in its epilogue, also against HBM."""
+    peak = PEAK_BF16_MFMA if w.precision == "bf16" else PEAK_FP32_MFMA
+    out = {}
+    for p in ("fwd_output", "igrad_output", "wgrad_output"):
+        if p not in phase_avg_s:
+            continue
+        t = phase_avg_s[p]
+        e = {"avg_us": round(t * 1e6, 2), "tflops": round(gemm_flops(w) / t / 1e12, 1),
+             "frac_mfma": round(gemm_flops(w) / t / peak, 4)}
+        if p == "wgrad_output" and w.precision == "bf16":
+            e.update(fused_adam=True, achieved_gbs=round(fused_adam_bytes(w) / t / 1e9, 1),
+                     frac_hbm=round(fused_adam_bytes(w) / t / PEAK_HBM, 4))
+        out[p] = e
+    out["peak_tflops"] = peak / 1e12
+    return out
+
+
+def reservoir_entry(w, r) -> dict:
+    """Put copies (whole rows into the slab: the reservoir's bandwidth at this
+    shape) and the batch gather, timed in the timed region."""
+    g_rate = gather_bytes(w) / r["gather_avg_s"]
+    out = {"gather": {"achieved": round(g_rate / 1e9, 1), "unit": "GB/s", "frac_hbm": round(g_rate / PEAK_HBM, 4),
+                      "avg_us": round(r["gather_avg_s"] * 1e6, 2), "bytes_per_launch": gather_bytes(w),
+                      "rows": "input rows only (the targets are read in place by the forward)"
+                      if not GATHERED_TARGETS else "input and field rows"}}
+    if r.get("put_avg_s"):
+        p_rate = put_bytes(w) / r["put_avg_s"]
+        out["put_copy"] = {"achieved": round(p_rate / 1e9, 1), "unit": "GB/s", "frac_hbm": round(p_rate / PEAK_HBM, 4),
+                           "avg_us": round(r["put_avg_s"] * 1e6, 2), "bytes_per_launch": put_bytes(w),
+                           "rows": f"{w.wave} whole rows read from the producer and written to the slab"}
+    return out
 
 
 def result_line(w, args, K, warmup, r, config: dict) -> dict:
     value = w.batch * K / (r["gpu_ms"] * 1e-3)
     win_sps = [10 * w.batch / (t * 1e-3) for t in r["windows"]] if r["windows"] else [value]
-    gather_rate = gather_bytes(w) / r["gather_avg_s"]
     return {
         "metric": METRIC, "value": round(value, 1), "unit": "samples/s", "n_gpus": 1, "steps": K,
         "warmup": warmup, "ms_per_step": round(r["gpu_ms"] / K, 4), "higher_is_better": True,
@@ -507,9 +627,8 @@ def result_line(w, args, K, warmup, r, config: dict) -> dict:
         "data": "synthetic", "config": config,
         "roofline": with_achievable(roofline_entry(w, r["dom_phase"], r["dom_avg_s"]), r["achievable"]),
         "achievable": r["achievable"],
-        "reservoir_gather": {"achieved": round(gather_rate / 1e9, 1), "unit": "GB/s",
-                             "frac_hbm": round(gather_rate / PEAK_HBM, 4),
-                             "avg_us": round(r["gather_avg_s"] * 1e6, 2)},
+        "output_layer": output_layer_entry(w, r["phase_avg_s"]),
+        "reservoir": reservoir_entry(w, r),
         "windows_of_10": {"median_samples_s": round(float(np.median(win_sps)), 1),
                           "mean_samples_s": round(float(np.mean(win_sps)), 1), "n": len(win_sps)},
         "wall_s": round(r["wall"], 3), "last_loss": r["loss"], "kernels": r["breakdown"], "cpu_baseline": None,
@@ -671,8 +790,10 @@ def run_field(args, w):
         xbuf[:, :5] = sims.to(torch.float32)
         xbuf[:, 5] = t.to(torch.float32)
 
+    P = max(1, args.producers)
+    producers = [torch.cuda.Stream(device=dev) for _ in range(P)]    # default priority, like every stream here
     with torch.cuda.stream(stream):
-        pool = 8
+        pool = max(P, 8)                        # pre-generated chunks the timed puts cycle through
         pool_x = [torch.empty(w.wave, 8, device=dev)[:, :6] for _ in range(pool)]
         pool_u = [torch.empty(w.wave, D, device=dev) for _ in range(pool)]
         first_pool_chunk = w.n_chunks // 2
@@ -681,7 +802,8 @@ def run_field(args, w):
         tr = OnlineTrainer(w.widths, w.batch, w.capacity, w.threshold, w.wave, w.tau, None, None,
                            w.reservoir_seed, w.init_seed, precision=OT_BF16, lr=w.lr, stream=stream,
                            chunk_fn=lambda c: (pool_x[c % pool], pool_u[c % pool]), n_chunks=1 << 40, device=dev,
-                           overlap=not one_stream(args, w), fused_targets=not args.gathered_targets)
+                           overlap=not one_stream(args, w), fused_targets=not args.gathered_targets,
+                           put_streams=producers)
         fx = torch.empty(w.wave, 8, device=dev)[:, :6]
         fu = torch.empty(w.wave, D, device=dev)
         t_fill = time.perf_counter()
@@ -700,19 +822,26 @@ def run_field(args, w):
         print(f"[bench] filled {n_stored} samples ({n_stored * D * 4 / 1e9:.0f} GB) in "
               f"{time.perf_counter() - t_fill:.1f} s; {tr.steps_done} warm-up steps",
               file=sys.stderr, flush=True)
-        r = timed_region(tr, w, K, args.profile_steps or 20, stream, (lambda: None) if args.prefilled else (lambda: tr.put_next(wrap=True)))
+        put = (lambda: None) if args.prefilled else (lambda: tr.put_next(wrap=True))
+        r = timed_region(tr, w, K, args.profile_steps or 20, stream, put)
+        # the other mode, same steps: production suspended (mode A) or running (mode B)
+        other = steps_rate(tr, w, K, stream, (lambda: tr.put_next(wrap=True)) if args.prefilled else (lambda: None))
+    mode_b = f"{P} producer streams, one put of {w.wave} samples per step in turn, concurrent with training"
+    mode_a = "production suspended: draws and train steps on the filled reservoir"
     config = {"workload": w.name, "fields": f"sine-mode {n}x{n}, {w.n_sims} sims x {w.tau} steps",
               "widths": list(w.widths), "batch": w.batch, "capacity": w.capacity, "threshold": w.threshold,
-              "put_rows_per_step": w.wave, "precision": w.precision,
+              "put_rows_per_step": 0 if args.prefilled else w.wave, "precision": w.precision,
               "reservoir_stream": stream_mode(args, w),
               "targets": "gathered into a batch buffer" if args.gathered_targets
               else "read in place from the reservoir by the forward (inputs gathered)",
-              "timed_puts": "none (pre-filled reservoir)" if args.prefilled else "one per step"}
+              "timed_puts": ("mode A: " + mode_a) if args.prefilled else ("mode B: " + mode_b)}
     line = result_line(w, args, K, warmup, r, config)
+    other.update(mode=("B: " + mode_b) if args.prefilled else ("A: " + mode_a))
+    line["other_mode"] = other
     tr.close()
     torch.cuda.empty_cache()
     if args.cpu_seconds > 0:
-        line["cpu_baseline"] = cpu_baseline_scaled(w, args.cpu_seconds)
+        line["cpu_baseline"] = cpu_baseline_field(w, args.cpu_seconds)
     return line
 
 

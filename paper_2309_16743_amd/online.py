@@ -119,7 +119,7 @@ class OnlineTrainer:
                  chunk_fn: Optional[Callable] = None, n_chunks: int = 0, device=None, flags: int = 0,
                  overlap: bool = False, policy: int = OT_POLICY_RESERVOIR,
                  lr_schedule: Optional[Callable[[int], float]] = None, reception_log: bool = False,
-                 fused_targets: bool = True):
+                 fused_targets: bool = True, put_streams: Optional[list] = None):
         self.stream = stream if stream is not None else torch.cuda.current_stream()
         self.widths = tuple(widths)
         self.batch, self.wave, self.tau = batch, wave, tau
@@ -176,6 +176,9 @@ class OnlineTrainer:
         self.lr = lr
         self.val_loss = torch.zeros(1, device=dev)
         self.log = ReceptionLog(dev, self.res_stream) if reception_log else None
+        # producer streams (the paper's clients): chunk c is put from put_streams[c mod P];
+        # default: the reservoir's own stream
+        self.put_streams = list(put_streams) if put_streams else None
 
     def chunk_views(self, c: int):
         if self.chunk_fn is not None:
@@ -206,8 +209,9 @@ class OnlineTrainer:
             self._train_done.record(self.stream)
             self.res_stream.wait_event(self._train_done)
         self._wait_targets_read()                 # a put may overwrite rows the last train step reads
+        put_stream = self.put_streams[c % len(self.put_streams)] if self.put_streams else self.res_stream
         if self.log is None:
-            self.res.put(x, u, stream=self.res_stream, accepted=self.accepted)
+            self.res.put(x, u, stream=put_stream, accepted=self.accepted)
             return
         keys = self.chunk_keys(c)
         keep = self.log.new_rows(keys)
@@ -220,7 +224,7 @@ class OnlineTrainer:
             while j < len(keys) and keep[j]:
                 j += 1
             slot = self.log.count_slot()
-            self.res.put(x[i:j], u[i:j], stream=self.res_stream, accepted=slot)
+            self.res.put(x[i:j], u[i:j], stream=put_stream, accepted=slot)
             self.log.record(keys[i:j], self.log.next_count - 1)
             i = j
 
