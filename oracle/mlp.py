@@ -144,6 +144,12 @@ def loss_and_grads(params: Params, X: np.ndarray, U: np.ndarray, bf16: bool = Fa
     loss = float(np.sum(R * R) / R.size)
     dZ_raw = 2.0 * R / R.size                 # dLoss/dY
     dZ = rnd("dY", dZ_raw)
+    return loss, _backprop(params, Zs, As, dZ, dZ_raw, rnd, points)
+
+
+def _backprop(params: Params, Zs, As, dZ, dZ_raw, rnd, points) -> Params:
+    """Gradients of every layer of `params`, from dLoss/dZ of the last one
+    (dZ as the GEMMs read it, dZ_raw before rounding), layer by layer down."""
     L = len(params)
     grads: Params = [None] * L                # type: ignore[list-item]
     for l in range(L - 1, -1, -1):
@@ -156,12 +162,82 @@ def loss_and_grads(params: Params, X: np.ndarray, U: np.ndarray, bf16: bool = Fa
             dA = dZ @ rnd("weight", W)
             dZ_raw = dA * (Zs[l - 1] > 0.0)
             dZ = rnd("dZ", dZ_raw)
-    return loss, grads
+    return grads
+
+
+def hidden_grads(params: Params, Zs, dA: np.ndarray, As, bf16: bool = False, rounded=None) -> Params:
+    """Gradients of the hidden layers `params` given dLoss/dA of the last of
+    them: the part of loss_and_grads below the output layer, for callers that
+    form the output layer's input gradient dA themselves (by column chunks at
+    full output width, output_layer_by_columns).  Zs, As: forward(params, X)
+    of the hidden layers alone (Zs[-1] is the last hidden pre-activation)."""
+    rnd, points = _rounder(bf16, rounded)
+    dZ_raw = np.asarray(dA, dtype=np.float64) * (Zs[-1] > 0.0)
+    return _backprop(params, Zs, As, rnd("dZ", dZ_raw), dZ_raw, rnd, points)
+
+
+def output_layer_by_columns(A_in: np.ndarray, weight_rows, bias: np.ndarray, target_cols, D: int, chunk: int,
+                            bf16: bool = False, rows=(), rounded=None):
+    """The output layer's share of loss_and_grads, formed over column chunks
+    of the D outputs so that a 10^6-wide layer need not be held at once:
+    A_in (B x H) is the last hidden activation (before rounding);
+    weight_rows(j0, j1) and target_cols(j0, j1) give W_L[j0:j1] (j1 - j0 x H)
+    and U[:, j0:j1].  Returns (loss, dA_in, db, dW rows) with dA_in = dY W_L
+    (what hidden_grads takes), db (D) and dW_L[rows] (len(rows) x H).  Each
+    chunk applies the same rounding points as loss_and_grads; the sums over
+    chunks (loss, dA_in) are fp64, in chunk order.  torch CPU fp64 carries
+    the products and the elementwise steps (multi-threaded)."""
+    import torch
+    rnd, points = _rounder(bf16, rounded)
+
+    def trnd(point, t):
+        return bf16_round_torch(t) if point in points else t
+
+    A = torch.from_numpy(np.asarray(A_in, dtype=np.float64))
+    B, H = A.shape
+    Ar = trnd("act", A)
+    rows = np.asarray(rows, dtype=np.int64)
+    loss_sum = 0.0
+    dA = torch.zeros(B, H, dtype=torch.float64)
+    db = np.zeros(D)
+    dW_rows = np.zeros((len(rows), H))
+    for j0 in range(0, D, chunk):
+        j1 = min(D, j0 + chunk)
+        W = trnd("weight", torch.from_numpy(np.asarray(weight_rows(j0, j1))).to(torch.float64))
+        U = trnd("target", torch.from_numpy(np.asarray(target_cols(j0, j1))).to(torch.float64))
+        R = torch.addmm(torch.from_numpy(np.asarray(bias[j0:j1], dtype=np.float64)), Ar, W.T)
+        R.sub_(U)
+        loss_sum += float(torch.sum(R * R))
+        dY_raw = R.mul_(2.0).div_(B * D)         # 2 R / (B D), as loss_and_grads forms it
+        dY = trnd("dY", dY_raw)
+        dA.addmm_(dY, W)
+        db[j0:j1] = (dY_raw if "db_raw" in points else dY).sum(dim=0).numpy()
+        sel = (rows >= j0) & (rows < j1)
+        if sel.any():
+            dW_rows[sel] = (dY[:, torch.from_numpy(rows[sel] - j0)].T @ Ar).numpy()
+    return loss_sum / (B * D), dA.numpy(), db, dW_rows
+
+
+def bf16_round_torch(t):
+    """bf16_round on a torch fp64 CPU tensor (the same bit operation: round the
+    fp32 value half to even at its 16th bit), fp64 out."""
+    import torch
+    b = t.to(torch.float32).view(torch.int32)
+    lsb = torch.bitwise_and(torch.bitwise_right_shift(b, 16), 1)
+    b = b.add_(0x7FFF).add_(lsb)
+    b = torch.bitwise_and(b, -65536, out=b)
+    return b.view(torch.float32).to(torch.float64)
 
 
 @dataclass
 class Adam:
-    """Adam with bias correction (Kingma and Ba, 2015, Algorithm 1)."""
+    """Adam with bias correction (Kingma and Ba, 2015, Algorithm 1).
+
+    state_dtype: None keeps parameters and moments in fp64; np.float32 rounds
+    them to fp32 after every step, as a path that stores fp32 master weights
+    and moments does.  The arithmetic of a step is fp64 either way; the
+    rounded variant exists to measure how far fp32 storage alone moves a long
+    run (the sensitivity of a comparison after many steps)."""
     lr: float = 1e-3
     beta1: float = 0.9
     beta2: float = 0.999
@@ -169,6 +245,7 @@ class Adam:
     t: int = 0
     m: list = field(default_factory=list)
     v: list = field(default_factory=list)
+    state_dtype: object = None
 
     def step(self, params: Params, grads: Params) -> Params:
         if not self.m:
@@ -183,8 +260,11 @@ class Adam:
             for i, (p, g) in enumerate(((W, gW), (b, gb))):
                 m = self.beta1 * self.m[l][i] + (1.0 - self.beta1) * g
                 v = self.beta2 * self.v[l][i] + (1.0 - self.beta2) * g * g
+                q = p - self.lr * (m / c1) / (np.sqrt(v / c2) + self.eps)
+                if self.state_dtype is not None:
+                    m, v, q = (np.asarray(a).astype(self.state_dtype).astype(np.float64) for a in (m, v, q))
                 self._store(l, i, m, v)
-                new.append(p - self.lr * (m / c1) / (np.sqrt(v / c2) + self.eps))
+                new.append(q)
             out.append((new[0], new[1]))
         return out
 

@@ -95,18 +95,21 @@ def chunk_arrays(w: Workload, inputs: np.ndarray, fields: np.ndarray, chunk: int
 def run(w: Workload, inputs: np.ndarray, fields: np.ndarray, n_steps: int,
         params=None, bf16: Optional[bool] = None, keep_grads: Iterable[int] = (),
         lr: Optional[float] = None, lr_halving: Optional[tuple] = None,
-        validation: Optional[tuple] = None) -> Dict:
+        validation: Optional[tuple] = None, state_fp32: bool = False) -> Dict:
     """Run the schedule until n_steps train steps are done; return the trace.
-    lr_halving: (every_samples, lr_min); validation: (X_val, U_val, every)."""
+    lr_halving: (every_samples, lr_min); validation: (X_val, U_val, every);
+    state_fp32: parameters and Adam moments stored in fp32 between steps
+    (Adam.state_dtype).  For each step in keep_grads the trace holds its
+    gradients, the parameters after it and the batch (X, U) it trained on."""
     if bf16 is None:
         bf16 = w.precision == "bf16"
     res = Reservoir(w.capacity, w.threshold, inputs.shape[-1], fields.shape[-1], w.reservoir_seed)
     if params is None:
         params = init_params(w.widths, w.init_seed)
     lr0 = w.lr if lr is None else lr
-    opt = Adam(lr=lr0)
+    opt = Adam(lr=lr0, state_dtype=np.float32 if state_fp32 else None)
     keep = set(keep_grads)
-    trace = dict(losses=[], slots=[], tickets=[], put_accepted=[], grads={}, params_at={}, lrs=[],
+    trace = dict(losses=[], slots=[], tickets=[], put_accepted=[], grads={}, params_at={}, batches={}, lrs=[],
                  val_losses={})
     i = done = 0
     while done < n_steps:
@@ -132,6 +135,7 @@ def run(w: Workload, inputs: np.ndarray, fields: np.ndarray, n_steps: int,
             if done in keep:
                 trace["grads"][done] = grads
                 trace["params_at"][done] = params
+                trace["batches"][done] = (xb, ub)
         elif st == NOT_READY and chunk is None:
             raise RuntimeError("schedule ran out of data before the buffer became ready")
         i += 1

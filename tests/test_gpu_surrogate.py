@@ -1,8 +1,10 @@
 """GPU surrogate against the fp64 oracle: initialisation (bit-exact), one train
 step (loss, every gradient, parameters after Adam) over shapes that span
 several tiles, ragged edges, split-K and the small-K first layer; prediction;
-and 100 online steps on the 16x16 workload (slots bit-exact, loss, gradients
-and parameters within 1e-3 relative L2)."""
+100 online steps on the 16x16 workload and on the 100x100 workload at its
+full shape (slots bit-exact, loss, gradients and parameters within 1e-3
+relative L2).  Gradients are also held element by element: every entry
+within the tolerance times the largest reference entry."""
 import numpy as np
 import pytest
 import torch
@@ -19,6 +21,19 @@ def rel(a, b):
     a = np.asarray(a, dtype=np.float64)
     b = np.asarray(b, dtype=np.float64)
     return float(np.linalg.norm(a - b) / max(np.linalg.norm(b), 1e-30))
+
+
+def elementwise(a, b):
+    """Largest entry difference relative to the largest reference entry."""
+    a = np.asarray(a, dtype=np.float64)
+    b = np.asarray(b, dtype=np.float64)
+    return float(np.max(np.abs(a - b))) / max(float(np.max(np.abs(b))), 1e-30)
+
+
+def close(a, b, tol):
+    """Relative L2 within tol and every element within tol of the largest
+    reference entry (so that one wrong output unit among thousands fails)."""
+    return rel(a, b) < tol and elementwise(a, b) < tol
 
 
 def padded_from(arr):
@@ -91,8 +106,8 @@ def test_one_train_step(widths, B):
     L = len(widths) - 1
     for l in range(L):
         gW, gb = s.get_grads(l)
-        assert rel(gW, o_grads[l][0]) < 1e-4, (l, rel(gW, o_grads[l][0]))
-        assert rel(gb, o_grads[l][1]) < 1e-4, (l, rel(gb, o_grads[l][1]))
+        assert close(gW, o_grads[l][0], 1e-4), (l, rel(gW, o_grads[l][0]))
+        assert close(gb, o_grads[l][1], 1e-4), (l, rel(gb, o_grads[l][1]))
         W, b = s.get_params(l)
         assert rel(W, o_new[l][0]) < 1e-4 and rel(b, o_new[l][1]) < 1e-4
         Wf, bf = f.get_params(l)
@@ -163,8 +178,8 @@ def test_tiny_workload_100_steps():
     grads100 = [tr.sur.get_grads(l) for l in range(3)]
     for l in range(3):
         for i in range(2):
-            assert rel(grads1[l][i], ref["grads"][1][l][i]) < 1e-3
-            assert rel(grads100[l][i], ref["grads"][100][l][i]) < 1e-3
+            assert close(grads1[l][i], ref["grads"][1][l][i], 1e-3)
+            assert rel(grads100[l][i], ref["grads"][100][l][i]) < 1e-3    # L2 after 99 Adam steps
         W, b = tr.sur.get_params(l)
         assert rel(W, ref["params"][l][0]) < 1e-3 and rel(b, ref["params"][l][1]) < 1e-3
     st = tr.res.stats()
@@ -472,4 +487,96 @@ def test_full_net_online_schedule_with_evictions():
     for l in range(3):
         W, b = tr.sur.get_params(l)
         assert rel(W, ref["params"][l][0]) < 1e-3 and rel(b, ref["params"][l][1]) < 1e-3
+    tr.close()
+
+
+_HEAT_FULL = {}
+
+
+def heat_full_shape_reference():
+    """Inputs and the oracle's 100-step run of the full-shape 100x100 workload
+    (computed once for both parametrisations of the test below)."""
+    if not _HEAT_FULL:
+        import dataclasses
+        w = dataclasses.replace(configs.HEAT100, n_sims=300)
+        X = heat.sample_parameters(w.n_sims, w.data_seed)
+        assert np.array_equal(X, heat.sample_parameters(configs.HEAT100.n_sims, w.data_seed)[:w.n_sims])
+        inputs = heat.inputs_for(X, w.tau)
+        fields = heat.heat_fields(X, w.grid, w.tau)
+        ref = runner.run(w, inputs, fields, n_steps=100, keep_grads=(1, 100))
+        ref["N"] = ref.pop("reservoir").N
+        _HEAT_FULL.update(w=w, inputs=inputs, fields=fields, ref=ref)
+    return _HEAT_FULL["w"], _HEAT_FULL["inputs"], _HEAT_FULL["fields"], _HEAT_FULL["ref"]
+
+
+@pytest.mark.parametrize("flags", ["keep_grads", "fused"])
+def test_heat_workload_full_shape_100_steps(flags):
+    """The 100x100 workload at its full shape: 6-256-256-10,000 fp32, batch
+    1024, a reservoir of 100,000 samples with threshold 16,667, chunks of the
+    100 concurrent simulations' time step, through the two-stream loop with
+    the targets read in place (as bench.py runs it), for 100 train steps (the
+    266 iterations they take stream the first 300 simulations of the
+    ensemble).  Slots bit-exact at every step; loss series and final
+    parameters within 1e-3 relative L2 of the oracle, every loss within 1e-3
+    of its own; with kept gradients, the gradients of step 1 and of step 100
+    within 1e-3 in L2 and element-wise, those of step 100 against the
+    oracle's gradients at the path's own parameters after step 99 on the
+    step's batch; with the output layer's Adam fused (the benchmark's path)
+    the same slots, losses and parameters."""
+    from paper_2309_16743_amd import OT_SURROGATE_KEEP_GRADS
+    from paper_2309_16743_amd.online import OnlineTrainer
+    print(f"100x100 workload at full shape, 100 steps ({flags})", flush=True)
+    w, inputs, fields, ref = heat_full_shape_reference()
+    assert (w.capacity, w.threshold, w.batch, w.wave) == (100_000, 16_667, 1024, 100)
+    assert ref["iterations"] == 266
+    keep = flags == "keep_grads"
+    tr = OnlineTrainer(w.widths, w.batch, w.capacity, w.threshold, w.wave, w.tau,
+                       torch.from_numpy(inputs).to(DEV), torch.from_numpy(fields).to(DEV),
+                       w.reservoir_seed, w.init_seed, lr=w.lr, record_steps=100, overlap=True,
+                       flags=OT_SURROGATE_KEEP_GRADS if keep else 0)
+    grads1 = params99 = None
+    while tr.steps_done < 100:
+        tr.iterate()
+        if keep and tr.steps_done == 1 and grads1 is None:
+            grads1 = [tr.sur.get_grads(l) for l in range(3)]
+        if keep and tr.steps_done == 99 and params99 is None:
+            params99 = [tuple(a.astype(np.float64) for a in tr.sur.get_params(l)) for l in range(3)]
+    torch.cuda.synchronize()
+    assert tr.iteration == 266
+    slots = tr.slot_log.cpu().numpy()
+    for i in range(100):
+        assert np.array_equal(slots[i], ref["slots"][i]), i
+    losses = tr.loss_log.cpu().numpy()
+    assert rel(losses, ref["losses"]) < 1e-3
+    assert np.max(np.abs(losses - ref["losses"]) / np.array(ref["losses"])) < 1e-3
+    if keep:
+        # Step 100's gradients are held against the oracle's gradients of the
+        # same batch at the path's own parameters after step 99: the 99 Adam
+        # steps before it leave the two trajectories apart in the last bits,
+        # and near-zero pre-activations then fall on different sides of the
+        # ReLU, which moves the layer-1 gradient (its inputs are raw
+        # temperatures of 100-500) by about 1.6e-3 in L2 even between the
+        # oracle and the oracle with its stored state rounded to fp32.  The
+        # distance to the oracle's own step 100 is printed, and bounded by
+        # four times that sensitivity.
+        grads100 = [tr.sur.get_grads(l) for l in range(3)]
+        xb, ub = ref["batches"][100]
+        assert xb.shape == (1024, 6) and ub.shape == (1024, 10_000)
+        _, o100 = mlp.loss_and_grads(params99, xb, ub)
+        for l in range(3):
+            for i in range(2):
+                g1, o1 = grads1[l][i], ref["grads"][1][l][i]
+                assert close(g1, o1, 1e-3), (1, l, i, rel(g1, o1), elementwise(g1, o1))
+                g, o = grads100[l][i], o100[l][i]
+                assert close(g, o, 1e-3), (100, l, i, rel(g, o), elementwise(g, o))
+                t = ref["grads"][100][l][i]
+                print(f"  step 100 layer {l} {'dW' if i == 0 else 'db'}: at the path's parameters rel L2 "
+                      f"{rel(g, o):.2e} element-wise {elementwise(g, o):.2e}; against the oracle's trajectory "
+                      f"rel L2 {rel(g, t):.2e}", flush=True)
+                assert rel(g, t) < 6.4e-3, (100, l, i, rel(g, t))
+    for l in range(3):
+        W, b = tr.sur.get_params(l)
+        assert rel(W, ref["params"][l][0]) < 1e-3 and rel(b, ref["params"][l][1]) < 1e-3, l
+    st = tr.res.stats()
+    assert st["n"] == ref["N"] == 26_600 and st["total_draws"] == 100 * 1024
     tr.close()

@@ -289,3 +289,67 @@ def test_bf16_mode_close_to_fp64():
     print("bf16 vs fp64 relative L2 (loss, dW1, db1, dW2, db2, dW3, db3):", ["%.2e" % r for r in rels])
     assert max(rels) < 2e-2
     assert rels[0] > 0                         # the modes do differ
+
+
+# ---- the output layer by column chunks (full-width parity checks use it) -------------------
+def test_bf16_round_torch_equals_bf16_round():
+    rng = np.random.default_rng(4)
+    x = rng.normal(size=200000) * 10.0 ** rng.integers(-20, 20, 200000)
+    ulp = 2.0 ** -7
+    ties = np.array([1 + ulp / 2, 1 + 3 * ulp / 2, -(1 + ulp / 2), 3 * (1 + ulp / 2), 0.0, -0.0])
+    for v in (x, ties):
+        got = mlp.bf16_round_torch(torch.from_numpy(v)).numpy()
+        assert np.array_equal(got, mlp.bf16_round(v))
+
+
+@pytest.mark.parametrize("bf16,rounded", [(False, None), (True, None), (True, mlp.BF16_ROUNDED - {"dY"}),
+                                          (True, mlp.BF16_ROUNDED | {"db_raw", "target"})])
+def test_output_layer_by_columns_equals_loss_and_grads(bf16, rounded):
+    """Column chunks (ragged last chunk) + hidden_grads reproduce loss_and_grads:
+    loss, every hidden gradient, the output bias gradient and sampled output
+    weight-gradient rows, up to the order of fp64 sums; with planted rounding
+    points too, so the chunked path honours each point."""
+    widths, B = (6, 40, 32, 1000), 24
+    rng = np.random.default_rng(8)
+    params = [(rng.uniform(-0.3, 0.3, (widths[l + 1], widths[l])), rng.uniform(-0.3, 0.3, widths[l + 1]))
+              for l in range(3)]
+    X = np.concatenate([rng.uniform(100, 500, (B, 5)), rng.uniform(0.01, 1, (B, 1))], axis=1)
+    U = rng.uniform(100, 500, (B, widths[-1]))
+    loss, grads = mlp.loss_and_grads(params, X, U, bf16=bf16, rounded=rounded)
+    Zs, As, Ah = mlp.forward(params[:2], X, bf16=bf16, rounded=rounded)
+    A_top = np.maximum(Ah, 0.0)
+    W3, b3 = params[2]
+    rows = np.array([0, 5, 128, 999])
+    l2, dA, db, dWr = mlp.output_layer_by_columns(A_top, lambda a, b: W3[a:b], b3, lambda a, b: U[:, a:b],
+                                                  widths[-1], 128, bf16=bf16, rows=rows, rounded=rounded)
+    assert abs(l2 - loss) <= 1e-12 * loss
+    assert np.allclose(db, grads[2][1], rtol=1e-12, atol=1e-18)
+    assert np.allclose(dWr, grads[2][0][rows], rtol=1e-12, atol=1e-18)
+    hg = mlp.hidden_grads(params[:2], Zs, dA, As, bf16=bf16, rounded=rounded)
+    for (a, c), (d, e) in zip(hg, grads[:2]):
+        assert np.allclose(a, d, rtol=1e-10, atol=1e-16) and np.allclose(c, e, rtol=1e-10, atol=1e-16)
+
+
+def test_adam_fp32_state_rounds_only_what_it_stores():
+    """state_dtype=float32: parameters and moments are fp32 values after a
+    step, each the fp64 step's result rounded once; fp64 mode is unchanged."""
+    params, X, U = tiny_problem((6, 8, 8, 5), b=6, seed=13)
+    params = [(W.astype(np.float32).astype(np.float64), b.astype(np.float32).astype(np.float64)) for W, b in params]
+    a64, a32 = mlp.Adam(lr=1e-3), mlp.Adam(lr=1e-3, state_dtype=np.float32)
+    p64, p32 = params, params
+    for _ in range(3):
+        _, g = mlp.loss_and_grads(p64, X, U)
+        q64 = a64.step(p64, g)
+        m_prev, v_prev = [tuple(x.copy() for x in t) for t in a32.m] or None, [tuple(x.copy() for x in t) for t in a32.v] or None
+        q32 = a32.step(p32, mlp.loss_and_grads(p32, X, U)[1])
+        for pair in q32 + a32.m + a32.v:
+            for x in pair:
+                assert np.array_equal(x.astype(np.float32).astype(np.float64), x)
+        p64, p32 = q64, q32
+    # one step from the same fp32 state: the rounded result is the fp64 result rounded
+    b64, b32 = mlp.Adam(lr=1e-3), mlp.Adam(lr=1e-3, state_dtype=np.float32)
+    _, g = mlp.loss_and_grads(params, X, U)
+    r64, r32 = b64.step(params, g), b32.step(params, g)
+    for (W64, c64), (W32, c32) in zip(r64, r32):
+        assert np.array_equal(W64.astype(np.float32).astype(np.float64), W32)
+        assert np.array_equal(c64.astype(np.float32).astype(np.float64), c32)
