@@ -587,12 +587,97 @@ __device__ __forceinline__ int kswz(int row) {
 }
 __device__ __forceinline__ int mswz(int row) { return 4 * (row & 3); }
 
+// Global offsets (elements, relative to the k tile's start) of a thread's
+// 16-byte chunks of one operand: chunk ci = (i * NW + wid) * 64 + lane of a
+// stage sits in LDS slot ci.  x0: the block tile's first row (KMajor) or
+// column (MNMajor) of the operand, lim: its rows / columns (clamped: rows
+// past the end are read from the last one), ld: its leading dimension.
+template <LayB L, int TILE, int BK, int NW, int N>
+__device__ __forceinline__ void stage_offsets(int64_t (&off)[N], int wid, int lane, int64_t x0, int64_t lim,
+                                              int64_t ld) {
+#pragma unroll
+  for (int i = 0; i < N; ++i) {
+    const int ci = (i * NW + wid) * 64 + lane;
+    if constexpr (L == LayB::KMajor) {
+      constexpr int KC = BK / 8;
+      const int row = ci / KC, pc = ci % KC, lc = pc ^ kswz<BK>(row);
+      off[i] = min(x0 + row, lim - 1) * ld + 8 * lc;
+    } else {
+      constexpr int CPR = TILE / 8;
+      const int row = ci / CPR, pc = ci % CPR, lc = pc ^ mswz(row);
+      off[i] = (int64_t)row * ld + min(x0 + 8 * lc, (lim - 1) / 8 * 8);
+    }
+  }
+}
+
+// Direct global -> LDS loads of one operand's k tile starting at k0 into the
+// stage area dst (global_load_lds_dwordx4: each lane's 16 bytes land at the
+// wave's LDS base + 16 * lane).
+template <LayB L, int NW, int N>
+__device__ __forceinline__ void stage_load(const uint16_t* base, const int64_t (&off)[N], int64_t k0, int64_t ld,
+                                           unsigned char* dst, int wid) {
+  typedef __attribute__((address_space(3))) void lds_void;
+#pragma unroll
+  for (int i = 0; i < N; ++i) {
+    const uint16_t* src = (L == LayB::KMajor) ? base + off[i] + k0 : base + off[i] + k0 * ld;
+    __builtin_amdgcn_global_load_lds(src, (lds_void*)(dst + (i * NW + wid) * 1024), 16, 0, 0);
+  }
+}
+
+// Operand of one 16-deep k step (kk) for the 32-wide fragment at `base` of a
+// stage area (cpr: 16-byte chunks per MNMajor row).
+// KMajor: lane l reads row base + l%32, 8 k-values at 16 kk + 8 (l/32).
+// MNMajor: 16-lane group q covers columns base + 16 (q%2) .. +15 and k rows
+// 16 kk + 8 (q/2) .. +7, read as two transposed 4-row blocks.
+// The reads are inline assembly: the compiler cannot tell a read of one stage
+// from the direct global -> LDS loads still in flight into the others, and
+// before the first read of every k tile it would wait for all of them
+// (vmcnt(0)), which removes the prefetch.  Stage completion is tracked by the
+// kernels' own vmcnt waits and barriers; frag_fence() waits for the reads.
+template <int BK>
+__device__ __forceinline__ bf16x8 stage_frag(const unsigned char* st, int cpr, bool kmajor, int base, int kk,
+                                             int lane) {
+  typedef int i32x4 __attribute__((ext_vector_type(4)));
+  typedef int i32x2 __attribute__((ext_vector_type(2)));
+  typedef __attribute__((address_space(3))) const unsigned char lds_u8;
+  constexpr int KC = BK / 8;
+  auto lds_addr = [](const unsigned char* p) -> uint32_t { return (uint32_t)(size_t)(lds_u8*)p; };
+  if (kmajor) {
+    const int row = base + lane % 32;
+    const int lc = 2 * kk + lane / 32;
+    i32x4 v;
+    asm volatile("ds_read_b128 %0, %1" : "=v"(v) : "v"(lds_addr(st + (row * KC + (lc ^ kswz<BK>(row))) * 16)));
+    return __builtin_bit_cast(bf16x8, v);
+  }
+  const int c = lane % 16, q = lane / 16;
+  const int col = base + 16 * (q & 1) + 4 * (c % 4);
+  const int r0 = 16 * kk + 8 * (q >> 1) + c / 4, r1 = r0 + 4;
+  const int ch = col / 8, half = (col / 4) & 1;
+  i32x2 lo, hi;
+  asm volatile("ds_read_b64_tr_b16 %0, %1" : "=v"(lo) : "v"(lds_addr(st + (r0 * cpr + (ch ^ mswz(r0))) * 16 + half * 8)));
+  asm volatile("ds_read_b64_tr_b16 %0, %1" : "=v"(hi) : "v"(lds_addr(st + (r1 * cpr + (ch ^ mswz(r1))) * 16 + half * 8)));
+  const bf16x4 l = __builtin_bit_cast(bf16x4, lo), h = __builtin_bit_cast(bf16x4, hi);
+  return bf16x8{l[0], l[1], l[2], l[3], h[0], h[1], h[2], h[3]};
+}
+
+// Wait for the outstanding fragment reads; each fragment then passes through
+// an empty statement, so that no use of it can move above the wait.
+template <int N>
+__device__ __forceinline__ void frag_fence_regs(bf16x8 (&x)[N]) {
+  typedef int i32x4 __attribute__((ext_vector_type(4)));
+#pragma unroll
+  for (int f = 0; f < N; ++f) {
+    i32x4 v = __builtin_bit_cast(i32x4, x[f]);
+    asm volatile("" : "+v"(v));
+    x[f] = __builtin_bit_cast(bf16x8, v);
+  }
+}
+
 template <int BM, int BN, int BK, int S, int OCC, LayB LA, LayB LB, EpiB EPI, int NWN = 2>
 __global__ __launch_bounds__(128 * NWN, OCC) void gemm_bf16_pipe_kernel(GemmBArgs g) {
   constexpr int NW = 2 * NWN, NT = 64 * NW;                       // 2 x NWN wavefronts
   constexpr int WM = BM / 2, WN = BN / NWN, FM = WM / 32, FN = WN / 32;
   static_assert(NW <= 8, "loss partial slots");
-  constexpr int KC = BK / 8;                                      // chunks per KMajor row
   constexpr int A_CH = BM * BK / 8, B_CH = BN * BK / 8;          // 16-byte chunks per stage
   constexpr int LA_N = A_CH / NT, LB_N = B_CH / NT;               // loads per thread per k tile
   static_assert(A_CH % NT == 0 && B_CH % NT == 0, "tile split");
@@ -626,137 +711,21 @@ __global__ __launch_bounds__(128 * NWN, OCC) void gemm_bf16_pipe_kernel(GemmBArg
   const int nk = (int)((kend - kbeg) / BK);
   if constexpr (EPI == EpiB::MseBf) load_target_rows<BM>(g, m0, s_trow);
 
-  // Per-thread global offsets (elements) of its chunks, relative to the k tile start.
-  // Chunk ci = (i * NW + wid) * 64 + lane of operand X sits in LDS slot ci.
   int64_t a_off[LA_N], b_off[LB_N];
-#pragma unroll
-  for (int i = 0; i < LA_N; ++i) {
-    const int ci = (i * NW + wid) * 64 + lane;
-    if constexpr (LA == LayB::KMajor) {
-      const int row = ci / KC, pc = ci % KC, lc = pc ^ kswz<BK>(row);
-      const int64_t m = min(m0 + row, g.M - 1);
-      a_off[i] = m * g.lda + 8 * lc;
-    } else {
-      constexpr int CPR = BM / 8;
-      const int row = ci / CPR, pc = ci % CPR, lc = pc ^ mswz(row);
-      const int64_t m = min(m0 + 8 * lc, (g.M - 1) / 8 * 8);
-      a_off[i] = (int64_t)row * g.lda + m;
-    }
-  }
-#pragma unroll
-  for (int i = 0; i < LB_N; ++i) {
-    const int ci = (i * NW + wid) * 64 + lane;
-    if constexpr (LB == LayB::KMajor) {
-      const int row = ci / KC, pc = ci % KC, lc = pc ^ kswz<BK>(row);
-      const int64_t n = min(n0 + row, g.N - 1);
-      b_off[i] = n * g.ldb + 8 * lc;
-    } else {
-      constexpr int CPR = BN / 8;
-      const int row = ci / CPR, pc = ci % CPR, lc = pc ^ mswz(row);
-      const int64_t n = min(n0 + 8 * lc, (g.N - 1) / 8 * 8);
-      b_off[i] = (int64_t)row * g.ldb + n;
-    }
-  }
-  typedef __attribute__((address_space(3))) void lds_void;
+  stage_offsets<LA, BM, BK, NW>(a_off, wid, lane, m0, g.M, g.lda);
+  stage_offsets<LB, BN, BK, NW>(b_off, wid, lane, n0, g.N, g.ldb);
   // k tile kt into stage st
   auto issue = [&](int kt, int st) {
     const int64_t k0 = kbeg + (int64_t)kt * BK;
     unsigned char* sa = smem + st * STAGE_BYTES;
-    unsigned char* sb = sa + A_CH * 16;
-#pragma unroll
-    for (int i = 0; i < LA_N; ++i) {
-      const uint16_t* src = (LA == LayB::KMajor) ? g.A + a_off[i] + k0 : g.A + a_off[i] + k0 * g.lda;
-      __builtin_amdgcn_global_load_lds(src, (lds_void*)(sa + (i * NW + wid) * 1024), 16, 0, 0);
-    }
-#pragma unroll
-    for (int i = 0; i < LB_N; ++i) {
-      const uint16_t* src = (LB == LayB::KMajor) ? g.B + b_off[i] + k0 : g.B + b_off[i] + k0 * g.ldb;
-      __builtin_amdgcn_global_load_lds(src, (lds_void*)(sb + (i * NW + wid) * 1024), 16, 0, 0);
-    }
+    stage_load<LA, NW>(g.A, a_off, k0, g.lda, sa, wid);
+    stage_load<LB, NW>(g.B, b_off, k0, g.ldb, sa + A_CH * 16, wid);
   };
-
-  // Operand staging.  Direct global -> LDS loads (issue) keep the registers
-  // free; register staging (load_regs one k tile early, write_regs into the
-  // stage freed one k tile before) was measured faster for the 8-wavefront
-  // 256 x 256 tiles (input gradients: 5.20 -> 4.83 ms at H = 2048, 1.32 ->
-  // 1.24 ms at H = 1024) and slower for the 4-wavefront tiles (forward 5.04
-  // -> 5.43 ms), so it is used for the former only.
-  constexpr bool RS = (NWN == 4);
-  static_assert(!RS || S >= 3, "register staging needs 3 stages");
-  typedef int rs_vec __attribute__((ext_vector_type(4)));
-  rs_vec ra[LA_N], rb[LB_N];
-  auto load_regs = [&](int kt) {
-    const int64_t k0 = kbeg + (int64_t)kt * BK;
-#pragma unroll
-    for (int i = 0; i < LA_N; ++i) {
-      const uint16_t* src = (LA == LayB::KMajor) ? g.A + a_off[i] + k0 : g.A + a_off[i] + k0 * g.lda;
-      ra[i] = *reinterpret_cast<const rs_vec*>(src);
-    }
-#pragma unroll
-    for (int i = 0; i < LB_N; ++i) {
-      const uint16_t* src = (LB == LayB::KMajor) ? g.B + b_off[i] + k0 : g.B + b_off[i] + k0 * g.ldb;
-      rb[i] = *reinterpret_cast<const rs_vec*>(src);
-    }
-  };
-  auto write_regs = [&](int st) {
-    unsigned char* sa = smem + st * STAGE_BYTES;
-    unsigned char* sb = sa + A_CH * 16;
-#pragma unroll
-    for (int i = 0; i < LA_N; ++i) *reinterpret_cast<rs_vec*>(sa + (i * NW + wid) * 1024 + lane * 16) = ra[i];
-#pragma unroll
-    for (int i = 0; i < LB_N; ++i) *reinterpret_cast<rs_vec*>(sb + (i * NW + wid) * 1024 + lane * 16) = rb[i];
-  };
-
   typedef float f32x16 __attribute__((ext_vector_type(16)));
-  typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
-  // Operand of one 16-deep k step (kk) for the 32-wide fragment at `base`.
-  // KMajor: lane l reads row base + l%32, 8 k-values at 16 kk + 8 (l/32).
-  // MNMajor: 16-lane group q covers columns base + 16 (q%2) .. +15 and k rows
-  // 16 kk + 8 (q/2) .. +7, read as two transposed 4-row blocks.
-  //
-  // The reads are inline assembly: the compiler cannot tell a read of one
-  // stage from the direct global -> LDS loads still in flight into the
-  // others, and before the first read of every k tile it would wait for all
-  // of them (vmcnt(0)), which removes the prefetch.  A stage is known to be
-  // complete from tile_ready(); frag_wait() waits for the reads themselves.
-  typedef int i32x4 __attribute__((ext_vector_type(4)));
-  typedef int i32x2 __attribute__((ext_vector_type(2)));
-  typedef __attribute__((address_space(3))) const unsigned char lds_u8;
-  auto lds_addr = [](const unsigned char* p) -> uint32_t { return (uint32_t)(size_t)(lds_u8*)p; };
-  auto frag = [&](const unsigned char* st, int cpr, bool kmajor, int base, int kk) -> bf16x8 {
-    if (kmajor) {
-      const int row = base + lane % 32;
-      const int lc = 2 * kk + lane / 32;
-      i32x4 v;
-      asm volatile("ds_read_b128 %0, %1" : "=v"(v) : "v"(lds_addr(st + (row * KC + (lc ^ kswz<BK>(row))) * 16)));
-      return __builtin_bit_cast(bf16x8, v);
-    }
-    const int c = lane % 16, q = lane / 16;
-    const int col = base + 16 * (q & 1) + 4 * (c % 4);
-    const int r0 = 16 * kk + 8 * (q >> 1) + c / 4, r1 = r0 + 4;
-    const int ch = col / 8, half = (col / 4) & 1;
-    i32x2 lo, hi;
-    asm volatile("ds_read_b64_tr_b16 %0, %1" : "=v"(lo) : "v"(lds_addr(st + (r0 * cpr + (ch ^ mswz(r0))) * 16 + half * 8)));
-    asm volatile("ds_read_b64_tr_b16 %0, %1" : "=v"(hi) : "v"(lds_addr(st + (r1 * cpr + (ch ^ mswz(r1))) * 16 + half * 8)));
-    const bf16x4 l = __builtin_bit_cast(bf16x4, lo), h = __builtin_bit_cast(bf16x4, hi);
-    return bf16x8{l[0], l[1], l[2], l[3], h[0], h[1], h[2], h[3]};
-  };
-  // Wait for the outstanding fragment reads; each fragment passes through an
-  // empty statement after the wait, so no use of it can move above the wait.
   auto frag_wait = [](bf16x8 (&af)[FM], bf16x8 (&bf)[FN]) {
     asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
-#pragma unroll
-    for (int f = 0; f < FM; ++f) {
-      i32x4 v = __builtin_bit_cast(i32x4, af[f]);
-      asm volatile("" : "+v"(v));
-      af[f] = __builtin_bit_cast(bf16x8, v);
-    }
-#pragma unroll
-    for (int h = 0; h < FN; ++h) {
-      i32x4 v = __builtin_bit_cast(i32x4, bf[h]);
-      asm volatile("" : "+v"(v));
-      bf[h] = __builtin_bit_cast(bf16x8, v);
-    }
+    frag_fence_regs(af);
+    frag_fence_regs(bf);
   };
 
   f32x16 acc[FM][FN];
@@ -783,9 +752,9 @@ __global__ __launch_bounds__(128 * NWN, OCC) void gemm_bf16_pipe_kernel(GemmBArg
     const unsigned char* sa = smem + (t % S) * STAGE_BYTES;
     const unsigned char* sb = sa + A_CH * 16;
 #pragma unroll
-    for (int f = 0; f < FM; ++f) af[f] = frag(sa, BM / 8, LA == LayB::KMajor, WM * wm + 32 * f, kk);
+    for (int f = 0; f < FM; ++f) af[f] = stage_frag<BK>(sa, BM / 8, LA == LayB::KMajor, WM * wm + 32 * f, kk, lane);
 #pragma unroll
-    for (int h = 0; h < FN; ++h) bf[h] = frag(sb, BN / 8, LB == LayB::KMajor, WN * wn + 32 * h, kk);
+    for (int h = 0; h < FN; ++h) bf[h] = stage_frag<BK>(sb, BN / 8, LB == LayB::KMajor, WN * wn + 32 * h, kk, lane);
   };
 
   // Software pipeline: the fragments of the next 16-deep step are read while
@@ -794,27 +763,13 @@ __global__ __launch_bounds__(128 * NWN, OCC) void gemm_bf16_pipe_kernel(GemmBArg
   // fragments are already in registers, so stage t % S is free after it and
   // receives tile t + S.
   bf16x8 af[FM], bfr[FN];
-  if constexpr (RS) {
-    for (int s = 0; s < S - 1; ++s)
-      if (s < nk) {
-        load_regs(s);
-        write_regs(s);
-      }
-    if (S - 1 < nk) load_regs(S - 1);
-    if (nk > 0) {
-      lds_barrier();
-      load_frags(0, 0, af, bfr);
-      frag_wait(af, bfr);
-    }
-  } else {
-    for (int s = 0; s < S - 1; ++s)
-      if (s < nk) issue(s, s);
-    if (nk > 0) {
-      tile_ready(0);
-      if (S - 1 < nk) issue(S - 1, S - 1);
-      load_frags(0, 0, af, bfr);
-      frag_wait(af, bfr);
-    }
+  for (int s = 0; s < S - 1; ++s)
+    if (s < nk) issue(s, s);
+  if (nk > 0) {
+    tile_ready(0);
+    if (S - 1 < nk) issue(S - 1, S - 1);
+    load_frags(0, 0, af, bfr);
+    frag_wait(af, bfr);
   }
   for (int kt = 0; kt < nk; ++kt) {
 #pragma unroll
@@ -824,14 +779,8 @@ __global__ __launch_bounds__(128 * NWN, OCC) void gemm_bf16_pipe_kernel(GemmBArg
       if (kk + 1 < KK) {
         load_frags(kt, kk + 1, an, bn);
       } else if (kt + 1 < nk) {
-        if constexpr (RS) {
-          lds_barrier();
-          if (kt + S - 1 < nk) write_regs((kt + S - 1) % S);
-          if (kt + S < nk) load_regs(kt + S);
-        } else {
-          tile_ready(kt + 1);
-          if (kt + S < nk) issue(kt + S, kt % S);
-        }
+        tile_ready(kt + 1);
+        if (kt + S < nk) issue(kt + S, kt % S);
         load_frags(kt + 1, 0, an, bn);
       }
       __builtin_amdgcn_sched_barrier(0);
@@ -891,6 +840,172 @@ hipError_t launch_gemm_bf16_pipe(const GemmBArgs& g, int64_t splits, hipStream_t
 template <int BM, int BN>
 constexpr int64_t gemm_bf16_pipe_tiles(int64_t M, int64_t N) {
   return ((M + BM - 1) / BM) * ((N + BN - 1) / BN);
+}
+
+// Ping-pong variant: 256 x 256 block tile, k tile 32, eight wavefronts in two
+// groups of four (waves 0-3 and 4-7; wave w runs on SIMD w % 4, so each SIMD
+// holds one wave of each group), wave tile 128 x 64 as in the pipelined
+// kernel.  The groups alternate between a load phase (issue this thread's
+// direct global -> LDS loads of tile t + S - 1, read the wave's fragments of
+// tile t for both 16-deep steps) and a compute phase (the 16 MFMAs of tile
+// t), one phase apart, with a block barrier between phases:
+//   phase 2t:     group 0 loads tile t,      group 1 computes tile t - 1
+//   phase 2t + 1: group 0 computes tile t,   group 1 loads tile t
+// so that on every SIMD one wave issues MFMAs while the other reads LDS, and
+// the computing wave runs at raised priority.  Stage (t - 1) % S receives tile
+// t + S - 1 from phase 2t on: both groups have read tile t - 1 by the end of
+// phase 2t - 1.  Before phase 2t every thread waits for its own loads of tile
+// t (vmcnt, loads complete in order) and the barrier publishes them.
+template <int S, LayB LA, LayB LB, EpiB EPI>
+__global__ __launch_bounds__(512, 1) void gemm_bf16_pp_kernel(GemmBArgs g) {
+  constexpr int BM = 256, BN = 256, BK = 32, NW = 8, NT = 512;
+  constexpr int WM = 128, WN = 64, FM = WM / 32, FN = WN / 32;
+  constexpr int A_CH = BM * BK / 8, B_CH = BN * BK / 8;
+  constexpr int LA_N = A_CH / NT, LB_N = B_CH / NT;
+  constexpr int STAGE_BYTES = (A_CH + B_CH) * 16;
+  constexpr int EP = WN + 4;
+  constexpr int CH_F = (NW * FM * 32 * EP * 4 <= S * STAGE_BYTES)         ? FM
+                       : (NW * (FM / 2) * 32 * EP * 4 <= S * STAGE_BYTES) ? FM / 2
+                                                                         : FM / 4;
+  static_assert(CH_F >= 1 && NW * CH_F * 32 * EP * 4 <= S * STAGE_BYTES, "epilogue staging");
+  static_assert(S >= 3 && S <= 4, "stages");
+  __shared__ __attribute__((aligned(16))) unsigned char smem[S * STAGE_BYTES];
+  __shared__ double s_red[8 + NW * WN / 2];
+  __shared__ int32_t s_trow[EPI == EpiB::MseBf ? BM : 1];
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wid = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int grp = wid >> 2;
+  const int wm = wid % 2, wn = wid / 2;
+  const int64_t tiles_m = (g.M + BM - 1) / BM, tiles_n = (g.N + BN - 1) / BN;
+  const int64_t lin = (int64_t)blockIdx.y * gridDim.x + blockIdx.x;
+  const int64_t l2 = xcd_remap_b(lin, (int64_t)gridDim.x * gridDim.y);
+  const int64_t logical = l2 % gridDim.x, split = l2 / gridDim.x;
+  int64_t tm, tn;
+  if (tiles_m <= tiles_n) { tm = logical % tiles_m; tn = logical / tiles_m; }
+  else { tn = logical % tiles_n; tm = logical / tiles_n; }
+  const int64_t m0 = tm * BM, n0 = tn * BN;
+  const int64_t kbeg = split * g.k_chunk;
+  const int64_t kend = (kbeg + g.k_chunk < g.K) ? kbeg + g.k_chunk : g.K;
+  const int nk = (int)((kend - kbeg) / BK);
+  if constexpr (EPI == EpiB::MseBf) load_target_rows<BM>(g, m0, s_trow);
+
+  int64_t a_off[LA_N], b_off[LB_N];
+  stage_offsets<LA, BM, BK, NW>(a_off, wid, lane, m0, g.M, g.lda);
+  stage_offsets<LB, BN, BK, NW>(b_off, wid, lane, n0, g.N, g.ldb);
+  auto issue = [&](int kt) {
+    const int64_t k0 = kbeg + (int64_t)kt * BK;
+    unsigned char* sa = smem + (kt % S) * STAGE_BYTES;
+    stage_load<LA, NW>(g.A, a_off, k0, g.lda, sa, wid);
+    stage_load<LB, NW>(g.B, b_off, k0, g.ldb, sa + A_CH * 16, wid);
+  };
+  typedef float f32x16 __attribute__((ext_vector_type(16)));
+  constexpr int KK = BK / 16;
+  bf16x8 af[KK][FM], bfr[KK][FN];
+  f32x16 acc[FM][FN];
+#pragma unroll
+  for (int f = 0; f < FM; ++f)
+#pragma unroll
+    for (int h = 0; h < FN; ++h) acc[f][h] = f32x16{};
+
+#define OT_WAIT_VM(n) __builtin_amdgcn_s_waitcnt(((n) & 0xF) | (0x7 << 4) | (0xF << 8) | (((n) >> 4) << 14))
+  constexpr int PER_TILE = LA_N + LB_N;
+  static_assert((S - 2) * PER_TILE <= 63, "vmcnt range");
+  // this thread's loads of tile t have landed (its loads of up to S - 2 later tiles may be in flight)
+  auto own_tile_landed = [&](int t) {
+    const int ahead = min(S - 2, nk - 1 - t);
+    if (ahead >= 2) OT_WAIT_VM(2 * PER_TILE);
+    else if (ahead == 1) OT_WAIT_VM(PER_TILE);
+    else OT_WAIT_VM(0);
+  };
+  auto load_phase = [&](int t) {
+    if (t + S - 1 < nk) issue(t + S - 1);
+    const unsigned char* sa = smem + (t % S) * STAGE_BYTES;
+    const unsigned char* sb = sa + A_CH * 16;
+#pragma unroll
+    for (int kk = 0; kk < KK; ++kk) {
+#pragma unroll
+      for (int f = 0; f < FM; ++f) af[kk][f] = stage_frag<BK>(sa, BM / 8, LA == LayB::KMajor, WM * wm + 32 * f, kk, lane);
+#pragma unroll
+      for (int h = 0; h < FN; ++h) bfr[kk][h] = stage_frag<BK>(sb, BN / 8, LB == LayB::KMajor, WN * wn + 32 * h, kk, lane);
+    }
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+#pragma unroll
+    for (int kk = 0; kk < KK; ++kk) {
+      frag_fence_regs(af[kk]);
+      frag_fence_regs(bfr[kk]);
+    }
+  };
+  auto compute_phase = [&]() {
+    __builtin_amdgcn_s_setprio(1);
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int kk = 0; kk < KK; ++kk)
+#pragma unroll
+      for (int f = 0; f < FM; ++f)
+#pragma unroll
+        for (int h = 0; h < FN; ++h)
+          acc[f][h] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[kk][f], bfr[kk][h], acc[f][h], 0, 0, 0);
+    __builtin_amdgcn_sched_barrier(0);
+    __builtin_amdgcn_s_setprio(0);
+  };
+
+  // prologue: tiles 0 .. S - 2 from every thread; tile 0 published
+  for (int t = 0; t < S - 1; ++t)
+    if (t < nk) issue(t);
+  if (nk > 0) own_tile_landed(0);
+  lds_barrier();
+  if (grp == 0) {
+    for (int t = 0; t < nk; ++t) {
+      load_phase(t);
+      lds_barrier();                                   // end of phase 2t
+      compute_phase();
+      if (t + 1 < nk) own_tile_landed(t + 1);
+      lds_barrier();                                   // end of phase 2t + 1
+    }
+    lds_barrier();                                     // end of phase 2 nk
+  } else {
+    lds_barrier();                                     // end of phase 0
+    for (int t = 0; t < nk; ++t) {
+      load_phase(t);
+      if (t + 1 < nk) own_tile_landed(t + 1);
+      lds_barrier();                                   // end of phase 2t + 1
+      compute_phase();
+      lds_barrier();                                   // end of phase 2t + 2
+    }
+  }
+#undef OT_WAIT_VM
+
+  float* ep = reinterpret_cast<float*>(smem) + wid * (CH_F * 32 * EP);
+  BEpi<WN, EPI, NW> e(g, n0 + WN * wn);
+  if constexpr (EPI == EpiB::MseBf) {
+    e.s_trow = s_trow;
+    e.tile_m0 = m0;
+  }
+#pragma unroll
+  for (int c0 = 0; c0 < FM; c0 += CH_F) {
+    e.template rows<CH_F * 32>(g, ep, m0 + WM * wm + 32 * c0, split, [&] {
+      lds_barrier();
+#pragma unroll
+      for (int f = 0; f < CH_F; ++f)
+#pragma unroll
+        for (int h = 0; h < FN; ++h)
+#pragma unroll
+          for (int r = 0; r < 16; ++r)
+            ep[(32 * f + 8 * (r / 4) + 4 * (lane / 32) + r % 4) * EP + 32 * h + lane % 32] = acc[c0 + f][h][r];
+      lds_barrier();
+    });
+  }
+  e.finish(g, tm, s_red);
+}
+
+template <int S, LayB LA, LayB LB, EpiB EPI>
+hipError_t launch_gemm_bf16_pp(const GemmBArgs& g, int64_t splits, hipStream_t stream, hipEvent_t t0 = nullptr,
+                               hipEvent_t t1 = nullptr) {
+  const int64_t tiles = ((g.M + 255) / 256) * ((g.N + 255) / 256);
+  hipExtLaunchKernelGGL((gemm_bf16_pp_kernel<S, LA, LB, EPI>), dim3((unsigned)tiles, (unsigned)splits), dim3(512), 0,
+                        stream, t0, t1, 0, g);
+  return hipGetLastError();
 }
 
 }  // namespace ot

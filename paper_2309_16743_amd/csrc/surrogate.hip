@@ -799,8 +799,9 @@ using ot::EpiB;
 using ot::GemmBArgs;
 using ot::LayB;
 
-// bf16 tiles: the pipelined 256 x 128 kernel (k tile 32, direct-to-LDS loads,
-// two blocks per CU) for large products; 128 x 128 (4 x 4 fragments per wave)
+// bf16 tiles: for large products the pipelined 256 x 128 kernel (k tile 32,
+// direct-to-LDS loads, two blocks per CU) or the ping-pong 256 x 256 kernel
+// (eight wavefronts, one block per CU); 128 x 128 (4 x 4 fragments per wave)
 // and 64 x 64 (2 x 2) with a k tile of 32 otherwise.
 enum CfgB : int { kB128 = 0, kB64 = 1, kBPipe = 2, kBPipeW = 3 };
 constexpr int kBK = 32;
@@ -812,17 +813,26 @@ int64_t tiles_b(int cfg, int64_t M, int64_t N) {
   return cfg == kB128 ? ot::gemm_bf16_tiles<4, 4>(M, N) : ot::gemm_bf16_tiles<2, 2>(M, N);
 }
 
-// The pipelined kernel when k is a multiple of its 32-deep k tile and its
-// tiles give about one block per CU or more: products split over long k
-// ranges take 256 x 256 tiles of eight wavefronts (one block per CU; splits
-// until about two blocks per CU, keeping at least 32 k tiles per split),
-// the others 256 x 128 tiles of four wavefronts (two blocks per CU).  Else
-// 128 x 128 tiles when they give about two blocks per CU; long k ranges are
-// split over 128 x 128 tiles, shorter ones over 64 x 64.
-// pipe_ok: the pipelined kernel may be used (it has no row-sum output).
-Plan make_plan_b(int64_t M, int64_t N, int64_t K, bool allow_split, bool pipe_ok = true) {
+// The 32-deep k tile kernels when k is a multiple of 32 and the tiles give
+// about one block per CU or more: products split over long k ranges take the
+// ping-pong kernel's 256 x 256 tiles (splits until about two blocks per CU,
+// keeping at least 32 k tiles per split), and so do unsplit products with the
+// fused MSE epilogue when wide_ok; the others 256 x 128 tiles of the
+// pipelined kernel (two blocks per CU).  Else 128 x 128 tiles when they give
+// about two blocks per CU; long k ranges are split over 128 x 128 tiles,
+// shorter ones over 64 x 64.
+// pipe_ok: the 32-deep k tile kernels may be used (they have no row-sum output).
+Plan make_plan_b(int64_t M, int64_t N, int64_t K, bool allow_split, bool pipe_ok = true, bool wide_ok = false) {
   constexpr int64_t kCUs = 256;
   Plan p;
+  if (wide_ok && pipe_ok && !allow_split && K % kPipeBK == 0 && M >= 256 && N >= 256 &&
+      tiles_b(kBPipeW, M, N) >= kCUs - 16) {
+    p.cfg = kBPipeW;
+    p.k_chunk = K;
+    p.splits = 1;
+    p.blocks = tiles_b(kBPipeW, M, N);
+    return p;
+  }
   if (pipe_ok && allow_split && K % kPipeBK == 0 && M >= 256 && N >= 256) {
     const int64_t t = tiles_b(kBPipeW, M, N);
     int64_t sp = 1;
@@ -875,9 +885,9 @@ hipError_t launch_cfg_b(int cfg, const GemmBArgs& g, int64_t splits, hipStream_t
     if (cfg == kBPipe) return ot::launch_gemm_bf16_pipe<128, 256, kPipeBK, 3, 2, LA, LB, E>(g, splits, st, t0, t1);
   }
   if (cfg == kBPipe) return ot::launch_gemm_bf16_pipe<256, 128, kPipeBK, 3, 2, LA, LB, E>(g, splits, st, t0, t1);
-  if constexpr (E != EpiB::AdamF32 && E != EpiB::MseBf) {
-    // split products: 256 x 256 tile, eight wavefronts, 4 stages (128 KB of LDS), one block per CU
-    if (cfg == kBPipeW) return ot::launch_gemm_bf16_pipe<256, 256, kPipeBK, 4, 1, LA, LB, E, 4>(g, splits, st, t0, t1);
+  if constexpr (E != EpiB::AdamF32) {
+    // 256 x 256 tile, eight wavefronts in ping-pong, 4 stages (128 KB of LDS), one block per CU
+    if (cfg == kBPipeW) return ot::launch_gemm_bf16_pp<4, LA, LB, E>(g, splits, st, t0, t1);
   }
   if (cfg == kB128) return ot::launch_gemm_bf16<4, 4, LA, LB, E, kBK>(g, splits, st, t0, t1);
   return ot::launch_gemm_bf16<2, 2, LA, LB, E, kBK>(g, splits, st, t0, t1);
@@ -888,7 +898,8 @@ hipError_t launch_cfg_b(int cfg, const GemmBArgs& g, int64_t splits, hipStream_t
 template <LayB LA, LayB LB, EpiB E>
 int run_gemm_b(ot_surrogate* s, GemmBArgs g, hipStream_t st, const char* what, bool allow_split,
                int ph_gemm = -1, int ph_reduce = -1, int64_t* blocks_out = nullptr) {
-  const Plan p = make_plan_b(g.M, g.N, g.K, allow_split && E != EpiB::MseBf && E != EpiB::AdamF32, g.rowsum == nullptr);
+  const Plan p = make_plan_b(g.M, g.N, g.K, allow_split && E != EpiB::MseBf && E != EpiB::AdamF32, g.rowsum == nullptr,
+                             E == EpiB::MseBf);
   if (blocks_out) *blocks_out = p.blocks;
   ot::PhaseTimer& tm = s->timer;
   if (p.splits == 1) {
@@ -1009,14 +1020,14 @@ int forward_mse_bf16(ot_surrogate* s, const float* x, int64_t ldx, const float* 
     g.colsum = s->colsum;
     g.colsum_ld = s->ld[L];
   }
-  const Plan pf = make_plan_b(g.M, g.N, g.K, false);
+  const Plan pf = make_plan_b(g.M, g.N, g.K, false, true, true);
   *n_partials = pf.blocks;
   if (pf.blocks > s->n_partials_cap) return ot::set_error(OT_E_STATE, "loss partial buffer too small");
   if ((rc = run_gemm_b<LayB::KMajor, LayB::KMajor, EpiB::MseBf>(s, g, st, "bf16 output forward+MSE", false,
                                                                 OT_PH_FWD_OUTPUT)))
     return rc;
   if (bias_grad) {
-    const int64_t used_mtiles = ot::ceil_div(b, pf.cfg == kBPipe ? 256 : (pf.cfg == kB128 ? 128 : 64));
+    const int64_t used_mtiles = ot::ceil_div(b, (pf.cfg == kBPipe || pf.cfg == kBPipeW) ? 256 : (pf.cfg == kB128 ? 128 : 64));
     hipLaunchKernelGGL(ot::colsum_reduce_kernel, dim3((unsigned)ot::ceil_div(D, 256)), dim3(256), 0, st, s->colsum,
                        used_mtiles, D, s->ld[L], s->grads + lo.b_off);
     OT_LAUNCHED("colsum_reduce_kernel");
