@@ -843,19 +843,22 @@ constexpr int64_t gemm_bf16_pipe_tiles(int64_t M, int64_t N) {
 }
 
 // Ping-pong variant: 256 x 256 block tile, k tile 32, eight wavefronts in two
-// groups of four (waves 0-3 and 4-7; wave w runs on SIMD w % 4, so each SIMD
-// holds one wave of each group), wave tile 128 x 64 as in the pipelined
-// kernel.  The groups alternate between a load phase (issue this thread's
-// direct global -> LDS loads of tile t + S - 1, read the wave's fragments of
-// tile t for both 16-deep steps) and a compute phase (the 16 MFMAs of tile
-// t), one phase apart, with a block barrier between phases:
-//   phase 2t:     group 0 loads tile t,      group 1 computes tile t - 1
-//   phase 2t + 1: group 0 computes tile t,   group 1 loads tile t
-// so that on every SIMD one wave issues MFMAs while the other reads LDS, and
-// the computing wave runs at raised priority.  Stage (t - 1) % S receives tile
-// t + S - 1 from phase 2t on: both groups have read tile t - 1 by the end of
-// phase 2t - 1.  Before phase 2t every thread waits for its own loads of tile
-// t (vmcnt, loads complete in order) and the barrier publishes them.
+// groups of four (waves 0-3 and 4-7: waves w and w + 4 of a workgroup share a
+// SIMD, so each SIMD holds one wave of each group), wave tile 128 x 64 as in
+// the pipelined kernel.  The groups alternate between a fragment phase (read
+// the wave's fragments of tile t from LDS, both 16-deep steps) and a compute
+// phase (issue this thread's direct global -> LDS loads of tile t + S - 1,
+// then the 16 MFMAs of tile t at raised wave priority), one phase apart, with
+// a block barrier between phases:
+//   phase 2t:     group 0 reads tile t,      group 1 computes tile t - 1
+//   phase 2t + 1: group 0 computes tile t,   group 1 reads tile t
+// so that on every SIMD one wave issues MFMAs while the other reads LDS.
+// (Issuing the global loads in the fragment phase, ahead of the reads, slowed
+// the reads: 4.49 -> 3.85 ms for the 1000x1000 deep net's input gradient when
+// moved.)  Stage (t - 1) % S receives tile t + S - 1 from phase 2t + 1 on
+// (group 0; group 1 at 2t + 2): both groups have read tile t - 1 by the end
+// of phase 2t - 1.  Before phase 2t every thread waits for its own loads of
+// tile t (vmcnt; loads complete in order) and the barrier publishes them.
 template <int S, LayB LA, LayB LB, EpiB EPI>
 __global__ __launch_bounds__(512, 1) void gemm_bf16_pp_kernel(GemmBArgs g) {
   constexpr int BM = 256, BN = 256, BK = 32, NW = 8, NT = 512;
@@ -912,14 +915,16 @@ __global__ __launch_bounds__(512, 1) void gemm_bf16_pp_kernel(GemmBArgs g) {
   constexpr int PER_TILE = LA_N + LB_N;
   static_assert((S - 2) * PER_TILE <= 63, "vmcnt range");
   // this thread's loads of tile t have landed (its loads of up to S - 2 later tiles may be in flight)
-  auto own_tile_landed = [&](int t) {
-    const int ahead = min(S - 2, nk - 1 - t);
+  // this thread's loads of tile t have landed; `later`: how many of its later
+  // tiles may still be in flight (group 0 has issued up to tile t + S - 2 when
+  // it waits, group 1 up to t + S - 3)
+  auto own_tile_landed = [&](int t, int later) {
+    const int ahead = min(later, nk - 1 - t);
     if (ahead >= 2) OT_WAIT_VM(2 * PER_TILE);
     else if (ahead == 1) OT_WAIT_VM(PER_TILE);
     else OT_WAIT_VM(0);
   };
-  auto load_phase = [&](int t) {
-    if (t + S - 1 < nk) issue(t + S - 1);
+  auto frag_phase = [&](int t) {
     const unsigned char* sa = smem + (t % S) * STAGE_BYTES;
     const unsigned char* sb = sa + A_CH * 16;
 #pragma unroll
@@ -936,7 +941,8 @@ __global__ __launch_bounds__(512, 1) void gemm_bf16_pp_kernel(GemmBArgs g) {
       frag_fence_regs(bfr[kk]);
     }
   };
-  auto compute_phase = [&]() {
+  auto compute_phase = [&](int t) {
+    if (t + S - 1 < nk) issue(t + S - 1);
     __builtin_amdgcn_s_setprio(1);
     __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
@@ -953,24 +959,24 @@ __global__ __launch_bounds__(512, 1) void gemm_bf16_pp_kernel(GemmBArgs g) {
   // prologue: tiles 0 .. S - 2 from every thread; tile 0 published
   for (int t = 0; t < S - 1; ++t)
     if (t < nk) issue(t);
-  if (nk > 0) own_tile_landed(0);
+  if (nk > 0) own_tile_landed(0, S - 2);
   lds_barrier();
   if (grp == 0) {
     for (int t = 0; t < nk; ++t) {
-      load_phase(t);
+      frag_phase(t);
       lds_barrier();                                   // end of phase 2t
-      compute_phase();
-      if (t + 1 < nk) own_tile_landed(t + 1);
+      compute_phase(t);
+      if (t + 1 < nk) own_tile_landed(t + 1, S - 2);
       lds_barrier();                                   // end of phase 2t + 1
     }
     lds_barrier();                                     // end of phase 2 nk
   } else {
     lds_barrier();                                     // end of phase 0
     for (int t = 0; t < nk; ++t) {
-      load_phase(t);
-      if (t + 1 < nk) own_tile_landed(t + 1);
+      frag_phase(t);
+      if (t + 1 < nk) own_tile_landed(t + 1, S - 3);
       lds_barrier();                                   // end of phase 2t + 1
-      compute_phase();
+      compute_phase(t);
       lds_barrier();                                   // end of phase 2t + 2
     }
   }
