@@ -30,6 +30,7 @@
 
 #include "common.h"
 #include "philox.h"
+#include "res_host.h"
 #include "reservoir.h"
 
 namespace ot {
@@ -89,58 +90,75 @@ __device__ int block_exclusive_scan(int v, int* wave_tot, int* total) {
 //             else base[j];
 //   taken_j = A[r_j] just before step j = pre_j if r_j = j, else pre_i for the
 //             latest i < j with r_i = r_j, else base[r_j].
-// The latest-writer searches run in parallel (O(E^2) comparisons in LDS) and
-// the pre_j chains are resolved by pointer jumping.  Inputs: r[0..E) in LDS.
-// Outputs: pre[0..E), taken[0..E) in LDS; last_writer[j] = 1 when no later
-// step writes position r_j (used by the drain to persist the shuffle).
-// base(p) returns base[p] (the identity for the eviction list).
+// The latest-writer queries go through a hash table of the steps keyed by
+// r_i (open addressing in LDS, at most half full, so every probe sequence
+// ends at an empty entry; the draws rarely collide, so most queries read one
+// or two entries), and the pre_j chains are resolved by pointer jumping,
+// skipped when no step has a predecessor.  Inputs: r[0..E) in LDS, a table of
+// 2^tbits ints (2^tbits >= 2 E).  Outputs: pre[0..E), taken[0..E) in LDS;
+// last_writer[j] = 1 when no later step writes position r_j (used by the
+// drain to persist the shuffle).  base(p) returns base[p] (the identity for
+// the eviction list).
+constexpr int kShuffleArrays = 7;       // r, par, par2, lv, pre, taken, last_writer
+__host__ __device__ inline int shuffle_table_bits(int64_t cap) {
+  int b = 1;
+  while ((int64_t(1) << b) < 2 * cap) ++b;
+  return b;
+}
+// ints of dynamic LDS that a kernel resolving a shuffle of up to cap steps
+// needs: the seven arrays and the hash table
+__host__ __device__ inline int64_t shuffle_lds_ints(int64_t cap) {
+  return kShuffleArrays * cap + (int64_t(1) << shuffle_table_bits(cap));
+}
+
 template <class Base>
-__device__ void resolve_partial_shuffle(int E, const int* r, Base base, int* par, int* par2,
+__device__ void resolve_partial_shuffle(int E, const int* r, Base base, int* table, int tbits, int* par, int* par2,
                                         int* lv, int* pre, int* taken, int* last_writer) {
-  const int nt = blockDim.x;
-  // The scans read 8 entries per step (independent LDS reads in flight) and
-  // examine them in index order, so they find the same indices as an
-  // entry-by-entry scan.
-  constexpr int U = 8;
-  for (int j = threadIdx.x; j < E; j += nt) {
+  const int nt = blockDim.x, tid = threadIdx.x;
+  const unsigned tmask = (1u << tbits) - 1u;
+  auto slot0 = [&](int x) { return (unsigned)(((uint32_t)x * 2654435761u) >> (32 - tbits)) & tmask; };
+  for (unsigned h = tid; h <= tmask; h += nt) table[h] = -1;
+  __syncthreads();
+  for (int j = tid; j < E; j += nt) {
+    unsigned h = slot0(r[j]);
+    while (atomicCAS(&table[h], -1, j) != -1) h = (h + 1) & tmask;
+  }
+  __syncthreads();
+  int chain = 0;
+  for (int j = tid; j < E; j += nt) {
     const int rj = r[j];
-    int lp = -1, lvj = -1;
-    for (int i0 = j - 1; i0 >= 0 && (lp < 0 || lvj < 0); i0 -= U) {
-      int v[U];
-#pragma unroll
-      for (int u = 0; u < U; ++u) v[u] = (i0 - u >= 0) ? r[i0 - u] : -1;
-#pragma unroll
-      for (int u = 0; u < U; ++u) {
-        if (i0 - u < 0) break;
-        if (lp < 0 && v[u] == j) lp = i0 - u;
-        if (lvj < 0 && v[u] == rj) lvj = i0 - u;
+    int lp = -1, lvj = -1, later = 1;
+    for (unsigned h = slot0(j);; h = (h + 1) & tmask) {      // steps i with r_i = j
+      const int i = table[h];
+      if (i < 0) break;
+      if (r[i] == j && i < j && i > lp) lp = i;
+    }
+    for (unsigned h = slot0(rj);; h = (h + 1) & tmask) {     // steps i with r_i = r_j
+      const int i = table[h];
+      if (i < 0) break;
+      if (r[i] == rj) {
+        if (i < j && i > lvj) lvj = i;
+        if (i > j) later = 0;
       }
     }
     par[j] = lp >= 0 ? lp : j;
     lv[j] = lvj;
-    int later = 1;
-    for (int i0 = j + 1; i0 < E && later; i0 += U) {
-      int v[U];
-#pragma unroll
-      for (int u = 0; u < U; ++u) v[u] = (i0 + u < E) ? r[i0 + u] : -1;
-#pragma unroll
-      for (int u = 0; u < U; ++u)
-        if (i0 + u < E && v[u] == rj) later = 0;
-    }
     last_writer[j] = later;
+    chain |= lp >= 0;
   }
-  __syncthreads();
   // Pointer jumping: after ceil(log2 E) rounds par[j] is the root of j's chain.
   int* src = par;
   int* dst = par2;
-  for (int span = 1; span < E; span <<= 1) {
-    for (int j = threadIdx.x; j < E; j += nt) dst[j] = src[src[j]];
-    __syncthreads();
-    int* t = src; src = dst; dst = t;
+  if (__syncthreads_or(chain)) {
+    for (int span = 1; span < E; span <<= 1) {
+      for (int j = tid; j < E; j += nt) dst[j] = src[src[j]];
+      __syncthreads();
+      int* t = src; src = dst; dst = t;
+    }
   }
-  for (int j = threadIdx.x; j < E; j += nt) pre[j] = base(src[j]);
+  for (int j = tid; j < E; j += nt) pre[j] = base(src[j]);
   __syncthreads();
-  for (int j = threadIdx.x; j < E; j += nt) {
+  for (int j = tid; j < E; j += nt) {
     const int rj = r[j];
     taken[j] = (rj == j) ? pre[j] : (lv[j] >= 0 ? pre[lv[j]] : base(rj));
   }
@@ -191,12 +209,13 @@ __global__ __launch_bounds__(kAssignThreads) void put_assign_kernel(
     int64_t k, uint64_t ticket, uint64_t seed, int64_t C, int may_evict, const int32_t* __restrict__ tile_cnt,
     int64_t ntiles, int32_t* __restrict__ tile_off, int32_t* __restrict__ victim_pos,
     int32_t* __restrict__ put_slots, ResCounters* __restrict__ ctr, long long* __restrict__ accepted_out) {
-  // seven arrays of max(k, 1) ints in dynamic LDS (sized by the launch, so a
-  // small put does not hold a CU's LDS)
+  // the shuffle's arrays of max(k, 1) ints and its table in dynamic LDS
+  // (sized by the launch, so a small put does not hold a CU's LDS)
   extern __shared__ int s_dyn[];
   const int64_t cap = k > 0 ? k : 1;
   int *s_r = s_dyn, *s_par = s_r + cap, *s_par2 = s_par + cap, *s_lv = s_par2 + cap, *s_pre = s_lv + cap,
-      *s_taken = s_pre + cap, *s_last = s_taken + cap;
+      *s_taken = s_pre + cap, *s_last = s_taken + cap, *s_tab = s_last + cap;
+  const int tbits = shuffle_table_bits(cap);
   __shared__ int s_wave[kAssignThreads / 64];
   __shared__ int s_total;
 
@@ -226,7 +245,8 @@ __global__ __launch_bounds__(kAssignThreads) void put_assign_kernel(
       s_r[j] = (int)(j + (long long)range_map(w, (uint64_t)(S - j)));
     }
     __syncthreads();
-    resolve_partial_shuffle((int)E, s_r, [](int p) { return p; }, s_par, s_par2, s_lv, s_pre, s_taken, s_last);
+    resolve_partial_shuffle((int)E, s_r, [](int p) { return p; }, s_tab, tbits, s_par, s_par2, s_lv, s_pre, s_taken,
+                            s_last);
     for (long long j = tid; j < E; j += nt) victim_pos[j] = s_taken[j];
   }
   __syncthreads();
@@ -289,6 +309,142 @@ __global__ __launch_bounds__(64) void put_victim_kernel(const int32_t* __restric
         --want;
       }
     }
+  }
+}
+
+// Put, metadata decisions in one launch, for reservoirs of up to
+// kFusedMaxC slots and puts of up to kFusedMaxPut rows: the decisions of
+// put_assign_kernel, with the ascending list of seen slots indexed inside the
+// block instead of by seen_tile_count_kernel and put_victim_kernel.  The
+// block reads the seen counts 256 slots per wavefront load (lane l: slots
+// 4l .. 4l + 3 of the chunk) and keeps, per chunk c, four ballot masks
+// (mask[c][i] bit l: slot 256c + 4l + i is seen) and the chunk's count; an
+// exclusive scan of the counts gives the list position of each chunk's first
+// seen slot.  Victim position p then maps to its chunk by binary search over
+// those offsets, to its lane by binary search over the per-lane prefix counts
+// of the chunk, and to the slot within the lane's four.  Same victims as the
+// three-kernel path (same draws, same ascending order of seen slots).
+constexpr int64_t kFusedMaxC = 262144;     // <= kAssignThreads chunks of 256 slots
+constexpr int64_t kFusedMaxPut = 1024;
+__global__ __launch_bounds__(kAssignThreads) void put_assign_fused_kernel(
+    int64_t k, uint64_t ticket, uint64_t seed, int64_t C, int may_evict, const int32_t* __restrict__ seen,
+    int32_t* __restrict__ put_slots, ResCounters* __restrict__ ctr, long long* __restrict__ accepted_out) {
+  // dynamic LDS: the shuffle's arrays of max(k, 1) ints and its table, then
+  // per chunk four 64-bit masks and (one more than the chunks) offsets
+  extern __shared__ int s_dyn[];
+  const int64_t cap = k > 0 ? k : 1;
+  const int nchunks = (int)((C + 255) / 256);
+  int *s_r = s_dyn, *s_par = s_r + cap, *s_par2 = s_par + cap, *s_lv = s_par2 + cap, *s_pre = s_lv + cap,
+      *s_taken = s_pre + cap, *s_last = s_taken + cap, *s_tab = s_last + cap;
+  const int tbits = shuffle_table_bits(cap);
+  unsigned long long* s_mask = reinterpret_cast<unsigned long long*>(s_dyn + ((shuffle_lds_ints(cap) + 1) & ~1LL));
+  int* s_off = reinterpret_cast<int*>(s_mask + 4 * (int64_t)nchunks);
+  __shared__ int s_wave[kAssignThreads / 64];
+  __shared__ int s_total;
+
+  const long long U = ctr->U, S = ctr->S, N = ctr->N, base_id = ctr->next_sample_id;
+  const long long a = min((long long)k, (long long)C - U);
+  const long long F = min(a, (long long)C - N);
+  const long long E = may_evict ? a - F : 0;
+  const int tid = threadIdx.x, nt = blockDim.x, lane = tid & 63, wid = tid >> 6;
+
+  for (long long i = tid; i < F; i += nt) put_slots[i] = (int32_t)(N + i);
+
+  if (E > 0) {
+    // seen masks: wavefront wid takes chunks wid, wid + 16, ...; eight
+    // 16-byte loads in flight per lane, issued without branches (a load whose
+    // first slot is past the end reads slot 0, and slots past the end are
+    // masked; the seen array is allocated with 16 bytes to spare, so a load
+    // that starts below C stays inside it)
+    constexpr int B = 8;
+    for (int c0 = wid; c0 < nchunks; c0 += B * (kAssignThreads / 64)) {
+      int4 v[B];
+#pragma unroll
+      for (int u = 0; u < B; ++u) {
+        const int64_t s0 = (int64_t)(c0 + u * (kAssignThreads / 64)) * 256 + 4 * lane;
+        v[u] = *reinterpret_cast<const int4*>(seen + (s0 < C ? s0 : 0));
+      }
+#pragma unroll
+      for (int u = 0; u < B; ++u) {
+        const int c = c0 + u * (kAssignThreads / 64);
+        const int64_t s0 = (int64_t)c * 256 + 4 * lane;
+        const unsigned long long m0 = __ballot(s0 < C && v[u].x >= 1), m1 = __ballot(s0 + 1 < C && v[u].y >= 1),
+                                 m2 = __ballot(s0 + 2 < C && v[u].z >= 1), m3 = __ballot(s0 + 3 < C && v[u].w >= 1);
+        if (c < nchunks && lane == 0) {
+          s_mask[4 * c + 0] = m0;
+          s_mask[4 * c + 1] = m1;
+          s_mask[4 * c + 2] = m2;
+          s_mask[4 * c + 3] = m3;
+          s_off[c] = __popcll(m0) + __popcll(m1) + __popcll(m2) + __popcll(m3);
+        }
+      }
+    }
+    __syncthreads();
+    // exclusive offsets of the chunks (s_off[nchunks] = S)
+    {
+      const int cnt = tid < nchunks ? s_off[tid] : 0;
+      __syncthreads();
+      const int off = block_exclusive_scan<kAssignThreads>(cnt, s_wave, &s_total);
+      if (tid < nchunks) s_off[tid] = off;
+      if (tid == 0) s_off[nchunks] = s_total;
+      __syncthreads();
+    }
+    for (long long j = tid; j < E; j += nt) {
+      const uint64_t w = draw_word(seed, (uint64_t)j, ticket, kKindEvict);
+      s_r[j] = (int)(j + (long long)range_map(w, (uint64_t)(S - j)));
+    }
+    __syncthreads();
+    resolve_partial_shuffle((int)E, s_r, [](int p) { return p; }, s_tab, tbits, s_par, s_par2, s_lv, s_pre, s_taken,
+                            s_last);
+    for (long long j = tid; j < E; j += nt) {
+      const int p = s_taken[j];
+      // chunk: last c with s_off[c] <= p
+      int lo = 0, hi = nchunks - 1;
+      while (lo < hi) {
+        const int mid = (lo + hi + 1) >> 1;
+        if (s_off[mid] <= p) lo = mid;
+        else hi = mid - 1;
+      }
+      const int c = lo;
+      const unsigned long long* m = s_mask + 4 * c;
+      int rank = p - s_off[c];
+      // lane: last l with (seen slots of lanes < l) <= rank
+      auto below = [&](int l) {
+        const unsigned long long lowm = l >= 64 ? ~0ull : ((1ull << l) - 1);
+        return __popcll(m[0] & lowm) + __popcll(m[1] & lowm) + __popcll(m[2] & lowm) + __popcll(m[3] & lowm);
+      };
+      int llo = 0, lhi = 63;
+      while (llo < lhi) {
+        const int mid = (llo + lhi + 1) >> 1;
+        if (below(mid) <= rank) llo = mid;
+        else lhi = mid - 1;
+      }
+      rank -= below(llo);
+      int slot = -1;
+      for (int i = 0; i < 4; ++i)
+        if ((m[i] >> llo) & 1ull) {
+          if (rank == 0) {
+            slot = c * 256 + 4 * llo + i;
+            break;
+          }
+          --rank;
+        }
+      put_slots[F + j] = slot;
+    }
+  }
+  __syncthreads();
+  if (tid == 0) {
+    ctr->U = U + a;
+    ctr->S = S - E;
+    ctr->N = N + F;
+    ctr->total_put += a;
+    ctr->total_evicted += E;
+    ctr->next_sample_id = base_id + a;
+    ctr->last_accepted = a;
+    ctr->last_free = F;
+    ctr->last_evicted = E;
+    ctr->last_base_id = base_id;
+    if (accepted_out) *accepted_out = a;
   }
 }
 
@@ -382,11 +538,12 @@ __global__ __launch_bounds__(kAssignThreads) void list_take_kernel(
     int32_t* __restrict__ occ, int32_t* __restrict__ free_q, int64_t free_tail, int32_t* __restrict__ slots,
     int32_t* __restrict__ seen, long long* __restrict__ sample_id, unsigned long long* __restrict__ hist,
     ResCounters* __restrict__ ctr) {
-  // seven arrays of max(bb, 1) ints in dynamic LDS, sized by the launch
+  // the shuffle's arrays of max(bb, 1) ints and its table in dynamic LDS, sized by the launch
   extern __shared__ int s_dyn[];
   const int64_t cap = bb > 0 ? bb : 1;
   int *s_r = s_dyn, *s_par = s_r + cap, *s_par2 = s_par + cap, *s_lv = s_par2 + cap, *s_pre = s_lv + cap,
-      *s_taken = s_pre + cap, *s_last = s_taken + cap;
+      *s_taken = s_pre + cap, *s_last = s_taken + cap, *s_tab = s_last + cap;
+  const int tbits = shuffle_table_bits(cap);
   __shared__ long long s_dU, s_dS;
   const int tid = threadIdx.x, nt = blockDim.x;
   auto pos = [&](int64_t p) { return (occ_base + p) % C; };
@@ -397,8 +554,8 @@ __global__ __launch_bounds__(kAssignThreads) void list_take_kernel(
       s_r[j] = (int)(j + (long long)range_map(w, (uint64_t)(N - j)));
     }
     __syncthreads();
-    resolve_partial_shuffle((int)bb, s_r, [&](int p) { return (int)occ[pos(p)]; }, s_par, s_par2, s_lv, s_pre,
-                            s_taken, s_last);
+    resolve_partial_shuffle((int)bb, s_r, [&](int p) { return (int)occ[pos(p)]; }, s_tab, tbits, s_par, s_par2,
+                            s_lv, s_pre, s_taken, s_last);
     // Persist the shuffle for positions that stay in the list.
     for (long long j = tid; j < bb; j += nt)
       if (s_r[j] >= bb && s_last[j]) occ[pos(s_r[j])] = s_pre[j];
@@ -496,8 +653,8 @@ using ot::ResCounters;
 
 struct ot_reservoir {
   int device = 0;
-  int policy = OT_POLICY_RESERVOIR;
-  int64_t C = 0, T = 0, x_dim = 0, u_dim = 0, ldxs = 0, ldus = 0;
+  ot::ResSeq seq;            // policy, C, T and the host-known state of the call sequence
+  int64_t x_dim = 0, u_dim = 0, ldxs = 0, ldus = 0;
   uint64_t seed = 0;
   float* xslab = nullptr;
   float* uslab = nullptr;
@@ -515,12 +672,7 @@ struct ot_reservoir {
   hipStream_t stream = nullptr;
   bool own_stream = false;
   hipEvent_t ev_in = nullptr, ev_out = nullptr;
-  std::mutex mu;
-  uint64_t next_ticket = 0;
-  int64_t n_host = 0;      // N, known from the call sequence
-  int64_t occ_base = 0;    // ring position of the list's first entry (drain, FIFO, FIRO)
-  int64_t free_head = 0;   // ring position of the first free slot (FIFO, FIRO)
-  bool reception_over = false;
+  std::mutex mu;             // guards seq and the timer; held for the whole of every call
   ot::PhaseTimer timer;
 };
 
@@ -577,6 +729,19 @@ int leave(ot_reservoir* r, hipStream_t caller) {
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
+// Dynamic LDS of put_assign_fused_kernel: the shuffle's seven arrays of
+// max(k, 1) ints (rounded to 8 bytes), four 64-bit masks per 256-slot chunk
+// and one offset per chunk plus one.
+unsigned fused_assign_lds(int64_t C, int64_t k) {
+  const int64_t cap = std::max<int64_t>(k, 1);
+  const int64_t nchunks = ot::ceil_div(C, 256);
+  return (unsigned)(((ot::shuffle_lds_ints(cap) + 1) & ~1LL) * sizeof(int) +
+                    4 * nchunks * sizeof(unsigned long long) + (nchunks + 1) * sizeof(int));
+}
+
+// Dynamic LDS of put_assign_kernel and list_take_kernel for up to n steps.
+unsigned shuffle_lds(int64_t n) { return (unsigned)(ot::shuffle_lds_ints(std::max<int64_t>(n, 1)) * sizeof(int)); }
+
 }  // namespace
 
 extern "C" int reservoir_create(ot_reservoir** out, int64_t capacity, int64_t threshold,
@@ -593,9 +758,9 @@ extern "C" int reservoir_create(ot_reservoir** out, int64_t capacity, int64_t th
   OT_REQUIRE(x_dim >= 1 && x_dim <= 4096, "reservoir_create: x_dim outside [1, 4096]");
   OT_REQUIRE(u_dim >= 1 && u_dim <= (1LL << 31), "reservoir_create: u_dim outside [1, 2^31]");
   ot_reservoir* r = new ot_reservoir();
-  r->policy = policy;
-  r->C = capacity;
-  r->T = threshold;
+  r->seq.policy = policy;
+  r->seq.C = capacity;
+  r->seq.T = threshold;
   r->x_dim = x_dim;
   r->u_dim = u_dim;
   r->ldxs = ot::round_up(x_dim, 4);
@@ -628,10 +793,13 @@ extern "C" int reservoir_create(ot_reservoir** out, int64_t capacity, int64_t th
     r->own_stream = true;
   }
   {
-    // the assignment and take kernels size their LDS per call, up to 7 ints per row of the largest call
-    const int max_dyn = (int)(7 * std::max(ot::kMaxPut, ot::kMaxDrainBatch) * sizeof(int));
+    // the assignment and take kernels size their LDS per call (the shuffle's arrays and table for the largest call)
+    const int max_dyn = (int)shuffle_lds(std::max(ot::kMaxPut, ot::kMaxDrainBatch));
     if (hipFuncSetAttribute(reinterpret_cast<const void*>(&ot::put_assign_kernel),
                             hipFuncAttributeMaxDynamicSharedMemorySize, max_dyn) != hipSuccess ||
+        hipFuncSetAttribute(reinterpret_cast<const void*>(&ot::put_assign_fused_kernel),
+                            hipFuncAttributeMaxDynamicSharedMemorySize,
+                            (int)fused_assign_lds(ot::kFusedMaxC, ot::kFusedMaxPut)) != hipSuccess ||
         hipFuncSetAttribute(reinterpret_cast<const void*>(&ot::list_take_kernel),
                             hipFuncAttributeMaxDynamicSharedMemorySize, max_dyn) != hipSuccess)
       return fail(ot::set_error(OT_E_HIP, "hipFuncSetAttribute (dynamic LDS) failed"));
@@ -668,20 +836,21 @@ extern "C" int reservoir_put(ot_reservoir* r, const float* x, int64_t ldx, const
   }
   hipStream_t cs = static_cast<hipStream_t>(stream);
   std::lock_guard<std::mutex> lock(r->mu);
-  if (r->reception_over) return ot::set_error(OT_E_CLOSED, "reservoir_put: reception is over");
+  if (ot::put_admit(r->seq) != OT_OK) return ot::set_error(OT_E_CLOSED, "reservoir_put: reception is over");
   // the ticket is taken only once the ordering stream waits for the caller:
   // a call that fails before enqueueing anything leaves the ticket sequence unchanged
   int rc = enter(r, cs);
   if (rc) return rc;
-  const uint64_t ticket = r->next_ticket++;
+  const ot::PutCall pc = ot::put_commit(r->seq, k);
+  const uint64_t ticket = pc.ticket;
   if (ticket_out) *ticket_out = ticket;
   ot::PhaseTimer& tm = r->timer;
-  if (r->policy != OT_POLICY_RESERVOIR) {
+  if (r->seq.policy != OT_POLICY_RESERVOIR) {
     // FIFO / FIRO: the accepted prefix and every ring position are host-known
-    const int64_t a = std::min<int64_t>(k, r->C - r->n_host);
+    const int64_t a = pc.accepted;
     tm.mark(r->stream, OT_PH_PUT_ASSIGN, 0);
     hipLaunchKernelGGL(ot::list_put_kernel, dim3((unsigned)std::max<int64_t>(1, ot::ceil_div(a, 256))), dim3(256),
-                       0, r->stream, a, r->n_host, r->occ_base, r->free_head, r->C, r->free_q, r->occ,
+                       0, r->stream, a, pc.n_before, r->seq.occ_base, pc.free_head, r->seq.C, r->free_q, r->occ,
                        r->put_slots, r->ctr, reinterpret_cast<long long*>(accepted_dev));
     OT_LAUNCHED("list_put_kernel");
     tm.mark(r->stream, OT_PH_PUT_ASSIGN, 1);
@@ -693,32 +862,37 @@ extern "C" int reservoir_put(ot_reservoir* r, const float* x, int64_t ldx, const
       hipExtLaunchKernelGGL(ot::put_copy_kernel, dim3((unsigned)(segs * a)), dim3(ot::kCopyThreads), 0, r->stream,
                             t0, t1, 0, x, ldx, u, ldu, r->put_slots, (const ot::ResCounters*)r->ctr, r->xslab,
                             r->ldxs, r->uslab, r->ldus, r->x_dim, r->u_dim, segs, vec_ok, r->seen, r->sample_id,
-                            r->hist, r->C);
+                            r->hist, r->seq.C);
       OT_LAUNCHED("put_copy_kernel");
     }
     tm.next_call();
-    r->n_host += a;
-    r->free_head = (r->free_head + a) % r->C;
     return leave(r, cs);
   }
   tm.mark(r->stream, OT_PH_PUT_ASSIGN, 0);
   // Replacement is possible only if N + k > C (host-known N); only then are
   // the seen slots indexed.
-  const int may_evict = (r->n_host + k > r->C) ? 1 : 0;
+  const int may_evict = pc.may_evict;
+  if (r->seq.C <= ot::kFusedMaxC && k <= ot::kFusedMaxPut) {
+    hipLaunchKernelGGL(ot::put_assign_fused_kernel, dim3(1), dim3(ot::kAssignThreads), fused_assign_lds(r->seq.C, k),
+                       r->stream, k, ticket, r->seed, r->seq.C, may_evict, (const int32_t*)r->seen, r->put_slots, r->ctr,
+                       reinterpret_cast<long long*>(accepted_dev));
+    OT_LAUNCHED("put_assign_fused_kernel");
+  } else {
   if (may_evict) {
     hipLaunchKernelGGL(ot::seen_tile_count_kernel, dim3((unsigned)r->ntiles), dim3(256), 0, r->stream, r->seen,
-                       r->C, r->tile_cnt);
+                       r->seq.C, r->tile_cnt);
     OT_LAUNCHED("seen_tile_count_kernel");
   }
   hipLaunchKernelGGL(ot::put_assign_kernel, dim3(1), dim3(ot::kAssignThreads),
-                     (unsigned)(7 * std::max<int64_t>(k, 1) * sizeof(int)), r->stream, k, ticket, r->seed,
-                     r->C, may_evict, r->tile_cnt, r->ntiles, r->tile_off, r->victim_pos, r->put_slots, r->ctr,
+                     shuffle_lds(k), r->stream, k, ticket, r->seed,
+                     r->seq.C, may_evict, r->tile_cnt, r->ntiles, r->tile_off, r->victim_pos, r->put_slots, r->ctr,
                      reinterpret_cast<long long*>(accepted_dev));
   OT_LAUNCHED("put_assign_kernel");
   if (may_evict && k > 0) {
-    hipLaunchKernelGGL(ot::put_victim_kernel, dim3((unsigned)k), dim3(64), 0, r->stream, r->seen, r->C,
+    hipLaunchKernelGGL(ot::put_victim_kernel, dim3((unsigned)k), dim3(64), 0, r->stream, r->seen, r->seq.C,
                        r->tile_off, r->ntiles, r->victim_pos, r->put_slots, r->ctr);
     OT_LAUNCHED("put_victim_kernel");
+  }
   }
   tm.mark(r->stream, OT_PH_PUT_ASSIGN, 1);
   if (k > 0) {
@@ -728,11 +902,10 @@ extern "C" int reservoir_put(ot_reservoir* r, const float* x, int64_t ldx, const
     const int64_t segs = ot::ceil_div(r->u_dim, ot::kCopySeg);
     hipExtLaunchKernelGGL(ot::put_copy_kernel, dim3((unsigned)(segs * k)), dim3(ot::kCopyThreads), 0, r->stream, t0,
                           t1, 0, x, ldx, u, ldu, r->put_slots, (const ot::ResCounters*)r->ctr, r->xslab, r->ldxs,
-                          r->uslab, r->ldus, r->x_dim, r->u_dim, segs, vec_ok, r->seen, r->sample_id, r->hist, r->C);
+                          r->uslab, r->ldus, r->x_dim, r->u_dim, segs, vec_ok, r->seen, r->sample_id, r->hist, r->seq.C);
     OT_LAUNCHED("put_copy_kernel");
   }
   tm.next_call();
-  r->n_host = std::min<int64_t>(r->C, r->n_host + k);
   return leave(r, cs);
 }
 
@@ -748,44 +921,34 @@ extern "C" int reservoir_sample_batch(ot_reservoir* r, int64_t b, void* stream, 
   OT_REQUIRE(u_out == nullptr || lduo >= r->u_dim, "reservoir_sample_batch: lduo < u_dim");
   OT_REQUIRE(x_out == nullptr || ldxo >= r->x_dim, "reservoir_sample_batch: ldxo < x_dim");
   hipStream_t cs = static_cast<hipStream_t>(stream);
-  const bool list_take = r->policy != OT_POLICY_RESERVOIR;   // FIFO / FIRO take samples out
+  const bool list_take = r->seq.policy != OT_POLICY_RESERVOIR;   // FIFO / FIRO take samples out
   if (list_take)
     OT_REQUIRE(b <= ot::kMaxDrainBatch, "reservoir_sample_batch: b=%lld above %lld for a FIFO / FIRO buffer",
                (long long)b, (long long)ot::kMaxDrainBatch);
   std::lock_guard<std::mutex> lock(r->mu);
   int64_t drawn = b;
-  if (r->reception_over) {
-    if (r->n_host == 0) return OT_EMPTY;
+  const int admit = ot::draw_admit(r->seq, b, &drawn);
+  if (admit != OT_OK) return admit;
+  if (r->seq.reception_over)
     OT_REQUIRE(b <= ot::kMaxDrainBatch, "reservoir_sample_batch: b=%lld above %lld while draining",
                (long long)b, (long long)ot::kMaxDrainBatch);
-    drawn = std::min<int64_t>(b, r->n_host);
-  } else if (r->policy == OT_POLICY_FIFO) {
-    if (r->n_host < b) return OT_NOT_READY;           // a batch as soon as the buffer holds one
-  } else if (r->policy == OT_POLICY_FIRO) {
-    if (r->n_host <= r->T || r->n_host < b) return OT_NOT_READY;
-  } else if (r->n_host <= r->T) {
-    return OT_NOT_READY;
-  }
   int rc = enter(r, cs);
   if (rc) return rc;
-  const uint64_t ticket = r->next_ticket++;
+  const ot::DrawCall dc = ot::draw_commit(r->seq, drawn);
+  const uint64_t ticket = dc.ticket;
   if (ticket_out) *ticket_out = ticket;
   ot::PhaseTimer& tm = r->timer;
   tm.mark(r->stream, OT_PH_SELECT, 0);
-  if (!r->reception_over && !list_take) {
+  if (!dc.take) {
     hipLaunchKernelGGL(ot::select_kernel, dim3((unsigned)ot::ceil_div(b, 256)), dim3(256), 0, r->stream,
-                       r->seed, ticket, r->n_host, b, slots, r->seen, r->ctr);
+                       r->seed, ticket, dc.n_before, b, slots, r->seen, r->ctr);
     OT_LAUNCHED("select_kernel");
   } else {
-    // free queue tail: C - N entries follow its head
-    const int64_t free_tail = (r->free_head + r->C - r->n_host) % r->C;
     hipLaunchKernelGGL(ot::list_take_kernel, dim3(1), dim3(ot::kAssignThreads),
-                       (unsigned)(7 * std::max<int64_t>(drawn, 1) * sizeof(int)), r->stream, r->seed, ticket,
-                       r->n_host, drawn, r->policy == OT_POLICY_FIFO ? 0 : 1, r->occ_base, r->C, r->occ,
-                       r->free_q, free_tail, slots, r->seen, r->sample_id, r->hist, r->ctr);
+                       shuffle_lds(drawn), r->stream, r->seed, ticket,
+                       dc.n_before, drawn, r->seq.policy == OT_POLICY_FIFO ? 0 : 1, dc.occ_base, r->seq.C, r->occ,
+                       r->free_q, dc.free_tail, slots, r->seen, r->sample_id, r->hist, r->ctr);
     OT_LAUNCHED("list_take_kernel");
-    r->occ_base = (r->occ_base + drawn) % r->C;
-    r->n_host -= drawn;
   }
   tm.mark(r->stream, OT_PH_SELECT, 1);
   if (x_out && !u_out) {
@@ -815,14 +978,11 @@ extern "C" int reservoir_end_reception(ot_reservoir* r) {
   ot::clear_error();
   OT_REQUIRE(r != nullptr, "reservoir_end_reception: NULL reservoir");
   std::lock_guard<std::mutex> lock(r->mu);
-  if (r->reception_over) return ot::set_error(OT_E_STATE, "reservoir_end_reception: already over");
-  r->reception_over = true;
-  r->T = 0;
-  if (r->policy != OT_POLICY_RESERVOIR) return OT_OK;   // the list is already maintained
-  r->occ_base = 0;
-  if (r->n_host > 0) {
-    hipLaunchKernelGGL(ot::iota_kernel, dim3((unsigned)ot::ceil_div(r->n_host, 256)), dim3(256), 0, r->stream,
-                       r->occ, r->n_host);
+  if (ot::end_commit(r->seq) != OT_OK) return ot::set_error(OT_E_STATE, "reservoir_end_reception: already over");
+  if (r->seq.policy != OT_POLICY_RESERVOIR) return OT_OK;   // the list is already maintained
+  if (r->seq.n_host > 0) {
+    hipLaunchKernelGGL(ot::iota_kernel, dim3((unsigned)ot::ceil_div(r->seq.n_host, 256)), dim3(256), 0, r->stream,
+                       r->occ, r->seq.n_host);
     OT_LAUNCHED("iota_kernel");
   }
   return OT_OK;
@@ -845,8 +1005,8 @@ extern "C" int reservoir_stats(ot_reservoir* r, ot_reservoir_stats* out) {
   OT_HIP(hipStreamSynchronize(r->stream));
   ResCounters c;
   OT_HIP(hipMemcpy(&c, r->ctr, sizeof c, hipMemcpyDeviceToHost));
-  out->capacity = r->C;
-  out->threshold = r->T;
+  out->capacity = r->seq.C;
+  out->threshold = r->seq.T;
   out->n = c.N;
   out->unseen = c.U;
   out->seen = c.S;
@@ -854,11 +1014,11 @@ extern "C" int reservoir_stats(ot_reservoir* r, ot_reservoir_stats* out) {
   out->total_evicted = c.total_evicted;
   out->total_deleted = c.total_deleted;
   out->total_draws = c.total_draws;
-  out->next_ticket = (int64_t)r->next_ticket;
+  out->next_ticket = (int64_t)r->seq.next_ticket;
   out->next_sample_id = c.next_sample_id;
-  out->reception_over = r->reception_over ? 1 : 0;
+  out->reception_over = r->seq.reception_over ? 1 : 0;
   out->hist_len = ot::kHistLen;
-  out->policy = r->policy;
+  out->policy = r->seq.policy;
   out->reserved = 0;
   return OT_OK;
 }
@@ -869,8 +1029,8 @@ extern "C" int reservoir_read_meta(ot_reservoir* r, int32_t* seen_count, int64_t
   OT_REQUIRE(r != nullptr, "reservoir_read_meta: NULL reservoir");
   std::lock_guard<std::mutex> lock(r->mu);
   OT_HIP(hipStreamSynchronize(r->stream));
-  if (seen_count) OT_HIP(hipMemcpy(seen_count, r->seen, r->C * sizeof(int32_t), hipMemcpyDeviceToHost));
-  if (sample_id) OT_HIP(hipMemcpy(sample_id, r->sample_id, r->C * sizeof(int64_t), hipMemcpyDeviceToHost));
+  if (seen_count) OT_HIP(hipMemcpy(seen_count, r->seen, r->seq.C * sizeof(int32_t), hipMemcpyDeviceToHost));
+  if (sample_id) OT_HIP(hipMemcpy(sample_id, r->sample_id, r->seq.C * sizeof(int64_t), hipMemcpyDeviceToHost));
   if (evict_hist)
     OT_HIP(hipMemcpy(evict_hist, r->hist, ot::kHistLen * sizeof(int64_t), hipMemcpyDeviceToHost));
   return OT_OK;
@@ -881,7 +1041,7 @@ extern "C" int reservoir_read_rows(ot_reservoir* r, const int32_t* slots_host, i
   ot::clear_error();
   OT_REQUIRE(r != nullptr && slots_host != nullptr && n >= 0, "reservoir_read_rows: bad argument");
   for (int64_t i = 0; i < n; ++i)
-    OT_REQUIRE(slots_host[i] >= 0 && slots_host[i] < r->C, "reservoir_read_rows: slot %d out of range",
+    OT_REQUIRE(slots_host[i] >= 0 && slots_host[i] < r->seq.C, "reservoir_read_rows: slot %d out of range",
                (int)slots_host[i]);
   std::lock_guard<std::mutex> lock(r->mu);
   OT_HIP(hipStreamSynchronize(r->stream));
@@ -910,7 +1070,7 @@ constexpr char kResMagic[8] = {'O', 'T', 'R', 'E', 'S', 'V', '1', 0};
 constexpr int64_t kResHeaderWords = 13;
 
 int64_t res_blob_bytes(const ot_reservoir* r, int64_t n_rows) {
-  return 8 + kResHeaderWords * 8 + (int64_t)sizeof(ResCounters) + ot::kHistLen * 8 + r->C * (4 + 8 + 4 + 4) +
+  return 8 + kResHeaderWords * 8 + (int64_t)sizeof(ResCounters) + ot::kHistLen * 8 + r->seq.C * (4 + 8 + 4 + 4) +
          n_rows * (r->x_dim + r->u_dim) * 4;
 }
 
@@ -949,7 +1109,7 @@ extern "C" int reservoir_checkpoint(ot_reservoir* r, void* buf, int64_t bytes) {
   OT_REQUIRE(r != nullptr && buf != nullptr, "reservoir_checkpoint: NULL argument");
   std::lock_guard<std::mutex> lock(r->mu);
   OT_HIP(hipStreamSynchronize(r->stream));
-  const int64_t C = r->C;
+  const int64_t C = r->seq.C;
   ResCounters c;
   std::vector<unsigned long long> hist(ot::kHistLen);
   std::vector<int32_t> seen(C), occ(C), freeq(C);
@@ -962,15 +1122,15 @@ extern "C" int reservoir_checkpoint(ot_reservoir* r, void* buf, int64_t bytes) {
   OT_HIP(hipMemcpy(freeq.data(), r->free_q, C * 4, hipMemcpyDeviceToHost));
   int64_t n_rows = 0;
   for (int32_t v : seen) n_rows += v >= 0;
-  if (n_rows != c.N || n_rows != r->n_host)
+  if (n_rows != c.N || n_rows != r->seq.n_host)
     return ot::set_error(OT_E_STATE, "reservoir_checkpoint: %lld occupied slots but N = %lld (host %lld)",
-                         (long long)n_rows, (long long)c.N, (long long)r->n_host);
+                         (long long)n_rows, (long long)c.N, (long long)r->seq.n_host);
   OT_REQUIRE(bytes >= res_blob_bytes(r, n_rows), "reservoir_checkpoint: buffer of %lld bytes, %lld needed",
              (long long)bytes, (long long)res_blob_bytes(r, n_rows));
   ot::BlobWriter w(buf, bytes);
   __builtin_memcpy(w.take(8), kResMagic, 8);
-  for (int64_t v : {(int64_t)r->policy, C, r->T, r->x_dim, r->u_dim, (int64_t)r->seed, (int64_t)r->next_ticket,
-                    r->n_host, r->occ_base, r->free_head, (int64_t)r->reception_over, n_rows,
+  for (int64_t v : {(int64_t)r->seq.policy, C, r->seq.T, r->x_dim, r->u_dim, (int64_t)r->seed, (int64_t)r->seq.next_ticket,
+                    r->seq.n_host, r->seq.occ_base, r->seq.free_head, (int64_t)r->seq.reception_over, n_rows,
                     (int64_t)ot::kHistLen})
     w.put(v);
   w.put(c);
@@ -1003,7 +1163,7 @@ extern "C" int reservoir_restore(ot_reservoir* r, const void* buf, int64_t bytes
   const int64_t policy = h[0], C = h[1], T = h[2], x_dim = h[3], u_dim = h[4], n_host = h[7], occ_base = h[8],
                 free_head = h[9], n_rows = h[11], hist_len = h[12];
   OT_REQUIRE(rd.good, "reservoir_restore: truncated header");
-  OT_REQUIRE(policy == r->policy && C == r->C && x_dim == r->x_dim && u_dim == r->u_dim,
+  OT_REQUIRE(policy == r->seq.policy && C == r->seq.C && x_dim == r->x_dim && u_dim == r->u_dim,
              "reservoir_restore: checkpoint of a different buffer (policy %lld, C %lld, x_dim %lld, u_dim %lld)",
              (long long)policy, (long long)C, (long long)x_dim, (long long)u_dim);
   OT_REQUIRE(hist_len == ot::kHistLen && T >= 0 && n_host >= 0 && n_host <= C && n_rows == n_host &&
@@ -1040,13 +1200,13 @@ extern "C" int reservoir_restore(ot_reservoir* r, const void* buf, int64_t bytes
     return OT_OK;
   });
   if (rc) return rc;
-  r->T = T;
+  r->seq.T = T;
   r->seed = (uint64_t)h[5];
-  r->next_ticket = (uint64_t)h[6];
-  r->n_host = n_host;
-  r->occ_base = occ_base;
-  r->free_head = free_head;
-  r->reception_over = h[10] != 0;
+  r->seq.next_ticket = (uint64_t)h[6];
+  r->seq.n_host = n_host;
+  r->seq.occ_base = occ_base;
+  r->seq.free_head = free_head;
+  r->seq.reception_over = h[10] != 0;
   return OT_OK;
 }
 

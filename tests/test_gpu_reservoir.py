@@ -296,3 +296,55 @@ def test_largest_put_and_take(policy):
     assert np.array_equal(slots.cpu().numpy(), np.array(oslots)) and np.array_equal(ub.cpu().numpy(), ou)
     compare_meta(g, o, 64)
     g.close()
+
+
+@pytest.mark.parametrize("C,k_evict", [
+    (262144, 100),     # the largest reservoir whose put decisions run in one launch (1024 chunks of 256 slots)
+    (262145, 100),     # one slot more: the tile-count / assign / victim kernels
+    (5000, 1024),      # the largest put that runs in one launch
+    (5000, 1025),      # one row more
+])
+def test_eviction_index_on_both_sides_of_the_one_launch_limits(C, k_evict):
+    """Puts that replace seen samples pick the same victims (slots, seen counts,
+    sample ids, eviction histogram bit-exact against the oracle) whether their
+    decisions run in the single-launch kernel (reservoirs of up to 262,144
+    slots, puts of up to 1024 rows) or in the three-kernel path."""
+    from paper_2309_16743_amd import OT_OK, Reservoir
+    print(f"eviction index C={C} k={k_evict}", flush=True)
+    d = 1
+    g = Reservoir(C, 0, 6, d, 11)
+    o = orv.Reservoir(C, 0, 6, d, 11)
+    key = 0
+
+    def put(k):
+        nonlocal key
+        keys = np.arange(key, key + k)
+        ud = padded(k, d)
+        ud.copy_(torch.from_numpy(hash_rows(keys, d)))
+        acc = torch.zeros(1, dtype=torch.int64, device=DEV)
+        t = g.put(None, ud, accepted=acc)
+        _, a, ot_, _ = o.put(None, hash_rows(keys, d), k=k)
+        assert t == ot_
+        torch.cuda.synchronize()
+        assert int(acc.item()) == a
+        key += a
+
+    def draw(b):
+        slots = torch.empty(b, dtype=torch.int32, device=DEV)
+        st, n, t = g.sample_batch(b, slots)
+        ost, oslots, _, _, ot_ = o.sample_batch(b)
+        assert st == ost == OT_OK and t == ot_
+        torch.cuda.synchronize()
+        assert np.array_equal(slots.cpu().numpy(), np.array(oslots))
+
+    while o.N < C:
+        put(min(4096, C - o.N))
+    for _ in range(3):
+        draw(8192)
+    compare_meta(g, o, 64)
+    for i in range(4):
+        put(k_evict)
+        draw(4096)
+    compare_meta(g, o, 64)
+    assert o.total_evicted >= 4 * k_evict
+    g.close()
