@@ -180,7 +180,7 @@ def kernel_matches(label: str, name: str) -> bool:
         return "gemm_f32_kernel<" in name and lay in name and name.split(">(")[0].endswith(", 1")
     lay = {"fwd_output": "(ot::LayB)0, (ot::LayB)0", "wgrad_output": "(ot::LayB)1, (ot::LayB)1",
            "igrad_output": "(ot::LayB)0, (ot::LayB)1"}[phase]
-    return "gemm_bf16_pipe_kernel<" in name and lay in name
+    return ("gemm_bf16_pipe_kernel<" in name or "gemm_bf16_pp_kernel<" in name) and lay in name
 
 
 def traffic_for(workload: str, label: str):

@@ -72,12 +72,15 @@ def test_pmc_readings_scaled_by_the_calibration_kernel(bench, tmp_path, monkeypa
 
 def test_roofline_labels_match_their_kernels(bench):
     fused = "void ot::gemm_bf16_pipe_kernel<128, 256, 32, 3, 2, (ot::LayB)1, (ot::LayB)1, (ot::EpiB)6, 2>(ot::GemmBArgs)"
-    igrad = "void ot::gemm_bf16_pipe_kernel<256, 256, 32, 4, 1, (ot::LayB)0, (ot::LayB)1, (ot::EpiB)1, 4>(ot::GemmBArgs)"
+    igrad = "void ot::gemm_bf16_pp_kernel<4, (ot::LayB)0, (ot::LayB)1, (ot::EpiB)1>(ot::GemmBArgs)"
+    fwd16 = "void ot::gemm_bf16_pp_kernel<4, (ot::LayB)0, (ot::LayB)0, (ot::EpiB)5>(ot::GemmBArgs)"
     fwd32 = "void ot::gemm_f32_kernel<2, 2, 2, 4, (ot::Lay)0, (ot::Lay)0, (ot::Epi)3, 16, 1>(ot::GemmArgs)"
     hidden32 = "void ot::gemm_f32_kernel<2, 2, 2, 4, (ot::Lay)0, (ot::Lay)0, (ot::Epi)2, 16, 0>(ot::GemmArgs)"
     assert bench.kernel_matches("gemm_bf16 (wgrad_output + fused Adam)", fused)
     assert not bench.kernel_matches("gemm_bf16 (wgrad_output + fused Adam)", igrad)
     assert bench.kernel_matches("gemm_bf16 (igrad_output)", igrad)
+    assert bench.kernel_matches("gemm_bf16 (fwd_output)", fwd16)
+    assert not bench.kernel_matches("gemm_bf16 (fwd_output)", igrad)
     assert bench.kernel_matches("gemm_fp32 (fwd_output)", fwd32)
     assert not bench.kernel_matches("gemm_fp32 (fwd_output)", hidden32)        # hidden layers: ROLE 0
     assert bench.kernel_matches("gather_x_kernel", "ot::gather_x_kernel(int const*, float const*, long)")
