@@ -10,7 +10,8 @@ trains (two batch buffers, ordered by events), as the paper's aggregator and
 training threads run concurrently; --one-stream runs everything on one stream,
 as does a workload whose batch targets are under 1 MiB (tiny-16x16), where the
 step is launch-latency-bound and two cross-stream waits cost more than the
-overlap gains.
+overlap gains; there the train step is captured once as a HIP graph and
+replayed each step (--no-graph launches its kernels every step).
 
 Default workload (--config deep-sine-1000x1000): 1000x1000 fields (smooth
 sine-mode stand-ins for heat solutions, generated on the GPU), MLP
@@ -85,6 +86,9 @@ def parse_args():
     p.add_argument("--gathered-targets", action="store_true",
                    help="gather the batch's field rows into a batch buffer before the train step (default: the "
                         "output layer's forward reads them in place from the reservoir through the drawn slots)")
+    p.add_argument("--no-graph", action="store_true",
+                   help="one-stream workloads: launch every train step's kernels instead of replaying the "
+                        "step captured as a HIP graph")
     p.add_argument("--one-stream", action="store_true",
                    help="run the reservoir and the train step on one stream (default: the reservoir's put, draw "
                         "and gather of the next batch overlap the current train step on a second stream, unless "
@@ -519,11 +523,14 @@ def timed_region(tr, w, K, profile_steps, stream, wrap_put):
     tr.sur.timing_begin(list(SURROGATE_PHASES), kp)
     tr.res.timing_begin(["put_assign", "put_copy", "select", "gather"], 2 * kp)
     tr.serialize = True             # breakdown with the reservoir and train step one after the other
+    graph = getattr(tr, "graph", False)
+    tr.graph_active = False          # phase events come from eager launches (a replayed step records none)
     for _ in range(kp):
         wrap_put()
         assert tr.sample_and_train()
     breakdown = kernel_table(w, tr.sur.timing_end(), tr.res.timing_end())
     tr.serialize = False
+    tr.graph_active = graph
     candidates = ("fwd_output", "wgrad_output", "igrad_output", "adam", "reservoir_gather")
     dominant = max((c for c in candidates if c in breakdown), key=lambda p: breakdown[p]["avg_us"])
     dom_phase = "gather" if dominant == "reservoir_gather" else dominant
@@ -531,7 +538,8 @@ def timed_region(tr, w, K, profile_steps, stream, wrap_put):
     # timed region: the dominant kernel, the three output-layer GEMMs, the put copies and the gather
     out_phases = [p for p in ("fwd_output", "wgrad_output", "igrad_output") if p in breakdown]
     sur_phases = [p for p in SURROGATE_PHASES if p in out_phases or p == dom_phase]
-    tr.sur.timing_begin(sur_phases, K)
+    if not graph:
+        tr.sur.timing_begin(sur_phases, K)
     tr.res.timing_begin(["put_copy", "gather"], 2 * K)
     n_win = K // 10
     ev = [torch.cuda.Event(enable_timing=True) for _ in range(n_win + 2)]
@@ -551,7 +559,20 @@ def timed_region(tr, w, K, profile_steps, stream, wrap_put):
     gpu_ms = ev[0].elapsed_time(ev[-1])
     windows = [ev[j].elapsed_time(ev[j + 1]) for j in range(n_win)]
     res_t = tr.res.timing_end()
-    sur_t = tr.sur.timing_end()
+    if graph:
+        # the timed steps replayed the captured train step, which records no
+        # phase events: the train step's kernels are timed on eager steps
+        # that follow the timed region
+        kt = min(K, 200)
+        tr.graph_active = False
+        tr.sur.timing_begin(sur_phases, kt)
+        for _ in range(kt):
+            wrap_put()
+            assert tr.sample_and_train()
+        sur_t = tr.sur.timing_end()
+        tr.graph_active = True
+    else:
+        sur_t = tr.sur.timing_end()
     g_ms, g_n = res_t["gather"]
     phase_avg_s = {p: sur_t[p][0] / sur_t[p][1] * 1e-3 for p in sur_phases if p in sur_t}
     put_avg_s = res_t["put_copy"][0] / res_t["put_copy"][1] * 1e-3 if "put_copy" in res_t else None
@@ -685,9 +706,10 @@ def run_heat(args, w):
     fields_d = torch.from_numpy(fields).to(dev)
     stream = torch.cuda.Stream(device=dev)
     with torch.cuda.stream(stream):
+        graph = one_stream(args, w) and not args.gathered_targets and not args.no_graph
         tr = OnlineTrainer(w.widths, w.batch, w.capacity, w.threshold, w.wave, w.tau, inputs_d, fields_d,
                            w.reservoir_seed, w.init_seed, lr=w.lr, stream=stream, overlap=not one_stream(args, w),
-                           fused_targets=not args.gathered_targets)
+                           fused_targets=not args.gathered_targets, graph=graph)
         for _ in range(w.n_chunks):             # stream the ensemble once (untimed)
             tr.iterate()
         for _ in range(warmup):
@@ -703,7 +725,10 @@ def run_heat(args, w):
               "reservoir_stream": stream_mode(args, w),
               "targets": "gathered into a batch buffer" if args.gathered_targets
               else "read in place from the reservoir by the forward (inputs gathered)",
-              "timed_puts": "none (pre-filled reservoir)" if args.prefilled else "one per step"}
+              "timed_puts": "none (pre-filled reservoir)" if args.prefilled else "one per step",
+              "train_step": ("captured once as a HIP graph and replayed (Adam's step counter in device memory; "
+                             "the reservoir's calls eager); its kernels timed on eager steps after the timed region")
+              if graph else "kernels launched per step"}
     line = result_line(w, args, K, warmup, r, config)
     line["instrumentation"] = instr
     tr.close()

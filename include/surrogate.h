@@ -85,6 +85,22 @@ int surrogate_get_adam_state(ot_surrogate* s, int32_t layer, float* mW_host, flo
 /* Set the learning rate used by later train steps (schedules). */
 int surrogate_set_lr(ot_surrogate* s, float lr);
 
+/* Device step counter, for callers that capture a train step once (HIP graph
+ * capture on their stream) and replay it.  Adam's bias corrections
+ * 1 - beta^t (Kingma and Ba's Algorithm 1, the optimizer of Sec. 4.1) depend
+ * on the step t, normally a host-side argument of the step's kernels; with
+ * enable = 1 the kernels read the number of completed steps from device
+ * memory instead and the step ends with a launch that advances it, so that
+ * the captured launches stay valid for every replay.  The corrections are
+ * formed the same way in both modes (binary exponentiation in double), so
+ * steps agree bit for bit.  Switching synchronises the device; with the
+ * counter on, surrogate_get_adam_state and surrogate_checkpoint read the
+ * device's count, surrogate_restore sets it, and enable = 0 copies it back to
+ * the host.  A captured step also fixes the learning rate, the batch size,
+ * the buffers and the stream it was captured with.  Errors: OT_E_INVAL,
+ * OT_E_NOMEM, OT_E_HIP. */
+int surrogate_set_device_step(ot_surrogate* s, int32_t enable);
+
 /* One train step on a batch of b rows: forward, MSE loss, backward, Adam.
  * x: b rows of widths[0] fp32 at stride ldx; u: b target rows of widths[L]
  * fp32 at stride ldu (multiple of 4).  loss_dev: device fp32 scalar that

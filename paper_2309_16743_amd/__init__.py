@@ -227,6 +227,11 @@ class Surrogate:
     def set_lr(self, lr: float) -> None:
         check("surrogate_set_lr", load().surrogate_set_lr(self._h, lr))
 
+    def set_device_step(self, enable: bool) -> None:
+        """Adam's step counter in device memory (include/surrogate.h), so that a
+        captured train step can be replayed."""
+        check("surrogate_set_device_step", load().surrogate_set_device_step(self._h, 1 if enable else 0))
+
     def train_step(self, x, u, stream=None, loss=None) -> None:
         xp, ldx = _rows(x, "x")
         up, ldu = _rows(u, "u")

@@ -73,6 +73,7 @@ SIGNATURES = {
     "reservoir_restore": (C.c_int, [vp, vp, i64]),
     "surrogate_get_adam_state": (C.c_int, [vp, i32, vp, vp, vp, vp, C.POINTER(i64)]),
     "surrogate_set_lr": (C.c_int, [vp, f32]),
+    "surrogate_set_device_step": (C.c_int, [vp, i32]),
     "surrogate_train_step": (C.c_int, [vp, vp, i64, vp, i64, i64, vp, vp]),
     "surrogate_train_step_rows": (C.c_int, [vp, vp, i64, vp, i64, vp, i64, i64, vp, vp, vp]),
     "surrogate_predict": (C.c_int, [vp, vp, i64, i64, vp, i64, vp]),

@@ -12,9 +12,38 @@
 
 namespace ot {
 
+// 1 - beta^t, the bias correction of step t (t >= 1), in double by binary
+// exponentiation: the same operations on the host and on the device, so a
+// step whose t is read from device memory uses the same corrections as one
+// whose corrections the host computed.
+__host__ __device__ inline float bias_correction(float beta, long long t) {
+  double r = 1.0, b = (double)beta;
+  for (long long e = t; e > 0; e >>= 1) {
+    if (e & 1) r *= b;
+    b *= b;
+  }
+  return (float)(1.0 - r);
+}
+
 struct AdamArgs {
   float lr, b1, b2, eps;
   float c1, c2;   // bias corrections 1 - b1^t, 1 - b2^t of the step being taken
+  // When set, the step is t = *t_done + 1 (steps completed, in device memory)
+  // and the kernel forms c1, c2 itself (resolved()), so that a captured step
+  // replays with the same arguments.
+  const long long* t_done;
+
+#ifdef __HIPCC__
+  __device__ __forceinline__ AdamArgs resolved() const {
+    AdamArgs a = *this;
+    if (t_done) {
+      const long long t = *t_done + 1;
+      a.c1 = bias_correction(b1, t);
+      a.c2 = bias_correction(b2, t);
+    }
+    return a;
+  }
+#endif
 };
 
 #ifdef __HIPCC__

@@ -257,7 +257,7 @@ struct BEpi {
           if (col + c >= g.N) break;
           const int64_t o = m * g.ldc + col + c;
           float p = P[o], mo = g.adam_m[o], vo = g.adam_v[o];
-          adam1(p, ep[rr * EP + 4 * cg + c], mo, vo, g.adam);
+          adam1(p, ep[rr * EP + 4 * cg + c], mo, vo, g.adam.resolved());
           P[o] = p;
           g.adam_m[o] = mo;
           g.adam_v[o] = vo;
@@ -266,6 +266,7 @@ struct BEpi {
       }
       return;
     }
+    const AdamArgs ad = g.adam.resolved();
     f32x4 pp[2][G], mm[2][G], vv[2][G];
     auto load = [&](int grp, int buf) {
 #pragma unroll
@@ -289,7 +290,7 @@ struct BEpi {
         const int64_t m = m0 + rr;
         if (m >= g.M) continue;
         const f32x4 gr = *reinterpret_cast<const f32x4*>(ep + rr * EP + 4 * cg);
-        adam4(pp[buf][u], gr, mm[buf][u], vv[buf][u], g.adam);
+        adam4(pp[buf][u], gr, mm[buf][u], vv[buf][u], ad);
         const int64_t o = m * g.ldc + col;
         __builtin_nontemporal_store(pp[buf][u], reinterpret_cast<f32x4*>(P + o));
         __builtin_nontemporal_store(mm[buf][u], reinterpret_cast<f32x4*>(g.adam_m + o));

@@ -332,6 +332,7 @@ __attribute__((amdgpu_waves_per_eu((EPI == Epi::Mse && FM * FN == 8) ? 5 : 1))) 
 
   // ---------------------------------------------------------------- epilogue
   float lsum = 0.f;
+  [[maybe_unused]] const AdamArgs ad = (EPI == Epi::Adam) ? g.adam.resolved() : g.adam;
   const int64_t row_base = m0 + 16 * FM * wm + 4 * FM * (lane / 16);
   const int64_t col_base = n0 + 16 * FN * wn + FN * (lane % 16);
   float* Cb = g.C + (EPI == Epi::SplitK ? split * g.split_stride : 0);
@@ -440,7 +441,7 @@ __attribute__((amdgpu_waves_per_eu((EPI == Epi::Mse && FM * FN == 8) ? 5 : 1))) 
         if (FN == 4 && full) {
           f32x4 P = *reinterpret_cast<const f32x4*>(cp), Mo = *reinterpret_cast<const f32x4*>(mp),
                 V = *reinterpret_cast<const f32x4*>(vp);
-          adam4(P, f32x4{v[0], v[FN > 1 ? 1 : 0], v[FN > 2 ? 2 : 0], v[FN > 3 ? 3 : 0]}, Mo, V, g.adam);
+          adam4(P, f32x4{v[0], v[FN > 1 ? 1 : 0], v[FN > 2 ? 2 : 0], v[FN > 3 ? 3 : 0]}, Mo, V, ad);
           *reinterpret_cast<f32x4*>(cp) = P;
           *reinterpret_cast<f32x4*>(mp) = Mo;
           *reinterpret_cast<f32x4*>(vp) = V;
@@ -449,7 +450,7 @@ __attribute__((amdgpu_waves_per_eu((EPI == Epi::Mse && FM * FN == 8) ? 5 : 1))) 
           for (int h = 0; h < FN; ++h) {
             if (col_base + h >= g.N) continue;
             float P = cp[h], Mo = mp[h], V = vp[h];
-            adam1(P, v[h], Mo, V, g.adam);
+            adam1(P, v[h], Mo, V, ad);
             cp[h] = P;
             mp[h] = Mo;
             vp[h] = V;

@@ -282,9 +282,15 @@ __device__ __forceinline__ void adam_groups(const AdamRest& r, const AdamArgs& a
 }
 
 // Standalone last pass: block 0 also forms the loss.
-__global__ __launch_bounds__(256) void adam_kernel(AdamRest r, AdamArgs a) {
+__global__ __launch_bounds__(256) void adam_kernel(AdamRest r, AdamArgs args) {
+  const AdamArgs a = args.resolved();
   if (blockIdx.x == 0 && r.partials) reduce_loss_256(r);
   adam_groups(r, a, (int64_t)blockIdx.x * 256 + threadIdx.x, (int64_t)gridDim.x * 256);
+}
+
+// Device step counter of a captured step: one more step completed.
+__global__ void step_done_kernel(long long* t_done) {
+  if (threadIdx.x == 0 && blockIdx.x == 0) *t_done += 1;
 }
 
 // Split-K reduction fused with Adam (fp32 output layer), blocks of 256: the
@@ -300,11 +306,12 @@ __global__ __launch_bounds__(256) void adam_kernel(AdamRest r, AdamArgs a) {
 __global__ __launch_bounds__(256) void splitk_adam_kernel(const float* __restrict__ ws, int64_t splits,
                                                           int64_t split_stride, int64_t M, int64_t N, int64_t ldws,
                                                           float* __restrict__ p, float* __restrict__ mo,
-                                                          float* __restrict__ vo, int64_t ldp, AdamArgs a,
+                                                          float* __restrict__ vo, int64_t ldp, AdamArgs args,
                                                           const float* __restrict__ rs, int64_t rs_stride,
                                                           float* __restrict__ rowsum_out, float* __restrict__ bias_p,
                                                           float* __restrict__ bias_m, float* __restrict__ bias_v,
                                                           int64_t main_blocks, AdamRest rest) {
+  const AdamArgs a = args.resolved();
   if ((int64_t)blockIdx.x >= main_blocks) {
     const int64_t rb = blockIdx.x - main_blocks;
     if (rb == 0 && rest.partials) reduce_loss_256(rest);
@@ -439,6 +446,11 @@ struct ot_surrogate {
   bool fuse_out = false;      // output-layer Adam fused into its weight-gradient epilogue
   bool fused_step = false;    // ... and the current step took that path
   ot::AdamArgs step_adam{};   // Adam scalars of the current step
+  // Device step counter (surrogate_set_device_step): steps completed, read by
+  // the Adam kernels of every step and advanced by the step's last launch, so
+  // that a step's launches can be captured once and replayed.
+  long long* t_done_dev = nullptr;
+  bool device_step = false;
   // Workspaces, sized for ws_rows batch rows.
   int64_t ws_rows = 0;
   std::vector<float*> act;   // act[l] = A_l, l = 1..L-1 (index 0 unused)
@@ -520,6 +532,7 @@ void free_surrogate(ot_surrogate* s) {
   (void)hipFree(s->v);
   (void)hipFree(s->loss_last);
   (void)hipFree(s->eval_acc);
+  (void)hipFree(s->t_done_dev);
   (void)hipFree(s->pb);
   (void)hipFree(s->colsum);
   delete s;
@@ -1290,11 +1303,24 @@ extern "C" int surrogate_get_grads(ot_surrogate* s, int32_t layer, float* dW_hos
   return copy_layer(s, layer, s->grads, dW_host, db_host);
 }
 
+// The host's step count after steps that ran with the device counter (a
+// captured step replayed advances only the device's).
+static int sync_step_count(ot_surrogate* s) {
+  if (!s->device_step) return OT_OK;
+  OT_HIP(hipDeviceSynchronize());
+  long long t = 0;
+  OT_HIP(hipMemcpy(&t, s->t_done_dev, sizeof t, hipMemcpyDeviceToHost));
+  s->t = t;
+  return OT_OK;
+}
+
 extern "C" int surrogate_get_adam_state(ot_surrogate* s, int32_t layer, float* mW_host, float* mb_host,
                                         float* vW_host, float* vb_host, int64_t* t_out) {
   ot::clear_error();
   OT_REQUIRE(s != nullptr, "surrogate_get_adam_state: NULL surrogate");
-  int rc = copy_layer(s, layer, s->m, mW_host, mb_host);
+  int rc = sync_step_count(s);
+  if (rc) return rc;
+  rc = copy_layer(s, layer, s->m, mW_host, mb_host);
   if (rc) return rc;
   rc = copy_layer(s, layer, s->v, vW_host, vb_host);
   if (rc) return rc;
@@ -1312,9 +1338,8 @@ extern "C" int surrogate_set_lr(ot_surrogate* s, float lr) {
 // Adam scalars of the step about to run (t counts from 1).
 static void begin_step(ot_surrogate* s) {
   s->t += 1;
-  const double c1 = 1.0 - std::pow((double)s->beta1, (double)s->t);
-  const double c2 = 1.0 - std::pow((double)s->beta2, (double)s->t);
-  s->step_adam = ot::AdamArgs{s->lr, s->beta1, s->beta2, s->eps, (float)c1, (float)c2};
+  s->step_adam = ot::AdamArgs{s->lr, s->beta1, s->beta2, s->eps, ot::bias_correction(s->beta1, s->t),
+                              ot::bias_correction(s->beta2, s->t), s->device_step ? s->t_done_dev : nullptr};
   const Layer& lo = s->layers[s->L - 1];
   // a single layer with a small input width takes the small-K gradient kernels, which store
   s->fused_step = s->fuse_out && !(s->L == 1 && lo.in <= ot::kMaxSmallK);
@@ -1403,9 +1428,9 @@ static int check_batch(ot_surrogate* s, const float* x, int64_t ldx, const float
 // The train step.  u_rows (nullable): target row j is u + u_rows[j] * ldu
 // (indices clamped to [0, u_rows_max]); targets_read (nullable): recorded on
 // the stream once every target has been read.
-static int train_step(ot_surrogate* s, const float* x, int64_t ldx, const float* u, int64_t ldu,
-                      const int32_t* u_rows, int64_t u_rows_max, int64_t b, void* stream, float* loss_dev,
-                      hipEvent_t targets_read) {
+static int train_step_launches(ot_surrogate* s, const float* x, int64_t ldx, const float* u, int64_t ldu,
+                               const int32_t* u_rows, int64_t u_rows_max, int64_t b, void* stream, float* loss_dev,
+                               hipEvent_t targets_read) {
   const int L = s->L;
   int rc;
   const int64_t D = s->widths[L];
@@ -1538,6 +1563,40 @@ static int train_step(ot_surrogate* s, const float* x, int64_t ldx, const float*
   return rc;
 }
 
+// One train step; with the device step counter on, its last launch advances
+// the counter that the step's Adam kernels read.
+static int train_step(ot_surrogate* s, const float* x, int64_t ldx, const float* u, int64_t ldu,
+                      const int32_t* u_rows, int64_t u_rows_max, int64_t b, void* stream, float* loss_dev,
+                      hipEvent_t targets_read) {
+  int rc = train_step_launches(s, x, ldx, u, ldu, u_rows, u_rows_max, b, stream, loss_dev, targets_read);
+  if (rc == OT_OK && s->device_step) {
+    hipLaunchKernelGGL(ot::step_done_kernel, dim3(1), dim3(64), 0, static_cast<hipStream_t>(stream), s->t_done_dev);
+    OT_LAUNCHED("step_done_kernel");
+  }
+  return rc;
+}
+
+extern "C" int surrogate_set_device_step(ot_surrogate* s, int32_t enable) {
+  ot::clear_error();
+  OT_REQUIRE(s != nullptr, "surrogate_set_device_step: NULL surrogate");
+  OT_REQUIRE(enable == 0 || enable == 1, "surrogate_set_device_step: enable must be 0 or 1");
+  if ((enable != 0) == s->device_step) return OT_OK;
+  if (enable) {
+    if (!s->t_done_dev) {
+      int rc = salloc((void**)&s->t_done_dev, sizeof(long long));
+      if (rc) return rc;
+    }
+    OT_HIP(hipDeviceSynchronize());
+    const long long t = s->t;
+    OT_HIP(hipMemcpy(s->t_done_dev, &t, sizeof t, hipMemcpyHostToDevice));
+    s->device_step = true;
+    return OT_OK;
+  }
+  int rc = sync_step_count(s);
+  s->device_step = false;
+  return rc;
+}
+
 extern "C" int surrogate_train_step(ot_surrogate* s, const float* x, int64_t ldx, const float* u, int64_t ldu,
                                     int64_t b, void* stream, float* loss_dev) {
   ot::clear_error();
@@ -1615,6 +1674,8 @@ extern "C" int surrogate_checkpoint(ot_surrogate* s, void* buf, int64_t bytes) {
   OT_REQUIRE(s != nullptr && buf != nullptr, "surrogate_checkpoint: NULL argument");
   OT_REQUIRE(bytes >= sur_blob_bytes(s), "surrogate_checkpoint: buffer of %lld bytes, %lld needed",
              (long long)bytes, (long long)sur_blob_bytes(s));
+  int rc = sync_step_count(s);
+  if (rc) return rc;
   OT_HIP(hipDeviceSynchronize());
   ot::BlobWriter w(buf, bytes);
   __builtin_memcpy(w.take(8), kSurMagic, 8);
@@ -1659,6 +1720,10 @@ extern "C" int surrogate_restore(ot_surrogate* s, const void* buf, int64_t bytes
   s->beta1 = hp[1];
   s->beta2 = hp[2];
   s->eps = hp[3];
+  if (s->device_step) {
+    const long long td = t;
+    OT_HIP(hipMemcpy(s->t_done_dev, &td, sizeof td, hipMemcpyHostToDevice));
+  }
   return OT_OK;
 }
 

@@ -2,7 +2,11 @@
 step per iteration, as the paper's server runs a data-aggregator thread that
 fills the buffer and a training thread that draws batches from it (Sec. 3.1).
 
-By default all work is enqueued on one HIP stream.  With overlap=True the
+By default all work is enqueued on one HIP stream.  With graph=True (one
+stream only) the train step is captured once as a HIP graph, with Adam's
+step counter in device memory (surrogate_set_device_step), and replayed for
+every later step of full batches: the reservoir's calls stay eager, the train
+step costs one launch.  With overlap=True the
 reservoir (put, draw, gather) runs on its own ordering stream and the train
 step on the trainer's stream, with two batch buffers: the draw and gather of
 batch i + 1 run while batch i trains, as the paper's two threads do.  Events
@@ -119,7 +123,7 @@ class OnlineTrainer:
                  chunk_fn: Optional[Callable] = None, n_chunks: int = 0, device=None, flags: int = 0,
                  overlap: bool = False, policy: int = OT_POLICY_RESERVOIR,
                  lr_schedule: Optional[Callable[[int], float]] = None, reception_log: bool = False,
-                 fused_targets: bool = True, put_streams: Optional[list] = None):
+                 fused_targets: bool = True, put_streams: Optional[list] = None, graph: bool = False):
         self.stream = stream if stream is not None else torch.cuda.current_stream()
         self.widths = tuple(widths)
         self.batch, self.wave, self.tau = batch, wave, tau
@@ -179,6 +183,12 @@ class OnlineTrainer:
         # producer streams (the paper's clients): chunk c is put from put_streams[c mod P];
         # default: the reservoir's own stream
         self.put_streams = list(put_streams) if put_streams else None
+        if graph and (overlap or not fused_targets or lr_schedule is not None):
+            raise ValueError("graph=True needs one stream, targets read in place and a constant learning rate")
+        self.graph = graph
+        self.graph_active = graph        # callers may run eager steps (e.g. with phase timing) meanwhile
+        self._graph = None
+        self._graph_warm = False
 
     def chunk_views(self, c: int):
         if self.chunk_fn is not None:
@@ -245,7 +255,8 @@ class OnlineTrainer:
     def sample_and_train(self) -> bool:
         rec = self.steps_done < self.record_steps
         j = self.steps_done % len(self.xbufs)
-        slots = self.slot_log[self.steps_done] if rec else self.slotbufs[j]
+        # a graph replays on the buffers it was captured with: its slots are copied to the log afterwards
+        slots = self.slot_log[self.steps_done] if rec and not self.graph else self.slotbufs[j]
         xb = self.xbufs[j]
         ub = None if self.fused_targets else self.ubufs[j]
         # the step two back has finished with buffer j
@@ -267,7 +278,9 @@ class OnlineTrainer:
             if lr != self.lr:
                 self.sur.set_lr(lr)       # host-side rate, taken by the next enqueued step
                 self.lr = lr
-        if self.fused_targets:
+        if self.graph and self.graph_active and n == self.batch:
+            self._graph_step(xb, slots, loss)
+        elif self.fused_targets:
             self.sur.train_step_rows(xb, self.u_slab, self.ldu_slab, slots, self.res.capacity, stream=self.stream,
                                      loss=loss, targets_read=self.targets_read if self.overlap else None)
             self.targets_read_recorded = self.overlap
@@ -277,8 +290,34 @@ class OnlineTrainer:
         if self.overlap and not self.fused_targets:
             self.released[j].record(self.stream)
             self.released_recorded[j] = True
+        if rec and self.graph:
+            with torch.cuda.stream(self.stream):
+                self.slot_log[self.steps_done, :n].copy_(slots)
         self.steps_done += 1
         return True
+
+    def _graph_step(self, xb, slots, loss) -> None:
+        """The train step as a replay of its captured launches (captured at the
+        second call, on this trainer's buffers, which the replays reuse; the
+        first runs eagerly, so that the step's workspaces exist before capture,
+        which allows no allocation)."""
+        if not self._graph_warm:
+            self._graph_warm = True
+            self.sur.train_step_rows(xb, self.u_slab, self.ldu_slab, slots, self.res.capacity, stream=self.stream,
+                                     loss=loss)
+            return
+        if self._graph is None:
+            torch.cuda.synchronize()
+            self.sur.set_device_step(True)
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g):
+                self.sur.train_step_rows(xb, self.u_slab, self.ldu_slab, slots, self.res.capacity,
+                                         stream=torch.cuda.current_stream(), loss=self.loss)
+            self._graph = g
+        with torch.cuda.stream(self.stream):
+            self._graph.replay()
+            if loss.data_ptr() != self.loss.data_ptr():
+                loss.copy_(self.loss)
 
     def iterate(self, wrap: bool = False) -> bool:
         """One iteration of the schedule; returns whether a train step ran."""

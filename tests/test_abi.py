@@ -70,6 +70,7 @@ def test_validation_errors_before_device_work(lib):
     assert b"NULL surrogate" in lib.ot_last_error()
     assert lib.surrogate_eval_loss(None, None, 0, None, 0, 1, None, None) == _abi.OT_E_INVAL
     assert lib.surrogate_set_lr(None, C.c_float(1e-3)) == _abi.OT_E_INVAL
+    assert lib.surrogate_set_device_step(None, 1) == _abi.OT_E_INVAL
     assert lib.reservoir_slab(None, None, None, None, None) == _abi.OT_E_INVAL
     assert b"NULL reservoir" in lib.ot_last_error()
     assert lib.reservoir_destroy(None) == _abi.OT_OK

@@ -212,6 +212,53 @@ def test_tiny_workload_100_steps_fused():
     tr.close()
 
 
+def test_tiny_workload_graph_replayed_train_step():
+    """The 16x16 schedule with the train step captured once as a HIP graph
+    (Adam's step counter in device memory) and replayed for every step, the
+    reservoir's calls and the log copies eager between the replays: slots,
+    every step's loss and the final parameters and Adam state equal those of
+    the eager run bit for bit (the step's arguments do not change between
+    replays, and both modes form Adam's bias corrections the same way), and
+    the oracle's within 1e-3."""
+    from paper_2309_16743_amd.online import OnlineTrainer
+    w = configs.TINY
+    X = heat.sample_parameters(w.n_sims, w.data_seed)
+    inputs = heat.inputs_for(X, w.tau)
+    fields = heat.heat_fields(X, w.grid, w.tau)
+    ref = runner.run(w, inputs, fields, n_steps=60)
+    runs = {}
+    for graph in (False, True):
+        tr = OnlineTrainer(w.widths, w.batch, w.capacity, w.threshold, w.wave, w.tau,
+                           torch.from_numpy(inputs).to(DEV), torch.from_numpy(fields).to(DEV),
+                           w.reservoir_seed, w.init_seed, lr=w.lr, record_steps=60, graph=graph)
+        while tr.steps_done < 60:
+            tr.iterate()
+            if tr.steps_done % 7 == 0:
+                torch.cuda.synchronize()          # host synchronisations between replays
+        torch.cuda.synchronize()
+        if graph:
+            assert tr._graph is not None
+        runs[graph] = (tr.slot_log.cpu().numpy(), tr.loss_log.cpu().numpy(),
+                       [tr.sur.get_params(l) for l in range(3)], [tr.sur.get_adam_state(l) for l in range(3)])
+        if graph:
+            tr.sur.set_device_step(False)
+            assert tr.sur.get_adam_state(0)[2] == 60
+        tr.close()
+    (s0, l0, p0, a0), (s1, l1, p1, a1) = runs[False], runs[True]
+    assert np.array_equal(s0, s1)
+    assert np.array_equal(l0, l1)
+    for l in range(3):
+        assert np.array_equal(p0[l][0], p1[l][0]) and np.array_equal(p0[l][1], p1[l][1])
+        (m0, v0, t0), (m1, v1, t1) = a0[l], a1[l]
+        assert t0 == t1 == 60
+        assert all(np.array_equal(x, y) for x, y in zip(m0 + v0, m1 + v1))
+    for i in range(60):
+        assert np.array_equal(s1[i], ref["slots"][i]), i
+    assert rel(l1, ref["losses"]) < 1e-3
+    for l in range(3):
+        assert rel(p1[l][0], ref["params"][l][0]) < 1e-3
+
+
 def test_tiny_workload_overlapped_streams():
     """The 16x16 schedule with the reservoir on its own stream and two batch
     buffers (the draw of batch i + 1 overlaps train step i): the same slots
