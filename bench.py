@@ -539,8 +539,11 @@ def timed_region(tr, w, K, profile_steps, stream, wrap_put):
     out_phases = [p for p in ("fwd_output", "wgrad_output", "igrad_output") if p in breakdown]
     sur_phases = [p for p in SURROGATE_PHASES if p in out_phases or p == dom_phase]
     if not graph:
+        # with the train step replayed as a graph the step is launch-bound and
+        # per-launch events would cost more host time than the step itself:
+        # those kernels are timed on eager steps after the timed region
         tr.sur.timing_begin(sur_phases, K)
-    tr.res.timing_begin(["put_copy", "gather"], 2 * K)
+        tr.res.timing_begin(["put_copy", "gather"], 2 * K)
     n_win = K // 10
     ev = [torch.cuda.Event(enable_timing=True) for _ in range(n_win + 2)]
     torch.cuda.synchronize()
@@ -558,21 +561,24 @@ def timed_region(tr, w, K, profile_steps, stream, wrap_put):
     wall = time.perf_counter() - t0
     gpu_ms = ev[0].elapsed_time(ev[-1])
     windows = [ev[j].elapsed_time(ev[j + 1]) for j in range(n_win)]
-    res_t = tr.res.timing_end()
     if graph:
         # the timed steps replayed the captured train step, which records no
-        # phase events: the train step's kernels are timed on eager steps
-        # that follow the timed region
+        # phase events: the train step's kernels, and the reservoir's put
+        # copies and gathers, are timed on eager steps that follow the timed
+        # region
         kt = min(K, 200)
         tr.graph_active = False
         tr.sur.timing_begin(sur_phases, kt)
+        tr.res.timing_begin(["put_copy", "gather"], 2 * kt)
         for _ in range(kt):
             wrap_put()
             assert tr.sample_and_train()
         sur_t = tr.sur.timing_end()
+        res_t = tr.res.timing_end()
         tr.graph_active = True
     else:
         sur_t = tr.sur.timing_end()
+        res_t = tr.res.timing_end()
     g_ms, g_n = res_t["gather"]
     phase_avg_s = {p: sur_t[p][0] / sur_t[p][1] * 1e-3 for p in sur_phases if p in sur_t}
     put_avg_s = res_t["put_copy"][0] / res_t["put_copy"][1] * 1e-3 if "put_copy" in res_t else None
@@ -624,7 +630,8 @@ def output_layer_entry(w, phase_avg_s: dict) -> dict:
 
 def reservoir_entry(w, r) -> dict:
     """Put copies (whole rows into the slab: the reservoir's bandwidth at this
-    shape) and the batch gather, timed in the timed region."""
+    shape) and the batch gather, timed in the timed region (on eager steps
+    after it when the train step is replayed as a graph)."""
     g_rate = gather_bytes(w) / r["gather_avg_s"]
     out = {"gather": {"achieved": round(g_rate / 1e9, 1), "unit": "GB/s", "frac_hbm": round(g_rate / PEAK_HBM, 4),
                       "avg_us": round(r["gather_avg_s"] * 1e6, 2), "bytes_per_launch": gather_bytes(w),
@@ -727,7 +734,8 @@ def run_heat(args, w):
               else "read in place from the reservoir by the forward (inputs gathered)",
               "timed_puts": "none (pre-filled reservoir)" if args.prefilled else "one per step",
               "train_step": ("captured once as a HIP graph and replayed (Adam's step counter in device memory; "
-                             "the reservoir's calls eager); its kernels timed on eager steps after the timed region")
+                             "the reservoir's calls eager); its kernels and the reservoir's copies timed on eager "
+                             "steps after the timed region")
               if graph else "kernels launched per step"}
     line = result_line(w, args, K, warmup, r, config)
     line["instrumentation"] = instr
