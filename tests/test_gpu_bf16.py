@@ -68,7 +68,8 @@ SHAPES = [
     ((6, 128, 128, 128, 300), 64),     # three hidden layers
     ((6, 512, 512, 20000), 512),       # pipelined 256 x 128 kernel, the bf16 workloads' batch
     ((6, 512, 512, 30001), 320),       # pipelined kernel with ragged M and N (clamped edges)
-    ((6, 1024, 1024, 69984), 512),     # split-K pipelined input gradient (63 splits, ragged last split)
+    ((6, 1024, 1024, 69984), 512),     # ping-pong forward, ragged N; split-K input gradient (63 splits, ragged last split)
+    ((6, 512, 512, 69984), 300),       # ping-pong forward and split-K input gradient with a ragged batch (M = 300)
     ((6, 2048, 2048, 2048, 4096), 1024),   # the deep 1000x1000 net's hidden widths and batch
     ((6, 16, 16, 1), 1),               # one sample, one output
     ((6, 40, 24, 9), 3),               # three samples, ragged narrow widths
