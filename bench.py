@@ -43,9 +43,11 @@ step (batch size x steps / time), from HIP events on the work stream over the
 timed steps.  `roofline` reports the dominant kernel's algorithmic rate
 against MI355X's datasheet peak, from HIP events that the library hands to
 that kernel's launch (hipExtLaunchKernel stamps them with the kernel's own
-start and end) on the stream it runs on, inside the same timed region;
-`output_layer` does the same for the three output-layer GEMMs and
-`reservoir` for the put copies and the gather.  `cpu_baseline` times the
+start and end) on the stream it runs on, inside the same timed region (the
+only launches there that carry events; a replayed train step carries none,
+and then its kernels are timed as below); `output_layer` does the same for
+the three output-layer GEMMs and `reservoir` for the put copies and the
+gather, on eager steps right after the timed region.  `cpu_baseline` times the
 plain fp64 CPU oracle on a bounded sample of the same workload on this host.
 """
 from __future__ import annotations
@@ -515,7 +517,8 @@ def cpu_baseline_field(w, seconds: float) -> dict:
 
 def timed_region(tr, w, K, profile_steps, stream, wrap_put):
     """Breakdown pass (all phases), then K timed steps with events on the
-    dominant kernel and the gather."""
+    dominant kernel, then eager steps that time the other output-layer GEMMs,
+    the put copies and the gather."""
     import torch
 
     from paper_2309_16743_amd._abi import SURROGATE_PHASES
@@ -535,15 +538,20 @@ def timed_region(tr, w, K, profile_steps, stream, wrap_put):
     dominant = max((c for c in candidates if c in breakdown), key=lambda p: breakdown[p]["avg_us"])
     dom_phase = "gather" if dominant == "reservoir_gather" else dominant
 
-    # timed region: the dominant kernel, the three output-layer GEMMs, the put copies and the gather
+    # timed region: HIP events on the launches of the dominant kernel only
+    # (each event pair on a launch costs host time and a few microseconds of
+    # GPU time between kernels, which would show in a short step); the other
+    # output-layer GEMMs, the put copies and the gather are timed on eager
+    # steps right after the timed region.  A train step replayed as a graph
+    # records no phase events, so then the dominant kernel is timed there too.
     out_phases = [p for p in ("fwd_output", "wgrad_output", "igrad_output") if p in breakdown]
     sur_phases = [p for p in SURROGATE_PHASES if p in out_phases or p == dom_phase]
-    if not graph:
-        # with the train step replayed as a graph the step is launch-bound and
-        # per-launch events would cost more host time than the step itself:
-        # those kernels are timed on eager steps after the timed region
-        tr.sur.timing_begin(sur_phases, K)
-        tr.res.timing_begin(["put_copy", "gather"], 2 * K)
+    live = not graph
+    if live:
+        if dom_phase == "gather":
+            tr.res.timing_begin(["gather"], 2 * K)
+        else:
+            tr.sur.timing_begin([dom_phase], K)
     n_win = K // 10
     ev = [torch.cuda.Event(enable_timing=True) for _ in range(n_win + 2)]
     torch.cuda.synchronize()
@@ -561,24 +569,25 @@ def timed_region(tr, w, K, profile_steps, stream, wrap_put):
     wall = time.perf_counter() - t0
     gpu_ms = ev[0].elapsed_time(ev[-1])
     windows = [ev[j].elapsed_time(ev[j + 1]) for j in range(n_win)]
-    if graph:
-        # the timed steps replayed the captured train step, which records no
-        # phase events: the train step's kernels, and the reservoir's put
-        # copies and gathers, are timed on eager steps that follow the timed
-        # region
-        kt = min(K, 200)
-        tr.graph_active = False
-        tr.sur.timing_begin(sur_phases, kt)
-        tr.res.timing_begin(["put_copy", "gather"], 2 * kt)
-        for _ in range(kt):
-            wrap_put()
-            assert tr.sample_and_train()
-        sur_t = tr.sur.timing_end()
-        res_t = tr.res.timing_end()
-        tr.graph_active = True
-    else:
-        sur_t = tr.sur.timing_end()
-        res_t = tr.res.timing_end()
+    live_t = {}
+    if live:
+        live_t = tr.res.timing_end() if dom_phase == "gather" else tr.sur.timing_end()
+    kt = min(K, 200)
+    tr.graph_active = False
+    post_sur = [p for p in sur_phases if not (live and p == dom_phase)]
+    if post_sur:
+        tr.sur.timing_begin(post_sur, kt)
+    tr.res.timing_begin(["put_copy", "gather"], 2 * kt)
+    for _ in range(kt):
+        wrap_put()
+        assert tr.sample_and_train()
+    sur_t = tr.sur.timing_end() if post_sur else {}
+    res_t = tr.res.timing_end()
+    tr.graph_active = graph
+    if live and dom_phase == "gather":
+        res_t["gather"] = live_t["gather"]
+    elif live:
+        sur_t[dom_phase] = live_t[dom_phase]
     g_ms, g_n = res_t["gather"]
     phase_avg_s = {p: sur_t[p][0] / sur_t[p][1] * 1e-3 for p in sur_phases if p in sur_t}
     put_avg_s = res_t["put_copy"][0] / res_t["put_copy"][1] * 1e-3 if "put_copy" in res_t else None
@@ -608,7 +617,8 @@ def steps_rate(tr, w, K, stream, wrap_put) -> dict:
 
 
 def output_layer_entry(w, phase_avg_s: dict) -> dict:
-    """Rates of the output layer's three GEMMs measured in the timed region:
+    """Rates of the output layer's three GEMMs (the dominant one measured in
+    the timed region, the others on the eager steps that follow it):
     forward (+ fused MSE) and input gradient against the MFMA peak of their
     precision; the weight gradient too, and in bf16, where it applies Adam to
     the output weights in its epilogue, also against HBM."""
@@ -630,8 +640,8 @@ def output_layer_entry(w, phase_avg_s: dict) -> dict:
 
 def reservoir_entry(w, r) -> dict:
     """Put copies (whole rows into the slab: the reservoir's bandwidth at this
-    shape) and the batch gather, timed in the timed region (on eager steps
-    after it when the train step is replayed as a graph)."""
+    shape) and the batch gather, timed on the eager steps that follow the
+    timed region (in it when the gather is the dominant kernel)."""
     g_rate = gather_bytes(w) / r["gather_avg_s"]
     out = {"gather": {"achieved": round(g_rate / 1e9, 1), "unit": "GB/s", "frac_hbm": round(g_rate / PEAK_HBM, 4),
                       "avg_us": round(r["gather_avg_s"] * 1e6, 2), "bytes_per_launch": gather_bytes(w),
